@@ -1,0 +1,224 @@
+"""CPU oracle for vocabulary alignment and masked greedy decoding.
+
+TEST INFRASTRUCTURE ONLY: the test suite, ``__graft_entry__.smoke()`` and the
+benchmark's ``cpu_baseline`` leg are the only callers.  The product path never
+imports this package.  It shares no code with the HIP library; the arithmetic
+lives in ``dv_oracle.c`` (plain scalar C loops), this module only marshals
+numpy arrays into it.
+
+What each function follows in the paper (DOMINO, "Guiding LLMs The Right
+Way"):
+
+* ``walk`` / ``align`` / ``align_rows``: Sec. 3.3 and Algorithm 2 -- every
+  scanner state is walked through every vocabulary token; at full lookahead
+  (Sec. 3.5, k = infinity) a token is allowed exactly when the walk survives.
+* ``masked_step`` / ``masked_argmax``: Algorithm 1 (mask, apply, decode,
+  update) with Algorithm 3's argmax over an admissible token set.
+
+All readings of the paper's silences (DEAD sentinel, byte alphabet, tie and
+NaN rules, bitmask layout) are stated in ``dv_oracle.c``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+DEAD = -1
+F32 = 0
+BF16 = 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "dv_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "libdv_oracle.so")
+_lib = None
+
+
+def build(force: bool = False, out: str | None = None, defines: tuple = ()) -> str:
+    """Compile ``dv_oracle.c`` with gcc into a shared library; returns its path."""
+    out = out or _LIB_PATH
+    if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(_SRC):
+        cmd = ["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-o", out, _SRC, "-lm"]
+        cmd += [f"-D{d}" for d in defines]
+        subprocess.run(cmd, check=True)
+    return out
+
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_u32p = ctypes.POINTER(ctypes.c_uint32)
+_u8p = ctypes.POINTER(ctypes.c_uint8)
+
+
+def _bind(lib):
+    lib.oracle_walk.restype = ctypes.c_int32
+    lib.oracle_walk.argtypes = [_i32p, ctypes.c_int32, ctypes.c_int32, _u8p, ctypes.c_int64]
+    lib.oracle_align_rows.restype = None
+    lib.oracle_align_rows.argtypes = [_i32p, ctypes.c_int32, _i32p, _u8p, ctypes.c_int32,
+                                      _i32p, ctypes.c_int64, _i32p, _u32p]
+    lib.oracle_align.restype = None
+    lib.oracle_align.argtypes = [_i32p, ctypes.c_int32, _i32p, _u8p, ctypes.c_int32, _i32p, _u32p]
+    lib.oracle_masked_argmax.restype = ctypes.c_int32
+    lib.oracle_masked_argmax.argtypes = [_u32p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int32]
+    lib.oracle_masked_step.restype = None
+    lib.oracle_masked_step.argtypes = [_i32p, _u32p, ctypes.c_int32, ctypes.c_int32, _i32p,
+                                       ctypes.c_void_p, ctypes.c_int, ctypes.c_int32,
+                                       ctypes.c_int64, _i32p, _i32p]
+    lib.oracle_walk_lookups.restype = ctypes.c_int64
+    lib.oracle_walk_lookups.argtypes = [_i32p, ctypes.c_int32, _i32p, _u8p, ctypes.c_int32,
+                                        _i32p, ctypes.c_int64]
+    return lib
+
+
+def load(path: str | None = None):
+    """Load the oracle library (compiling it first if it is not built)."""
+    global _lib
+    if path is not None:
+        return _bind(ctypes.CDLL(path))
+    if _lib is None:
+        _lib = _bind(ctypes.CDLL(build()))
+    return _lib
+
+
+def _p(a, ct):
+    return a.ctypes.data_as(ct)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def words(num_tokens: int) -> int:
+    return (num_tokens + 31) // 32
+
+
+def walk(trans, s: int, token: bytes, lib=None) -> int:
+    lib = lib or load()
+    trans = _c(trans, np.int32)
+    buf = np.frombuffer(bytes(token), dtype=np.uint8) if len(token) else np.zeros(1, np.uint8)
+    buf = _c(buf, np.uint8)
+    return int(lib.oracle_walk(_p(trans, _i32p), trans.shape[0], int(s), _p(buf, _u8p), len(token)))
+
+
+def align_rows(trans, offsets, tok_bytes, rows, lib=None):
+    """(next_state[len(rows)][V], allow[len(rows)][ceil(V/32)]) for the given states."""
+    lib = lib or load()
+    trans = _c(trans, np.int32)
+    offsets = _c(offsets, np.int32)
+    tok_bytes = _c(tok_bytes if len(tok_bytes) else np.zeros(1, np.uint8), np.uint8)
+    rows = _c(rows, np.int32)
+    V = offsets.shape[0] - 1
+    ns = np.empty((rows.shape[0], V), np.int32)
+    al = np.empty((rows.shape[0], words(V)), np.uint32)
+    lib.oracle_align_rows(_p(trans, _i32p), trans.shape[0], _p(offsets, _i32p),
+                          _p(tok_bytes, _u8p), V, _p(rows, _i32p), rows.shape[0],
+                          _p(ns, _i32p), _p(al, _u32p))
+    return ns, al
+
+
+def align(trans, offsets, tok_bytes, lib=None):
+    """Full table: (next_state[S][V] int32, allow[S][ceil(V/32)] uint32)."""
+    lib = lib or load()
+    trans = _c(trans, np.int32)
+    offsets = _c(offsets, np.int32)
+    tok_bytes = _c(tok_bytes if len(tok_bytes) else np.zeros(1, np.uint8), np.uint8)
+    S = trans.shape[0]
+    V = offsets.shape[0] - 1
+    ns = np.empty((S, V), np.int32)
+    al = np.empty((S, words(V)), np.uint32)
+    lib.oracle_align(_p(trans, _i32p), S, _p(offsets, _i32p), _p(tok_bytes, _u8p), V,
+                     _p(ns, _i32p), _p(al, _u32p))
+    return ns, al
+
+
+def _logit_array(logits):
+    """numpy fp32 array -> (array, F32); numpy uint16 (bf16 bit patterns) -> (array, BF16)."""
+    if logits.dtype == np.float32:
+        return logits, F32
+    if logits.dtype == np.uint16:
+        return logits, BF16
+    raise TypeError(f"logits must be float32 or uint16 bf16 bits, got {logits.dtype}")
+
+
+def masked_argmax(allow_row, logits_row, lib=None) -> int:
+    lib = lib or load()
+    allow_row = _c(allow_row, np.uint32)
+    logits_row, dt = _logit_array(np.ascontiguousarray(logits_row))
+    V = logits_row.shape[0]
+    assert allow_row.shape[0] >= words(V)
+    return int(lib.oracle_masked_argmax(_p(allow_row, _u32p), logits_row.ctypes.data, dt, V))
+
+
+def masked_step(next_state, allow, states, logits, num_tokens: int | None = None, lib=None):
+    """One batch step.  ``logits`` is [B][ld] (ld >= V) fp32 or bf16 bits (uint16)."""
+    lib = lib or load()
+    next_state = _c(next_state, np.int32)
+    allow = _c(allow, np.uint32)
+    states = _c(states, np.int32)
+    logits, dt = _logit_array(np.ascontiguousarray(logits))
+    S, V = next_state.shape
+    if num_tokens is not None:
+        assert num_tokens == V
+    B = states.shape[0]
+    ld = logits.shape[1] if B else V
+    tok = np.empty(B, np.int32)
+    nst = np.empty(B, np.int32)
+    if B:
+        lib.oracle_masked_step(_p(next_state, _i32p), _p(allow, _u32p), S, V, _p(states, _i32p),
+                               logits.ctypes.data, dt, B, ld, _p(tok, _i32p), _p(nst, _i32p))
+    return tok, nst
+
+
+def walk_lookups(trans, offsets, tok_bytes, rows, lib=None) -> int:
+    """Total DFA transitions taken over all (row state, token) walks."""
+    lib = lib or load()
+    trans = _c(trans, np.int32)
+    offsets = _c(offsets, np.int32)
+    tok_bytes = _c(tok_bytes if len(tok_bytes) else np.zeros(1, np.uint8), np.uint8)
+    rows = _c(rows, np.int32)
+    return int(lib.oracle_walk_lookups(_p(trans, _i32p), trans.shape[0], _p(offsets, _i32p),
+                                       _p(tok_bytes, _u8p), offsets.shape[0] - 1,
+                                       _p(rows, _i32p), rows.shape[0]))
+
+
+class RowCache:
+    """Oracle table rows computed on demand, for full-size workloads whose whole
+    table would be too slow or too large for the CPU (the rows are the same
+    definition as ``align``)."""
+
+    def __init__(self, trans, offsets, tok_bytes, lib=None):
+        self.trans = _c(trans, np.int32)
+        self.offsets = _c(offsets, np.int32)
+        self.tok_bytes = _c(tok_bytes, np.uint8)
+        self.lib = lib or load()
+        self.rows: dict[int, tuple[np.ndarray, np.ndarray]] = {}
+
+    def get(self, s: int):
+        if s not in self.rows:
+            ns, al = align_rows(self.trans, self.offsets, self.tok_bytes,
+                                np.array([s], np.int32), lib=self.lib)
+            self.rows[s] = (ns[0], al[0])
+        return self.rows[s]
+
+
+def masked_chain(cache: RowCache, init_state: int, logits_rows, lib=None):
+    """Greedy chain of one batch row over several steps: ``logits_rows`` is
+    [steps][V] for that row.  Returns (tokens[steps], states[steps + 1])."""
+    lib = lib or cache.lib
+    steps = logits_rows.shape[0]
+    S = cache.trans.shape[0]
+    toks = np.full(steps, -1, np.int32)
+    sts = np.full(steps + 1, DEAD, np.int32)
+    s = int(init_state) if 0 <= int(init_state) < S else DEAD
+    sts[0] = s
+    for k in range(steps):
+        if s == DEAD:
+            toks[k], sts[k + 1] = -1, DEAD
+            continue
+        ns_row, al_row = cache.get(s)
+        t = masked_argmax(al_row, logits_rows[k], lib=lib)
+        toks[k] = t
+        s = DEAD if t == -1 else int(ns_row[t])
+        sts[k + 1] = s
+    return toks, sts

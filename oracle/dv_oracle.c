@@ -1,0 +1,178 @@
+/*
+ * CPU oracle for vocabulary alignment and masked greedy decoding.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the slow, obviously correct
+ * statement of what the GPU path computes.  Only the test suite, the smoke
+ * check and the benchmark's CPU-baseline leg may load it.  It shares no code,
+ * header, table or constant with the HIP library and never includes it.
+ *
+ * Definitions followed (paper: "Guiding LLMs The Right Way", DOMINO):
+ *   - Alignment (Sec. 3.3, Algorithm 2): for every scanner state q and every
+ *     vocabulary token, follow the scanner's transitions on the token's
+ *     characters and record where the token leads.  For a regular constraint
+ *     walked to full depth (Sec. 3.5, k = infinity) the landing state of a
+ *     token is all that matters: the token is a valid continuation exactly
+ *     when the walk does not die.
+ *   - Mask (Sec. 2, Algorithm 1, "compute mask"): the set of tokens that are
+ *     valid continuations of the current state.
+ *   - Decode (Algorithm 1 "decode", Appendix B Algorithm 3): argmax of the
+ *     logits restricted to the admissible token set.
+ *
+ * Readings where the paper is silent (listed again in the design notes):
+ *   - Alphabet: bytes (256 symbols); tokens are byte strings.
+ *   - DEAD = -1 is a sentinel, never a row.  Any transition target or input
+ *     state outside [0, S) reads as DEAD; walking from DEAD stays DEAD.
+ *   - A zero-length token leaves the state unchanged.
+ *   - Ties go to the lowest token index.  NaN logits rank as -infinity.
+ *     -0.0 and +0.0 compare equal (IEEE), so they tie.
+ *   - A row whose state is DEAD or that has no allowed token yields
+ *     token = -1 and new_state = DEAD.
+ *   - Allow bitmask: word t/32, bit t%32 (least significant bit first),
+ *     row stride ceil(V/32) words, bits for t >= V are zero.
+ *   - Logit values are compared in double precision after exact conversion
+ *     (fp32 -> double, bf16 -> fp32 by placing the 16 bits in the high half).
+ *
+ * Build: gcc -O2 -shared -fPIC -o libdv_oracle.so dv_oracle.c
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#define ORACLE_DEAD (-1)
+
+/* Any value outside [0, S) is the dead sentinel. */
+static int32_t oracle_canon(int64_t x, int32_t num_states)
+{
+    if (x >= 0 && x < num_states)
+        return (int32_t)x;
+    return ORACLE_DEAD;
+}
+
+/* Walk one byte string through the DFA from state s (Algorithm 2, the
+ * q.traverse(token) step, restricted to a deterministic scanner). */
+int32_t oracle_walk(const int32_t *trans, int32_t num_states, int32_t s,
+                    const uint8_t *str, int64_t len)
+{
+    int32_t st = oracle_canon(s, num_states);
+    for (int64_t i = 0; i < len; ++i) {
+        if (st == ORACLE_DEAD)
+            return ORACLE_DEAD;
+        st = oracle_canon(trans[(int64_t)st * 256 + str[i]], num_states);
+    }
+    return st;
+}
+
+/* next_state / allow rows for an explicit list of source states.
+ * next_state is [nrows][V] and allow is [nrows][ceil(V/32)]. */
+void oracle_align_rows(const int32_t *trans, int32_t num_states,
+                       const int32_t *offsets, const uint8_t *bytes,
+                       int32_t num_tokens, const int32_t *rows, int64_t nrows,
+                       int32_t *next_state, uint32_t *allow)
+{
+    int64_t words = ((int64_t)num_tokens + 31) / 32;
+    for (int64_t r = 0; r < nrows; ++r) {
+        int32_t s = rows[r];
+        int32_t *ns_row = next_state + r * (int64_t)num_tokens;
+        uint32_t *al_row = allow + r * words;
+        memset(al_row, 0, (size_t)words * sizeof(uint32_t));
+        for (int32_t t = 0; t < num_tokens; ++t) {
+            int64_t begin = offsets[t];
+            int64_t len = (int64_t)offsets[t + 1] - begin;
+            int32_t ns = oracle_walk(trans, num_states, s, bytes + begin, len);
+            ns_row[t] = ns;
+            if (ns != ORACLE_DEAD)
+                al_row[t / 32] |= (uint32_t)1u << (t % 32);
+        }
+    }
+}
+
+/* The whole table: every state 0..S-1 in order. */
+void oracle_align(const int32_t *trans, int32_t num_states,
+                  const int32_t *offsets, const uint8_t *bytes,
+                  int32_t num_tokens, int32_t *next_state, uint32_t *allow)
+{
+    int64_t words = ((int64_t)num_tokens + 31) / 32;
+    for (int32_t s = 0; s < num_states; ++s)
+        oracle_align_rows(trans, num_states, offsets, bytes, num_tokens, &s, 1,
+                          next_state + (int64_t)s * num_tokens,
+                          allow + (int64_t)s * words);
+}
+
+/* Exact conversion of one logit to double.  dtype 0 = fp32, 1 = bf16. */
+static double oracle_logit(const void *row, int64_t i, int dtype)
+{
+    float f;
+    if (dtype == 0) {
+        f = ((const float *)row)[i];
+    } else {
+        uint32_t bits = (uint32_t)((const uint16_t *)row)[i] << 16;
+        memcpy(&f, &bits, sizeof f);
+    }
+    return (double)f;
+}
+
+/* Masked greedy choice over one row: argmax of the logits over the tokens
+ * whose allow bit is set (Algorithm 1 mask/apply/decode, Algorithm 3's
+ * set-restricted argmax).  Returns -1 when no token is allowed. */
+int32_t oracle_masked_argmax(const uint32_t *allow_row, const void *logits_row,
+                             int dtype, int32_t num_tokens)
+{
+    int32_t best = -1;
+    double best_v = 0.0;
+    for (int32_t i = 0; i < num_tokens; ++i) {
+        if (((allow_row[i / 32] >> (i % 32)) & 1u) == 0)
+            continue;
+        double v = oracle_logit(logits_row, i, dtype);
+        if (isnan(v))
+            v = -INFINITY;
+        if (best == -1 || v > best_v) {
+            best = i;
+            best_v = v;
+        }
+    }
+    return best;
+}
+
+/* One masked decode step for a batch (Algorithm 1: mask, apply, decode,
+ * then update the checker's state with the chosen token). */
+void oracle_masked_step(const int32_t *next_state, const uint32_t *allow,
+                        int32_t num_states, int32_t num_tokens,
+                        const int32_t *states, const void *logits, int dtype,
+                        int32_t batch, int64_t ld_logits, int32_t *token,
+                        int32_t *new_state)
+{
+    int64_t words = ((int64_t)num_tokens + 31) / 32;
+    size_t elt = dtype == 0 ? 4 : 2;
+    for (int32_t b = 0; b < batch; ++b) {
+        int32_t s = oracle_canon(states[b], num_states);
+        int32_t tok = -1;
+        if (s != ORACLE_DEAD) {
+            const void *row = (const char *)logits + (size_t)b * (size_t)ld_logits * elt;
+            tok = oracle_masked_argmax(allow + (int64_t)s * words, row, dtype, num_tokens);
+        }
+        token[b] = tok;
+        new_state[b] = tok == -1 ? ORACLE_DEAD
+                                 : next_state[(int64_t)s * num_tokens + tok];
+    }
+}
+
+/* Count the transitions a walk takes (the lookups an implementation must
+ * make): the number of bytes consumed before the walk ends or dies. */
+int64_t oracle_walk_lookups(const int32_t *trans, int32_t num_states,
+                            const int32_t *offsets, const uint8_t *bytes,
+                            int32_t num_tokens, const int32_t *rows, int64_t nrows)
+{
+    int64_t total = 0;
+    for (int64_t r = 0; r < nrows; ++r) {
+        for (int32_t t = 0; t < num_tokens; ++t) {
+            int32_t st = oracle_canon(rows[r], num_states);
+            for (int64_t i = offsets[t]; i < offsets[t + 1]; ++i) {
+                if (st == ORACLE_DEAD)
+                    break;
+                st = oracle_canon(trans[(int64_t)st * 256 + bytes[i]], num_states);
+                ++total;
+            }
+        }
+    }
+    return total;
+}

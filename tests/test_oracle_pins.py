@@ -1,0 +1,385 @@
+"""Pins for the CPU oracle: checks against what the paper and mathematics fix,
+not against the oracle itself.
+
+* brute force through an independent formulation (the DFA's transition
+  monoid as 0/1 matrices; a token's matrix is the product of its bytes');
+* the paper's worked examples (fig:nfa, fig:overview (b)-(d)) from
+  ``tests/golden``;
+* invariants: single-byte rows, the dead row, concatenation, prefix closure,
+  emitted-token-is-allowed, allow bit iff not dead, padding bits zero;
+* reductions to library routines (numpy argmax, numpy packbits, torch's
+  bf16 -> fp32 conversion);
+* the minimal-invasiveness property (Sec. 2 definition);
+* planted ties and special values with expected indices known by construction.
+"""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _tiny_dfa(rng, S, symbols, junk=True):
+    """Random DFA over ``symbols`` with DEAD moves and (optionally) junk
+    out-of-range targets that must read as DEAD."""
+    trans = np.full((S, 256), -1, np.int32)
+    for s in range(S):
+        for b in symbols:
+            r = rng.random()
+            if r < 0.6:
+                trans[s, b] = rng.integers(0, S)
+            elif junk and r < 0.75:
+                trans[s, b] = S + int(rng.integers(0, 5))  # out of range -> DEAD
+            elif junk and r < 0.85:
+                trans[s, b] = -int(rng.integers(2, 9))     # negative -> DEAD
+    return trans
+
+
+def _matrix_table(trans, tokens):
+    """Independent formulation: M_b is the (S+1)x(S+1) 0/1 matrix of byte b
+    with index S standing for DEAD (absorbing); a token maps s to the column of
+    the single 1 in row s of the product of its bytes' matrices."""
+    S = trans.shape[0]
+    D = S
+    mats = {}
+    for b in range(256):
+        M = np.zeros((S + 1, S + 1), np.int64)
+        for s in range(S):
+            tgt = int(trans[s, b])
+            M[s, tgt if 0 <= tgt < S else D] = 1
+        M[D, D] = 1
+        mats[b] = M
+    ns = np.empty((S, len(tokens)), np.int32)
+    for t, tok in enumerate(tokens):
+        P = np.eye(S + 1, dtype=np.int64)
+        for b in tok:
+            P = P @ mats[b]
+        assert (P.sum(axis=1) == 1).all()
+        cols = P.argmax(axis=1)[:S]
+        ns[:, t] = np.where(cols == D, -1, cols)
+    return ns
+
+
+def _pack_allow(alive):
+    """Library packing: numpy packbits (little bit order) into uint32 words."""
+    S, V = alive.shape
+    Wd = (V + 31) // 32
+    padded = np.zeros((S, Wd * 32), bool)
+    padded[:, :V] = alive
+    return np.packbits(padded, axis=1, bitorder="little").view("<u4").reshape(S, Wd)
+
+
+# ------------------------------------------------------------------ P1 brute force
+
+@pytest.mark.parametrize("seed", range(6))
+def test_align_matches_transition_monoid(seed, oracle_lib):
+    rng = np.random.default_rng(1000 + seed)
+    S = int(rng.integers(1, 6))
+    alphabet = [ord("a"), ord("b"), ord("c"), ord("x"), 0xFF]
+    trans = _tiny_dfa(rng, S, alphabet[:3])
+    tokens = [bytes(p) for n in range(0, 5) for p in itertools.product(alphabet, repeat=n)]
+    assert len(tokens) == 781
+    offsets, data = W.vocab_from_tokens(tokens)
+    ns, al = oracle.align(trans, offsets, data, lib=oracle_lib)
+    expect = _matrix_table(trans, tokens)
+    np.testing.assert_array_equal(ns, expect)
+    np.testing.assert_array_equal(al, _pack_allow(expect != -1))
+
+
+def test_align_rows_equals_full_table(oracle_lib):
+    rng = np.random.default_rng(7)
+    trans = _tiny_dfa(rng, 9, [ord(c) for c in "abcd"])
+    tokens = [bytes(p) for n in range(1, 4) for p in itertools.product(b"abcdz", repeat=n)]
+    offsets, data = W.vocab_from_tokens(tokens)
+    ns, al = oracle.align(trans, offsets, data, lib=oracle_lib)
+    rows = np.array([8, 0, 3, -1, 9, 100, 3], np.int32)
+    ns_r, al_r = oracle.align_rows(trans, offsets, data, rows, lib=oracle_lib)
+    for i, s in enumerate(rows):
+        if 0 <= s < 9:
+            np.testing.assert_array_equal(ns_r[i], ns[s])
+            np.testing.assert_array_equal(al_r[i], al[s])
+        else:  # the dead row: every token dead, no bit set
+            assert (ns_r[i] == -1).all() and (al_r[i] == 0).all()
+
+
+# ----------------------------------------------------------- P2 paper worked examples
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def test_fig_nfa_int_rows(oracle_lib):
+    g = _golden("fig_nfa_int.json")
+    trans = W.dfa_from_spec(len(g["states"]), g["moves"])
+    offsets, data = W.vocab_from_tokens([t.encode() for t in g["vocab"]])
+    ns, al = oracle.align(trans, offsets, data, lib=oracle_lib)
+    np.testing.assert_array_equal(ns, np.array(g["expected_next_state"], np.int32))
+    np.testing.assert_array_equal(al[:, 0], np.array([int(x, 16) for x in g["expected_allow"]],
+                                                     np.uint32))
+
+
+def test_fig_overview_subterminal_landing(oracle_lib):
+    g = _golden("fig_overview_scanner.json")
+    trans = W.dfa_from_spec(len(g["states"]), g["moves"])
+    toks = g["vocab"]
+    offsets, data = W.vocab_from_tokens([t.encode() for t in toks])
+    ns, al = oracle.align(trans, offsets, data, lib=oracle_lib)
+    q = g["from_state"]
+    for i, t in enumerate(toks):
+        assert ns[q, i] == g["expected_landing"][t], t
+        assert ns[0, i] == g["expected_from_start"][t], t
+    # every byte token of (c) is a valid scanner continuation from the int state
+    assert al[q, 0] == (1 << len(toks)) - 1
+    # a token with no continuation (Sec. 3.3 adds 'a' as the example)
+    assert oracle.walk(trans, q, b"a", lib=oracle_lib) == -1
+
+
+# --------------------------------------------------------------------- P3 invariants
+
+@pytest.fixture(scope="module")
+def tiny_table(oracle_lib):
+    trans, _ = W.dfa(1)
+    offsets, data = W.vocab(1)
+    ns, al = oracle.align(trans, offsets, data, lib=oracle_lib)
+    return trans, offsets, data, ns, al
+
+
+def test_single_byte_rows_equal_transition_row(tiny_table):
+    trans, offsets, data, ns, _ = tiny_table
+    lens = np.diff(offsets)
+    S = trans.shape[0]
+    for t in np.nonzero(lens == 1)[0]:
+        b = data[offsets[t]]
+        col = trans[:, b]
+        np.testing.assert_array_equal(ns[:, t], np.where((col >= 0) & (col < S), col, -1))
+
+
+def test_allow_bit_iff_alive_and_padding_zero(tiny_table):
+    _, _, _, ns, al = tiny_table
+    np.testing.assert_array_equal(al, _pack_allow(ns != -1))
+    V = ns.shape[1]
+    if V % 32:
+        assert (al[:, -1] >> np.uint32(V % 32) == 0).all()
+
+
+def test_concatenation_homomorphism(tiny_table, oracle_lib):
+    trans, offsets, data, ns, _ = tiny_table
+    toks = W.tokens_of(offsets, data)
+    rng = np.random.default_rng(3)
+    S, V = ns.shape
+    for _ in range(3000):
+        s = int(rng.integers(0, S))
+        t1, t2 = (int(x) for x in rng.integers(0, V, 2))
+        mid = ns[s, t1]
+        via_table = -1 if mid == -1 else ns[mid, t2]
+        assert oracle.walk(trans, s, toks[t1] + toks[t2], lib=oracle_lib) == via_table
+
+
+def test_prefix_closure(tiny_table, oracle_lib):
+    trans, offsets, data, ns, _ = tiny_table
+    toks = W.tokens_of(offsets, data)
+    S = ns.shape[0]
+    for t, tok in enumerate(toks):
+        for s in range(S):
+            if ns[s, t] != -1:
+                for k in range(len(tok)):
+                    assert oracle.walk(trans, s, tok[:k], lib=oracle_lib) != -1
+
+
+def test_dead_row_is_empty(tiny_table, oracle_lib):
+    trans, offsets, data, ns, al = tiny_table
+    V = ns.shape[1]
+    x = np.random.default_rng(0).standard_normal((3, V)).astype(np.float32)
+    tok, nst = oracle.masked_step(ns, al, np.array([-1, 16, 1 << 30], np.int32), x, lib=oracle_lib)
+    assert (tok == -1).all() and (nst == -1).all()
+
+
+def test_emitted_token_is_allowed_and_state_follows_walk(tiny_table, oracle_lib):
+    trans, offsets, data, ns, al = tiny_table
+    toks = W.tokens_of(offsets, data)
+    S, V = ns.shape
+    rng = np.random.default_rng(11)
+    states = rng.integers(0, S, 64).astype(np.int32)
+    x = (rng.standard_normal((64, V)) * 2).astype(np.float32)
+    tok, nst = oracle.masked_step(ns, al, states, x, lib=oracle_lib)
+    for b in range(64):
+        if tok[b] == -1:
+            assert (al[states[b]] == 0).all() and nst[b] == -1
+            continue
+        assert (al[states[b], tok[b] // 32] >> np.uint32(tok[b] % 32)) & 1
+        assert nst[b] == oracle.walk(trans, int(states[b]), toks[tok[b]], lib=oracle_lib) != -1
+
+
+def test_walk_lookup_count_small_case(oracle_lib):
+    g = _golden("fig_nfa_int.json")
+    trans = W.dfa_from_spec(len(g["states"]), g["moves"])
+    offsets, data = W.vocab_from_tokens([t.encode() for t in g["vocab"]])
+    # from state 0: 0,1,2 one move each; 12 two; ) ( + one (dies);
+    # +1 one (dies at '+'); '1 (' two ('1' then dies at ' ') -> 11
+    assert oracle.walk_lookups(trans, offsets, data, np.array([0], np.int32), lib=oracle_lib) == 11
+
+
+# ------------------------------------------------------- P4 reductions to library calls
+
+def _reference_choice(x_f32, allowed):
+    return int(np.argmax(np.where(allowed, x_f32, -np.inf)))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_masked_step_equals_numpy_argmax(dtype, tiny_table, oracle_lib):
+    _, _, _, ns, al = tiny_table
+    S, V = ns.shape
+    rng = np.random.default_rng(5)
+    B, ld = 40, V + 13
+    states = rng.integers(0, S, B).astype(np.int32)
+    xt = torch.from_numpy(rng.standard_normal((B, ld)).astype(np.float32) * 3)
+    if dtype == "bf16":
+        xt = xt.to(torch.bfloat16)
+        arr = xt.view(torch.int16).numpy().view(np.uint16)
+        ref = xt.float().numpy()          # torch's own bf16 -> fp32 conversion
+    else:
+        arr = xt.numpy()
+        ref = arr
+    tok, _ = oracle.masked_step(ns, al, states, arr, lib=oracle_lib)
+    alive = ns != -1
+    checked = 0
+    for b in range(B):
+        allowed = alive[states[b]]
+        if allowed.any():
+            assert tok[b] == _reference_choice(ref[b, :V], allowed)
+            checked += 1
+        else:
+            assert tok[b] == -1
+    assert checked > B // 2
+
+
+def test_single_accepting_state_is_unconstrained_argmax(oracle_lib):
+    trans = np.zeros((1, 256), np.int32)  # every byte loops on state 0
+    offsets, data = W.vocab(1)
+    ns, al = oracle.align(trans, offsets, data, lib=oracle_lib)
+    assert (ns == 0).all()
+    x = np.random.default_rng(9).standard_normal((8, ns.shape[1])).astype(np.float32)
+    tok, nst = oracle.masked_step(ns, al, np.zeros(8, np.int32), x, lib=oracle_lib)
+    np.testing.assert_array_equal(tok, np.argmax(x, axis=1))
+    assert (nst == 0).all()
+
+
+# ------------------------------------------------ P5 minimal invasiveness (Sec. 2)
+
+def test_minimally_invasive_when_unconstrained_choice_is_valid(tiny_table, oracle_lib):
+    _, _, _, ns, al = tiny_table
+    S, V = ns.shape
+    rng = np.random.default_rng(21)
+    hits = 0
+    for trial in range(200):
+        s = int(rng.integers(0, S))
+        x = rng.standard_normal(V).astype(np.float32)
+        allowed_idx = np.nonzero(ns[s] != -1)[0]
+        if trial % 2 and allowed_idx.size:
+            x[allowed_idx[rng.integers(0, allowed_idx.size)]] = 50.0  # model prefers a valid token
+        free = int(np.argmax(x))
+        tok, _ = oracle.masked_step(ns, al, np.array([s], np.int32), x[None], lib=oracle_lib)
+        if ns[s, free] != -1:
+            assert tok[0] == free
+            hits += 1
+        else:
+            assert tok[0] != free
+    assert hits >= 90
+
+
+# ------------------------------------------------------------- P6 planted specials
+
+def _one_row(values, allowed_idx, dtype="f32"):
+    V = len(values)
+    ns = np.full((1, V), -1, np.int32)
+    ns[0, list(allowed_idx)] = 0
+    al = _pack_allow(ns != -1)
+    if dtype == "f32":
+        x = np.array(values, np.float32)[None]
+    else:
+        x = np.array(values, np.uint16)[None]
+    return ns, al, x
+
+
+@pytest.mark.parametrize("values,allowed,expect", [
+    ([100, 9, 9, 5, 1, 9, 0, 9, 0, 0.5], [1, 2, 5, 7, 9], 1),       # equal maxima: lowest index
+    ([0, 1, -0.0, 7, 7, 0.0, 9], [2, 5], 2),                          # -0 ties +0
+    ([0, 1, 0.0, 7, 7, -0.0, 9], [2, 5], 2),
+    ([5, float("nan"), 3, 3, -np.inf], [1, 4], 1),                    # NaN ranks as -inf: tie
+    ([5, -np.inf, 3, 3, float("nan")], [1, 4], 1),
+    ([float("nan")] * 6, [3, 5], 3),                                  # all NaN: lowest allowed
+    ([float("nan"), 2.0, 1.0], [0, 1, 2], 1),                         # NaN first, a number wins
+    ([float("nan"), -3e38, 1.0], [0, 1], 1),
+    ([np.inf, 1e30, np.inf, 2, 3], [1, 3], 1),                        # disallowed +inf ignored
+    ([1, np.inf, 1e38, np.inf], [1, 2, 3], 1),
+    ([-np.inf, -np.inf, -3e38], [0, 1], 0),
+    ([-1e-45, 0.0, 1e-45, -0.0], [0, 1, 3], 1),                       # subnormals
+    ([-1e-45, 0.0, 1e-45, -0.0], [0, 2, 3], 2),
+    ([1, 2, 3], [], -1),                                              # empty row
+])
+def test_planted_ties_and_specials_f32(values, allowed, expect, oracle_lib):
+    ns, al, x = _one_row(values, allowed)
+    tok, nst = oracle.masked_step(ns, al, np.array([0], np.int32), x, lib=oracle_lib)
+    assert tok[0] == expect
+    assert nst[0] == (0 if expect >= 0 else -1)
+
+
+@pytest.mark.parametrize("bits,allowed,expect", [
+    ([0x3F80, 0x3F80, 0x3F80], [1, 2], 1),                 # 1.0 ties
+    ([0x8000, 0x0000, 0x0001], [0, 1], 0),                 # -0 vs +0 tie
+    ([0x8000, 0x0000, 0x0001], [0, 1, 2], 2),              # smallest positive subnormal wins
+    ([0x7FC1, 0xFF80, 0xFFC1], [0, 1, 2], 0),              # +NaN, -inf, -NaN all rank -inf
+    ([0x7FC1, 0xC000, 0x7F80], [0, 1], 1),                 # NaN first, -2 wins
+    ([0xFFC1, 0xFF7F], [0, 1], 1),                         # -NaN first, lowest finite wins
+    ([0x7F80, 0x7F7F, 0xFF80], [1, 2], 1),                 # largest finite vs -inf
+    ([0xBF80, 0xC000, 0xBF80], [0, 1, 2], 0),              # -1 beats -2, tie to lowest
+])
+def test_planted_ties_and_specials_bf16(bits, allowed, expect, oracle_lib):
+    ns, al, x = _one_row(bits, allowed, "bf16")
+    tok, _ = oracle.masked_step(ns, al, np.array([0], np.int32), x, lib=oracle_lib)
+    assert tok[0] == expect
+
+
+def test_leading_dimension_and_row_independence(tiny_table, oracle_lib):
+    _, _, _, ns, al = tiny_table
+    S, V = ns.shape
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((6, V + 7)).astype(np.float32)
+    states = rng.integers(0, S, 6).astype(np.int32)
+    tok, nst = oracle.masked_step(ns, al, states, x, lib=oracle_lib)
+    for b in range(6):
+        t1, n1 = oracle.masked_step(ns, al, states[b:b + 1], np.ascontiguousarray(x[b:b + 1, :V]),
+                                    lib=oracle_lib)
+        assert (t1[0], n1[0]) == (tok[b], nst[b])
+
+
+def test_oracle_is_deterministic(tiny_table, oracle_lib):
+    trans, offsets, data, ns, al = tiny_table
+    ns2, al2 = oracle.align(trans, offsets, data, lib=oracle_lib)
+    np.testing.assert_array_equal(ns, ns2)
+    np.testing.assert_array_equal(al, al2)
+
+
+def test_masked_chain_matches_batch_steps(tiny_table, oracle_lib):
+    trans, offsets, data, ns, al = tiny_table
+    S, V = ns.shape
+    rng = np.random.default_rng(4)
+    steps = 12
+    x = rng.standard_normal((steps, 3, V)).astype(np.float32)
+    states = np.array([0, 5, 11], np.int32)
+    cache = oracle.RowCache(trans, offsets, data, lib=oracle_lib)
+    chains = [oracle.masked_chain(cache, states[b], x[:, b]) for b in range(3)]
+    cur = states
+    for k in range(steps):
+        tok, nxt = oracle.masked_step(ns, al, cur, x[k], lib=oracle_lib)
+        for b in range(3):
+            assert chains[b][0][k] == tok[b] and chains[b][1][k + 1] == nxt[b]
+        cur = nxt
