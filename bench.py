@@ -1,0 +1,256 @@
+#!/usr/bin/env python3
+"""Throughput of the constrained-decoding hot path on one MI355X.
+
+One benchmark step is one whole job of the hot path on one batch of
+synthetic input: build the alignment table of the DFA and the vocabulary
+(dv_align), then run the workload's greedy decoding chain (one dv_masked_step
+per decoding step, each step's states feeding the next).  Inputs (DFA,
+vocabulary, every step's logits) are resident in HBM before timing starts.
+
+Reported (one JSON line):
+  value        masked decode steps / s over the timed decode launches
+  align        (state, token) alignments / s of dv_align
+  ms_per_step  wall time of one whole job (align + all decode steps)
+  roofline     the dominant kernel (the masked step) against HBM bandwidth:
+               algorithmic bytes per launch / mean launch time (HIP events
+               around every launch on the launch stream)
+  roofline_align  dv_align against the HBM write roofline (4.125 B / pair)
+  cpu_baseline the CPU oracle on a bounded sample of the same workload
+
+Usage: python bench.py [--steps K] [--warmup W] [--workload 1..5] [--no-cpu]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "(state,token) alignments/sec for dv_align; masked decode steps/sec at V=128k"
+HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2403_06988_amd", "csrc", f)
+                  for f in ("dv_step.hip", "dv_align.hip", "dv_internal.h")]
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10, help="timed jobs")
+    ap.add_argument("--warmup", type=int, default=2, help="untimed jobs")
+    ap.add_argument("--workload", type=int, default=4)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def step_bytes(w, live_rows, B):
+    """Algorithmic HBM bytes of one masked step: each live row streams its
+    logits (V elements) and its allow row (4 * ceil(V/32) B) and gathers one
+    next_state entry; every row reads its state and writes token and new state."""
+    per_live = w.V * w.elt + 4 * w.words + 4
+    return live_rows * per_live + 12 * B
+
+
+def traffic_record(name):
+    """HBM bytes per launch from a committed rocprofv3 --pmc summary, if it was
+    taken on the current kernel source; else None."""
+    path = os.path.join(PROFILES, f"{name}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, wid, trans, offsets, data, init, x_dev, budget_s):
+    """The oracle as it stands, single-threaded, on a bounded sample: greedy
+    masked steps for a subset of rows (table rows built beforehand, untimed,
+    as the decode throughput excludes the table build), and alignment rows."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from tests.gpu_common import to_oracle
+
+    lib = oracle.load()
+    # decode: the first n_rows rows, stepped as far as the budget allows
+    n_rows = min(w.B, 8)
+    n_steps = min(w.steps, 64)
+    xs = to_oracle(x_dev[:n_steps, :n_rows])
+    cache = oracle.RowCache(trans, offsets, data, lib=lib)
+    cur = [int(s) for s in init[:n_rows]]
+    row_steps = 0
+    t_dec = 0.0
+    for k in range(n_steps):
+        for b in range(n_rows):
+            s = cur[b]
+            if s < 0:
+                continue
+            ns_row, al_row = cache.get(s)         # untimed: table build
+            t0 = time.perf_counter()
+            tok = oracle.masked_argmax(al_row, xs[k, b], lib=lib)
+            t_dec += time.perf_counter() - t0
+            cur[b] = -1 if tok < 0 else int(ns_row[tok])
+            row_steps += 1
+        if t_dec > budget_s / 2:
+            break
+    dec_steps_per_s = (row_steps / w.B) / t_dec if t_dec > 0 else None
+    # alignment: whole rows of the table
+    rng = np.random.default_rng(0)
+    pairs = 0
+    t_al = 0.0
+    while t_al < budget_s / 2:
+        rows = rng.integers(0, w.S, 4).astype(np.int32)
+        t0 = time.perf_counter()
+        oracle.align_rows(trans, offsets, data, rows, lib=lib)
+        t_al += time.perf_counter() - t0
+        pairs += len(rows) * w.V
+    return {
+        "value": dec_steps_per_s, "unit": "steps/s", "cores": 1, "kind": "oracle",
+        "sample": (f"{row_steps} row-steps ({n_rows} rows x up to {n_steps} steps of B={w.B}) of "
+                   f"masked argmax, scaled to full B; table rows built untimed"),
+        "align_value": pairs / t_al, "align_unit": "alignments/s",
+        "align_sample": f"{pairs} (state, token) pairs in whole table rows",
+        "seconds": round(t_dec + t_al, 2),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the multi-GPU "
+              "sharding of this path is a design, not a measurement.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2403_06988_amd as dv
+    import workloads as W
+
+    wid = args.workload
+    w = W.WORKLOADS[wid]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    log(f"inputs: {w.describe()}")
+    trans, _ = W.dfa(wid)
+    offsets, data = W.vocab(wid)
+    init = W.init_states(wid)
+    trans_d = torch.from_numpy(trans).to(dev)
+    offsets_d = torch.from_numpy(offsets).to(dev)
+    data_d = torch.from_numpy(data).to(dev)
+    init_d = torch.from_numpy(init).to(dev)
+    x = W.logits_all(wid, device=dev)
+    ns = torch.empty((w.S, w.V), dtype=torch.int32, device=dev)
+    al = torch.empty((w.S, w.words), dtype=torch.int32, device=dev)
+    ws_align = torch.empty(dv.align_workspace_bytes(w.S, w.V), dtype=torch.uint8, device=dev)
+    ws_step = dv.step_workspace(w.B, w.V, dev)
+    states_all = torch.empty((w.steps + 1, w.B), dtype=torch.int32, device=dev)
+    tokens_all = torch.empty((w.steps, w.B), dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    log("inputs resident in HBM")
+
+    def job(events=None):
+        if events is not None:
+            events["align"][0].record(stream)
+        dv.align(trans_d, offsets_d, data_d, next_state=ns, allow=al, workspace=ws_align,
+                 stream=stream)
+        if events is not None:
+            events["align"][1].record(stream)
+        states_all[0].copy_(init_d)
+        for k in range(w.steps):
+            if events is not None:
+                events["step"][k][0].record(stream)
+            dv.masked_step(ns, al, states_all[k], x[k], token=tokens_all[k],
+                           new_state=states_all[k + 1], workspace=ws_step, stream=stream)
+            if events is not None:
+                events["step"][k][1].record(stream)
+
+    for _ in range(args.warmup):
+        job()
+    torch.cuda.synchronize()
+
+    def mk():
+        return torch.cuda.Event(enable_timing=True)
+
+    ev = [{"align": (mk(), mk()), "step": [(mk(), mk()) for _ in range(w.steps)]}
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for j in range(args.steps):
+        job(ev[j])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    align_ms = [e["align"][0].elapsed_time(e["align"][1]) for e in ev]
+    step_ms = [s.elapsed_time(t) for e in ev for (s, t) in e["step"]]
+    decode_ms_per_job = [sum(s.elapsed_time(t) for (s, t) in e["step"]) for e in ev]
+    live_per_step = (states_all[:-1] >= 0).sum(dim=1).cpu().numpy()
+    dead_final = int((states_all[-1] < 0).sum())
+
+    pairs = w.S * w.V
+    align_s = float(np.mean(align_ms)) / 1e3
+    dec_s = float(np.mean(decode_ms_per_job)) / 1e3
+    bytes_per_launch = float(np.mean([step_bytes(w, int(n), w.B) for n in live_per_step]))
+    mean_launch_s = float(np.mean(step_ms)) / 1e3
+    achieved = bytes_per_launch / mean_launch_s / 1e9
+    align_bytes = pairs * 4.125
+    align_achieved = align_bytes / align_s / 1e9
+
+    out = {
+        "metric": METRIC,
+        "value": w.steps / dec_s,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded DFA, vocabulary and logits; no model weights)",
+        "config": {"workload": w.describe(), "S": w.S, "V": w.V, "B": w.B,
+                   "decode_steps_per_job": w.steps, "logits_dtype": w.dtype},
+        "align": {"value": pairs / align_s, "unit": "alignments/s", "ms": align_s * 1e3},
+        "decode": {"us_per_step_mean": mean_launch_s * 1e6,
+                   "us_per_step_min": float(np.min(step_ms)) * 1e3,
+                   "rows_steps_per_s": w.B * w.steps / dec_s,
+                   "live_rows_first_last": [int(live_per_step[0]), int(live_per_step[-1])],
+                   "dead_rows_at_end": dead_final},
+        "roofline": {"kernel": "masked_step_kernel", "bound": "hbm", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "bytes_per_launch": bytes_per_launch,
+                     "traffic": traffic_record("masked_step_traffic")},
+        "roofline_align": {"kernel": "dv_align (4 kernels)", "bound": "hbm",
+                           "achieved": align_achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": align_achieved / HBM_PEAK_GBS, "bytes_per_launch": align_bytes,
+                           "traffic": traffic_record("align_walk_traffic")},
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    if not args.no_cpu:
+        log("cpu baseline (oracle, 1 thread)")
+        out["cpu_baseline"] = cpu_baseline(w, wid, trans, offsets, data, init, x, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,172 @@
+/*
+ * dv.h -- vocabulary alignment and masked greedy decoding on one MI355X.
+ *
+ * C ABI of libdv.so.  Two operations, from "Guiding LLMs The Right Way: Fast,
+ * Non-Invasive Constrained Generation" (DOMINO, ICML 2024):
+ *
+ *   dv_align        the offline vocabulary alignment of Sec. 3.3 /
+ *                   Algorithm 2 for a regular (DFA) constraint walked to full
+ *                   depth (Sec. 3.5, lookahead k = infinity): every scanner
+ *                   state is walked through every token's bytes.
+ *   dv_masked_step  one step of Algorithm 1: look up the mask of each
+ *                   sequence's current state, apply it to the logits, decode
+ *                   greedily (Algorithm 3's argmax over the admissible set)
+ *                   and advance the state with the chosen token.
+ *
+ * Conventions shared by every call:
+ *   - Every array argument is a DEVICE pointer (hipMalloc'd or a torch CUDA
+ *     tensor's data_ptr) owned by the caller.  The library allocates nothing,
+ *     keeps no pointer after it returns, and has no global state except a
+ *     per-thread error message.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream)
+ *     and runs asynchronously to the host.  Outputs are valid once the stream
+ *     has reached the call; inputs must stay unchanged until then.  Two calls
+ *     that share a workspace must be ordered on one stream.
+ *   - Arguments are checked on the host before any HIP call.  On a failed
+ *     check nothing is enqueued and the call returns an error status; a
+ *     message is available from dv_last_error() on the calling thread.
+ *   - The alphabet is bytes (256 symbols).  DV_DEAD (-1) is the dead state:
+ *     a sentinel, never a table row.  A transition target or an input state
+ *     outside [0, num_states) reads as DV_DEAD; nothing leaves DV_DEAD.
+ */
+#ifndef DV_H
+#define DV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define DV_API __attribute__((visibility("default")))
+#else
+#define DV_API
+#endif
+
+#define DV_DEAD (-1)
+
+/* Limits checked by every call (inclusive). */
+#define DV_MAX_STATES 65535        /* num_states  in [1, DV_MAX_STATES]  */
+#define DV_MAX_TOKENS 16777216     /* num_tokens  in [1, DV_MAX_TOKENS]  */
+#define DV_MAX_BATCH  1048576      /* batch       in [0, DV_MAX_BATCH]   */
+
+typedef enum dv_status {
+    DV_OK = 0,
+    DV_ERR_INVALID_ARG = 1,  /* a required pointer is NULL                         */
+    DV_ERR_SHAPE = 2,        /* a size is outside its limit or ld_logits < V       */
+    DV_ERR_DTYPE = 3,        /* unknown logits dtype                               */
+    DV_ERR_ALIAS = 4,        /* an output overlaps an input or another output      */
+    DV_ERR_WORKSPACE = 5,    /* workspace missing, too small or misaligned         */
+    DV_ERR_HIP = 6           /* a HIP launch or runtime call failed                */
+} dv_status;
+
+typedef enum dv_dtype {
+    DV_F32 = 0,              /* IEEE binary32 logits                               */
+    DV_BF16 = 1              /* bfloat16 logits (high half of a binary32)          */
+} dv_dtype;
+
+/*
+ * dv_align_workspace_bytes -- device workspace dv_align needs for a DFA with
+ * `num_states` states (the compacted transition table and the byte-class
+ * map).  Returns 0 when a size is outside its limit.
+ */
+DV_API size_t dv_align_workspace_bytes(int32_t num_states, int32_t num_tokens);
+
+/*
+ * dv_align -- the vocabulary alignment table (Sec. 3.3, Algorithm 2, at
+ * full depth as in Sec. 3.5).
+ *
+ * For every state s in [0, S) and every token t in [0, V):
+ *     next_state[s*V + t] = the state reached by reading the bytes of token t
+ *                           one by one from s, or DV_DEAD if a transition on
+ *                           the way is dead (the walk stops there);
+ *     bit (t % 32) of allow[s*W + t/32] = 1 exactly when next_state != DV_DEAD,
+ * with W = ceil(V/32).  Bits for t >= V are written as 0.  A zero-length
+ * token leaves the state unchanged (next_state = s, allowed).
+ *
+ * Inputs (device, read only):
+ *   trans      [S][256] int32, row-major: trans[s*256 + b] is the move of
+ *              state s on byte b.  Values outside [0, S) read as DV_DEAD.
+ *   offsets    [V+1] int32, offsets[0] = 0, non-decreasing (precondition,
+ *              not checked on the device): token t is bytes[offsets[t] ..
+ *              offsets[t+1]).
+ *   bytes      [offsets[V]] uint8, the concatenated token strings.  May be
+ *              NULL only when every token is empty.
+ * Outputs (device, written in full):
+ *   next_state [S][V] int32; allow [S][W] uint32.
+ * Workspace: at least dv_align_workspace_bytes(S, V) bytes of device memory,
+ *   256-byte aligned; contents on entry are ignored, on exit undefined.
+ * Errors: DV_ERR_INVALID_ARG (NULL pointer), DV_ERR_SHAPE (S or V out of
+ *   range), DV_ERR_ALIAS (next_state/allow overlap each other or an input,
+ *   checked on the address ranges implied by S and V), DV_ERR_WORKSPACE,
+ *   DV_ERR_HIP.
+ */
+DV_API dv_status dv_align(const int32_t *trans, int32_t num_states,
+                   const int32_t *offsets, const uint8_t *bytes, int32_t num_tokens,
+                   int32_t *next_state, uint32_t *allow,
+                   void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * dv_masked_step_workspace_bytes -- device workspace dv_masked_step needs for
+ * `batch` rows (per-row partial results of a split-row reduction).
+ * Returns 0 when a size is outside its limit.
+ */
+DV_API size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens);
+
+/*
+ * dv_masked_step -- one greedy constrained decoding step (Algorithm 1:
+ * mask, apply, decode, update; the argmax of Algorithm 3 restricted to the
+ * admissible tokens).
+ *
+ * For every row b in [0, B):
+ *     s = states[b];  if s is outside [0, S) the row is dead;
+ *     token[b] = the index i in [0, V) with allow bit (s, i) set whose logit
+ *                logits[b*ld_logits + i] is largest; ties go to the lowest
+ *                index; NaN ranks as -infinity; -0.0 equals +0.0;
+ *                -1 when the row is dead or has no allowed token;
+ *     new_state[b] = next_state[s*V + token[b]], or DV_DEAD when token = -1.
+ *
+ * Inputs (device, read only):
+ *   next_state [S][V] int32 and allow [S][ceil(V/32)] uint32 as written by
+ *              dv_align (any table with that layout is accepted; new_state
+ *              is read from it as is).
+ *   states     [B] int32.
+ *   logits     [B][ld_logits] of `dtype` (dv_dtype), row stride ld_logits
+ *              elements (ld_logits >= V).  Rows whose address is 16-byte
+ *              aligned take a vector path; others a scalar path with the
+ *              same results.
+ * Outputs (device): token [B] int32, new_state [B] int32.  They must not
+ *   overlap each other or any input (callers ping-pong two state buffers).
+ * Workspace: at least dv_masked_step_workspace_bytes(B, V) bytes of device
+ *   memory, 256-byte aligned, ZERO-FILLED before its first use; every call
+ *   leaves it zero-filled again when it completes, so a buffer zeroed once
+ *   can be reused for any later call on the same stream.
+ * B = 0 is valid and enqueues nothing; states, logits, token and new_state
+ *   may then be NULL (the pointers of empty tensors).
+ * Errors: DV_ERR_INVALID_ARG, DV_ERR_SHAPE (S, V, B out of range or
+ *   ld_logits < V), DV_ERR_DTYPE, DV_ERR_ALIAS, DV_ERR_WORKSPACE, DV_ERR_HIP.
+ */
+DV_API dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow,
+                         int32_t num_states, int32_t num_tokens,
+                         const int32_t *states, const void *logits, int32_t dtype,
+                         int32_t batch, int64_t ld_logits,
+                         int32_t *token, int32_t *new_state,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/* Static, human-readable name of a status code ("DV_OK", ...). */
+DV_API const char *dv_status_string(int32_t status);
+
+/* Detail of the last error returned on the calling thread ("" if none).
+ * The string stays valid until the next dv_* call on that thread. */
+DV_API const char *dv_last_error(void);
+
+/* Library ABI version: major * 10000 + minor * 100 + patch. */
+DV_API int32_t dv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DV_H */

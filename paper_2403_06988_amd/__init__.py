@@ -1,0 +1,177 @@
+"""Vocabulary alignment and masked greedy decoding on MI355X (gfx950).
+
+Thin Python binding over ``libdv.so`` (C ABI in ``include/dv.h``).  It only
+marshals torch tensors into device pointers and a HIP stream; every step of
+the computation runs in the library's HIP kernels.  There is no CPU fallback:
+importing this package fails if the library is not built.
+
+    next_state, allow = align(trans, offsets, tok_bytes)
+    token, new_state = masked_step(next_state, allow, states, logits)
+
+``align`` is the offline vocabulary alignment of the DOMINO paper (Sec. 3.3,
+Algorithm 2, walked to full depth as in Sec. 3.5) for a byte-level DFA;
+``masked_step`` is one step of its Algorithm 1 with greedy decoding.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = ["align", "masked_step", "align_workspace_bytes", "masked_step_workspace_bytes",
+           "step_workspace", "DvError", "DEAD", "library_path", "lib"]
+
+DEAD = -1
+DV_OK = 0
+DV_F32, DV_BF16 = 0, 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.environ.get("DV_LIBRARY", os.path.join(_HERE, "libdv.so"))
+
+
+class DvError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(
+            f"libdv.so not found at {_LIB_PATH}: build it first "
+            "(python -c 'import __graft_entry__ as g; g.build()' or "
+            "python paper_2403_06988_amd/_build.py); there is no CPU fallback")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    lib.dv_version.restype = i32
+    lib.dv_version.argtypes = []
+    lib.dv_status_string.restype = ctypes.c_char_p
+    lib.dv_status_string.argtypes = [i32]
+    lib.dv_last_error.restype = ctypes.c_char_p
+    lib.dv_last_error.argtypes = []
+    lib.dv_align_workspace_bytes.restype = sz
+    lib.dv_align_workspace_bytes.argtypes = [i32, i32]
+    lib.dv_align.restype = ctypes.c_int
+    lib.dv_align.argtypes = [vp, i32, vp, vp, i32, vp, vp, vp, sz, vp]
+    lib.dv_masked_step_workspace_bytes.restype = sz
+    lib.dv_masked_step_workspace_bytes.argtypes = [i32, i32]
+    lib.dv_masked_step.restype = ctypes.c_int
+    lib.dv_masked_step.argtypes = [vp, vp, i32, i32, vp, vp, i32, i32, i64, vp, vp, vp, sz, vp]
+    return lib
+
+
+lib = _load()
+library_path = _LIB_PATH
+
+
+def _check(status: int, what: str):
+    if status != DV_OK:
+        name = lib.dv_status_string(status).decode()
+        detail = lib.dv_last_error().decode()
+        raise DvError(status, f"{what}: {name}: {detail}")
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream, device) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _want(t, name, dtype, device=None):
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def align_workspace_bytes(num_states: int, num_tokens: int) -> int:
+    return int(lib.dv_align_workspace_bytes(num_states, num_tokens))
+
+
+def masked_step_workspace_bytes(batch: int, num_tokens: int) -> int:
+    return int(lib.dv_masked_step_workspace_bytes(batch, num_tokens))
+
+
+def align(trans, offsets, tok_bytes, next_state=None, allow=None, workspace=None, stream=None):
+    """Alignment table of a byte DFA and a vocabulary (device tensors).
+
+    trans [S][256] int32, offsets [V+1] int32, tok_bytes [offsets[V]] uint8.
+    Returns (next_state [S][V] int32, allow [S][ceil(V/32)] int32 holding the
+    uint32 bit pattern)."""
+    dev = trans.device
+    _want(trans, "trans", torch.int32, dev)
+    _want(offsets, "offsets", torch.int32, dev)
+    _want(tok_bytes, "tok_bytes", torch.uint8, dev)
+    if trans.dim() != 2 or trans.shape[1] != 256:
+        raise ValueError("trans must be [S][256]")
+    S, V = trans.shape[0], offsets.shape[0] - 1
+    Wd = (V + 31) // 32
+    if next_state is None:
+        next_state = torch.empty((S, V), dtype=torch.int32, device=dev)
+    if allow is None:
+        allow = torch.empty((S, Wd), dtype=torch.int32, device=dev)
+    _want(next_state, "next_state", torch.int32, dev)
+    _want(allow, "allow", torch.int32, dev)
+    if next_state.numel() != S * V or allow.numel() != S * Wd:
+        raise ValueError("next_state / allow have the wrong size")
+    need = align_workspace_bytes(S, max(V, 1))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _want(workspace, "workspace", torch.uint8, dev)
+    st = lib.dv_align(_ptr(trans), S, _ptr(offsets), _ptr(tok_bytes) if tok_bytes.numel() else None,
+                      V, _ptr(next_state), _ptr(allow), _ptr(workspace), workspace.numel(),
+                      _stream(stream, dev))
+    _check(st, "dv_align")
+    return next_state, allow
+
+
+def step_workspace(batch: int, num_tokens: int, device) -> torch.Tensor:
+    """A zero-filled workspace for ``masked_step`` (reusable across calls on
+    one stream: every call leaves it zero-filled)."""
+    n = masked_step_workspace_bytes(batch, num_tokens)
+    return torch.zeros(max(n, 1), dtype=torch.uint8, device=device)
+
+
+def masked_step(next_state, allow, states, logits, token=None, new_state=None, workspace=None,
+                stream=None):
+    """One greedy masked decoding step.  logits [B][ld] (fp32 or bf16, unit
+    stride along the vocabulary).  Returns (token [B] int32, new_state [B] int32)."""
+    dev = states.device
+    _want(next_state, "next_state", torch.int32, dev)
+    _want(allow, "allow", torch.int32, dev)
+    _want(states, "states", torch.int32, dev)
+    if logits.dtype == torch.float32:
+        dt = DV_F32
+    elif logits.dtype == torch.bfloat16:
+        dt = DV_BF16
+    else:
+        raise TypeError(f"logits must be float32 or bfloat16, got {logits.dtype}")
+    if not logits.is_cuda or logits.device != dev:
+        raise ValueError("logits must be on the same device as states")
+    S, V = next_state.shape
+    B = states.shape[0]
+    if logits.dim() != 2 or logits.shape[0] != B or logits.shape[1] != V:
+        raise ValueError(f"logits must be [{B}][{V}] (a wider row stride is allowed)")
+    if B and logits.stride(1) != 1:
+        raise ValueError("logits must have unit stride along the vocabulary")
+    ld = logits.stride(0) if B > 1 else max(V, logits.stride(0))
+    if token is None:
+        token = torch.empty(B, dtype=torch.int32, device=dev)
+    if new_state is None:
+        new_state = torch.empty(B, dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = step_workspace(B, V, dev)
+    st = lib.dv_masked_step(_ptr(next_state), _ptr(allow), S, V, _ptr(states), _ptr(logits), dt, B,
+                            ld, _ptr(token), _ptr(new_state), _ptr(workspace), workspace.numel(),
+                            _stream(stream, dev))
+    _check(st, "dv_masked_step")
+    return token, new_state

@@ -1,0 +1,156 @@
+// C ABI of libdv.so (declared in include/dv.h): argument checks, then the
+// launches.  Every check runs on the host before any HIP call, so a rejected
+// call enqueues nothing and touches no device state.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "../../include/dv.h"
+#include "dv_internal.h"
+
+namespace {
+
+thread_local char g_error[512] = "";
+
+dv_status fail(dv_status st, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_error, sizeof g_error, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+// Byte range [p, p + n) of a device pointer, for overlap checks.
+struct Range {
+    uintptr_t lo, hi;
+};
+Range range_of(const void *p, size_t n) { return {reinterpret_cast<uintptr_t>(p), reinterpret_cast<uintptr_t>(p) + n}; }
+bool overlap(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi && a.lo != a.hi && b.lo != b.hi; }
+
+dv_status hip_status(hipError_t e, const char *what)
+{
+    if (e == hipSuccess)
+        return DV_OK;
+    return fail(DV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t dv_version(void) { return 100; }
+
+const char *dv_status_string(int32_t status)
+{
+    switch (status) {
+    case DV_OK: return "DV_OK";
+    case DV_ERR_INVALID_ARG: return "DV_ERR_INVALID_ARG";
+    case DV_ERR_SHAPE: return "DV_ERR_SHAPE";
+    case DV_ERR_DTYPE: return "DV_ERR_DTYPE";
+    case DV_ERR_ALIAS: return "DV_ERR_ALIAS";
+    case DV_ERR_WORKSPACE: return "DV_ERR_WORKSPACE";
+    case DV_ERR_HIP: return "DV_ERR_HIP";
+    default: return "DV_ERR_UNKNOWN";
+    }
+}
+
+const char *dv_last_error(void) { return g_error; }
+
+size_t dv_align_workspace_bytes(int32_t num_states, int32_t num_tokens)
+{
+    if (num_states < 1 || num_states > DV_MAX_STATES || num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
+        return 0;
+    return dv::align_workspace_bytes(num_states);
+}
+
+dv_status dv_align(const int32_t *trans, int32_t num_states, const int32_t *offsets,
+                   const uint8_t *bytes, int32_t num_tokens, int32_t *next_state, uint32_t *allow,
+                   void *workspace, size_t workspace_bytes, void *stream)
+{
+    g_error[0] = '\0';
+    if (!trans || !offsets || !next_state || !allow)
+        return fail(DV_ERR_INVALID_ARG, "dv_align: trans, offsets, next_state and allow must be non-NULL");
+    if (num_states < 1 || num_states > DV_MAX_STATES)
+        return fail(DV_ERR_SHAPE, "dv_align: num_states=%d outside [1, %d]", num_states, DV_MAX_STATES);
+    if (num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
+        return fail(DV_ERR_SHAPE, "dv_align: num_tokens=%d outside [1, %d]", num_tokens, DV_MAX_TOKENS);
+    const size_t S = (size_t)num_states, V = (size_t)num_tokens, W = (V + 31) / 32;
+    const Range r_ns = range_of(next_state, S * V * 4), r_al = range_of(allow, S * W * 4);
+    const Range r_tr = range_of(trans, S * 256 * 4), r_off = range_of(offsets, (V + 1) * 4);
+    if (overlap(r_ns, r_al) || overlap(r_ns, r_tr) || overlap(r_ns, r_off) || overlap(r_al, r_tr) ||
+        overlap(r_al, r_off))
+        return fail(DV_ERR_ALIAS, "dv_align: next_state / allow overlap each other or an input");
+    const size_t need = dv::align_workspace_bytes(num_states);
+    if (!workspace || workspace_bytes < need)
+        return fail(DV_ERR_WORKSPACE, "dv_align: workspace of %zu bytes given, %zu needed", workspace_bytes, need);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255)
+        return fail(DV_ERR_WORKSPACE, "dv_align: workspace must be 256-byte aligned");
+    const Range r_ws = range_of(workspace, need);
+    if (overlap(r_ws, r_ns) || overlap(r_ws, r_al) || overlap(r_ws, r_tr) || overlap(r_ws, r_off))
+        return fail(DV_ERR_ALIAS, "dv_align: workspace overlaps an input or output");
+    // bytes == NULL is accepted; the kernels read it only for non-empty tokens.
+    return hip_status(dv::launch_align(trans, num_states, offsets, bytes, num_tokens, next_state, allow,
+                                       workspace, static_cast<hipStream_t>(stream)),
+                      "dv_align launch");
+}
+
+size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens)
+{
+    if (batch < 0 || batch > DV_MAX_BATCH || num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
+        return 0;
+    return dv::step_workspace_bytes(batch > 0 ? batch : 1);
+}
+
+dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow, int32_t num_states,
+                         int32_t num_tokens, const int32_t *states, const void *logits, int32_t dtype,
+                         int32_t batch, int64_t ld_logits, int32_t *token, int32_t *new_state,
+                         void *workspace, size_t workspace_bytes, void *stream)
+{
+    g_error[0] = '\0';
+    if (!next_state || !allow)
+        return fail(DV_ERR_INVALID_ARG, "dv_masked_step: next_state and allow must be non-NULL");
+    if (batch > 0 && (!states || !logits || !token || !new_state))
+        return fail(DV_ERR_INVALID_ARG, "dv_masked_step: states, logits, token and new_state must be "
+                                        "non-NULL when batch > 0");
+    if (num_states < 1 || num_states > DV_MAX_STATES)
+        return fail(DV_ERR_SHAPE, "dv_masked_step: num_states=%d outside [1, %d]", num_states, DV_MAX_STATES);
+    if (num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
+        return fail(DV_ERR_SHAPE, "dv_masked_step: num_tokens=%d outside [1, %d]", num_tokens, DV_MAX_TOKENS);
+    if (batch < 0 || batch > DV_MAX_BATCH)
+        return fail(DV_ERR_SHAPE, "dv_masked_step: batch=%d outside [0, %d]", batch, DV_MAX_BATCH);
+    if (ld_logits < num_tokens || ld_logits > ((int64_t)1 << 40))
+        return fail(DV_ERR_SHAPE, "dv_masked_step: ld_logits=%lld must be >= num_tokens=%d",
+                    (long long)ld_logits, num_tokens);
+    if (dtype != DV_F32 && dtype != DV_BF16)
+        return fail(DV_ERR_DTYPE, "dv_masked_step: unknown dtype %d", dtype);
+    if (batch == 0)
+        return DV_OK;
+    const size_t S = (size_t)num_states, V = (size_t)num_tokens, W = (V + 31) / 32, B = (size_t)batch;
+    const size_t elt = dtype == DV_F32 ? 4 : 2;
+    const Range r_tok = range_of(token, B * 4), r_new = range_of(new_state, B * 4);
+    const Range r_ns = range_of(next_state, S * V * 4), r_al = range_of(allow, S * W * 4);
+    const Range r_st = range_of(states, B * 4);
+    const Range r_lg = range_of(logits, ((B - 1) * (size_t)ld_logits + V) * elt);
+    if (overlap(r_tok, r_new))
+        return fail(DV_ERR_ALIAS, "dv_masked_step: token and new_state overlap");
+    for (Range out : {r_tok, r_new})
+        if (overlap(out, r_ns) || overlap(out, r_al) || overlap(out, r_st) || overlap(out, r_lg))
+            return fail(DV_ERR_ALIAS, "dv_masked_step: an output overlaps an input "
+                                      "(ping-pong two state buffers instead of updating in place)");
+    const size_t need = dv::step_workspace_bytes(batch);
+    if (!workspace || workspace_bytes < need)
+        return fail(DV_ERR_WORKSPACE, "dv_masked_step: workspace of %zu bytes given, %zu needed",
+                    workspace_bytes, need);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255)
+        return fail(DV_ERR_WORKSPACE, "dv_masked_step: workspace must be 256-byte aligned");
+    const Range r_ws = range_of(workspace, need);
+    for (Range r : {r_tok, r_new, r_ns, r_al, r_st, r_lg})
+        if (overlap(r_ws, r))
+            return fail(DV_ERR_ALIAS, "dv_masked_step: workspace overlaps an input or output");
+    return hip_status(dv::launch_masked_step(next_state, allow, num_states, num_tokens, states, logits,
+                                             dtype, batch, ld_logits, token, new_state, workspace,
+                                             static_cast<hipStream_t>(stream)),
+                      "dv_masked_step launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,50 @@
+// Internal declarations shared by the translation units of libdv.so.
+// Not installed; the public interface is include/dv.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dv {
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------- alignment
+//
+// Workspace of dv_align (all offsets 256-byte aligned):
+//   [0, 4)        int32  number of live byte columns C
+//   [4, 8)        int32  row stride Cp of the compacted table (C rounded up to 2)
+//   [256, 512)    uint8  class of each byte (0xFF: the byte is dead from every state)
+//   [512, 768)    uint8  byte of each class
+//   [1024, ...)   uint32 per-block live-column bit sets, 8 words per block
+//   [table, ...)  uint16 compacted table [S][Cp], DEAD = 0xFFFF
+constexpr int kAlignMetaBytes = 1024;
+constexpr int kLiveRowsPerBlock = 64;
+constexpr uint16_t kDead16 = 0xFFFF;
+constexpr uint8_t kDeadClass = 0xFF;
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+inline size_t align_live_blocks(int S) { return (size_t)(S + kLiveRowsPerBlock - 1) / kLiveRowsPerBlock; }
+inline size_t align_table_offset(int S) { return align_up(kAlignMetaBytes + align_live_blocks(S) * 32, 256); }
+inline size_t align_workspace_bytes(int S) { return align_table_offset(S) + (size_t)S * 256 * sizeof(uint16_t); }
+
+hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, const uint8_t *bytes,
+                        int V, int32_t *next_state, uint32_t *allow, void *workspace,
+                        hipStream_t stream);
+
+// ------------------------------------------------------------- masked step
+//
+// Workspace of dv_masked_step: uint64 best key per row, then uint32 arrival
+// counter per row (at an offset rounded up to 256 bytes).  Both zero between
+// calls: the last block of each row resets them.
+inline size_t step_counter_offset(int B) { return align_up((size_t)B * sizeof(uint64_t), 256); }
+inline size_t step_workspace_bytes(int B) { return step_counter_offset(B) + align_up((size_t)B * 4, 256); }
+
+hipError_t launch_masked_step(const int32_t *next_state, const uint32_t *allow, int S, int V,
+                              const int32_t *states, const void *logits, int dtype, int B,
+                              int64_t ld, int32_t *token, int32_t *new_state, void *workspace,
+                              hipStream_t stream);
+
+}  // namespace dv

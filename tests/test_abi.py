@@ -1,0 +1,130 @@
+"""The C ABI on the host (no GPU needed): the library loads, exports every
+function include/dv.h declares, and rejects bad arguments before any HIP call.
+
+Pointer arguments here are fake non-NULL addresses: each call is built so that
+a host-side check rejects it, so nothing is ever launched or dereferenced."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2403_06988_amd as dv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dv.h")
+lib = dv.lib
+
+OK, INVALID, SHAPE, DTYPE, ALIAS, WORKSPACE, HIP = range(7)
+P = 0x7F0000000000  # fake device address (never dereferenced)
+GB = 1 << 30
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return re.findall(r"^DV_API\s+[\w\s\*]+?\b(dv_\w+)\s*\(", text, flags=re.M)
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert set(names) == {"dv_align_workspace_bytes", "dv_align", "dv_masked_step_workspace_bytes",
+                          "dv_masked_step", "dv_status_string", "dv_last_error", "dv_version"}
+    raw = ctypes.CDLL(dv.library_path)
+    for n in names:
+        assert hasattr(raw, n), n
+
+
+def test_status_strings_and_version():
+    assert lib.dv_status_string(OK) == b"DV_OK"
+    assert lib.dv_status_string(ALIAS) == b"DV_ERR_ALIAS"
+    assert lib.dv_status_string(99) == b"DV_ERR_UNKNOWN"
+    assert lib.dv_version() >= 100
+
+
+def test_workspace_queries():
+    assert lib.dv_align_workspace_bytes(0, 10) == 0
+    assert lib.dv_align_workspace_bytes(70000, 10) == 0
+    a = lib.dv_align_workspace_bytes(8192, 128256)
+    assert a >= 8192 * 256 * 2  # compacted table of at most 256 uint16 columns
+    assert lib.dv_masked_step_workspace_bytes(-1, 10) == 0
+    assert lib.dv_masked_step_workspace_bytes(256, 128256) >= 256 * 12
+    assert lib.dv_masked_step_workspace_bytes(0, 10) > 0
+
+
+def _align(trans=P, S=16, offsets=P + GB, bytes_=P + 2 * GB, V=1000, ns=P + 3 * GB,
+           allow=P + 4 * GB, ws=P + 5 * GB, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = lib.dv_align_workspace_bytes(max(S, 1), max(V, 1))
+    return lib.dv_align(trans, S, offsets, bytes_, V, ns, allow, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(trans=None), INVALID),
+    (dict(offsets=None), INVALID),
+    (dict(ns=None), INVALID),
+    (dict(allow=None), INVALID),
+    (dict(S=0), SHAPE),
+    (dict(S=65536), SHAPE),
+    (dict(V=0), SHAPE),
+    (dict(V=-5), SHAPE),
+    (dict(allow=P + 3 * GB + 4), ALIAS),          # allow inside next_state
+    (dict(ns=P), ALIAS),                          # next_state over trans
+    (dict(allow=P + GB), ALIAS),                  # allow over offsets
+    (dict(ws=None), WORKSPACE),
+    (dict(ws_bytes=100), WORKSPACE),
+    (dict(ws=P + 5 * GB + 8), WORKSPACE),         # not 256-byte aligned
+    (dict(ws=P + 3 * GB), ALIAS),                 # workspace over next_state
+])
+def test_align_rejects_before_launch(kw, status):
+    assert _align(**kw) == status
+    assert lib.dv_last_error().startswith(b"dv_align")
+
+
+def _step(ns=P, allow=P + GB, S=16, V=1000, states=P + 2 * GB, logits=P + 3 * GB, dtype=0, B=8,
+          ld=1000, tok=P + 4 * GB, new=P + 5 * GB, ws=P + 6 * GB, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = lib.dv_masked_step_workspace_bytes(max(B, 0), max(V, 1))
+    return lib.dv_masked_step(ns, allow, S, V, states, logits, dtype, B, ld, tok, new, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(ns=None), INVALID),
+    (dict(states=None), INVALID),
+    (dict(logits=None), INVALID),
+    (dict(tok=None), INVALID),
+    (dict(S=0), SHAPE),
+    (dict(V=0), SHAPE),
+    (dict(B=-1), SHAPE),
+    (dict(ld=999), SHAPE),
+    (dict(dtype=2), DTYPE),
+    (dict(dtype=-1), DTYPE),
+    (dict(new=P + 4 * GB + 4), ALIAS),            # token / new_state overlap
+    (dict(new=P + 2 * GB), ALIAS),                # in-place state update
+    (dict(tok=P + 3 * GB + 100), ALIAS),          # output inside logits
+    (dict(tok=P + 8), ALIAS),                     # output inside next_state
+    (dict(ws=None), WORKSPACE),
+    (dict(ws_bytes=8), WORKSPACE),
+    (dict(ws=P + 6 * GB + 64), WORKSPACE),
+    (dict(ws=P + 2 * GB), ALIAS),
+])
+def test_masked_step_rejects_before_launch(kw, status):
+    assert _step(**kw) == status
+    assert lib.dv_last_error().startswith(b"dv_masked_step")
+
+
+def test_masked_step_empty_batch_is_a_noop():
+    assert _step(B=0) == OK
+    assert lib.dv_last_error() == b""
+    # empty tensors have NULL data pointers
+    assert _step(B=0, states=None, logits=None, tok=None, new=None) == OK
+    assert _step(B=0, ns=None) == INVALID
+
+
+def test_binding_type_checks():
+    import torch
+    with pytest.raises((TypeError, ValueError)):
+        dv.align(torch.zeros((2, 256), dtype=torch.int64), torch.zeros(3, dtype=torch.int32),
+                 torch.zeros(1, dtype=torch.uint8))
+    with pytest.raises((TypeError, ValueError)):
+        dv.align(torch.zeros((2, 256), dtype=torch.int32), torch.zeros(3, dtype=torch.int32),
+                 torch.zeros(1, dtype=torch.uint8))  # CPU tensors are refused

@@ -1,0 +1,374 @@
+"""GPU parity: the HIP path against the CPU oracle, bit for bit.
+
+Alignment tables (next_state, allow with padding bits) and greedy decoding
+chains (token, new_state at every step) are compared with the oracle, which
+computes from the same seeded inputs with its own table and its own previous
+states.  Workloads 1-3 are compared in full; workloads 4-5 (4.2 GB tables) on
+sampled state rows and sampled batch rows, plus properties over the whole
+table.  The launch configuration is the benchmark's (same shapes, same
+calls)."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from tests.gpu_common import run_chain, to_oracle, u32
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module")
+def dv():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2403_06988_amd as dv_mod
+    return dv_mod
+
+
+DEV = torch.device("cuda:0")
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def _align(dv, trans, offsets, data):
+    ns, al = dv.align(_dev(trans), _dev(offsets), _dev(data if len(data) else np.zeros(1, np.uint8)))
+    torch.cuda.synchronize()
+    return ns, al
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+# ------------------------------------------------------------- worked examples
+
+@pytest.mark.parametrize("name", ["fig_nfa_int.json", "fig_overview_scanner.json"])
+def test_align_paper_examples(dv, name):
+    g = json.load(open(os.path.join(GOLDEN, name)))
+    trans = W.dfa_from_spec(len(g["states"]), g["moves"])
+    offsets, data = W.vocab_from_tokens([t.encode() for t in g["vocab"]])
+    ns, al = _align(dv, trans, offsets, data)
+    ns_o, al_o = oracle.align(trans, offsets, data)
+    np.testing.assert_array_equal(ns.cpu().numpy(), ns_o)
+    np.testing.assert_array_equal(u32(al), al_o)
+    if "expected_next_state" in g:
+        np.testing.assert_array_equal(ns.cpu().numpy(), np.array(g["expected_next_state"]))
+
+
+# ------------------------------------------------------------ alignment edges
+
+def _random_case(seed, S, V, max_len, p_empty=0.0, junk=True, alphabet=None):
+    rng = np.random.default_rng(seed)
+    alphabet = alphabet if alphabet is not None else np.arange(256)
+    trans = np.full((S, 256), -1, np.int32)
+    for s in range(S):
+        k = int(rng.integers(1, len(alphabet) + 1))
+        cols = rng.choice(alphabet, size=k, replace=False)
+        trans[s, cols] = rng.integers(0, S, size=k)
+    if junk:
+        mask = rng.random(trans.shape) < 0.05
+        trans[mask] = rng.choice(np.array([S, S + 7, -2, -(1 << 30), 1 << 30], np.int32), mask.sum())
+    toks = []
+    for _ in range(V):
+        L = 0 if rng.random() < p_empty else int(rng.integers(1, max_len + 1))
+        toks.append(bytes(rng.choice(alphabet, size=L).astype(np.uint8)))
+    offsets, data = W.vocab_from_tokens(toks)
+    return trans, offsets, data
+
+
+@pytest.mark.parametrize("S,V,max_len,p_empty", [
+    (1, 1, 3, 0.0), (3, 31, 4, 0.0), (5, 33, 4, 0.1), (7, 63, 5, 0.0), (9, 64, 5, 0.0),
+    (33, 65, 6, 0.0), (40, 1023, 6, 0.05), (64, 1025, 8, 0.0), (100, 4097, 12, 0.02),
+    (37, 3000, 200, 0.0),                   # a few very long tokens
+])
+def test_align_edge_shapes(dv, S, V, max_len, p_empty):
+    _say(f"align edge S={S} V={V} max_len={max_len}")
+    trans, offsets, data = _random_case(S * 1000 + V, S, V, max_len, p_empty,
+                                        alphabet=np.arange(0x20, 0x30))
+    ns, al = _align(dv, trans, offsets, data)
+    ns_o, al_o = oracle.align(trans, offsets, data)
+    np.testing.assert_array_equal(ns.cpu().numpy(), ns_o)
+    np.testing.assert_array_equal(u32(al), al_o)
+
+
+def test_align_all_tokens_empty(dv):
+    trans = np.zeros((4, 256), np.int32)
+    offsets = np.zeros(70, np.int32)
+    ns, al = _align(dv, trans, offsets, np.zeros(0, np.uint8))
+    ns_o, al_o = oracle.align(trans, offsets, np.zeros(0, np.uint8))
+    np.testing.assert_array_equal(ns.cpu().numpy(), ns_o)
+    np.testing.assert_array_equal(u32(al), al_o)
+
+
+def test_align_all_transitions_dead(dv):
+    trans = np.full((5, 256), -1, np.int32)
+    trans[2, 7] = 99  # out of range: still dead
+    offsets, data = W.vocab(1)
+    ns, al = _align(dv, trans, offsets, data)
+    assert (ns.cpu().numpy() == -1).all() and (u32(al) == 0).all()
+
+
+def test_align_every_byte_value(dv):
+    # every byte 0x00..0xFF is a live column: Cp = 256, no compaction
+    rng = np.random.default_rng(5)
+    S = 50
+    trans = rng.integers(0, S, size=(S, 256)).astype(np.int32)
+    trans[:, 0xFF] = -1
+    toks = [bytes([b]) for b in range(256)] + [bytes(rng.integers(0, 256, 3).astype(np.uint8))
+                                               for _ in range(700)]
+    offsets, data = W.vocab_from_tokens(toks)
+    ns, al = _align(dv, trans, offsets, data)
+    ns_o, al_o = oracle.align(trans, offsets, data)
+    np.testing.assert_array_equal(ns.cpu().numpy(), ns_o)
+    np.testing.assert_array_equal(u32(al), al_o)
+
+
+def test_align_is_deterministic(dv):
+    trans, _ = W.dfa(2)
+    offsets, data = W.vocab(2)
+    a = _align(dv, trans, offsets, data)
+    b = _align(dv, trans, offsets, data)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+# --------------------------------------------------------- workload tables
+
+class _Cache:
+    wid = None
+    data = None
+
+
+def _workload_table(dv, wid):
+    if _Cache.wid != wid:
+        _Cache.wid, _Cache.data = None, None
+        torch.cuda.empty_cache()
+        trans, _ = W.dfa(wid)
+        offsets, data = W.vocab(wid)
+        ns, al = _align(dv, trans, offsets, data)
+        _Cache.wid, _Cache.data = wid, (trans, offsets, data, ns, al)
+    return _Cache.data
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3])
+def test_align_workload_full(dv, wid):
+    _say(f"align workload {W.WORKLOADS[wid].describe()}")
+    trans, offsets, data, ns, al = _workload_table(dv, wid)
+    ns_o, al_o = oracle.align(trans, offsets, data)
+    np.testing.assert_array_equal(ns.cpu().numpy(), ns_o)
+    np.testing.assert_array_equal(u32(al), al_o)
+
+
+@pytest.mark.parametrize("wid", [4, 5])
+def test_align_workload_sampled(dv, wid):
+    w = W.WORKLOADS[wid]
+    _say(f"align workload {w.describe()} (sampled rows)")
+    trans, offsets, data, ns, al = _workload_table(dv, wid)
+    rng = np.random.default_rng(wid)
+    rows = np.unique(np.concatenate([[0, 1, w.S - 1], rng.integers(0, w.S, 45)])).astype(np.int32)
+    ns_o, al_o = oracle.align_rows(trans, offsets, data, rows)
+    idx = torch.from_numpy(rows.astype(np.int64)).to(DEV)
+    np.testing.assert_array_equal(ns.index_select(0, idx).cpu().numpy(), ns_o)
+    np.testing.assert_array_equal(u32(al.index_select(0, idx)), al_o)
+    # properties over the whole table, row block by row block
+    lens = np.diff(offsets)
+    single = np.nonzero(lens == 1)[0]
+    tcol = torch.from_numpy(trans[:, data[offsets[single]]]).to(DEV)
+    tcol = torch.where((tcol >= 0) & (tcol < w.S), tcol, torch.full_like(tcol, -1))
+    assert torch.equal(ns[:, torch.from_numpy(single).to(DEV)], tcol)  # single-byte columns
+    bits = torch.arange(32, device=DEV, dtype=torch.int32)
+    for r0 in range(0, w.S, 512):
+        blk = ns[r0:r0 + 512]
+        alive = (blk != -1)
+        pad = torch.zeros((blk.shape[0], w.words * 32), dtype=torch.bool, device=DEV)
+        pad[:, :w.V] = alive
+        words = (pad.view(blk.shape[0], w.words, 32).to(torch.int64) << bits.to(torch.int64)).sum(-1)
+        assert torch.equal(words.to(torch.int64) & 0xFFFFFFFF,
+                           al[r0:r0 + 512].to(torch.int64) & 0xFFFFFFFF)
+        assert bool(((blk >= -1) & (blk < w.S)).all())
+
+
+# ------------------------------------------------------------ greedy chains
+
+def _chain_check(dv, wid, sample_rows):
+    w = W.WORKLOADS[wid]
+    trans, offsets, data, ns, al = _workload_table(dv, wid)
+    init = W.init_states(wid)
+    x = W.logits_all(wid, device=DEV)
+    ws = dv.step_workspace(w.B, w.V, DEV)
+    toks, sts = run_chain(dv, ns, al, _dev(init), x, ws)
+    torch.cuda.synchronize()
+    toks_h, sts_h = toks.cpu().numpy(), sts.cpu().numpy()
+    rows = np.arange(w.B) if sample_rows is None else sample_rows
+    cache = oracle.RowCache(trans, offsets, data)
+    xr = to_oracle(x[:, torch.from_numpy(rows.astype(np.int64)).to(DEV)])
+    del x
+    dead = 0
+    for i, b in enumerate(rows):
+        t_o, s_o = oracle.masked_chain(cache, init[b], xr[:, i])
+        np.testing.assert_array_equal(toks_h[:, b], t_o, err_msg=f"workload {wid} row {b}")
+        np.testing.assert_array_equal(sts_h[1:, b], s_o[1:], err_msg=f"workload {wid} row {b}")
+        dead += int(s_o[-1] == -1)
+    _say(f"chain workload {wid}: {len(rows)} rows x {w.steps} steps bit-exact, {dead} rows died")
+    # every emitted token is allowed from the state it was chosen in (all rows)
+    st = sts[:-1].to(torch.int64)
+    tk = toks.to(torch.int64)
+    live = (st >= 0) & (tk >= 0)
+    word = al[st.clamp(min=0), (tk.clamp(min=0) // 32)].to(torch.int64) & 0xFFFFFFFF
+    assert bool((((word >> (tk.clamp(min=0) % 32)) & 1) == 1)[live].all())
+    assert bool(((tk == -1) == (sts[1:] == -1)).all())
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3])
+def test_chain_workload_full(dv, wid):
+    _say(f"chain workload {W.WORKLOADS[wid].describe()}")
+    _chain_check(dv, wid, None)
+
+
+@pytest.mark.parametrize("wid", [4, 5])
+def test_chain_workload_sampled(dv, wid):
+    w = W.WORKLOADS[wid]
+    _say(f"chain workload {w.describe()} (sampled rows)")
+    rng = np.random.default_rng(100 + wid)
+    rows = np.unique(np.concatenate([[0, w.B - 1], rng.integers(0, w.B, 30)]))
+    _chain_check(dv, wid, rows)
+
+
+# ---------------------------------------------------------- masked step edges
+
+def _one_row_table(V, allowed):
+    ns = np.full((1, V), -1, np.int32)
+    ns[0, list(allowed)] = 0
+    alive = ns != -1
+    Wd = (V + 31) // 32
+    pad = np.zeros((1, Wd * 32), bool)
+    pad[:, :V] = alive
+    al = np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(1, Wd)
+    return ns, al
+
+
+PLANTED_F32 = [
+    ([100, 9, 9, 5, 1, 9, 0, 9, 0, 0.5], [1, 2, 5, 7, 9], 1),
+    ([0, 1, -0.0, 7, 7, 0.0, 9], [2, 5], 2),
+    ([0, 1, 0.0, 7, 7, -0.0, 9], [2, 5], 2),
+    ([5, float("nan"), 3, 3, -np.inf], [1, 4], 1),
+    ([float("nan"), 2.0, 1.0], [0, 1, 2], 1),
+    ([float("nan")] * 6, [3, 5], 3),
+    ([np.inf, 1e30, np.inf, 2, 3], [1, 3], 1),
+    ([-np.inf, -np.inf, -3e38], [0, 1], 0),
+    ([-1e-45, 0.0, 1e-45, -0.0], [0, 2, 3], 2),
+    ([1, 2, 3], [], -1),
+]
+
+
+@pytest.mark.parametrize("spread", [1, 37, 20011])
+@pytest.mark.parametrize("case", range(len(PLANTED_F32)))
+def test_step_planted_specials_f32(dv, case, spread):
+    """Planted values at indices i * spread, so large spreads cross vector,
+    wave, block and chunk boundaries (multi-block rows)."""
+    vals, allowed, expect = PLANTED_F32[case]
+    V = len(vals) * spread + 5
+    x = np.full((1, V), 1e38, np.float32)       # disallowed everywhere else
+    x[0, np.arange(len(vals)) * spread] = np.array(vals, np.float32)
+    ns, al = _one_row_table(V, [a * spread for a in allowed])
+    tok, new = dv.masked_step(_dev(ns), _dev(al.view(np.int32)), _dev(np.zeros(1, np.int32)), _dev(x))
+    tok_o, new_o = oracle.masked_step(ns, al, np.zeros(1, np.int32), x)
+    assert int(tok.item()) == int(tok_o[0]) == (expect * spread if expect >= 0 else -1)
+    assert int(new.item()) == int(new_o[0])
+
+
+@pytest.mark.parametrize("bits,allowed,expect", [
+    ([0x3F80, 0x3F80, 0x3F80], [1, 2], 1),
+    ([0x8000, 0x0000, 0x0001], [0, 1], 0),
+    ([0x8000, 0x0000, 0x0001], [0, 1, 2], 2),
+    ([0x7FC1, 0xFF80, 0xFFC1], [0, 1, 2], 0),
+    ([0x7FC1, 0xC000, 0x7F80], [0, 1], 1),
+    ([0xFFC1, 0xFF7F], [0, 1], 1),
+    ([0xBF80, 0xC000, 0xBF80], [0, 1, 2], 0),
+])
+@pytest.mark.parametrize("spread", [1, 9, 50021])
+def test_step_planted_specials_bf16(dv, bits, allowed, expect, spread):
+    V = len(bits) * spread + 3
+    x = np.full((1, V), 0x7F00, np.uint16)
+    x[0, np.arange(len(bits)) * spread] = np.array(bits, np.uint16)
+    ns, al = _one_row_table(V, [a * spread for a in allowed])
+    xt = _dev(x.view(np.int16)).view(torch.bfloat16)
+    tok, _ = dv.masked_step(_dev(ns), _dev(al.view(np.int32)), _dev(np.zeros(1, np.int32)), xt)
+    tok_o, _ = oracle.masked_step(ns, al, np.zeros(1, np.int32), x)
+    assert int(tok.item()) == int(tok_o[0]) == expect * spread
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("B,V,extra_ld,offset", [
+    (1, 1, 0, 0), (3, 7, 0, 0), (5, 33, 3, 0), (4, 1000, 0, 1), (17, 4099, 5, 1),
+    (2, 70001, 0, 0), (9, 70001, 11, 3), (300, 2048, 0, 0), (3000, 129, 0, 0),
+])
+def test_step_shapes_ld_and_alignment(dv, dtype, B, V, extra_ld, offset):
+    """Random tables and states (including dead and out-of-range states),
+    row strides wider than V and row starts that are not 16-byte aligned."""
+    _say(f"step shapes B={B} V={V} ld=V+{extra_ld} offset={offset} {dtype}")
+    rng = np.random.default_rng(B * 7 + V)
+    S = 13
+    alive = rng.random((S, V)) < rng.choice([0.0, 0.002, 0.05, 0.5, 1.0], size=(S, 1))
+    ns = np.where(alive, rng.integers(0, S, (S, V)), -1).astype(np.int32)
+    Wd = (V + 31) // 32
+    pad = np.zeros((S, Wd * 32), bool)
+    pad[:, :V] = alive
+    al = np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(S, Wd)
+    states = rng.integers(-2, S + 2, B).astype(np.int32)
+    ld = V + extra_ld
+    buf = torch.from_numpy((rng.standard_normal(B * ld + offset + 8) * 4).astype(np.float32))
+    buf = buf.to(dtype)
+    special = torch.tensor([float("nan"), float("inf"), -float("inf"), -0.0, 0.0], dtype=dtype)
+    pos = torch.from_numpy(rng.integers(0, buf.numel(), 64))
+    buf[pos] = special[torch.from_numpy(rng.integers(0, 5, 64))]
+    buf_d = buf.to(DEV)
+    x = buf_d[offset:offset + B * ld].view(B, ld)[:, :V]
+    tok, new = dv.masked_step(_dev(ns), _dev(al.view(np.int32)), _dev(states), x)
+    xo = to_oracle(buf[offset:offset + B * ld].view(B, ld))
+    tok_o, new_o = oracle.masked_step(ns, al, states, xo)
+    np.testing.assert_array_equal(tok.cpu().numpy(), tok_o)
+    np.testing.assert_array_equal(new.cpu().numpy(), new_o)
+
+
+def test_step_empty_batch(dv):
+    ns = torch.zeros((2, 10), dtype=torch.int32, device=DEV)
+    al = torch.full((2, 1), 0x3FF, dtype=torch.int32, device=DEV)
+    tok, new = dv.masked_step(ns, al, torch.zeros(0, dtype=torch.int32, device=DEV),
+                              torch.zeros((0, 10), device=DEV))
+    assert tok.numel() == 0 and new.numel() == 0
+
+
+def test_step_workspace_reuse_and_determinism(dv):
+    trans, offsets, data, ns, al = _workload_table(dv, 2)
+    w = W.WORKLOADS[2]
+    ws = dv.step_workspace(64, w.V, DEV)
+    rng = np.random.default_rng(0)
+    outs = []
+    for B in (64, 8, 64, 1, 33):
+        st = _dev(rng.integers(0, w.S, B).astype(np.int32))
+        x = W.logits(2, 7, device=DEV, batch=B)
+        a = dv.masked_step(ns, al, st, x, workspace=ws)
+        b = dv.masked_step(ns, al, st, x, workspace=ws)
+        assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+        fresh = dv.masked_step(ns, al, st, x)  # its own zeroed workspace
+        assert torch.equal(a[0], fresh[0]) and torch.equal(a[1], fresh[1])
+        outs.append(a)
+    torch.cuda.synchronize()
+    assert int(ws.count_nonzero()) == 0  # left zero-filled
+
+
+def test_step_rejects_in_place_update(dv):
+    ns = torch.zeros((2, 10), dtype=torch.int32, device=DEV)
+    al = torch.zeros((2, 1), dtype=torch.int32, device=DEV)
+    st = torch.zeros(4, dtype=torch.int32, device=DEV)
+    with pytest.raises(dv.DvError) as e:
+        dv.masked_step(ns, al, st, torch.zeros((4, 10), device=DEV), new_state=st)
+    assert e.value.status == 4
