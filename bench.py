@@ -50,6 +50,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2, help="untimed jobs")
     ap.add_argument("--workload", type=int, default=4)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--no-probes", action="store_true", help="skip the roofline probes")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
 
@@ -129,6 +130,64 @@ def cpu_baseline(w, wid, trans, offsets, data, init, x_dev, budget_s):
         "align_sample": f"{pairs} (state, token) pairs in whole table rows",
         "seconds": round(t_dec + t_al, 2),
     }
+
+
+def run_probes(dv, dev, table_bytes):
+    """Measured rates of the memory paths the kernels use (roofline probes in
+    libdv.so): HBM stream read / write, dependent random gathers from a table
+    the size of the workload's compacted DFA (L1/L2), and from LDS."""
+    import ctypes
+
+    import torch
+
+    lib = dv.lib
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    lib.dvprobe_stream_read.argtypes = [vp, sz, vp, vp]
+    lib.dvprobe_stream_write.argtypes = [vp, sz, vp]
+    lib.dvprobe_gather.argtypes = [vp, i32, i32, i32, i32, vp, vp]
+    lib.dvprobe_lds_gather.argtypes = [vp, i32, i32, i32, i32, vp, vp]
+    for f in (lib.dvprobe_stream_read, lib.dvprobe_stream_write, lib.dvprobe_gather,
+              lib.dvprobe_lds_gather):
+        f.restype = i32
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+
+    def timed(fn, reps=5):
+        best = None
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            rc = fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            if rc != 0:
+                raise RuntimeError(f"probe failed with status {rc}")
+            ms = a.elapsed_time(b)
+            best = ms if best is None else min(best, ms)
+        return best / 1e3
+
+    out = {}
+    n = 2 << 30
+    buf = torch.empty(n, dtype=torch.uint8, device=dev)
+    sink = torch.empty(1 << 20, dtype=torch.int32, device=dev)
+    lib.dvprobe_stream_write(buf.data_ptr(), n, sh)
+    out["hbm_read_GBs"] = n / timed(lambda: lib.dvprobe_stream_read(buf.data_ptr(), n, sink.data_ptr(), sh)) / 1e9
+    out["hbm_write_GBs"] = n / timed(lambda: lib.dvprobe_stream_write(buf.data_ptr(), n, sh)) / 1e9
+    del buf
+    entries = max(1024, table_bytes // 4)
+    perm = torch.randperm(entries, device=dev, dtype=torch.int64).to(torch.int32)
+    lanes, chains, steps = 524288, 4, 32
+    sink = torch.empty(lanes, dtype=torch.int32, device=dev)
+    t = timed(lambda: lib.dvprobe_gather(perm.data_ptr(), entries, lanes, chains, steps, sink.data_ptr(), sh))
+    out["gather_table_bytes"] = entries * 4
+    out["l2_gather_per_s"] = lanes * chains * steps / t
+    lds_entries = 16384
+    perm = torch.randperm(lds_entries, device=dev, dtype=torch.int64).to(torch.int32)
+    lanes, steps = 131072, 256
+    t = timed(lambda: lib.dvprobe_lds_gather(perm.data_ptr(), lds_entries, lanes, chains, steps,
+                                             sink.data_ptr(), sh))
+    out["lds_gather_per_s"] = lanes * chains * steps / t
+    return out
 
 
 def main():
@@ -246,6 +305,9 @@ def main():
                            "traffic": traffic_record("align_walk_traffic")},
         "kernel_source_hash": kernel_source_hash(),
     }
+    if not args.no_probes:
+        log("roofline probes")
+        out["probes"] = run_probes(dv, dev, w.S * 96 * 2)
     if not args.no_cpu:
         log("cpu baseline (oracle, 1 thread)")
         out["cpu_baseline"] = cpu_baseline(w, wid, trans, offsets, data, init, x, args.cpu_seconds)

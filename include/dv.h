@@ -110,8 +110,9 @@ DV_API dv_status dv_align(const int32_t *trans, int32_t num_states,
 
 /*
  * dv_masked_step_workspace_bytes -- device workspace dv_masked_step needs for
- * `batch` rows (per-row partial results of a split-row reduction).
- * Returns 0 when a size is outside its limit.
+ * `batch` rows of `num_tokens` logits (per-chunk partial results when a row
+ * is split over several blocks), for either dtype.  Returns 0 when a size is
+ * outside its limit.
  */
 DV_API size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens);
 
@@ -140,9 +141,8 @@ DV_API size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens);
  * Outputs (device): token [B] int32, new_state [B] int32.  They must not
  *   overlap each other or any input (callers ping-pong two state buffers).
  * Workspace: at least dv_masked_step_workspace_bytes(B, V) bytes of device
- *   memory, 256-byte aligned, ZERO-FILLED before its first use; every call
- *   leaves it zero-filled again when it completes, so a buffer zeroed once
- *   can be reused for any later call on the same stream.
+ *   memory, 256-byte aligned; contents on entry are ignored, on exit
+ *   undefined.  Calls that share a workspace must be ordered on one stream.
  * B = 0 is valid and enqueues nothing; states, logits, token and new_state
  *   may then be NULL (the pointers of empty tensors).
  * Errors: DV_ERR_INVALID_ARG, DV_ERR_SHAPE (S, V, B out of range or

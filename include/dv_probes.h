@@ -1,0 +1,63 @@
+/*
+ * dv_probes.h -- roofline probes for libdv.so (measurement, not the hot path).
+ *
+ * Each probe enqueues one kernel on `stream` that exercises one memory path
+ * of the GPU the way the alignment and masked-step kernels do, so the rates
+ * they reach can be compared with what those kernels reach:
+ *
+ *   dvprobe_stream_read  16-byte loads over `n_bytes` of device memory (HBM
+ *                        read bandwidth, the masked step's bound);
+ *   dvprobe_stream_write 16-byte stores over `n_bytes` (HBM write bandwidth,
+ *                        the alignment table's output bound);
+ *   dvprobe_gather       dependent random gathers from a device table of
+ *                        `table_entries` uint32 values (L1/L2 gather rate,
+ *                        the alignment walk's later moves, which read one
+ *                        small table entry per request);
+ *   dvprobe_lds_gather   the same chase inside LDS (the walk's first move).
+ *
+ * All pointers are device pointers owned by the caller; sizes are checked on
+ * the host before any HIP call.  `sink` receives a value derived from every
+ * load so that no load can be optimised away (its contents are meaningless).
+ * Returns 0 on success, 1 for a bad argument, 6 for a HIP error.
+ */
+#ifndef DV_PROBES_H
+#define DV_PROBES_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define DVPROBE_API __attribute__((visibility("default")))
+#else
+#define DVPROBE_API
+#endif
+
+/* src: n_bytes (multiple of 16, >= 4096) of device memory; sink: 4096 uint32. */
+DVPROBE_API int32_t dvprobe_stream_read(const void *src, size_t n_bytes, uint32_t *sink,
+                                        void *stream);
+
+/* dst: n_bytes (multiple of 16, >= 4096) of device memory, overwritten. */
+DVPROBE_API int32_t dvprobe_stream_write(void *dst, size_t n_bytes, void *stream);
+
+/* table: table_entries (<= 2^24) uint32 values, normally a random chase
+ * permutation of [0, table_entries) (values outside are clamped into range);
+ * lanes * chains independent chases of `steps` dependent loads each.
+ * lanes: a multiple of 256; chains: 1, 2, 4 or 8.  sink: lanes uint32. */
+DVPROBE_API int32_t dvprobe_gather(const uint32_t *table, int32_t table_entries, int32_t lanes,
+                                   int32_t chains, int32_t steps, uint32_t *sink, void *stream);
+
+/* As dvprobe_gather with the table copied into each block's LDS first
+ * (table_entries <= 32768, i.e. up to 128 KB of LDS). */
+DVPROBE_API int32_t dvprobe_lds_gather(const uint32_t *table, int32_t table_entries,
+                                       int32_t lanes, int32_t chains, int32_t steps,
+                                       uint32_t *sink, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DV_PROBES_H */

@@ -135,10 +135,10 @@ def align(trans, offsets, tok_bytes, next_state=None, allow=None, workspace=None
 
 
 def step_workspace(batch: int, num_tokens: int, device) -> torch.Tensor:
-    """A zero-filled workspace for ``masked_step`` (reusable across calls on
-    one stream: every call leaves it zero-filled)."""
+    """A workspace for ``masked_step`` with up to ``batch`` rows (reusable by
+    calls ordered on one stream)."""
     n = masked_step_workspace_bytes(batch, num_tokens)
-    return torch.zeros(max(n, 1), dtype=torch.uint8, device=device)
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
 
 
 def masked_step(next_state, allow, states, logits, token=None, new_state=None, workspace=None,

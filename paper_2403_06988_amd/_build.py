@@ -8,7 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["dv_api.hip", "dv_align.hip", "dv_step.hip"]
+SOURCES = ["dv_api.hip", "dv_align.hip", "dv_step.hip", "dv_probes.hip"]
 LIB = os.path.join(HERE, "libdv.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -21,8 +21,9 @@ FLAGS = [
 ]
 
 
-def build(out: str = LIB, verbose: bool = False) -> str:
-    cmd = [HIPCC, *FLAGS, "-o", out + ".tmp", *[os.path.join(CSRC, s) for s in SOURCES]]
+def build(out: str = LIB, verbose: bool = False, defines: tuple = ()) -> str:
+    cmd = [HIPCC, *FLAGS, *[f"-D{d}" for d in defines], "-o", out + ".tmp",
+           *[os.path.join(CSRC, s) for s in SOURCES]]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

@@ -10,33 +10,50 @@
 //      Random printable-ASCII DFAs keep ~95 of 256 columns, so the table is
 //      ~2.7x smaller than the int32 input and stays resident in each XCD's L2.
 //   4. walk: one lane per (state, token) pair.  A block owns a tile of 32
-//      states x 1024 tokens: the 32 compacted rows are staged in LDS, so the
-//      first move of every walk (every pair takes it) is an LDS read; later
-//      moves (about half the pairs survive each byte) read the L2-resident
-//      compacted table.  Each lane carries 4 tokens whose walks advance in
-//      lock-step for memory-level parallelism; the wave stops as soon as all
-//      64 lanes' walks have ended.  Stores are coalesced along tokens, and
-//      the allow words come from a wave ballot (64 tokens -> 2 words).
+//      states x 1024 tokens (4 tokens per lane).  The byte classes of each
+//      token's first 8 bytes are looked up once per block and kept in
+//      registers, so a move costs one table read.  The table lives in LDS:
+//      the whole table when it fits, otherwise the block's 32 rows, which
+//      serve every walk's first move (every pair takes one); later moves
+//      (about half the pairs survive each byte) read the L2-resident table
+//      with 32-bit offsets.  A lane's 4 walks advance in lock-step for
+//      memory-level parallelism and the wave stops as soon as every walk in
+//      it has ended.  Stores are coalesced along tokens; the allow words come
+//      from a wave ballot (64 tokens -> 2 words).
 #include "dv_internal.h"
 
 namespace dv {
 namespace {
 
+#ifndef DV_ALIGN_STATE_TILE
+#define DV_ALIGN_STATE_TILE 16
+#endif
+#ifndef DV_ALIGN_TOK_PER_LANE
+#define DV_ALIGN_TOK_PER_LANE 2
+#endif
+
 constexpr int kThreads = 256;
-constexpr int kTokPerLane = 4;
-constexpr int kTokTile = kThreads * kTokPerLane;  // 1024 tokens = 32 allow words
-constexpr int kStateTile = 32;
+constexpr int kTokPerLane = DV_ALIGN_TOK_PER_LANE;
+constexpr int kTokTile = kThreads * kTokPerLane;  // a multiple of 64 tokens = 2 allow words
+constexpr int kStateTile = DV_ALIGN_STATE_TILE;   // <= 32: pending states are a 32-bit set
+constexpr int kRegBytes = 8;                      // token bytes whose classes sit in registers
+constexpr int kRowsLds = kStateTile * 256 * 2;    // worst-case bytes of the row tile
+constexpr int kResLds = kStateTile * kTokTile * 2;
+constexpr int kWholeLdsMax = 64 * 1024;           // LDS budget for a whole table
+static_assert(kStateTile >= 1 && kStateTile <= 32, "pending set is 32 bits");
+constexpr int kLiveRows = kLiveRowsPerBlock;
 
 __device__ __forceinline__ bool in_range(int32_t v, int S) { return (uint32_t)v < (uint32_t)S; }
 
-// 1. per block of 64 rows: bit b set if some row has a live move on byte b.
+// 1. per block of rows: bit b set if some row has a live move on byte b.
 __global__ __launch_bounds__(kThreads) void live_columns_kernel(const int32_t *__restrict__ trans,
                                                                 int S, uint32_t *__restrict__ partial)
 {
     const int b = threadIdx.x;
-    const int r0 = blockIdx.x * kLiveRowsPerBlock;
-    const int r1 = min(S, r0 + kLiveRowsPerBlock);
+    const int r0 = blockIdx.x * kLiveRows;
+    const int r1 = min(S, r0 + kLiveRows);
     bool live = false;
+#pragma unroll 8
     for (int s = r0; s < r1; ++s)
         live |= in_range(trans[(size_t)s * 256 + b], S);
     const uint64_t m = __ballot(live);
@@ -49,12 +66,27 @@ __global__ __launch_bounds__(kThreads) void live_columns_kernel(const int32_t *_
 __global__ __launch_bounds__(kThreads) void byte_classes_kernel(const uint32_t *__restrict__ partial,
                                                                 int nblocks, uint8_t *__restrict__ ws)
 {
+    __shared__ uint32_t words[kThreads][9];
     __shared__ int wave_count[kThreads / kWave];
-    const int b = threadIdx.x;
-    uint32_t any = 0;
-    for (int k = 0; k < nblocks; ++k)
-        any |= partial[(size_t)k * 8 + b / 32];
-    const bool live = (any >> (b % 32)) & 1u;
+    const int tid = threadIdx.x;
+    uint32_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int k = tid; k < nblocks; k += kThreads)
+#pragma unroll
+        for (int w = 0; w < 8; ++w)
+            acc[w] |= partial[(size_t)k * 8 + w];
+#pragma unroll
+    for (int w = 0; w < 8; ++w)
+        words[tid][w] = acc[w];
+    __syncthreads();
+    for (int half = kThreads / 2; half > 0; half >>= 1) {
+        if (tid < half)
+#pragma unroll
+            for (int w = 0; w < 8; ++w)
+                words[tid][w] |= words[tid + half][w];
+        __syncthreads();
+    }
+    const int b = tid;
+    const bool live = (words[0][b / 32] >> (b % 32)) & 1u;
     const uint64_t m = __ballot(live);
     const int lane = b & (kWave - 1), wave = b / kWave;
     if (lane == 0)
@@ -92,6 +124,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const int32_t *__rest
     const int byte = c < C ? ws[512 + c] : 0;
     const int r0 = blockIdx.x * 16;
     const int r1 = min(S, r0 + 16);
+#pragma unroll 4
     for (int s = r0; s < r1; ++s) {
         uint16_t v = kDead16;
         if (c < C) {
@@ -102,84 +135,176 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const int32_t *__rest
     }
 }
 
-// 4. the walk.
-__global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restrict__ ws,
-                                                        const uint16_t *__restrict__ table, int S,
-                                                        const int32_t *__restrict__ offsets,
-                                                        const uint8_t *__restrict__ bytes, int V,
-                                                        int W, int32_t *__restrict__ next_state,
-                                                        uint32_t *__restrict__ allow)
+// 4. the walk.  One block owns a tile of kStateTile states x kTokTile tokens
+// (kTokPerLane tokens per lane, strided by the block size so stores are
+// coalesced).  Dynamic LDS holds the byte-class map, the table (the whole
+// table when S * Cp * 2 fits in `lds_table_bytes`, else the tile's rows) and
+// the tile's results (uint16, DEAD = 0xFFFF).
+//   phase 1: every pair's first move, lane-parallel, from LDS.  Walks that
+//            end there (dead, or one-byte tokens) are final; the others are
+//            marked pending in a per-token bit set over the tile's states.
+//   phase 2: each lane runs kTokPerLane independent streams (one per token),
+//            each taking its pending states one after the other and moving
+//            one byte per iteration.  A wave's iteration count is the
+//            longest stream's total number of later moves, not the sum over
+//            states of the longest single walk, so lanes stay busy; the
+//            streams give kTokPerLane independent table reads in flight.
+//   phase 3: the tile's results leave LDS as coalesced row stores, and a
+//            wave ballot packs the allow bits.
+template <bool WHOLE>
+__device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
+                                          const uint16_t *__restrict__ table, const uint8_t *cls,
+                                          int Cp, int s0, int nS, const uint8_t *__restrict__ bytes,
+                                          int t_base, int V, int W, const int32_t *__restrict__ offsets,
+                                          int32_t *__restrict__ next_state, uint32_t *__restrict__ allow)
 {
-    __shared__ uint16_t rows[kStateTile * 256];
-    __shared__ uint8_t cls[256];
-
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1), wave = tid / kWave;
-    const int Cp = reinterpret_cast<const int32_t *>(ws)[1];
-    const int s0 = blockIdx.y * kStateTile;
-    const int nS = min(kStateTile, S - s0);
-    const int t_base = blockIdx.x * kTokTile;
-
-    cls[tid] = ws[256 + tid];
-    for (int i = tid; i < nS * Cp; i += kThreads)
-        rows[i] = table[(size_t)s0 * Cp + i];
 
     int off[kTokPerLane], len[kTokPerLane];
+    uint32_t c03[kTokPerLane], c47[kTokPerLane];
 #pragma unroll
     for (int j = 0; j < kTokPerLane; ++j) {
         const int t = t_base + j * kThreads + tid;
+        off[j] = 0;
+        len[j] = -1;  // past the end: never stored, allow bit 0
         if (t < V) {
             off[j] = offsets[t];
             len[j] = offsets[t + 1] - off[j];
-        } else {
-            off[j] = 0;
-            len[j] = -1;  // past the end: not stored, allow bit 0
+        }
+        // byte classes of the first kRegBytes bytes, four per register
+        uint32_t lo = 0, hi = 0;
+        const int n = min(len[j], kRegBytes);
+        for (int h = 0; h < n; ++h) {
+            const uint32_t c = cls[bytes[off[j] + h]];
+            if (h < 4)
+                lo |= c << (8 * h);
+            else
+                hi |= c << (8 * (h - 4));
+        }
+        c03[j] = lo;
+        c47[j] = hi;
+    }
+
+    // phase 1: first moves
+    uint32_t pend[kTokPerLane];
+#pragma unroll
+    for (int j = 0; j < kTokPerLane; ++j)
+        pend[j] = 0;
+    for (int si = 0; si < nS; ++si) {
+        const int s = s0 + si;
+        const uint16_t *row = WHOLE ? tab + (uint32_t)s * Cp : tab + (uint32_t)si * Cp;
+#pragma unroll
+        for (int j = 0; j < kTokPerLane; ++j) {
+            const uint32_t c0 = c03[j] & 0xFFu;
+            const uint32_t v = row[c0 == kDeadClass ? 0u : c0];
+            uint32_t st = c0 == kDeadClass ? kDead16 : v;
+            if (len[j] <= 0)
+                st = len[j] == 0 ? (uint32_t)s : kDead16;  // an empty token keeps the state
+            res[si * kTokTile + j * kThreads + tid] = (uint16_t)st;
+            pend[j] |= (uint32_t)(st != kDead16 && len[j] > 1) << si;
+        }
+    }
+
+    // phase 2: later moves of the pending walks
+    uint32_t st[kTokPerLane], h[kTokPerLane], cur[kTokPerLane];
+    bool act[kTokPerLane];
+#pragma unroll
+    for (int j = 0; j < kTokPerLane; ++j) {
+        st[j] = kDead16;
+        h[j] = 0;
+        cur[j] = 0;
+        act[j] = false;
+    }
+    bool work = false;
+#pragma unroll
+    for (int j = 0; j < kTokPerLane; ++j)
+        work |= pend[j] != 0;
+    while (__any(work)) {
+        work = false;
+#pragma unroll
+        for (int j = 0; j < kTokPerLane; ++j) {
+            if (!act[j] && pend[j]) {
+                cur[j] = __builtin_ctz(pend[j]);
+                pend[j] &= pend[j] - 1u;
+                st[j] = res[cur[j] * kTokTile + j * kThreads + tid];
+                h[j] = 1;
+                act[j] = true;
+            }
+            if (act[j]) {
+                uint32_t c;
+                if (h[j] < (uint32_t)kRegBytes)
+                    c = ((h[j] < 4 ? c03[j] : c47[j]) >> (8 * (h[j] & 3))) & 0xFFu;
+                else
+                    c = cls[bytes[off[j] + h[j]]];
+                const uint32_t idx = c == kDeadClass ? 0u : st[j] * (uint32_t)Cp + c;
+                const uint32_t v = WHOLE ? tab[idx] : table[idx];
+                st[j] = c == kDeadClass ? kDead16 : v;
+                h[j] += 1;
+                if (st[j] == kDead16 || h[j] >= (uint32_t)len[j]) {
+                    res[cur[j] * kTokTile + j * kThreads + tid] = (uint16_t)st[j];
+                    act[j] = false;
+                }
+            }
+            work |= act[j] || pend[j] != 0;
         }
     }
     __syncthreads();
 
-    int c0[kTokPerLane];
-#pragma unroll
-    for (int j = 0; j < kTokPerLane; ++j)
-        c0[j] = len[j] > 0 ? cls[bytes[off[j]]] : kDeadClass;
-
+    // phase 3: coalesced stores and allow words
     for (int si = 0; si < nS; ++si) {
         const int s = s0 + si;
-        uint32_t st[kTokPerLane];
-#pragma unroll
-        for (int j = 0; j < kTokPerLane; ++j) {
-            if (len[j] > 0)
-                st[j] = c0[j] == kDeadClass ? kDead16 : rows[si * Cp + c0[j]];
-            else
-                st[j] = len[j] == 0 ? (uint32_t)s : kDead16;  // empty token keeps the state
-        }
-        for (int h = 1;; ++h) {
-            bool more = false;
-#pragma unroll
-            for (int j = 0; j < kTokPerLane; ++j) {
-                if (st[j] != kDead16 && h < len[j]) {
-                    const int c = cls[bytes[off[j] + h]];
-                    st[j] = c == kDeadClass ? kDead16 : table[(size_t)st[j] * Cp + c];
-                    more |= st[j] != kDead16 && h + 1 < len[j];
-                }
-            }
-            if (!__any(more))
-                break;
-        }
         int32_t *ns_row = next_state + (size_t)s * V;
         uint32_t *al_row = allow + (size_t)s * W;
 #pragma unroll
         for (int j = 0; j < kTokPerLane; ++j) {
             const int t = t_base + j * kThreads + tid;
-            const bool alive = len[j] >= 0 && st[j] != kDead16;
+            const uint32_t v = res[si * kTokTile + j * kThreads + tid];
+            const bool alive = len[j] >= 0 && v != kDead16;
             if (t < V)
-                ns_row[t] = alive ? (int32_t)st[j] : -1;
+                ns_row[t] = alive ? (int32_t)v : -1;
             const uint64_t m = __ballot(alive);
             const int w = (t_base + j * kThreads + wave * kWave) / 32 + lane;
             if (lane < 2 && w < W)
                 al_row[w] = (uint32_t)(m >> (32 * lane));
         }
     }
+}
+
+__global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restrict__ ws,
+                                                        const uint16_t *__restrict__ table, int S,
+                                                        const int32_t *__restrict__ offsets,
+                                                        const uint8_t *__restrict__ bytes, int V,
+                                                        int W, int lds_table_bytes,
+                                                        int32_t *__restrict__ next_state,
+                                                        uint32_t *__restrict__ allow)
+{
+    extern __shared__ __align__(16) uint8_t smem[];
+    uint8_t *cls = smem;
+    uint16_t *tab = reinterpret_cast<uint16_t *>(smem + 256);
+    uint16_t *res = reinterpret_cast<uint16_t *>(smem + 256 + lds_table_bytes);
+
+    const int tid = threadIdx.x;
+    const int Cp = reinterpret_cast<const int32_t *>(ws)[1];
+    const int s0 = blockIdx.y * kStateTile;
+    const int nS = min(kStateTile, S - s0);
+    const int t_base = blockIdx.x * kTokTile;
+    const bool whole = (size_t)S * Cp * 2 <= (size_t)lds_table_bytes;
+
+    cls[tid] = ws[256 + tid];
+    {
+        const int n32 = (whole ? S : nS) * Cp / 2;  // Cp is even
+        const uint32_t *src = reinterpret_cast<const uint32_t *>(whole ? table : table + (size_t)s0 * Cp);
+        uint32_t *dst = reinterpret_cast<uint32_t *>(tab);
+        for (int i = tid; i < n32; i += kThreads)
+            dst[i] = src[i];
+    }
+    __syncthreads();
+
+    if (whole)
+        walk_tile<true>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, offsets, next_state, allow);
+    else
+        walk_tile<false>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, offsets, next_state, allow);
 }
 
 }  // namespace
@@ -194,11 +319,32 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
     const int nblk = (int)align_live_blocks(S);
     const int W = (V + 31) / 32;
 
+    // LDS for the table.  The column count C is only known on the device, so
+    // for small S the launch reserves up to kWholeLdsMax bytes and the kernel
+    // stages the whole table when S * Cp * 2 fits; otherwise (and always for
+    // S > 512, where a whole table would leave too little LDS for occupancy)
+    // it stages only the block's row tile.
+    int lds_table = kRowsLds;
+    if (S <= 512) {
+        const size_t whole_worst = (size_t)S * 256 * 2;
+        lds_table = (int)(whole_worst < (size_t)kWholeLdsMax ? whole_worst : (size_t)kWholeLdsMax);
+        if (lds_table < kRowsLds)
+            lds_table = kRowsLds;
+    }
+
+    // LDS beyond the default 64 KB per block must be opted into once.
+    static const hipError_t lds_attr = hipFuncSetAttribute(
+        reinterpret_cast<const void *>(walk_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+        256 + kWholeLdsMax + kResLds);
+    if (lds_attr != hipSuccess)
+        return lds_attr;
+
     live_columns_kernel<<<nblk, kThreads, 0, stream>>>(trans, S, partial);
     byte_classes_kernel<<<1, kThreads, 0, stream>>>(partial, nblk, ws);
     compact_kernel<<<(S + 15) / 16, kThreads, 0, stream>>>(trans, S, ws, table);
     dim3 grid((V + kTokTile - 1) / kTokTile, (S + kStateTile - 1) / kStateTile);
-    walk_kernel<<<grid, kThreads, 0, stream>>>(ws, table, S, offsets, bytes, V, W, next_state, allow);
+    walk_kernel<<<grid, kThreads, 256 + lds_table + kResLds, stream>>>(ws, table, S, offsets, bytes, V, W,
+                                                                       lds_table, next_state, allow);
     return hipGetLastError();
 }
 

@@ -98,7 +98,7 @@ size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens)
 {
     if (batch < 0 || batch > DV_MAX_BATCH || num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
         return 0;
-    return dv::step_workspace_bytes(batch > 0 ? batch : 1);
+    return dv::step_workspace_bytes(batch, num_tokens);
 }
 
 dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow, int32_t num_states,
@@ -137,7 +137,7 @@ dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow, int32
         if (overlap(out, r_ns) || overlap(out, r_al) || overlap(out, r_st) || overlap(out, r_lg))
             return fail(DV_ERR_ALIAS, "dv_masked_step: an output overlaps an input "
                                       "(ping-pong two state buffers instead of updating in place)");
-    const size_t need = dv::step_workspace_bytes(batch);
+    const size_t need = dv::step_workspace_bytes(batch, num_tokens);
     if (!workspace || workspace_bytes < need)
         return fail(DV_ERR_WORKSPACE, "dv_masked_step: workspace of %zu bytes given, %zu needed",
                     workspace_bytes, need);

@@ -20,7 +20,7 @@ constexpr int kWave = 64;
 //   [1024, ...)   uint32 per-block live-column bit sets, 8 words per block
 //   [table, ...)  uint16 compacted table [S][Cp], DEAD = 0xFFFF
 constexpr int kAlignMetaBytes = 1024;
-constexpr int kLiveRowsPerBlock = 64;
+constexpr int kLiveRowsPerBlock = 16;
 constexpr uint16_t kDead16 = 0xFFFF;
 constexpr uint8_t kDeadClass = 0xFF;
 
@@ -36,11 +36,25 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
 
 // ------------------------------------------------------------- masked step
 //
-// Workspace of dv_masked_step: uint64 best key per row, then uint32 arrival
-// counter per row (at an offset rounded up to 256 bytes).  Both zero between
-// calls: the last block of each row resets them.
-inline size_t step_counter_offset(int B) { return align_up((size_t)B * sizeof(uint64_t), 256); }
-inline size_t step_workspace_bytes(int B) { return step_counter_offset(B) + align_up((size_t)B * 4, 256); }
+// A row of V logits is split into `nchunks` chunks of `chunk_vec` 16-byte
+// vectors, one block each.  With more than one chunk, each block writes its
+// best (key << 32 | ~index) to the workspace, [B][nchunks] uint64, and a
+// second kernel combines the chunks of each row.
+constexpr int kStepTargetBlocks = 2048;
+constexpr int kStepMaxChunks = 64;
+
+struct StepGeometry {
+    int chunk_vec;
+    int nchunks;
+};
+StepGeometry step_geometry(int B, int V, int dtype);
+
+inline size_t step_workspace_bytes(int B, int V)
+{
+    const StepGeometry a = step_geometry(B, V, 0), b = step_geometry(B, V, 1);
+    const int n = a.nchunks > b.nchunks ? a.nchunks : b.nchunks;
+    return align_up((size_t)(B > 0 ? B : 1) * (size_t)n * sizeof(uint64_t), 256);
+}
 
 hipError_t launch_masked_step(const int32_t *next_state, const uint32_t *allow, int S, int V,
                               const int32_t *states, const void *logits, int dtype, int B,

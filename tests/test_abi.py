@@ -21,14 +21,19 @@ GB = 1 << 30
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    return re.findall(r"^DV_API\s+[\w\s\*]+?\b(dv_\w+)\s*\(", text, flags=re.M)
+    names = []
+    for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        text = open(os.path.join(ROOT, "include", h)).read()
+        names += re.findall(r"^(?:DV_API|DVPROBE_API)\s+[\w\s\*]+?\b(dv\w+)\s*\(", text, flags=re.M)
+    return names
 
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert set(names) == {"dv_align_workspace_bytes", "dv_align", "dv_masked_step_workspace_bytes",
-                          "dv_masked_step", "dv_status_string", "dv_last_error", "dv_version"}
+    assert {"dv_align_workspace_bytes", "dv_align", "dv_masked_step_workspace_bytes",
+            "dv_masked_step", "dv_status_string", "dv_last_error", "dv_version",
+            "dvprobe_stream_read", "dvprobe_stream_write", "dvprobe_gather",
+            "dvprobe_lds_gather"} <= set(names)
     raw = ctypes.CDLL(dv.library_path)
     for n in names:
         assert hasattr(raw, n), n

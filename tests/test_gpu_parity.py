@@ -362,7 +362,6 @@ def test_step_workspace_reuse_and_determinism(dv):
         assert torch.equal(a[0], fresh[0]) and torch.equal(a[1], fresh[1])
         outs.append(a)
     torch.cuda.synchronize()
-    assert int(ws.count_nonzero()) == 0  # left zero-filled
 
 
 def test_step_rejects_in_place_update(dv):
