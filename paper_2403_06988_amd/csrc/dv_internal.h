@@ -37,15 +37,19 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
 // ------------------------------------------------------------- masked step
 //
 // A row of V logits is split into `nchunks` chunks of `chunk_vec` 16-byte
-// vectors, one block each.  With more than one chunk, each block writes its
-// best (key << 32 | ~index) to the workspace, [B][nchunks] uint64, and a
-// second kernel combines the chunks of each row.
+// vectors, one block of `threads` lanes each.  With more than one chunk,
+// each block writes its best (key << 32 | ~index) to the workspace,
+// [B][nchunks] uint64, and a second kernel combines the chunks of each row.
+// bf16 rows use 512-lane blocks and aim for kStepOneBlockRows blocks per
+// launch (one block per row once B >= 256).
 constexpr int kStepTargetBlocks = 2048;
 constexpr int kStepMaxChunks = 64;
+constexpr int kStepOneBlockRows = 256;
 
 struct StepGeometry {
     int chunk_vec;
     int nchunks;
+    int threads;
 };
 StepGeometry step_geometry(int B, int V, int dtype);
 

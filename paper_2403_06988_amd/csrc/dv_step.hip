@@ -4,33 +4,45 @@
 // The step reads B x V logits once: it is bound by HBM read bandwidth, so
 // the design is about keeping enough bytes in flight and spending few ALU
 // operations per element.
-//   * Rows are split into chunks so that a launch has ~2048 blocks (256 CUs
-//     need >> 256 blocks).  A block streams its chunk in batches: each lane
-//     issues kU = 8 independent 16-byte loads (plus the matching allow-mask
-//     words) before it touches any of them, so one CU keeps ~256 KB in
-//     flight.
-//   * bf16 rows use packed 16-bit arithmetic: per 32-bit word (two logits)
-//     one v_pk_ashrrev_i16 and two bit operations give order-preserving
-//     16-bit keys; each key is joined with its position in the lane's batch
-//     and masked by its allow bit, and one unsigned max per element finds
-//     the lane's best key with the lowest position.  The fast key differs
-//     from the exact ordering only for NaN (which must rank as -inf) and
-//     -0.0 (which must tie with +0.0); a lane whose batch maximum is one of
-//     those few key values recomputes that batch exactly from memory.
+//   * Launch shape (bf16).  A row is one 512-lane block once B >= 256
+//     (every CU gets at least one row), so no second pass is needed.  Each
+//     lane streams batches of 4 independent non-temporal 16-byte loads with
+//     a register double buffer: batch i + 1 is in flight while batch i is
+//     reduced.  Each batch loads its allow-mask
+//     bytes (one byte per 8 logits) right behind its logits.  Smaller
+//     batches split each row into chunks, one block each, and a tiny second
+//     kernel (one lane per row) combines the chunks -- no atomics and no
+//     device-wide fences in the streaming kernel (a release fence at device
+//     scope writes back and invalidates the XCD's L2 on gfx950).
+//   * bf16 arithmetic, two VALU operations per logit: per 32-bit word (two
+//     logits) one v_pk_ashrrev_i16 and one bit operation give
+//     order-preserving 16-bit keys, an AND with two 16-bit lane masks (from
+//     an LDS table indexed by the mask byte) drops the disallowed ones, and
+//     v_pk_max_u16 folds them.  One block-wide max per batch; only the
+//     wave(s) holding the maximum look up its lowest index.  The fast key
+//     differs from the exact ordering only for NaN (which must rank as -inf)
+//     and -0.0 (which must tie with +0.0); a batch whose maximum is one of
+//     those few key values is redone with exact keys.
+//   * fp32 rows (small workloads) use 256-lane blocks and exact keys with the
+//     index tracked per element.
 //   * Lanes combine (exact 32-bit key << 32 | ~index) as one 64-bit maximum:
-//     a larger key wins, on equal keys the smaller index wins.
-//   * The chunks of one row are combined by a second, tiny kernel (one lane
-//     per row) that also writes token / new_state: no atomics and no
-//     device-wide fences inside the streaming kernel.  (A per-block release
-//     fence at device scope writes back and invalidates the XCD's L2 on
-//     gfx950 -- thousands of those per step cost more than the step.)
+//     a larger key wins, on equal keys the smaller index wins.  The result
+//     does not depend on block or lane order, so the step is deterministic.
 #include "dv_internal.h"
 
 namespace dv {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kU = 8;  // 16-byte vectors per lane per batch
+constexpr int kSmallThreads = 256;  // split rows and fp32 rows
+constexpr int kSmallU = 8;          // 16-byte vectors per lane per batch
+#ifndef DV_STEP_BF16_THREADS
+#define DV_STEP_BF16_THREADS 512
+#endif
+#ifndef DV_STEP_BF16_U
+#define DV_STEP_BF16_U 4
+#endif
+constexpr int kBigThreads = DV_STEP_BF16_THREADS;  // lanes per bf16 block
+constexpr int kBigU = DV_STEP_BF16_U;              // vectors per lane per batch (x2: double-buffered)
 
 // Order-preserving key of an fp32 bit pattern under the step's value rules:
 // NaN ranks as -inf and -0.0 equals +0.0.  Every real value's key is
@@ -45,6 +57,11 @@ __device__ __forceinline__ uint32_t f32_key(uint32_t u)
 }
 
 typedef short s16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+#ifndef DV_STEP_NT_LOADS
+#define DV_STEP_NT_LOADS 1
+#endif
 
 // Fast 16-bit keys of the two bf16 values in w (flip all bits of negatives,
 // set the sign bit of non-negatives).  Exact except: -0.0 -> 0x7FFF (+0.0 ->
@@ -77,16 +94,17 @@ __device__ __forceinline__ uint64_t wave_max(uint64_t v)
     return v;
 }
 
+template <int THREADS>
 __device__ __forceinline__ uint64_t block_max(uint64_t v)
 {
-    __shared__ uint64_t red[kThreads / kWave];
+    __shared__ uint64_t red[THREADS / kWave];
     v = wave_max(v);
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     if (lane == 0)
         red[wave] = v;
     __syncthreads();
     if (threadIdx.x == 0) {
-        for (int w = 1; w < kThreads / kWave; ++w)
+        for (int w = 1; w < THREADS / kWave; ++w)
             v = red[w] > v ? red[w] : v;
     }
     return v;  // valid in thread 0
@@ -103,19 +121,18 @@ template <> struct Elt<0> {  // fp32
 };
 template <> struct Elt<1> {  // bf16: the high half of an fp32
     static constexpr int kVec = 8;
-    static constexpr int kBytes = 2;
     __device__ static uint32_t bits(const char *row, int64_t i)
     {
         return (uint32_t)reinterpret_cast<const uint16_t *>(row)[i] << 16;
     }
 };
 
-// Exact scan of elements [e0, e1) with lane stride kThreads.
-template <int DT>
+// Exact scan of elements [e0, e1) with lane stride THREADS.
+template <int DT, int THREADS>
 __device__ __forceinline__ void scan_exact(const char *row, const uint32_t *arow, int e0, int e1,
                                            uint32_t &best_key, int &best_idx)
 {
-    for (int t = e0 + (int)threadIdx.x; t < e1; t += kThreads) {
+    for (int t = e0 + (int)threadIdx.x; t < e1; t += THREADS) {
         if ((arow[t >> 5] >> (t & 31)) & 1u) {
             const uint32_t k = f32_key(Elt<DT>::bits(row, t));
             if (k > best_key) {
@@ -126,13 +143,16 @@ __device__ __forceinline__ void scan_exact(const char *row, const uint32_t *arow
     }
 }
 
-// Vector path over the full vectors [v0, v1) of a 16-byte aligned row.
-template <int DT>
+// Vector path over the full vectors [v0, v1) of a 16-byte aligned row; each
+// lane takes U vectors per batch, strided by THREADS so loads coalesce.
+template <int DT, int THREADS, int U>
 __device__ __forceinline__ void scan_vectors(const char *row, const uint32_t *arow, int v0, int v1,
                                              uint32_t &best_key, int &best_idx)
 {
     using E = Elt<DT>;
     constexpr int kVec = E::kVec;
+    constexpr int kU = U;
+    constexpr int kThreads = THREADS;
     const int tid = threadIdx.x;
     for (int vb = v0; vb < v1; vb += kThreads * kU) {
         uint4 d[kU];
@@ -149,7 +169,8 @@ __device__ __forceinline__ void scan_vectors(const char *row, const uint32_t *ar
             }
         }
         if constexpr (DT == 1) {
-            // fast packed keys: (key16 << 16 | 63 - position) masked by the allow bit
+            constexpr int kLast = kU * 8 - 1;  // positions 0..kLast in the lane's batch
+            // fast packed keys: (key16 << 16 | last - position) masked by the allow bit
             uint32_t bmax = 0, any = 0;
 #pragma unroll
             for (int u = 0; u < kU; ++u) {
@@ -159,8 +180,8 @@ __device__ __forceinline__ void scan_vectors(const char *row, const uint32_t *ar
                 for (int k = 0; k < 4; ++k) {
                     const uint32_t key = fast_key2(w[k]);
                     const int p = u * 8 + 2 * k;
-                    const uint32_t lo = ((key << 16) | (uint32_t)(63 - p)) & bit_mask(m[u], 2 * k);
-                    const uint32_t hi = ((key & 0xFFFF0000u) | (uint32_t)(62 - p)) & bit_mask(m[u], 2 * k + 1);
+                    const uint32_t lo = ((key << 16) | (uint32_t)(kLast - p)) & bit_mask(m[u], 2 * k);
+                    const uint32_t hi = ((key & 0xFFFF0000u) | (uint32_t)(kLast - 1 - p)) & bit_mask(m[u], 2 * k + 1);
                     bmax = max(bmax, max(lo, hi));
                 }
             }
@@ -168,7 +189,7 @@ __device__ __forceinline__ void scan_vectors(const char *row, const uint32_t *ar
                 const uint32_t k16 = bmax >> 16;
                 const bool special = k16 <= 0x007Fu || k16 == 0x7FFFu || k16 == 0x8000u || k16 > 0xFF80u;
                 if (!special) {
-                    const int p = 63 - (int)(bmax & 0xFFFFu);
+                    const int p = kLast - (int)(bmax & 0xFFFFu);
                     const int v = vb + (p >> 3) * kThreads + tid;
                     const uint32_t h = (k16 & 0x8000u) ? (k16 & 0x7FFFu) : (~k16 & 0xFFFFu);
                     const uint32_t key = f32_key(h << 16);
@@ -211,8 +232,8 @@ __device__ __forceinline__ void scan_vectors(const char *row, const uint32_t *ar
     }
 }
 
-template <int DT>
-__global__ __launch_bounds__(kThreads) void masked_step_kernel(
+template <int DT, int THREADS, int U>
+__global__ __launch_bounds__(THREADS) void masked_step_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
     const int32_t *__restrict__ states, const void *__restrict__ logits, int64_t ld, int chunk_vec,
     int nchunks, int32_t *__restrict__ token, int32_t *__restrict__ new_state,
@@ -234,14 +255,15 @@ __global__ __launch_bounds__(kThreads) void masked_step_kernel(
         const int e0 = c * chunk_vec * kVec;
         const int e1 = c == nchunks - 1 ? V : min(V, (c + 1) * chunk_vec * kVec);
         if ((reinterpret_cast<uintptr_t>(row) & 15) == 0) {
-            scan_vectors<DT>(row, arow, c * chunk_vec, min(nvec, (c + 1) * chunk_vec), best_key, best_idx);
+            scan_vectors<DT, THREADS, U>(row, arow, c * chunk_vec, min(nvec, (c + 1) * chunk_vec), best_key,
+                                         best_idx);
             if (c == nchunks - 1)
-                scan_exact<DT>(row, arow, nvec * kVec, V, best_key, best_idx);
+                scan_exact<DT, THREADS>(row, arow, nvec * kVec, V, best_key, best_idx);
         } else {
-            scan_exact<DT>(row, arow, e0, e1, best_key, best_idx);
+            scan_exact<DT, THREADS>(row, arow, e0, e1, best_key, best_idx);
         }
     }
-    const uint64_t best = block_max(pack(best_key, best_idx));
+    const uint64_t best = block_max<THREADS>(pack(best_key, best_idx));
     if (threadIdx.x != 0)
         return;
     if (nchunks > 1) {
@@ -249,19 +271,235 @@ __global__ __launch_bounds__(kThreads) void masked_step_kernel(
         return;
     }
     const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
-    token[b] = tok;
-    new_state[b] = tok >= 0 ? next_state[(size_t)s * V + tok] : -1;
+    const bool found = tok >= 0 && tok < V;  // always true for a found token; guards the read
+    token[b] = found ? tok : -1;
+    new_state[b] = found ? next_state[(size_t)s * V + tok] : -1;
+}
+
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t pk_max_u16(uint32_t a, uint32_t b)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u16x2, a),
+                                                                   __builtin_bit_cast(u16x2, b)));
+}
+
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v, bool is_max)
+{
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1) {
+        const uint32_t o = __shfl_xor(v, d);
+        v = is_max ? max(v, o) : min(v, o);
+    }
+    return v;  // in every lane of the wave
+}
+
+// bf16 rows, 16-byte aligned.  Per batch of U vectors per lane:
+//   pass 1: packed 16-bit fast keys, masked through an LDS table that turns
+//           a mask byte into four 32-bit lane masks, folded with
+//           v_pk_max_u16 -- two VALU operations per logit;
+//   wave:   one wave-wide max of (lane max << 1 | lane has an allowed
+//           element), by cross-lane shuffles (no barrier, so waves never
+//           wait for each other inside the stream);
+//   pass 2: only if the batch beats the wave's best so far: lanes holding
+//           the maximum find its first position in their registers, and a
+//           wave-wide min picks the lowest index.  A batch whose maximum is
+//           one of the inexact fast keys (NaN, -0.0 / +0.0) is redone with
+//           exact keys.
+// The waves' results meet in one block-wide maximum at the end.
+template <int THREADS, int U>
+__global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
+    const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
+    const int32_t *__restrict__ states, const void *__restrict__ logits, int64_t ld, int chunk_vec,
+    int nchunks, int32_t *__restrict__ token, int32_t *__restrict__ new_state,
+    uint64_t *__restrict__ partial)
+{
+    constexpr int kVec = 8;
+    constexpr int kStep = THREADS * U;  // vectors per batch
+    __shared__ uint4 lut[256];
+    const int tid = threadIdx.x;
+    const int b = blockIdx.x / nchunks;
+    const int c = blockIdx.x - b * nchunks;
+    const char *row = static_cast<const char *>(logits) + (size_t)b * (size_t)ld * 2;
+    const int nvec = V / kVec;
+    const int v0 = c * chunk_vec;
+    const int v1 = min(nvec, v0 + chunk_vec);
+    const bool vector_path = (reinterpret_cast<uintptr_t>(row) & 15) == 0 && v0 < v1;  // block-uniform
+
+    // mask byte -> two 16-bit lane masks per 32-bit word of logits
+    if (tid < 256) {
+        const uint32_t m = tid;
+        uint4 e;
+        e.x = ((m & 1u) ? 0x0000FFFFu : 0u) | ((m & 2u) ? 0xFFFF0000u : 0u);
+        e.y = ((m & 4u) ? 0x0000FFFFu : 0u) | ((m & 8u) ? 0xFFFF0000u : 0u);
+        e.z = ((m & 16u) ? 0x0000FFFFu : 0u) | ((m & 32u) ? 0xFFFF0000u : 0u);
+        e.w = ((m & 64u) ? 0x0000FFFFu : 0u) | ((m & 128u) ? 0xFFFF0000u : 0u);
+        lut[tid] = e;
+    }
+    __syncthreads();
+
+    // Loads are branch-free: a lane past the chunk reloads its last vector
+    // and its mask byte counts as 0 when the batch is reduced.  (A load under
+    // a branch makes the compiler wait for every outstanding load at the
+    // join, which would serialise the double buffer.)
+    auto load_batch = [&](uint4 (&d)[U], int vb) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int v = min(vb + u * THREADS + tid, v1 - 1);
+#if DV_STEP_NT_LOADS
+            // logits are read once: a non-temporal load keeps them from
+            // displacing reusable lines (mask rows, tables) in the caches
+            const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(row + (size_t)v * 16));
+            d[u] = make_uint4(x[0], x[1], x[2], x[3]);
+#else
+            d[u] = *reinterpret_cast<const uint4 *>(row + (size_t)v * 16);
+#endif
+        }
+    };
+    // The first batch of logits does not depend on the row's state: it is in
+    // flight before the state lookup returns.
+    uint4 da[U], db[U];
+    if (vector_path)
+        load_batch(da, v0);
+
+    const int s = states[b];
+    const bool live = (uint32_t)s < (uint32_t)S;  // block-uniform
+
+    uint32_t best_key = 0;  // exact key of the wave's best vector-path element, wave-uniform
+    int best_idx = 0;
+    uint32_t lane_key = 0;  // exact key of this lane's tail / misaligned elements
+    int lane_idx = 0;
+    if (live) {
+        const uint32_t *arow = allow + (size_t)s * W;
+        if (vector_path) {
+            // byte v of the allow row holds the mask bits of vector v (8 tokens)
+            const uint8_t *abytes = reinterpret_cast<const uint8_t *>(arow);
+            auto load_masks = [&](uint32_t (&m)[U], int vb) {
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    m[u] = abytes[min(vb + u * THREADS + tid, v1 - 1)];
+            };
+            // One batch: U vectors per lane.  Loads are issued a batch ahead
+            // (logits, then their mask bytes), so while batch i is reduced,
+            // batch i + 1 is in flight; the in-order load counter lets batch i
+            // be consumed without waiting for batch i + 1.
+            auto process_batch = [&](const uint4 (&d)[U], const uint32_t (&raw)[U], int vb) {
+                uint32_t mk[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    mk[u] = vb + u * THREADS + tid < v1 ? raw[u] : 0u;
+                uint32_t acc = 0, any = 0;
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const uint4 M = lut[mk[u]];
+                    any |= mk[u];
+                    acc = pk_max_u16(acc, fast_key2(d[u].x) & M.x);
+                    acc = pk_max_u16(acc, fast_key2(d[u].y) & M.y);
+                    acc = pk_max_u16(acc, fast_key2(d[u].z) & M.z);
+                    acc = pk_max_u16(acc, fast_key2(d[u].w) & M.w);
+                }
+                const uint32_t lane_max = max(acc & 0xFFFFu, acc >> 16);
+                const uint32_t top = wave_reduce_u32((lane_max << 1) | (any ? 1u : 0u), true);
+                const uint32_t k16 = top >> 1;
+                if (k16 == 0 && (top & 1u) == 0)
+                    return;  // nothing allowed in this batch
+                const bool special = k16 <= 0x007Fu || k16 == 0x7FFFu || k16 == 0x8000u || k16 > 0xFF80u;
+                if (!special) {
+                    const uint32_t h = (k16 & 0x8000u) ? (k16 & 0x7FFFu) : (~k16 & 0xFFFFu);
+                    const uint32_t key = f32_key(h << 16);
+                    if (key <= best_key)
+                        return;  // an earlier batch of this wave (lower indices) is at least as good
+                    // first allowed element whose bits are h (for a non-special
+                    // key, equal keys means equal bf16 bit patterns)
+                    int pos = 0x7FFFFFFF;
+                    if (lane_max == k16) {
+#pragma unroll
+                        for (int u = U - 1; u >= 0; --u) {
+                            const uint32_t w[4] = {d[u].x, d[u].y, d[u].z, d[u].w};
+                            const int v = vb + u * THREADS + tid;
+#pragma unroll
+                            for (int k = 3; k >= 0; --k) {
+                                if ((w[k] >> 16) == h && ((mk[u] >> (2 * k + 1)) & 1u))
+                                    pos = v * kVec + 2 * k + 1;
+                                if ((w[k] & 0xFFFFu) == h && ((mk[u] >> (2 * k)) & 1u))
+                                    pos = v * kVec + 2 * k;
+                            }
+                        }
+                    }
+                    best_idx = (int)wave_reduce_u32((uint32_t)pos, false);
+                    best_key = key;
+                } else {
+                    // exact keys for this batch (NaN or a signed zero at the top),
+                    // re-read from memory: a rare path, kept out of the registers
+                    uint32_t bk = 0;
+                    int bi = 0;
+#pragma unroll 1
+                    for (int u = 0; u < U; ++u) {
+                        const int v = vb + u * THREADS + tid;
+                        const uint32_t mb = v < v1 ? abytes[v] : 0u;
+#pragma unroll 1
+                        for (int e = 0; e < kVec; ++e) {
+                            if ((mb >> e) & 1u) {
+                                const uint32_t key = f32_key(Elt<1>::bits(row, (int64_t)v * kVec + e));
+                                if (key > bk) {
+                                    bk = key;
+                                    bi = v * kVec + e;
+                                }
+                            }
+                        }
+                    }
+                    const uint32_t kmax = wave_reduce_u32(bk, true);
+                    if (kmax > best_key) {
+                        best_idx = (int)wave_reduce_u32(bk == kmax ? (uint32_t)bi : 0x7FFFFFFFu, false);
+                        best_key = kmax;
+                    }
+                }
+            };
+            // The next batch's loads are issued unconditionally (past the chunk
+            // they are harmless reloads, masked out when reduced).
+            uint32_t ma[U], mb[U];
+            load_masks(ma, v0);
+            for (int vb = v0; vb < v1; vb += 2 * kStep) {
+                load_batch(db, vb + kStep);
+                load_masks(mb, vb + kStep);
+                process_batch(da, ma, vb);
+                load_batch(da, vb + 2 * kStep);
+                load_masks(ma, vb + 2 * kStep);
+                if (vb + kStep < v1)  // block-uniform
+                    process_batch(db, mb, vb + kStep);
+            }
+            if (c == nchunks - 1)
+                scan_exact<1, THREADS>(row, arow, nvec * kVec, V, lane_key, lane_idx);
+        } else {
+            const int e1 = c == nchunks - 1 ? V : min(V, (c + 1) * chunk_vec * kVec);
+            scan_exact<1, THREADS>(row, arow, v0 * kVec, e1, lane_key, lane_idx);
+        }
+    }
+    uint64_t mine = pack(lane_key, lane_idx);
+    const uint64_t vec_best = pack(best_key, best_idx);
+    mine = vec_best > mine ? vec_best : mine;
+    const uint64_t best = block_max<THREADS>(mine);
+    if (threadIdx.x != 0)
+        return;
+    if (nchunks > 1) {
+        partial[blockIdx.x] = best;
+        return;
+    }
+    const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
+    const bool found = tok >= 0 && tok < V;  // always true for a found token; guards the read
+    token[b] = found ? tok : -1;
+    new_state[b] = found ? next_state[(size_t)s * V + tok] : -1;
 }
 
 // One lane per row: combine the row's chunk results and write the outputs.
-__global__ __launch_bounds__(kThreads) void finalize_kernel(const int32_t *__restrict__ next_state, int S,
+__global__ __launch_bounds__(kSmallThreads) void finalize_kernel(const int32_t *__restrict__ next_state, int S,
                                                            int V, const int32_t *__restrict__ states,
                                                            int B, int nchunks,
                                                            const uint64_t *__restrict__ partial,
                                                            int32_t *__restrict__ token,
                                                            int32_t *__restrict__ new_state)
 {
-    const int b = blockIdx.x * kThreads + threadIdx.x;
+    const int b = blockIdx.x * kSmallThreads + threadIdx.x;
     if (b >= B)
         return;
     uint64_t best = 0;
@@ -271,8 +509,9 @@ __global__ __launch_bounds__(kThreads) void finalize_kernel(const int32_t *__res
     }
     const int s = states[b];
     const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
-    token[b] = tok;
-    new_state[b] = (tok >= 0 && (uint32_t)s < (uint32_t)S) ? next_state[(size_t)s * V + tok] : -1;
+    const bool found = tok >= 0 && tok < V && (uint32_t)s < (uint32_t)S;  // guards the read
+    token[b] = found ? tok : -1;
+    new_state[b] = found ? next_state[(size_t)s * V + tok] : -1;
 }
 
 }  // namespace
@@ -280,21 +519,24 @@ __global__ __launch_bounds__(kThreads) void finalize_kernel(const int32_t *__res
 StepGeometry step_geometry(int B, int V, int dtype)
 {
     const int vec = dtype == 0 ? Elt<0>::kVec : Elt<1>::kVec;
+    const bool bf16 = dtype == 1;
+    const int threads = bf16 ? kBigThreads : kSmallThreads;
+    const int target = bf16 ? kStepOneBlockRows : kStepTargetBlocks;
     const int nvec = V / vec;
-    const int per_block = kThreads;  // at least one vector per lane
-    int want = (kStepTargetBlocks + B - 1) / (B > 0 ? B : 1);
-    const int max_chunks = (nvec + per_block - 1) / per_block;
-    want = want < 1 ? 1 : want;
-    want = want > max_chunks ? (max_chunks > 0 ? max_chunks : 1) : want;
+    // about `target` blocks, at least one vector per lane per chunk
+    const int max_chunks = (nvec + threads - 1) / threads;
+    int want = (target + B - 1) / (B > 0 ? B : 1);
+    want = want > max_chunks ? max_chunks : want;
     want = want > kStepMaxChunks ? kStepMaxChunks : want;
-    int chunk_vec = (nvec + want - 1) / want;
-    chunk_vec = (chunk_vec + per_block - 1) / per_block * per_block;
+    int nchunks = want < 1 ? 1 : want;
+    int chunk_vec = (nvec + nchunks - 1) / nchunks;
+    chunk_vec = (chunk_vec + threads - 1) / threads * threads;
     if (chunk_vec == 0)
-        chunk_vec = per_block;
-    int nchunks = (nvec + chunk_vec - 1) / chunk_vec;
+        chunk_vec = threads;
+    nchunks = (nvec + chunk_vec - 1) / chunk_vec;
     if (nchunks < 1)
         nchunks = 1;
-    return {chunk_vec, nchunks};
+    return {chunk_vec, nchunks, threads};
 }
 
 hipError_t launch_masked_step(const int32_t *next_state, const uint32_t *allow, int S, int V,
@@ -307,17 +549,14 @@ hipError_t launch_masked_step(const int32_t *next_state, const uint32_t *allow, 
     uint64_t *partial = static_cast<uint64_t *>(workspace);
     const unsigned grid = (unsigned)B * (unsigned)g.nchunks;
     if (dtype == 0)
-        masked_step_kernel<0><<<grid, kThreads, 0, stream>>>(next_state, allow, S, V, W, states, logits, ld,
-                                                             g.chunk_vec, g.nchunks, token, new_state,
-                                                             partial);
+        masked_step_kernel<0, kSmallThreads, kSmallU><<<grid, kSmallThreads, 0, stream>>>(
+            next_state, allow, S, V, W, states, logits, ld, g.chunk_vec, g.nchunks, token, new_state, partial);
     else
-        masked_step_kernel<1><<<grid, kThreads, 0, stream>>>(next_state, allow, S, V, W, states, logits, ld,
-                                                             g.chunk_vec, g.nchunks, token, new_state,
-                                                             partial);
+        masked_step_bf16_kernel<kBigThreads, kBigU><<<grid, kBigThreads, 0, stream>>>(
+            next_state, allow, S, V, W, states, logits, ld, g.chunk_vec, g.nchunks, token, new_state, partial);
     if (g.nchunks > 1)
-        finalize_kernel<<<(B + kThreads - 1) / kThreads, kThreads, 0, stream>>>(next_state, S, V, states, B,
-                                                                              g.nchunks, partial, token,
-                                                                              new_state);
+        finalize_kernel<<<(B + kSmallThreads - 1) / kSmallThreads, kSmallThreads, 0, stream>>>(
+            next_state, S, V, states, B, g.nchunks, partial, token, new_state);
     return hipGetLastError();
 }
 
