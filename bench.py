@@ -13,7 +13,8 @@ Reported (one JSON line):
   ms_per_step  wall time of one whole job (align + all decode steps)
   roofline     the dominant kernel (the masked step) against HBM bandwidth:
                algorithmic bytes per launch / mean launch time (HIP events
-               around every launch on the launch stream)
+               around the replay of the job's decode steps, captured once as
+               a HIP graph, on the launch stream; divided by the step count)
   roofline_align  dv_align against the HBM write roofline (4.125 B / pair)
   cpu_baseline the CPU oracle on a bounded sample of the same workload
 
@@ -227,49 +228,69 @@ def main():
     torch.cuda.synchronize()
     log("inputs resident in HBM")
 
-    def job(events=None):
-        if events is not None:
-            events["align"][0].record(stream)
-        dv.align(trans_d, offsets_d, data_d, next_state=ns, allow=al, workspace=ws_align,
-                 stream=stream)
-        if events is not None:
-            events["align"][1].record(stream)
-        states_all[0].copy_(init_d)
+    def decode_launches():
         for k in range(w.steps):
-            if events is not None:
-                events["step"][k][0].record(stream)
             dv.masked_step(ns, al, states_all[k], x[k], token=tokens_all[k],
-                           new_state=states_all[k + 1], workspace=ws_step, stream=stream)
-            if events is not None:
-                events["step"][k][1].record(stream)
+                           new_state=states_all[k + 1], workspace=ws_step)
 
+    def align_launch():
+        dv.align(trans_d, offsets_d, data_d, next_state=ns, allow=al, workspace=ws_align)
+
+    # Eager warm-up (also the reference the graph replays are checked against).
     for _ in range(args.warmup):
-        job()
+        align_launch()
+        states_all[0].copy_(init_d)
+        decode_launches()
     torch.cuda.synchronize()
+    eager_tokens = tokens_all.clone()
+    eager_states = states_all.clone()
+
+    # The per-token decode loop is launch-bound from Python (a ctypes call per
+    # step costs more host time than the kernel takes), so it is captured once
+    # in a HIP graph and replayed, as a serving loop would run it.
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(side):
+        states_all[0].copy_(init_d)
+        decode_launches()
+    torch.cuda.current_stream(dev).wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        decode_launches()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
 
     def mk():
         return torch.cuda.Event(enable_timing=True)
 
-    ev = [{"align": (mk(), mk()), "step": [(mk(), mk()) for _ in range(w.steps)]}
-          for _ in range(args.steps)]
+    ev = [(mk(), mk(), mk(), mk()) for _ in range(args.steps)]
+    graph_ok = True
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for j in range(args.steps):
-        job(ev[j])
+        a0, a1, d0, d1 = ev[j]
+        a0.record(stream)
+        align_launch()
+        a1.record(stream)
+        states_all[0].copy_(init_d)
+        d0.record(stream)
+        graph.replay()
+        d1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    graph_ok = bool(torch.equal(tokens_all, eager_tokens) and torch.equal(states_all, eager_states))
 
-    align_ms = [e["align"][0].elapsed_time(e["align"][1]) for e in ev]
-    step_ms = [s.elapsed_time(t) for e in ev for (s, t) in e["step"]]
-    decode_ms_per_job = [sum(s.elapsed_time(t) for (s, t) in e["step"]) for e in ev]
+    align_ms = [a0.elapsed_time(a1) for (a0, a1, _, _) in ev]
+    decode_ms = [d0.elapsed_time(d1) for (_, _, d0, d1) in ev]
     live_per_step = (states_all[:-1] >= 0).sum(dim=1).cpu().numpy()
     dead_final = int((states_all[-1] < 0).sum())
 
     pairs = w.S * w.V
     align_s = float(np.mean(align_ms)) / 1e3
-    dec_s = float(np.mean(decode_ms_per_job)) / 1e3
+    dec_s = float(np.mean(decode_ms)) / 1e3
     bytes_per_launch = float(np.mean([step_bytes(w, int(n), w.B) for n in live_per_step]))
-    mean_launch_s = float(np.mean(step_ms)) / 1e3
+    mean_launch_s = dec_s / w.steps
     achieved = bytes_per_launch / mean_launch_s / 1e9
     align_bytes = pairs * 4.125
     align_achieved = align_bytes / align_s / 1e9
@@ -291,15 +312,18 @@ def main():
                    "decode_steps_per_job": w.steps, "logits_dtype": w.dtype},
         "align": {"value": pairs / align_s, "unit": "alignments/s", "ms": align_s * 1e3},
         "decode": {"us_per_step_mean": mean_launch_s * 1e6,
-                   "us_per_step_min": float(np.min(step_ms)) * 1e3,
+                   "us_per_job_min": float(np.min(decode_ms)) * 1e3,
+                   "launch": "HIP graph of the job's decode steps, replayed",
+                   "graph_matches_eager": graph_ok,
                    "rows_steps_per_s": w.B * w.steps / dec_s,
                    "live_rows_first_last": [int(live_per_step[0]), int(live_per_step[-1])],
                    "dead_rows_at_end": dead_final},
-        "roofline": {"kernel": "masked_step_kernel", "bound": "hbm", "achieved": achieved,
+        "roofline": {"kernel": "masked_step_bf16_kernel" if w.dtype == "bf16" else "masked_step_kernel",
+                     "bound": "hbm", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "bytes_per_launch": bytes_per_launch,
                      "traffic": traffic_record("masked_step_traffic")},
-        "roofline_align": {"kernel": "dv_align (4 kernels)", "bound": "hbm",
+        "roofline_align": {"kernel": "dv_align (walk_kernel + 3 small prep kernels)", "bound": "hbm",
                            "achieved": align_achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                            "frac": align_achieved / HBM_PEAK_GBS, "bytes_per_launch": align_bytes,
                            "traffic": traffic_record("align_walk_traffic")},

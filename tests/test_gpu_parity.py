@@ -371,3 +371,42 @@ def test_step_rejects_in_place_update(dv):
     with pytest.raises(dv.DvError) as e:
         dv.masked_step(ns, al, st, torch.zeros((4, 10), device=DEV), new_state=st)
     assert e.value.status == 4
+
+
+@pytest.mark.parametrize("wid", [2, 3, 4])
+def test_step_graph_replay_matches_eager(dv, wid):
+    """The decode loop captured as a HIP graph (as the benchmark runs it) gives
+    the eager results on every replay, with eager work in between."""
+    w = W.WORKLOADS[wid]
+    trans, offsets, data, ns, al = _workload_table(dv, wid)
+    steps = 16
+    x = W.logits_all(wid, device=DEV, steps=steps)
+    ws = dv.step_workspace(w.B, w.V, DEV)
+    init = _dev(W.init_states(wid))
+    st = torch.empty((steps + 1, w.B), dtype=torch.int32, device=DEV)
+    tk = torch.empty((steps, w.B), dtype=torch.int32, device=DEV)
+
+    def launches():
+        for k in range(steps):
+            dv.masked_step(ns, al, st[k], x[k], token=tk[k], new_state=st[k + 1], workspace=ws)
+
+    st[0].copy_(init)
+    launches()
+    torch.cuda.synchronize()
+    ref_t, ref_s = tk.clone(), st.clone()
+    side = torch.cuda.Stream(DEV)
+    side.wait_stream(torch.cuda.current_stream(DEV))
+    with torch.cuda.stream(side):
+        launches()
+    torch.cuda.current_stream(DEV).wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        launches()
+    for rep in range(3):
+        tk.fill_(-7)
+        st[1:].fill_(-7)
+        _ = (x[0].float().sum() + rep).item()  # eager work and a sync between replays
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(tk, ref_t) and torch.equal(st, ref_s), f"replay {rep}"
