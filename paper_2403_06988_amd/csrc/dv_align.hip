@@ -9,7 +9,8 @@
 //   3. compact: uint16 table [S][Cp] over the live columns only (DEAD = 0xFFFF).
 //      Random printable-ASCII DFAs keep ~95 of 256 columns, so the table is
 //      ~2.7x smaller than the int32 input and stays resident in each XCD's L2.
-//   4. walk: one lane per (state, token) pair.  A block owns a tile of 32
+//   4. token_info: each token's first 8 byte classes, length and offset.
+//   5. walk: one lane per (state, token) pair.  A block owns a tile of 32
 //      states x 1024 tokens (4 tokens per lane).  The byte classes of each
 //      token's first 8 bytes are looked up once per block and kept in
 //      registers, so a move costs one table read.  The table lives in LDS:
@@ -135,7 +136,35 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const int32_t *__rest
     }
 }
 
-// 4. the walk.  One block owns a tile of kStateTile states x kTokTile tokens
+// 4. per token: the classes of its first kRegBytes bytes (four per word),
+// its length and offset -- read once per block by the walk instead of
+// re-deriving them from the bytes in every block.
+__global__ __launch_bounds__(kThreads) void token_info_kernel(const int32_t *__restrict__ offsets,
+                                                              const uint8_t *__restrict__ bytes, int V,
+                                                              const uint8_t *__restrict__ ws,
+                                                              uint4 *__restrict__ tokinfo)
+{
+    __shared__ uint8_t cls[256];
+    cls[threadIdx.x] = ws[256 + threadIdx.x];
+    __syncthreads();
+    const int t = blockIdx.x * kThreads + threadIdx.x;
+    if (t >= V)
+        return;
+    const int off = offsets[t];
+    const int len = offsets[t + 1] - off;
+    uint32_t lo = 0, hi = 0;
+    const int n = min(len, kRegBytes);
+    for (int h = 0; h < n; ++h) {
+        const uint32_t c = cls[bytes[off + h]];
+        if (h < 4)
+            lo |= c << (8 * h);
+        else
+            hi |= c << (8 * (h - 4));
+    }
+    tokinfo[t] = make_uint4(lo, hi, (uint32_t)len, (uint32_t)off);
+}
+
+// 5. the walk.  One block owns a tile of kStateTile states x kTokTile tokens
 // (kTokPerLane tokens per lane, strided by the block size so stores are
 // coalesced).  Dynamic LDS holds the byte-class map, the table (the whole
 // table when S * Cp * 2 fits in `lds_table_bytes`, else the tile's rows) and
@@ -155,7 +184,7 @@ template <bool WHOLE>
 __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
                                           const uint16_t *__restrict__ table, const uint8_t *cls,
                                           int Cp, int s0, int nS, const uint8_t *__restrict__ bytes,
-                                          int t_base, int V, int W, const int32_t *__restrict__ offsets,
+                                          int t_base, int V, int W, const uint4 *__restrict__ tokinfo,
                                           int32_t *__restrict__ next_state, uint32_t *__restrict__ allow)
 {
     const int tid = threadIdx.x;
@@ -166,24 +195,11 @@ __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
 #pragma unroll
     for (int j = 0; j < kTokPerLane; ++j) {
         const int t = t_base + j * kThreads + tid;
-        off[j] = 0;
-        len[j] = -1;  // past the end: never stored, allow bit 0
-        if (t < V) {
-            off[j] = offsets[t];
-            len[j] = offsets[t + 1] - off[j];
-        }
-        // byte classes of the first kRegBytes bytes, four per register
-        uint32_t lo = 0, hi = 0;
-        const int n = min(len[j], kRegBytes);
-        for (int h = 0; h < n; ++h) {
-            const uint32_t c = cls[bytes[off[j] + h]];
-            if (h < 4)
-                lo |= c << (8 * h);
-            else
-                hi |= c << (8 * (h - 4));
-        }
-        c03[j] = lo;
-        c47[j] = hi;
+        const uint4 ti = t < V ? tokinfo[t] : make_uint4(0, 0, 0xFFFFFFFFu, 0);
+        c03[j] = ti.x;
+        c47[j] = ti.y;
+        len[j] = (int)ti.z;  // -1 past the end: never stored, allow bit 0
+        off[j] = (int)ti.w;
     }
 
     // phase 1: first moves
@@ -273,7 +289,7 @@ __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
 
 __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restrict__ ws,
                                                         const uint16_t *__restrict__ table, int S,
-                                                        const int32_t *__restrict__ offsets,
+                                                        const uint4 *__restrict__ tokinfo,
                                                         const uint8_t *__restrict__ bytes, int V,
                                                         int W, int lds_table_bytes,
                                                         int32_t *__restrict__ next_state,
@@ -302,9 +318,9 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
     __syncthreads();
 
     if (whole)
-        walk_tile<true>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, offsets, next_state, allow);
+        walk_tile<true>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, next_state, allow);
     else
-        walk_tile<false>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, offsets, next_state, allow);
+        walk_tile<false>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, next_state, allow);
 }
 
 }  // namespace
@@ -316,6 +332,7 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
     uint8_t *ws = static_cast<uint8_t *>(workspace);
     uint32_t *partial = reinterpret_cast<uint32_t *>(ws + kAlignMetaBytes);
     uint16_t *table = reinterpret_cast<uint16_t *>(ws + align_table_offset(S));
+    uint4 *tokinfo = reinterpret_cast<uint4 *>(ws + align_tokinfo_offset(S));
     const int nblk = (int)align_live_blocks(S);
     const int W = (V + 31) / 32;
 
@@ -342,8 +359,9 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
     live_columns_kernel<<<nblk, kThreads, 0, stream>>>(trans, S, partial);
     byte_classes_kernel<<<1, kThreads, 0, stream>>>(partial, nblk, ws);
     compact_kernel<<<(S + 15) / 16, kThreads, 0, stream>>>(trans, S, ws, table);
+    token_info_kernel<<<(V + kThreads - 1) / kThreads, kThreads, 0, stream>>>(offsets, bytes, V, ws, tokinfo);
     dim3 grid((V + kTokTile - 1) / kTokTile, (S + kStateTile - 1) / kStateTile);
-    walk_kernel<<<grid, kThreads, 256 + lds_table + kResLds, stream>>>(ws, table, S, offsets, bytes, V, W,
+    walk_kernel<<<grid, kThreads, 256 + lds_table + kResLds, stream>>>(ws, table, S, tokinfo, bytes, V, W,
                                                                        lds_table, next_state, allow);
     return hipGetLastError();
 }

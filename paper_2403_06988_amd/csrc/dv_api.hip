@@ -60,7 +60,7 @@ size_t dv_align_workspace_bytes(int32_t num_states, int32_t num_tokens)
 {
     if (num_states < 1 || num_states > DV_MAX_STATES || num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
         return 0;
-    return dv::align_workspace_bytes(num_states);
+    return dv::align_workspace_bytes(num_states, num_tokens);
 }
 
 dv_status dv_align(const int32_t *trans, int32_t num_states, const int32_t *offsets,
@@ -80,7 +80,7 @@ dv_status dv_align(const int32_t *trans, int32_t num_states, const int32_t *offs
     if (overlap(r_ns, r_al) || overlap(r_ns, r_tr) || overlap(r_ns, r_off) || overlap(r_al, r_tr) ||
         overlap(r_al, r_off))
         return fail(DV_ERR_ALIAS, "dv_align: next_state / allow overlap each other or an input");
-    const size_t need = dv::align_workspace_bytes(num_states);
+    const size_t need = dv::align_workspace_bytes(num_states, num_tokens);
     if (!workspace || workspace_bytes < need)
         return fail(DV_ERR_WORKSPACE, "dv_align: workspace of %zu bytes given, %zu needed", workspace_bytes, need);
     if (reinterpret_cast<uintptr_t>(workspace) & 255)

@@ -19,6 +19,7 @@ constexpr int kWave = 64;
 //   [512, 768)    uint8  byte of each class
 //   [1024, ...)   uint32 per-block live-column bit sets, 8 words per block
 //   [table, ...)  uint16 compacted table [S][Cp], DEAD = 0xFFFF
+//   [tokinfo, ...) uint4 per token: classes of bytes 0-3, 4-7, length, offset
 constexpr int kAlignMetaBytes = 1024;
 constexpr int kLiveRowsPerBlock = 16;
 constexpr uint16_t kDead16 = 0xFFFF;
@@ -28,7 +29,9 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 inline size_t align_live_blocks(int S) { return (size_t)(S + kLiveRowsPerBlock - 1) / kLiveRowsPerBlock; }
 inline size_t align_table_offset(int S) { return align_up(kAlignMetaBytes + align_live_blocks(S) * 32, 256); }
-inline size_t align_workspace_bytes(int S) { return align_table_offset(S) + (size_t)S * 256 * sizeof(uint16_t); }
+inline size_t align_tokinfo_offset(int S) { return align_up(align_table_offset(S) + (size_t)S * 256 * sizeof(uint16_t), 256); }
+// per token: byte classes of its first 8 bytes (4 per word), its length, its offset
+inline size_t align_workspace_bytes(int S, int V) { return align_tokinfo_offset(S) + (size_t)V * 16; }
 
 hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, const uint8_t *bytes,
                         int V, int32_t *next_state, uint32_t *allow, void *workspace,
