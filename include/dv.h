@@ -68,9 +68,10 @@ typedef enum dv_dtype {
 } dv_dtype;
 
 /*
- * dv_align_workspace_bytes -- device workspace dv_align needs for a DFA with
- * `num_states` states (the compacted transition table and the byte-class
- * map).  Returns 0 when a size is outside its limit.
+ * dv_align_workspace_bytes -- device workspace dv_align / dv_align_eos need
+ * for `num_states` states and `num_tokens` tokens (the compacted transition
+ * table, the byte-class map and per-token byte classes).  Returns 0 when a
+ * size is outside its limit.
  */
 DV_API size_t dv_align_workspace_bytes(int32_t num_states, int32_t num_tokens);
 
@@ -107,6 +108,32 @@ DV_API dv_status dv_align(const int32_t *trans, int32_t num_states,
                    const int32_t *offsets, const uint8_t *bytes, int32_t num_tokens,
                    int32_t *next_state, uint32_t *allow,
                    void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * dv_align_eos -- dv_align with an end-of-sequence token (Algorithm 1 stops
+ * on EOS; Sec. 3.2 treats EOS as one more terminal of the scanner, so it may
+ * follow wherever a terminal sequence may end).
+ *
+ * Every token except `eos_token` is aligned exactly as by dv_align.  For the
+ * EOS column (its bytes are ignored):
+ *     next_state[s*V + eos_token] = s        if accepting[s] != 0,
+ *                                   DV_DEAD  otherwise,
+ * with the allow bit set exactly when it is not DV_DEAD, so the masked step
+ * can choose EOS only where the constraint may end; the state is left
+ * unchanged and the caller stops decoding the sequence.
+ *
+ * accepting  [S] uint8 (device), nonzero for states where the constraint may
+ *            end (accepting states; the start state if the empty output is
+ *            valid).  NULL means no state accepts: EOS is never allowed.
+ * eos_token  in [0, V).
+ * Workspace, outputs and errors as dv_align (DV_ERR_SHAPE also for an
+ * eos_token outside [0, V)).
+ */
+DV_API dv_status dv_align_eos(const int32_t *trans, int32_t num_states,
+                       const int32_t *offsets, const uint8_t *bytes, int32_t num_tokens,
+                       const uint8_t *accepting, int32_t eos_token,
+                       int32_t *next_state, uint32_t *allow,
+                       void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * dv_masked_step_workspace_bytes -- device workspace dv_masked_step needs for

@@ -57,6 +57,10 @@ def _bind(lib):
     lib.oracle_align_rows.restype = None
     lib.oracle_align_rows.argtypes = [_i32p, ctypes.c_int32, _i32p, _u8p, ctypes.c_int32,
                                       _i32p, ctypes.c_int64, _i32p, _u32p]
+    lib.oracle_align_rows_eos.restype = None
+    lib.oracle_align_rows_eos.argtypes = [_i32p, ctypes.c_int32, _i32p, _u8p, ctypes.c_int32,
+                                          ctypes.c_void_p, ctypes.c_int32, _i32p, ctypes.c_int64,
+                                          _i32p, _u32p]
     lib.oracle_align.restype = None
     lib.oracle_align.argtypes = [_i32p, ctypes.c_int32, _i32p, _u8p, ctypes.c_int32, _i32p, _u32p]
     lib.oracle_masked_argmax.restype = ctypes.c_int32
@@ -114,6 +118,25 @@ def align_rows(trans, offsets, tok_bytes, rows, lib=None):
     lib.oracle_align_rows(_p(trans, _i32p), trans.shape[0], _p(offsets, _i32p),
                           _p(tok_bytes, _u8p), V, _p(rows, _i32p), rows.shape[0],
                           _p(ns, _i32p), _p(al, _u32p))
+    return ns, al
+
+
+def align_eos(trans, offsets, tok_bytes, accepting, eos_token: int, rows=None, lib=None):
+    """Table rows with an end-of-sequence token: EOS is allowed exactly in the
+    states flagged in ``accepting`` (None: no state) and keeps the state."""
+    lib = lib or load()
+    trans = _c(trans, np.int32)
+    offsets = _c(offsets, np.int32)
+    tok_bytes = _c(tok_bytes if len(tok_bytes) else np.zeros(1, np.uint8), np.uint8)
+    S = trans.shape[0]
+    rows = np.arange(S, dtype=np.int32) if rows is None else _c(rows, np.int32)
+    acc = None if accepting is None else _c(accepting, np.uint8)
+    V = offsets.shape[0] - 1
+    ns = np.empty((rows.shape[0], V), np.int32)
+    al = np.empty((rows.shape[0], words(V)), np.uint32)
+    lib.oracle_align_rows_eos(_p(trans, _i32p), S, _p(offsets, _i32p), _p(tok_bytes, _u8p), V,
+                              None if acc is None else acc.ctypes.data, int(eos_token),
+                              _p(rows, _i32p), rows.shape[0], _p(ns, _i32p), _p(al, _u32p))
     return ns, al
 
 

@@ -62,12 +62,18 @@ int32_t oracle_walk(const int32_t *trans, int32_t num_states, int32_t s,
     return st;
 }
 
-/* next_state / allow rows for an explicit list of source states.
+/* next_state / allow rows for an explicit list of source states, with an
+ * optional end-of-sequence token (eos_token >= 0).  Algorithm 1 stops on
+ * EOS, and Sec. 3.2 makes EOS one more terminal of the scanner, so EOS may
+ * follow wherever a terminal sequence may end: it is allowed exactly in
+ * the states flagged in `accepting` (NULL: none), and leaves the state
+ * unchanged; its bytes are ignored.
  * next_state is [nrows][V] and allow is [nrows][ceil(V/32)]. */
-void oracle_align_rows(const int32_t *trans, int32_t num_states,
-                       const int32_t *offsets, const uint8_t *bytes,
-                       int32_t num_tokens, const int32_t *rows, int64_t nrows,
-                       int32_t *next_state, uint32_t *allow)
+void oracle_align_rows_eos(const int32_t *trans, int32_t num_states,
+                           const int32_t *offsets, const uint8_t *bytes,
+                           int32_t num_tokens, const uint8_t *accepting,
+                           int32_t eos_token, const int32_t *rows, int64_t nrows,
+                           int32_t *next_state, uint32_t *allow)
 {
     int64_t words = ((int64_t)num_tokens + 31) / 32;
     for (int64_t r = 0; r < nrows; ++r) {
@@ -76,14 +82,30 @@ void oracle_align_rows(const int32_t *trans, int32_t num_states,
         uint32_t *al_row = allow + r * words;
         memset(al_row, 0, (size_t)words * sizeof(uint32_t));
         for (int32_t t = 0; t < num_tokens; ++t) {
-            int64_t begin = offsets[t];
-            int64_t len = (int64_t)offsets[t + 1] - begin;
-            int32_t ns = oracle_walk(trans, num_states, s, bytes + begin, len);
+            int32_t ns;
+            if (t == eos_token) {
+                int32_t cs = oracle_canon(s, num_states);
+                ns = (cs != ORACLE_DEAD && accepting != NULL && accepting[cs]) ? cs : ORACLE_DEAD;
+            } else {
+                int64_t begin = offsets[t];
+                int64_t len = (int64_t)offsets[t + 1] - begin;
+                ns = oracle_walk(trans, num_states, s, bytes + begin, len);
+            }
             ns_row[t] = ns;
             if (ns != ORACLE_DEAD)
                 al_row[t / 32] |= (uint32_t)1u << (t % 32);
         }
     }
+}
+
+/* The same rows without an end-of-sequence token. */
+void oracle_align_rows(const int32_t *trans, int32_t num_states,
+                       const int32_t *offsets, const uint8_t *bytes,
+                       int32_t num_tokens, const int32_t *rows, int64_t nrows,
+                       int32_t *next_state, uint32_t *allow)
+{
+    oracle_align_rows_eos(trans, num_states, offsets, bytes, num_tokens, NULL, -1,
+                          rows, nrows, next_state, allow);
 }
 
 /* The whole table: every state 0..S-1 in order. */

@@ -54,6 +54,8 @@ def _load():
     lib.dv_align_workspace_bytes.argtypes = [i32, i32]
     lib.dv_align.restype = ctypes.c_int
     lib.dv_align.argtypes = [vp, i32, vp, vp, i32, vp, vp, vp, sz, vp]
+    lib.dv_align_eos.restype = ctypes.c_int
+    lib.dv_align_eos.argtypes = [vp, i32, vp, vp, i32, vp, i32, vp, vp, vp, sz, vp]
     lib.dv_masked_step_workspace_bytes.restype = sz
     lib.dv_masked_step_workspace_bytes.argtypes = [i32, i32]
     lib.dv_masked_step.restype = ctypes.c_int
@@ -101,10 +103,13 @@ def masked_step_workspace_bytes(batch: int, num_tokens: int) -> int:
     return int(lib.dv_masked_step_workspace_bytes(batch, num_tokens))
 
 
-def align(trans, offsets, tok_bytes, next_state=None, allow=None, workspace=None, stream=None):
+def align(trans, offsets, tok_bytes, next_state=None, allow=None, workspace=None, stream=None,
+          accepting=None, eos_token=None):
     """Alignment table of a byte DFA and a vocabulary (device tensors).
 
     trans [S][256] int32, offsets [V+1] int32, tok_bytes [offsets[V]] uint8.
+    With ``eos_token`` (and optionally ``accepting`` [S] uint8), that token is
+    allowed exactly in accepting states (dv_align_eos).
     Returns (next_state [S][V] int32, allow [S][ceil(V/32)] int32 holding the
     uint32 bit pattern)."""
     dev = trans.device
@@ -127,10 +132,22 @@ def align(trans, offsets, tok_bytes, next_state=None, allow=None, workspace=None
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     _want(workspace, "workspace", torch.uint8, dev)
-    st = lib.dv_align(_ptr(trans), S, _ptr(offsets), _ptr(tok_bytes) if tok_bytes.numel() else None,
-                      V, _ptr(next_state), _ptr(allow), _ptr(workspace), workspace.numel(),
-                      _stream(stream, dev))
-    _check(st, "dv_align")
+    bytes_ptr = _ptr(tok_bytes) if tok_bytes.numel() else None
+    if eos_token is None:
+        if accepting is not None:
+            raise ValueError("accepting is only meaningful with eos_token")
+        st = lib.dv_align(_ptr(trans), S, _ptr(offsets), bytes_ptr, V, _ptr(next_state), _ptr(allow),
+                          _ptr(workspace), workspace.numel(), _stream(stream, dev))
+        _check(st, "dv_align")
+    else:
+        if accepting is not None:
+            _want(accepting, "accepting", torch.uint8, dev)
+            if accepting.numel() != S:
+                raise ValueError("accepting must have one flag per state")
+        st = lib.dv_align_eos(_ptr(trans), S, _ptr(offsets), bytes_ptr, V, _ptr(accepting),
+                              int(eos_token), _ptr(next_state), _ptr(allow), _ptr(workspace),
+                              workspace.numel(), _stream(stream, dev))
+        _check(st, "dv_align_eos")
     return next_state, allow
 
 

@@ -44,6 +44,10 @@ constexpr int kWholeLdsMax = 64 * 1024;           // LDS budget for a whole tabl
 static_assert(kStateTile >= 1 && kStateTile <= 32, "pending set is 32 bits");
 constexpr int kLiveRows = kLiveRowsPerBlock;
 
+// token lengths with a special meaning in the walk
+constexpr int kPastEnd = -1;  // a lane slot past the last token: never stored
+constexpr int kEosLen = -2;   // the end-of-sequence token
+
 __device__ __forceinline__ bool in_range(int32_t v, int S) { return (uint32_t)v < (uint32_t)S; }
 
 // 1. per block of rows: bit b set if some row has a live move on byte b.
@@ -141,7 +145,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const int32_t *__rest
 // re-deriving them from the bytes in every block.
 __global__ __launch_bounds__(kThreads) void token_info_kernel(const int32_t *__restrict__ offsets,
                                                               const uint8_t *__restrict__ bytes, int V,
-                                                              const uint8_t *__restrict__ ws,
+                                                              int eos_token, const uint8_t *__restrict__ ws,
                                                               uint4 *__restrict__ tokinfo)
 {
     __shared__ uint8_t cls[256];
@@ -150,6 +154,10 @@ __global__ __launch_bounds__(kThreads) void token_info_kernel(const int32_t *__r
     const int t = blockIdx.x * kThreads + threadIdx.x;
     if (t >= V)
         return;
+    if (t == eos_token) {  // its bytes are ignored: allowed exactly in accepting states
+        tokinfo[t] = make_uint4(0, 0, (uint32_t)kEosLen, 0);
+        return;
+    }
     const int off = offsets[t];
     const int len = offsets[t + 1] - off;
     uint32_t lo = 0, hi = 0;
@@ -185,6 +193,7 @@ __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
                                           const uint16_t *__restrict__ table, const uint8_t *cls,
                                           int Cp, int s0, int nS, const uint8_t *__restrict__ bytes,
                                           int t_base, int V, int W, const uint4 *__restrict__ tokinfo,
+                                          const uint8_t *__restrict__ accepting,
                                           int32_t *__restrict__ next_state, uint32_t *__restrict__ allow)
 {
     const int tid = threadIdx.x;
@@ -195,10 +204,10 @@ __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
 #pragma unroll
     for (int j = 0; j < kTokPerLane; ++j) {
         const int t = t_base + j * kThreads + tid;
-        const uint4 ti = t < V ? tokinfo[t] : make_uint4(0, 0, 0xFFFFFFFFu, 0);
+        const uint4 ti = t < V ? tokinfo[t] : make_uint4(0, 0, (uint32_t)kPastEnd, 0);
         c03[j] = ti.x;
         c47[j] = ti.y;
-        len[j] = (int)ti.z;  // -1 past the end: never stored, allow bit 0
+        len[j] = (int)ti.z;  // kPastEnd: never stored, allow bit 0; kEosLen: the EOS token
         off[j] = (int)ti.w;
     }
 
@@ -210,13 +219,20 @@ __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
     for (int si = 0; si < nS; ++si) {
         const int s = s0 + si;
         const uint16_t *row = WHOLE ? tab + (uint32_t)s * Cp : tab + (uint32_t)si * Cp;
+        const bool acc = accepting != nullptr && accepting[s] != 0;
 #pragma unroll
         for (int j = 0; j < kTokPerLane; ++j) {
             const uint32_t c0 = c03[j] & 0xFFu;
             const uint32_t v = row[c0 == kDeadClass ? 0u : c0];
             uint32_t st = c0 == kDeadClass ? kDead16 : v;
-            if (len[j] <= 0)
-                st = len[j] == 0 ? (uint32_t)s : kDead16;  // an empty token keeps the state
+            if (len[j] <= 0) {
+                if (len[j] == 0)
+                    st = (uint32_t)s;  // an empty token keeps the state
+                else if (len[j] == kEosLen)
+                    st = acc ? (uint32_t)s : kDead16;  // EOS: only where the scanner may stop
+                else
+                    st = kDead16;
+            }
             res[si * kTokTile + j * kThreads + tid] = (uint16_t)st;
             pend[j] |= (uint32_t)(st != kDead16 && len[j] > 1) << si;
         }
@@ -276,7 +292,7 @@ __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
         for (int j = 0; j < kTokPerLane; ++j) {
             const int t = t_base + j * kThreads + tid;
             const uint32_t v = res[si * kTokTile + j * kThreads + tid];
-            const bool alive = len[j] >= 0 && v != kDead16;
+            const bool alive = len[j] != kPastEnd && v != kDead16;
             if (t < V)
                 ns_row[t] = alive ? (int32_t)v : -1;
             const uint64_t m = __ballot(alive);
@@ -292,6 +308,7 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
                                                         const uint4 *__restrict__ tokinfo,
                                                         const uint8_t *__restrict__ bytes, int V,
                                                         int W, int lds_table_bytes,
+                                                        const uint8_t *__restrict__ accepting,
                                                         int32_t *__restrict__ next_state,
                                                         uint32_t *__restrict__ allow)
 {
@@ -318,16 +335,18 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
     __syncthreads();
 
     if (whole)
-        walk_tile<true>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, next_state, allow);
+        walk_tile<true>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state,
+                        allow);
     else
-        walk_tile<false>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, next_state, allow);
+        walk_tile<false>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state,
+                         allow);
 }
 
 }  // namespace
 
 hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, const uint8_t *bytes,
-                        int V, int32_t *next_state, uint32_t *allow, void *workspace,
-                        hipStream_t stream)
+                        int V, const uint8_t *accepting, int eos_token, int32_t *next_state,
+                        uint32_t *allow, void *workspace, hipStream_t stream)
 {
     uint8_t *ws = static_cast<uint8_t *>(workspace);
     uint32_t *partial = reinterpret_cast<uint32_t *>(ws + kAlignMetaBytes);
@@ -359,10 +378,11 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
     live_columns_kernel<<<nblk, kThreads, 0, stream>>>(trans, S, partial);
     byte_classes_kernel<<<1, kThreads, 0, stream>>>(partial, nblk, ws);
     compact_kernel<<<(S + 15) / 16, kThreads, 0, stream>>>(trans, S, ws, table);
-    token_info_kernel<<<(V + kThreads - 1) / kThreads, kThreads, 0, stream>>>(offsets, bytes, V, ws, tokinfo);
+    token_info_kernel<<<(V + kThreads - 1) / kThreads, kThreads, 0, stream>>>(offsets, bytes, V, eos_token, ws,
+                                                                              tokinfo);
     dim3 grid((V + kTokTile - 1) / kTokTile, (S + kStateTile - 1) / kStateTile);
     walk_kernel<<<grid, kThreads, 256 + lds_table + kResLds, stream>>>(ws, table, S, tokinfo, bytes, V, W,
-                                                                       lds_table, next_state, allow);
+                                                                       lds_table, accepting, next_state, allow);
     return hipGetLastError();
 }
 

@@ -63,35 +63,61 @@ size_t dv_align_workspace_bytes(int32_t num_states, int32_t num_tokens)
     return dv::align_workspace_bytes(num_states, num_tokens);
 }
 
+static dv_status align_common(const char *name, const int32_t *trans, int32_t num_states,
+                              const int32_t *offsets, const uint8_t *bytes, int32_t num_tokens,
+                              const uint8_t *accepting, int32_t eos_token, int32_t *next_state,
+                              uint32_t *allow, void *workspace, size_t workspace_bytes, void *stream)
+{
+    g_error[0] = '\0';
+    if (!trans || !offsets || !next_state || !allow)
+        return fail(DV_ERR_INVALID_ARG, "%s: trans, offsets, next_state and allow must be non-NULL", name);
+    if (num_states < 1 || num_states > DV_MAX_STATES)
+        return fail(DV_ERR_SHAPE, "%s: num_states=%d outside [1, %d]", name, num_states, DV_MAX_STATES);
+    if (num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
+        return fail(DV_ERR_SHAPE, "%s: num_tokens=%d outside [1, %d]", name, num_tokens, DV_MAX_TOKENS);
+    if (eos_token < -1 || eos_token >= num_tokens)
+        return fail(DV_ERR_SHAPE, "%s: eos_token=%d outside [0, %d)", name, eos_token, num_tokens);
+    const size_t S = (size_t)num_states, V = (size_t)num_tokens, W = (V + 31) / 32;
+    const Range r_ns = range_of(next_state, S * V * 4), r_al = range_of(allow, S * W * 4);
+    const Range r_tr = range_of(trans, S * 256 * 4), r_off = range_of(offsets, (V + 1) * 4);
+    const Range r_acc = range_of(accepting, accepting ? S : 0);
+    if (overlap(r_ns, r_al) || overlap(r_ns, r_tr) || overlap(r_ns, r_off) || overlap(r_al, r_tr) ||
+        overlap(r_al, r_off) || overlap(r_ns, r_acc) || overlap(r_al, r_acc))
+        return fail(DV_ERR_ALIAS, "%s: next_state / allow overlap each other or an input", name);
+    const size_t need = dv::align_workspace_bytes(num_states, num_tokens);
+    if (!workspace || workspace_bytes < need)
+        return fail(DV_ERR_WORKSPACE, "%s: workspace of %zu bytes given, %zu needed", name, workspace_bytes, need);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255)
+        return fail(DV_ERR_WORKSPACE, "%s: workspace must be 256-byte aligned", name);
+    const Range r_ws = range_of(workspace, need);
+    if (overlap(r_ws, r_ns) || overlap(r_ws, r_al) || overlap(r_ws, r_tr) || overlap(r_ws, r_off) ||
+        overlap(r_ws, r_acc))
+        return fail(DV_ERR_ALIAS, "%s: workspace overlaps an input or output", name);
+    // bytes == NULL is accepted; the kernels read it only for non-empty tokens.
+    return hip_status(dv::launch_align(trans, num_states, offsets, bytes, num_tokens, accepting, eos_token,
+                                       next_state, allow, workspace, static_cast<hipStream_t>(stream)),
+                      "launch");
+}
+
 dv_status dv_align(const int32_t *trans, int32_t num_states, const int32_t *offsets,
                    const uint8_t *bytes, int32_t num_tokens, int32_t *next_state, uint32_t *allow,
                    void *workspace, size_t workspace_bytes, void *stream)
 {
-    g_error[0] = '\0';
-    if (!trans || !offsets || !next_state || !allow)
-        return fail(DV_ERR_INVALID_ARG, "dv_align: trans, offsets, next_state and allow must be non-NULL");
-    if (num_states < 1 || num_states > DV_MAX_STATES)
-        return fail(DV_ERR_SHAPE, "dv_align: num_states=%d outside [1, %d]", num_states, DV_MAX_STATES);
-    if (num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
-        return fail(DV_ERR_SHAPE, "dv_align: num_tokens=%d outside [1, %d]", num_tokens, DV_MAX_TOKENS);
-    const size_t S = (size_t)num_states, V = (size_t)num_tokens, W = (V + 31) / 32;
-    const Range r_ns = range_of(next_state, S * V * 4), r_al = range_of(allow, S * W * 4);
-    const Range r_tr = range_of(trans, S * 256 * 4), r_off = range_of(offsets, (V + 1) * 4);
-    if (overlap(r_ns, r_al) || overlap(r_ns, r_tr) || overlap(r_ns, r_off) || overlap(r_al, r_tr) ||
-        overlap(r_al, r_off))
-        return fail(DV_ERR_ALIAS, "dv_align: next_state / allow overlap each other or an input");
-    const size_t need = dv::align_workspace_bytes(num_states, num_tokens);
-    if (!workspace || workspace_bytes < need)
-        return fail(DV_ERR_WORKSPACE, "dv_align: workspace of %zu bytes given, %zu needed", workspace_bytes, need);
-    if (reinterpret_cast<uintptr_t>(workspace) & 255)
-        return fail(DV_ERR_WORKSPACE, "dv_align: workspace must be 256-byte aligned");
-    const Range r_ws = range_of(workspace, need);
-    if (overlap(r_ws, r_ns) || overlap(r_ws, r_al) || overlap(r_ws, r_tr) || overlap(r_ws, r_off))
-        return fail(DV_ERR_ALIAS, "dv_align: workspace overlaps an input or output");
-    // bytes == NULL is accepted; the kernels read it only for non-empty tokens.
-    return hip_status(dv::launch_align(trans, num_states, offsets, bytes, num_tokens, next_state, allow,
-                                       workspace, static_cast<hipStream_t>(stream)),
-                      "dv_align launch");
+    return align_common("dv_align", trans, num_states, offsets, bytes, num_tokens, nullptr, -1, next_state,
+                        allow, workspace, workspace_bytes, stream);
+}
+
+dv_status dv_align_eos(const int32_t *trans, int32_t num_states, const int32_t *offsets,
+                       const uint8_t *bytes, int32_t num_tokens, const uint8_t *accepting,
+                       int32_t eos_token, int32_t *next_state, uint32_t *allow, void *workspace,
+                       size_t workspace_bytes, void *stream)
+{
+    if (eos_token < 0) {
+        g_error[0] = '\0';
+        return fail(DV_ERR_SHAPE, "dv_align_eos: eos_token=%d must be a token id", eos_token);
+    }
+    return align_common("dv_align_eos", trans, num_states, offsets, bytes, num_tokens, accepting, eos_token,
+                        next_state, allow, workspace, workspace_bytes, stream);
 }
 
 size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens)

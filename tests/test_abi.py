@@ -133,3 +133,16 @@ def test_binding_type_checks():
     with pytest.raises((TypeError, ValueError)):
         dv.align(torch.zeros((2, 256), dtype=torch.int32), torch.zeros(3, dtype=torch.int32),
                  torch.zeros(1, dtype=torch.uint8))  # CPU tensors are refused
+
+
+def test_align_eos_rejects_bad_token_before_launch():
+    ws_bytes = lib.dv_align_workspace_bytes(16, 1000)
+    for eos in (-1, 1000, 5000):
+        st = lib.dv_align_eos(P, 16, P + GB, P + 2 * GB, 1000, P + 6 * GB, eos, P + 3 * GB, P + 4 * GB,
+                              P + 5 * GB, ws_bytes, None)
+        assert st == SHAPE
+        assert lib.dv_last_error().startswith(b"dv_align_eos")
+    # accepting flags overlapping an output
+    st = lib.dv_align_eos(P, 16, P + GB, P + 2 * GB, 1000, P + 3 * GB + 8, 3, P + 3 * GB, P + 4 * GB,
+                          P + 5 * GB, ws_bytes, None)
+    assert st == ALIAS

@@ -410,3 +410,72 @@ def test_step_graph_replay_matches_eager(dv, wid):
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(tk, ref_t) and torch.equal(st, ref_s), f"replay {rep}"
+
+
+# ------------------------------------------------------- end-of-sequence column
+
+def test_align_eos_paper_example(dv):
+    g = json.load(open(os.path.join(GOLDEN, "fig_nfa_int.json")))
+    e = g["eos"]
+    trans = W.dfa_from_spec(len(g["states"]), g["moves"])
+    offsets, data = W.vocab_from_tokens([t.encode() for t in g["vocab"]] + [b"</s>"])
+    acc = np.array(e["accepting"], np.uint8)
+    ns, al = dv.align(_dev(trans), _dev(offsets), _dev(data), accepting=_dev(acc), eos_token=e["eos_token"])
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(ns.cpu().numpy()[:, e["eos_token"]], e["expected_eos_column"])
+    np.testing.assert_array_equal(u32(al)[:, 0], np.array([int(x, 16) for x in e["expected_allow"]], np.uint32))
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3])
+@pytest.mark.parametrize("where", ["first", "middle", "last"])
+def test_align_eos_workloads(dv, wid, where):
+    w = W.WORKLOADS[wid]
+    trans, acc = W.dfa(wid)
+    offsets, data = W.vocab(wid)
+    eos = {"first": 0, "middle": w.V // 2 + 3, "last": w.V - 1}[where]
+    ns, al = dv.align(_dev(trans), _dev(offsets), _dev(data), accepting=_dev(acc), eos_token=eos)
+    torch.cuda.synchronize()
+    rows = np.arange(w.S, dtype=np.int32) if w.S <= 256 else np.unique(
+        np.concatenate([[0, w.S - 1], np.random.default_rng(wid).integers(0, w.S, 40)])).astype(np.int32)
+    ns_o, al_o = oracle.align_eos(trans, offsets, data, acc, eos, rows=rows)
+    idx = torch.from_numpy(rows.astype(np.int64)).to(DEV)
+    np.testing.assert_array_equal(ns.index_select(0, idx).cpu().numpy(), ns_o)
+    np.testing.assert_array_equal(u32(al.index_select(0, idx)), al_o)
+
+
+def test_align_eos_without_accepting_flags(dv):
+    trans, _ = W.dfa(1)
+    offsets, data = W.vocab(1)
+    ns, al = dv.align(_dev(trans), _dev(offsets), _dev(data), eos_token=7)
+    torch.cuda.synchronize()
+    ns_o, al_o = oracle.align_eos(trans, offsets, data, None, 7)
+    np.testing.assert_array_equal(ns.cpu().numpy(), ns_o)
+    np.testing.assert_array_equal(u32(al), al_o)
+
+
+def test_chain_stops_on_eos(dv):
+    """A greedy chain whose logits favour EOS stops (picks EOS) exactly in
+    accepting states, as the oracle's chain does."""
+    w = W.WORKLOADS[2]
+    trans, acc = W.dfa(2)
+    offsets, data = W.vocab(2)
+    eos = w.V - 1
+    ns, al = dv.align(_dev(trans), _dev(offsets), _dev(data), accepting=_dev(acc), eos_token=eos)
+    ns_o, al_o = oracle.align_eos(trans, offsets, data, acc, eos)
+    steps = 32
+    x = W.logits_all(2, device=DEV, steps=steps)
+    x[:, :, eos] = 50.0  # the model always wants to stop: EOS wins wherever it is allowed
+    ws = dv.step_workspace(w.B, w.V, DEV)
+    init = W.init_states(2)
+    toks, sts = run_chain(dv, ns, al, _dev(init), x, ws)
+    xs = to_oracle(x)
+    cur = init
+    for k in range(steps):
+        t_o, n_o = oracle.masked_step(ns_o, al_o, cur, xs[k])
+        np.testing.assert_array_equal(toks[k].cpu().numpy(), t_o)
+        np.testing.assert_array_equal(sts[k + 1].cpu().numpy(), n_o)
+        # EOS is chosen exactly where the constraint may end
+        live = cur >= 0
+        np.testing.assert_array_equal(t_o[live] == eos, acc[cur[live]].astype(bool))
+        cur = n_o
+    assert (toks == eos).any()

@@ -32,6 +32,8 @@ MUTANTS = {
     "leading dimension ignored": ("(size_t)ld_logits", "(size_t)num_tokens"),
     "stale allow word kept": ("memset(al_row, 0,", "(void)(al_row + 0,"),
     "dead walk continues from state 0": ("return ORACLE_DEAD;\n        st =", "st = 0;\n        st ="),
+    "eos allowed in every state": ("accepting != NULL && accepting[cs]", "accepting != NULL"),
+    "eos moves to the start state": ("accepting[cs]) ? cs : ORACLE_DEAD", "accepting[cs]) ? 0 : ORACLE_DEAD"),
     "zero-length token dies": ("int32_t st = oracle_canon(s, num_states);\n    for",
                                "int32_t st = len ? oracle_canon(s, num_states) : ORACLE_DEAD;\n    for"),
 }
@@ -64,6 +66,8 @@ def _checks(lib):
                               for v, a, e in [([100, 9, 9, 5], [1, 2], 1),
                                               ([5, float("nan"), 3, 3, -np.inf], [1, 4], 1),
                                               ([float("nan"), 2.0, 1.0], [0, 1, 2], 1)]]),
+        ("eos_fig_nfa", lambda: P.test_fig_nfa_eos_column(lib)),
+        ("eos_invariants", lambda: P.test_eos_column_invariants(table, lib)),
         ("ties_bf16", lambda: [P.test_planted_ties_and_specials_bf16(b, a, e, lib)
                                for b, a, e in [([0x8000, 0x0000, 0x0001], [0, 1, 2], 2),
                                                ([0x3F80, 0x3F80, 0x3F80], [1, 2], 1),

@@ -383,3 +383,52 @@ def test_masked_chain_matches_batch_steps(tiny_table, oracle_lib):
         for b in range(3):
             assert chains[b][0][k] == tok[b] and chains[b][1][k + 1] == nxt[b]
         cur = nxt
+
+
+# ------------------------------------------------- end-of-sequence token (EOS)
+
+def test_fig_nfa_eos_column(oracle_lib):
+    g = _golden("fig_nfa_int.json")
+    e = g["eos"]
+    trans = W.dfa_from_spec(len(g["states"]), g["moves"])
+    toks = [t.encode() for t in g["vocab"]] + [b"</s>"]
+    offsets, data = W.vocab_from_tokens(toks)
+    ns, al = oracle.align_eos(trans, offsets, data, np.array(e["accepting"], np.uint8),
+                              e["eos_token"], lib=oracle_lib)
+    np.testing.assert_array_equal(ns[:, e["eos_token"]], e["expected_eos_column"])
+    np.testing.assert_array_equal(ns[:, :9], np.array(g["expected_next_state"]))
+    np.testing.assert_array_equal(al[:, 0], np.array([int(x, 16) for x in e["expected_allow"]],
+                                                     np.uint32))
+
+
+def test_eos_column_invariants(tiny_table, oracle_lib):
+    trans, offsets, data, ns, al = tiny_table
+    _, acc = W.dfa(1)
+    S, V = ns.shape
+    for eos in (0, 17, V - 1):
+        ns_e, al_e = oracle.align_eos(trans, offsets, data, acc, eos, lib=oracle_lib)
+        expect = np.where(acc.astype(bool), np.arange(S), -1)
+        np.testing.assert_array_equal(ns_e[:, eos], expect)
+        others = np.ones(V, bool)
+        others[eos] = False
+        np.testing.assert_array_equal(ns_e[:, others], ns[:, others])  # every other column unchanged
+        np.testing.assert_array_equal(al_e, _pack_allow(ns_e != -1))
+    # no accepting flags: EOS never allowed; dead / out-of-range rows stay empty
+    ns_n, al_n = oracle.align_eos(trans, offsets, data, None, 5, rows=np.array([0, -1, S]), lib=oracle_lib)
+    assert (ns_n[:, 5] == -1).all() and (al_n[1:] == 0).all()
+
+
+def test_eos_is_chosen_when_it_is_the_best_allowed(tiny_table, oracle_lib):
+    trans, offsets, data, ns, al = tiny_table
+    _, acc = W.dfa(1)
+    S, V = ns.shape
+    eos = V - 1
+    ns_e, al_e = oracle.align_eos(trans, offsets, data, acc, eos, lib=oracle_lib)
+    x = np.random.default_rng(8).standard_normal((S, V)).astype(np.float32)
+    x[:, eos] = 100.0  # the model wants to stop everywhere
+    tok, nxt = oracle.masked_step(ns_e, al_e, np.arange(S, dtype=np.int32), x, lib=oracle_lib)
+    for s in range(S):
+        if acc[s]:
+            assert tok[s] == eos and nxt[s] == s  # stops, state unchanged
+        else:
+            assert tok[s] != eos
