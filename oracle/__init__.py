@@ -14,6 +14,11 @@ Way"):
   (Sec. 3.5, k = infinity) a token is allowed exactly when the walk survives.
 * ``masked_step`` / ``masked_argmax``: Algorithm 1 (mask, apply, decode,
   update) with Algorithm 3's argmax over an admissible token set.
+* ``align_eos``: the same table with an end-of-sequence column (Algorithm 1
+  stops on EOS; Sec. 3.2 makes EOS a terminal), allowed in accepting states.
+* ``spec_walk`` / ``spec_verify``: the speculative chain check of Sec. 3.6 --
+  how many proposed tokens the constraint admits, and greedy verification of
+  the proposals against the model's logits at every proposed position.
 
 All readings of the paper's silences (DEAD sentinel, byte alphabet, tie and
 NaN rules, bitmask layout) are stated in ``dv_oracle.c``.
@@ -69,6 +74,14 @@ def _bind(lib):
     lib.oracle_masked_step.argtypes = [_i32p, _u32p, ctypes.c_int32, ctypes.c_int32, _i32p,
                                        ctypes.c_void_p, ctypes.c_int, ctypes.c_int32,
                                        ctypes.c_int64, _i32p, _i32p]
+    lib.oracle_spec_walk.restype = None
+    lib.oracle_spec_walk.argtypes = [_i32p, _u32p, ctypes.c_int32, ctypes.c_int32, _i32p, _i32p,
+                                     ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, _i32p, _i32p]
+    lib.oracle_spec_verify.restype = None
+    lib.oracle_spec_verify.argtypes = [_i32p, _u32p, ctypes.c_int32, ctypes.c_int32, _i32p, _i32p,
+                                       ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int,
+                                       ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, _i32p, _i32p,
+                                       _i32p]
     lib.oracle_walk_lookups.restype = ctypes.c_int64
     lib.oracle_walk_lookups.argtypes = [_i32p, ctypes.c_int32, _i32p, _u8p, ctypes.c_int32,
                                         _i32p, ctypes.c_int64]
@@ -191,6 +204,57 @@ def masked_step(next_state, allow, states, logits, num_tokens: int | None = None
         lib.oracle_masked_step(_p(next_state, _i32p), _p(allow, _u32p), S, V, _p(states, _i32p),
                                logits.ctypes.data, dt, B, ld, _p(tok, _i32p), _p(nst, _i32p))
     return tok, nst
+
+
+def spec_walk(next_state, allow, states, proposals, lib=None):
+    """Speculative chain check (Sec. 3.6): (accepted[B], final_state[B]) for
+    ``proposals`` [B][s] int32 walked from ``states`` through the table."""
+    lib = lib or load()
+    next_state = _c(next_state, np.int32)
+    allow = _c(allow, np.uint32)
+    states = _c(states, np.int32)
+    proposals = _c(proposals, np.int32).reshape(states.shape[0], -1)
+    S, V = next_state.shape
+    B, s = proposals.shape
+    acc = np.empty(B, np.int32)
+    fin = np.empty(B, np.int32)
+    if B:
+        lib.oracle_spec_walk(_p(next_state, _i32p), _p(allow, _u32p), S, V, _p(states, _i32p),
+                             _p(proposals if proposals.size else np.zeros(1, np.int32), _i32p),
+                             s, max(s, 1), B, _p(acc, _i32p), _p(fin, _i32p))
+    return acc, fin
+
+
+def spec_verify(next_state, allow, states, proposals, logits, lib=None):
+    """Speculative verification with greedy decoding (Sec. 3.6, Algorithm 1).
+
+    ``proposals`` is [B][s] int32; ``logits`` is [B][s+1][V'] (V' >= V) fp32
+    or bf16 bits (uint16), any strides with a unit last one: position j of
+    row b holds the logits scored after the first j proposals.  Returns
+    (token[B][s+1], accepted[B], new_state[B])."""
+    lib = lib or load()
+    next_state = _c(next_state, np.int32)
+    allow = _c(allow, np.uint32)
+    states = _c(states, np.int32)
+    B = states.shape[0]
+    proposals = _c(proposals, np.int32).reshape(B, -1)
+    s = proposals.shape[1]
+    S, V = next_state.shape
+    logits, dt = _logit_array(logits)
+    if logits.ndim != 3 or logits.shape[0] != B or logits.shape[1] != s + 1 or logits.shape[2] < V:
+        raise ValueError(f"logits must be [B][s+1][>=V], got {logits.shape}")
+    if logits.strides[2] != logits.itemsize or any(x % logits.itemsize for x in logits.strides):
+        logits = np.ascontiguousarray(logits)
+    ld_row, ld_pos = (x // logits.itemsize for x in logits.strides[:2])
+    tok = np.empty((B, s + 1), np.int32)
+    acc = np.empty(B, np.int32)
+    nst = np.empty(B, np.int32)
+    if B:
+        lib.oracle_spec_verify(_p(next_state, _i32p), _p(allow, _u32p), S, V, _p(states, _i32p),
+                               _p(proposals if proposals.size else np.zeros(1, np.int32), _i32p),
+                               s, max(s, 1), logits.ctypes.data, dt, ld_row, ld_pos, B,
+                               _p(tok, _i32p), _p(acc, _i32p), _p(nst, _i32p))
+    return tok, acc, nst
 
 
 def walk_lookups(trans, offsets, tok_bytes, rows, lib=None) -> int:

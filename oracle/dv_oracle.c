@@ -198,3 +198,95 @@ int64_t oracle_walk_lookups(const int32_t *trans, int32_t num_states,
     }
     return total;
 }
+
+/* Whether proposal t may follow state s (a live state, t a token id whose
+ * allow bit is set): the mask of Algorithm 1 applied to a proposed token. */
+static int oracle_legal(const uint32_t *allow, int32_t num_states, int32_t num_tokens,
+                        int32_t s, int64_t t)
+{
+    int64_t words = ((int64_t)num_tokens + 31) / 32;
+    if (oracle_canon(s, num_states) == ORACLE_DEAD || t < 0 || t >= num_tokens)
+        return 0;
+    return (int)((allow[(int64_t)s * words + t / 32] >> (t % 32)) & 1u);
+}
+
+/* Speculative chain check (Sec. 3.6): the proposals of row b are
+ * proposals[b*ld_proposals + j], j < num_proposed.  accepted[b] is the number
+ * of leading proposals that are each allowed in the state the earlier ones
+ * lead to; final_state[b] is the state after them (states[b], or DEAD if it
+ * is not a state, when none is accepted; else the table entry of the last
+ * accepted proposal). */
+void oracle_spec_walk(const int32_t *next_state, const uint32_t *allow, int32_t num_states,
+                      int32_t num_tokens, const int32_t *states, const int32_t *proposals,
+                      int32_t num_proposed, int64_t ld_proposals, int32_t batch,
+                      int32_t *accepted, int32_t *final_state)
+{
+    for (int32_t b = 0; b < batch; ++b) {
+        const int32_t *prop = proposals + (int64_t)b * ld_proposals;
+        int32_t st = oracle_canon(states[b], num_states);
+        int32_t fin = st;
+        int32_t a = 0;
+        while (a < num_proposed && oracle_legal(allow, num_states, num_tokens, st, prop[a])) {
+            fin = next_state[(int64_t)st * num_tokens + prop[a]];
+            st = oracle_canon(fin, num_states);
+            ++a;
+        }
+        accepted[b] = a;
+        final_state[b] = fin;
+    }
+}
+
+/* Speculative verification with greedy decoding (Sec. 3.6 with Algorithm 1
+ * as the decoder).  Row b proposes num_proposed tokens; the model's logits
+ * for its position j (j = 0 .. num_proposed, scored after the first j
+ * proposals) are at element b*ld_row + j*ld_pos of `logits`.
+ *
+ * Decoding goes through the positions in order, as Algorithm 1 would one
+ * step at a time: at position j the masked greedy choice is made in the
+ * state the first j proposals lead to; while it equals proposal j the
+ * proposal is accepted and decoding moves on.  The first position whose
+ * choice differs (or has no allowed token, or j = num_proposed) ends the
+ * row: its choice is the one extra token the model contributes.
+ *   token[b*(num_proposed+1) + j]  the masked greedy choice at position j in
+ *                                  the state reached by proposals 0..j-1
+ *                                  (-1 where that state is DEAD: an earlier
+ *                                  proposal was not allowed);
+ *   accepted[b]                    the number of accepted proposals a; the
+ *                                  tokens emitted are token[b][0..a] (a + 1
+ *                                  of them, a if token[b][a] = -1);
+ *   new_state[b]                   the state after the emitted tokens
+ *                                  (table entry of token[b][a]; DEAD if -1). */
+void oracle_spec_verify(const int32_t *next_state, const uint32_t *allow, int32_t num_states,
+                        int32_t num_tokens, const int32_t *states, const int32_t *proposals,
+                        int32_t num_proposed, int64_t ld_proposals, const void *logits, int dtype,
+                        int64_t ld_row, int64_t ld_pos, int32_t batch, int32_t *token,
+                        int32_t *accepted, int32_t *new_state)
+{
+    int64_t words = ((int64_t)num_tokens + 31) / 32;
+    size_t elt = dtype == 0 ? 4 : 2;
+    for (int32_t b = 0; b < batch; ++b) {
+        const int32_t *prop = proposals + (int64_t)b * ld_proposals;
+        int32_t *tok_row = token + (int64_t)b * (num_proposed + 1);
+        int32_t st = oracle_canon(states[b], num_states);
+        int32_t a = -1, ns = ORACLE_DEAD;
+        for (int32_t j = 0; j <= num_proposed; ++j) {
+            const void *row = (const char *)logits + (size_t)(b * ld_row + j * ld_pos) * elt;
+            int32_t tok = -1;
+            if (st != ORACLE_DEAD)
+                tok = oracle_masked_argmax(allow + (int64_t)st * words, row, dtype, num_tokens);
+            tok_row[j] = tok;
+            if (a < 0 && (j == num_proposed || tok == -1 || tok != prop[j])) {
+                a = j;
+                ns = tok == -1 ? ORACLE_DEAD : next_state[(int64_t)st * num_tokens + tok];
+            }
+            if (j < num_proposed) {
+                if (oracle_legal(allow, num_states, num_tokens, st, prop[j]))
+                    st = oracle_canon(next_state[(int64_t)st * num_tokens + prop[j]], num_states);
+                else
+                    st = ORACLE_DEAD;
+            }
+        }
+        accepted[b] = a;
+        new_state[b] = ns;
+    }
+}

@@ -34,6 +34,17 @@ MUTANTS = {
     "dead walk continues from state 0": ("return ORACLE_DEAD;\n        st =", "st = 0;\n        st ="),
     "eos allowed in every state": ("accepting != NULL && accepting[cs]", "accepting != NULL"),
     "eos moves to the start state": ("accepting[cs]) ? cs : ORACLE_DEAD", "accepting[cs]) ? 0 : ORACLE_DEAD"),
+    "spec compares with the next proposal": ("tok != prop[j])", "tok != prop[j + (j + 1 < num_proposed)])"),
+    "spec keeps the state after an illegal proposal": ("else\n                    st = ORACLE_DEAD;",
+                                                       "else\n                    st = st;"),
+    "spec matches a -1 choice with a -1 proposal": ("tok == -1 || tok != prop[j]", "tok != prop[j]"),
+    "spec walk ignores the allow bit": ("return (int)((allow[", "return 1 | (int)((allow["),
+    "spec walk does not advance": ("fin = next_state[(int64_t)st * num_tokens + prop[a]];", "fin = st;"),
+    "spec new state from the row's start state": (
+        "ns = tok == -1 ? ORACLE_DEAD : next_state[(int64_t)st * num_tokens + tok];",
+        "ns = tok == -1 ? ORACLE_DEAD : next_state[(int64_t)oracle_canon(states[b], num_states) * num_tokens + tok];"),
+    "spec position stride ignored": ("j * ld_pos", "j * (int64_t)num_tokens"),
+    "spec stops one position late": ("a = j;\n", "a = j + (j < num_proposed);\n"),
     "zero-length token dies": ("int32_t st = oracle_canon(s, num_states);\n    for",
                                "int32_t st = len ? oracle_canon(s, num_states) : ORACLE_DEAD;\n    for"),
 }
@@ -68,6 +79,14 @@ def _checks(lib):
                                               ([float("nan"), 2.0, 1.0], [0, 1, 2], 1)]]),
         ("eos_fig_nfa", lambda: P.test_fig_nfa_eos_column(lib)),
         ("eos_invariants", lambda: P.test_eos_column_invariants(table, lib)),
+        ("spec_fig_nfa", lambda: P.test_fig_nfa_spec_walk_and_verify(lib)),
+        ("spec_sequential", lambda: [P.test_spec_verify_equals_sequential_greedy(d, l, table, lib)
+                                     for d, l in [("f32", "rows"), ("bf16", "rows"), ("f32", "steps")]]),
+        ("spec_later", lambda: P.test_spec_verify_later_positions_follow_the_proposals(table, lib)),
+        ("spec_bytes", lambda: P.test_spec_walk_matches_byte_walk(table, lib)),
+        ("spec_legal", lambda: P.test_spec_verify_accepts_only_legal_prefixes(table, lib)),
+        ("spec_zero", lambda: P.test_spec_zero_proposals_is_one_masked_step(table, lib)),
+        ("spec_perfect", lambda: P.test_spec_perfect_draft_is_fully_accepted(table, lib)),
         ("ties_bf16", lambda: [P.test_planted_ties_and_specials_bf16(b, a, e, lib)
                                for b, a, e in [([0x8000, 0x0000, 0x0001], [0, 1, 2], 2),
                                                ([0x3F80, 0x3F80, 0x3F80], [1, 2], 1),

@@ -432,3 +432,167 @@ def test_eos_is_chosen_when_it_is_the_best_allowed(tiny_table, oracle_lib):
             assert tok[s] == eos and nxt[s] == s  # stops, state unchanged
         else:
             assert tok[s] != eos
+
+
+# ------------------------------------------- speculative chain check (Sec. 3.6)
+
+def _fig_nfa_spec_case():
+    g = _golden("fig_nfa_int.json")
+    e, sp = g["eos"], g["spec"]
+    trans = W.dfa_from_spec(len(g["states"]), g["moves"])
+    offsets, data = W.vocab_from_tokens([t.encode() for t in g["vocab"]] + [b"</s>"])
+    lg = np.array([[[float(v) for v in r] for r in rows] for rows in sp["logits"]], np.float32)
+    return trans, offsets, data, np.array(e["accepting"], np.uint8), e["eos_token"], sp, lg
+
+
+def test_fig_nfa_spec_walk_and_verify(oracle_lib):
+    trans, offsets, data, acc, eos, sp, lg = _fig_nfa_spec_case()
+    ns, al = oracle.align_eos(trans, offsets, data, acc, eos, lib=oracle_lib)
+    states, props = np.array(sp["states"], np.int32), np.array(sp["proposals"], np.int32)
+    a, fin = oracle.spec_walk(ns, al, states, props, lib=oracle_lib)
+    np.testing.assert_array_equal(a, sp["expected_walk_accepted"])
+    np.testing.assert_array_equal(fin, sp["expected_walk_final_state"])
+    tok, a, nst = oracle.spec_verify(ns, al, states, props, lg, lib=oracle_lib)
+    np.testing.assert_array_equal(tok, sp["expected_token"])
+    np.testing.assert_array_equal(a, sp["expected_accepted"])
+    np.testing.assert_array_equal(nst, sp["expected_new_state"])
+
+
+def _bf16_bits(x):
+    return (np.ascontiguousarray(x, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
+def _spec_inputs(ns, al, rng, B, s, keep, lib, dtype="f32"):
+    """States (some dead or out of range), position logits [B][s+1][V] and
+    proposals that follow the greedy chain with probability ``keep`` per
+    position (otherwise: a random id, possibly out of range)."""
+    S, V = ns.shape
+    states = rng.integers(0, S, B).astype(np.int32)
+    states[rng.random(B) < 0.1] = -1
+    states[rng.random(B) < 0.05] = S
+    x = rng.standard_normal((B, s + 1, V)).astype(np.float32)
+    lg = _bf16_bits(x) if dtype == "bf16" else x
+    props = np.empty((B, s), np.int32)
+    cur = states
+    for j in range(s):
+        t, nxt = oracle.masked_step(ns, al, cur, lg[:, j], lib=lib)
+        other = rng.integers(-2, V + 2, B).astype(np.int32)
+        props[:, j] = np.where(rng.random(B) < keep, t, other)
+        cur = nxt
+    return states, props, lg
+
+
+def _sequential_greedy(ns, al, state, props, pos_logits, lib):
+    """Algorithm 1 one step at a time over the positions, stopping at the first
+    choice that differs from the proposal: (tokens, accepted, new_state)."""
+    s = props.shape[0]
+    toks, cur, j = [], int(state), 0
+    while True:
+        t, n = oracle.masked_step(ns, al, np.array([cur], np.int32), pos_logits[j][None], lib=lib)
+        toks.append(int(t[0]))
+        if j == s or t[0] == -1 or t[0] != props[j]:
+            return toks, j, int(n[0])
+        cur, j = int(n[0]), j + 1
+
+
+@pytest.mark.parametrize("dtype,layout", [("f32", "rows"), ("bf16", "rows"), ("f32", "steps")])
+def test_spec_verify_equals_sequential_greedy(dtype, layout, tiny_table, oracle_lib):
+    """Speculation only saves model passes: the emitted tokens and the state are
+    those of plain greedy decoding, and the accepted count is where the two
+    first disagree (Sec. 3.6)."""
+    _, _, _, ns, al = tiny_table
+    rng = np.random.default_rng(31)
+    B, s = 24, 5
+    states, props, lg = _spec_inputs(ns, al, rng, B, s, 0.8, oracle_lib, dtype)
+    if layout == "steps":  # the model's output as [positions][B][V], seen through strides
+        lg = np.ascontiguousarray(lg.transpose(1, 0, 2)).transpose(1, 0, 2)
+    tok, acc, nst = oracle.spec_verify(ns, al, states, props, lg, lib=oracle_lib)
+    seen = set()
+    for b in range(B):
+        toks, a, n = _sequential_greedy(ns, al, states[b], props[b], lg[b], oracle_lib)
+        assert acc[b] == a and nst[b] == n
+        np.testing.assert_array_equal(tok[b, :a + 1], toks)
+        seen.add(a)
+    assert len(seen) >= 3  # early, middle and full acceptance all occur
+
+
+def test_spec_verify_later_positions_follow_the_proposals(tiny_table, oracle_lib):
+    """token[b][j] is the masked greedy choice in the state the first j proposals
+    lead to; DEAD (token -1) once a proposal was not allowed."""
+    _, _, _, ns, al = tiny_table
+    rng = np.random.default_rng(32)
+    B, s = 16, 4
+    states, props, lg = _spec_inputs(ns, al, rng, B, s, 0.6, oracle_lib)
+    tok, _, _ = oracle.spec_verify(ns, al, states, props, lg, lib=oracle_lib)
+    for j in range(s + 1):
+        a, fin = oracle.spec_walk(ns, al, states, props[:, :j], lib=oracle_lib)
+        st_j = np.where(a == j, fin, -1).astype(np.int32)
+        t, _ = oracle.masked_step(ns, al, st_j, lg[:, j], lib=oracle_lib)
+        np.testing.assert_array_equal(tok[:, j], t)
+
+
+def test_spec_walk_matches_byte_walk(tiny_table, oracle_lib):
+    """The accepted proposals, read as one byte string from the row's state,
+    land on the final state; the first rejected one is out of range or makes
+    that byte walk die (concatenation of walks, Sec. 3.3)."""
+    trans, offsets, data, ns, al = tiny_table
+    S, V = ns.shape
+    rng = np.random.default_rng(33)
+    B, s = 40, 6
+    states, props, _ = _spec_inputs(ns, al, rng, B, s, 0.85, oracle_lib)
+    acc, fin = oracle.spec_walk(ns, al, states, props, lib=oracle_lib)
+    tok_bytes = [bytes(data[offsets[t]:offsets[t + 1]]) for t in range(V)]
+    for b in range(B):
+        a = int(acc[b])
+        text = b"".join(tok_bytes[t] for t in props[b, :a])
+        assert oracle.walk(trans, states[b], text, lib=oracle_lib) == fin[b]
+        if a < s:
+            t = int(props[b, a])
+            assert not (0 <= t < V) or oracle.walk(trans, states[b], text + tok_bytes[t],
+                                                   lib=oracle_lib) == -1
+    assert 0 < (acc == s).sum() < B
+
+
+def test_spec_verify_accepts_only_legal_prefixes(tiny_table, oracle_lib):
+    _, _, _, ns, al = tiny_table
+    rng = np.random.default_rng(34)
+    states, props, lg = _spec_inputs(ns, al, rng, 32, 6, 0.7, oracle_lib)
+    walk_acc, _ = oracle.spec_walk(ns, al, states, props, lib=oracle_lib)
+    _, acc, _ = oracle.spec_verify(ns, al, states, props, lg, lib=oracle_lib)
+    assert (acc <= walk_acc).all()
+
+
+def test_spec_zero_proposals_is_one_masked_step(tiny_table, oracle_lib):
+    _, _, _, ns, al = tiny_table
+    S, V = ns.shape
+    rng = np.random.default_rng(35)
+    states = np.array([0, 3, -1, S, 7], np.int32)
+    x = rng.standard_normal((5, 1, V)).astype(np.float32)
+    tok, acc, nst = oracle.spec_verify(ns, al, states, np.zeros((5, 0), np.int32), x, lib=oracle_lib)
+    t, n = oracle.masked_step(ns, al, states, x[:, 0], lib=oracle_lib)
+    np.testing.assert_array_equal(tok[:, 0], t)
+    np.testing.assert_array_equal(nst, n)
+    assert (acc == 0).all()
+    a, fin = oracle.spec_walk(ns, al, states, np.zeros((5, 0), np.int32), lib=oracle_lib)
+    assert (a == 0).all()
+    np.testing.assert_array_equal(fin, [0, 3, -1, -1, 7])
+
+
+def test_spec_perfect_draft_is_fully_accepted(tiny_table, oracle_lib):
+    _, _, _, ns, al = tiny_table
+    rng = np.random.default_rng(36)
+    B, s = 12, 7
+    states = rng.integers(0, ns.shape[0], B).astype(np.int32)
+    lg = rng.standard_normal((B, s + 1, ns.shape[1])).astype(np.float32)
+    props = np.empty((B, s), np.int32)
+    cur = states
+    for j in range(s):  # proposals = the greedy chain from these states
+        t, cur = oracle.masked_step(ns, al, cur, lg[:, j], lib=oracle_lib)
+        props[:, j] = t
+    bonus, after = oracle.masked_step(ns, al, cur, lg[:, s], lib=oracle_lib)
+    tok, acc, nst = oracle.spec_verify(ns, al, states, props, lg, lib=oracle_lib)
+    live = (props != -1).all(axis=1)
+    assert live.sum() >= B // 2
+    assert (acc[live] == s).all()
+    np.testing.assert_array_equal(tok[live, s], bonus[live])
+    np.testing.assert_array_equal(nst[live], after[live])
