@@ -16,6 +16,8 @@ Reported (one JSON line):
                around the replay of the job's decode steps, captured once as
                a HIP graph, on the launch stream; divided by the step count)
   roofline_align  dv_align against the HBM write roofline (4.125 B / pair)
+  spec_verify  greedy verification of s = 8 proposed tokens per row (Sec. 3.6)
+               over windows of the job's decode chain, with its own roofline
   cpu_baseline the CPU oracle on a bounded sample of the same workload
 
 Usage: python bench.py [--steps K] [--warmup W] [--workload 1..5] [--no-cpu]
@@ -57,6 +59,7 @@ def parse():
     ap.add_argument("--workload", type=int, default=4)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-probes", action="store_true", help="skip the roofline probes")
+    ap.add_argument("--no-spec", action="store_true", help="skip the speculative-verification leg")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
 
@@ -208,6 +211,79 @@ def run_probes(dv, dev, table_bytes):
     return out
 
 
+def bench_spec(dv, w, ns, al, x, tokens_all, states_all, dev, s=8, keep=0.9, reps=3):
+    """Speculative verification (Sec. 3.6) over the job's decode chain: window
+    k proposes the chain's tokens of steps k(s+1) .. k(s+1)+s-1, each kept with
+    probability ``keep`` (else replaced by the next token id), and verifies
+    them against the logits of those s + 1 steps, seen as [B][s+1][V] through
+    strides.  All windows are captured in one HIP graph; HIP events around
+    its replay give the time per verification call."""
+    import numpy as np
+    import torch
+
+    n_win = w.steps // (s + 1)
+    g = torch.Generator(device=dev)
+    g.manual_seed(2024)
+    props, starts, views = [], [], []
+    for k in range(n_win):
+        k0 = k * (s + 1)
+        p = tokens_all[k0:k0 + s].t().contiguous()
+        repl = torch.rand(p.shape, generator=g, device=dev) >= keep
+        props.append(torch.where(repl, (p + 1) % w.V, p).to(torch.int32).contiguous())
+        starts.append(states_all[k0].clone())
+        views.append(x[k0:k0 + s + 1].transpose(0, 1))       # [B][s+1][V], ld_row = V, ld_pos = B V
+    tok = torch.empty((n_win, w.B, s + 1), dtype=torch.int32, device=dev)
+    acc = torch.empty((n_win, w.B), dtype=torch.int32, device=dev)
+    nst = torch.empty((n_win, w.B), dtype=torch.int32, device=dev)
+    ws = dv.spec_workspace(w.B, s, w.V, dev)
+
+    def launches():
+        for k in range(n_win):
+            dv.spec_verify(ns, al, starts[k], props[k], views[k], token=tok[k], accepted=acc[k],
+                           new_state=nst[k], workspace=ws)
+
+    launches()
+    torch.cuda.synchronize()
+    ref = (tok.clone(), acc.clone(), nst.clone())
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(side):
+        launches()
+    torch.cuda.current_stream(dev).wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        launches()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    times = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        graph.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b) / 1e3 / n_win)
+    same = bool(torch.equal(tok, ref[0]) and torch.equal(acc, ref[1]) and torch.equal(nst, ref[2]))
+    t = float(np.median(times))
+    live_pos = int((tok != -1).sum()) / n_win
+    emitted = float((acc + (tok.gather(2, acc.to(torch.int64)[..., None])[..., 0] != -1)).sum()) / n_win
+    per_live = w.V * w.elt + 4 * w.words + 4
+    bytes_call = live_pos * per_live + w.B * (s * 12 + (s + 1) * 4 + 12)
+    achieved = bytes_call / t / 1e9
+    return {
+        "proposed_per_row": s, "keep_probability": keep, "calls": n_win,
+        "us_per_call": t * 1e6, "calls_per_s": 1.0 / t,
+        "emitted_tokens_per_s": emitted / t, "positions_per_s": w.B * (s + 1) / t,
+        "mean_accepted": float(acc.float().mean()), "live_positions_per_call": live_pos,
+        "graph_matches_eager": same,
+        "roofline": {"kernel": "masked_step_bf16_kernel over B(s+1) positions + chain and accept kernels"
+                     if w.dtype == "bf16" else "masked_step_kernel over B(s+1) positions",
+                     "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "bytes_per_launch": bytes_call},
+    }
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -346,6 +422,9 @@ def main():
                            "traffic": traffic_record("align", wid)},
         "kernel_source_hash": {k: kernel_source_hash(k) for k in KERNEL_SOURCES},
     }
+    if not args.no_spec:
+        log("speculative verification")
+        out["spec_verify"] = bench_spec(dv, w, ns, al, x, tokens_all, states_all, dev)
     if not args.no_probes:
         log("roofline probes")
         out["probes"] = run_probes(dv, dev, w.S * 96 * 2)

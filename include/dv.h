@@ -12,6 +12,12 @@
  *                   sequence's current state, apply it to the logits, decode
  *                   greedily (Algorithm 3's argmax over the admissible set)
  *                   and advance the state with the chosen token.
+ *   dv_align_eos    dv_align with an end-of-sequence token that is allowed
+ *                   exactly in accepting states.
+ *   dv_spec_walk,   the speculative chain check of Sec. 3.6: how many
+ *   dv_spec_verify  proposed tokens the constraint admits, and greedy
+ *                   verification of the proposals against the model's logits
+ *                   at every proposed position.
  *
  * Conventions shared by every call:
  *   - Every array argument is a DEVICE pointer (hipMalloc'd or a torch CUDA
@@ -51,6 +57,8 @@ extern "C" {
 #define DV_MAX_STATES 65535        /* num_states  in [1, DV_MAX_STATES]  */
 #define DV_MAX_TOKENS 16777216     /* num_tokens  in [1, DV_MAX_TOKENS]  */
 #define DV_MAX_BATCH  1048576      /* batch       in [0, DV_MAX_BATCH]   */
+#define DV_MAX_PROPOSED 1024       /* num_proposed in [0, DV_MAX_PROPOSED];
+                                      batch * (num_proposed + 1) <= DV_MAX_BATCH */
 
 typedef enum dv_status {
     DV_OK = 0,
@@ -180,6 +188,93 @@ DV_API dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow
                          const int32_t *states, const void *logits, int32_t dtype,
                          int32_t batch, int64_t ld_logits,
                          int32_t *token, int32_t *new_state,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * dv_spec_walk -- speculative chain check (Sec. 3.6): how many of a row's
+ * proposed tokens the constraint admits, one after the other.
+ *
+ * For every row b in [0, B), with s = num_proposed proposals
+ * p_j = proposals[b*ld_proposals + j] and q_0 = states[b] (DV_DEAD if
+ * outside [0, S)):
+ *     p_j is admitted when q_j is a state in [0, S), p_j is in [0, V) and
+ *         the allow bit (q_j, p_j) is set; then q_{j+1} = next_state[q_j*V + p_j];
+ *     accepted[b]    = the number a of leading admitted proposals;
+ *     final_state[b] = the table entry reached by the last admitted proposal
+ *                      (q_0 when a = 0).
+ * Proposal ids outside [0, V) are not errors: they are not admitted.
+ *
+ * Inputs (device, read only): next_state, allow, states as for
+ *   dv_masked_step; proposals [B][ld_proposals] int32 (ld_proposals >= s;
+ *   may be NULL when s = 0).
+ * Outputs (device): accepted [B], final_state [B] int32; they must not
+ *   overlap each other or any input.  No workspace.
+ * B = 0 is valid and enqueues nothing (then only next_state and allow must
+ *   be non-NULL).
+ * Errors: DV_ERR_INVALID_ARG, DV_ERR_SHAPE (S, V, B or s out of range,
+ *   ld_proposals < s), DV_ERR_ALIAS, DV_ERR_HIP.
+ */
+DV_API dv_status dv_spec_walk(const int32_t *next_state, const uint32_t *allow,
+                       int32_t num_states, int32_t num_tokens,
+                       const int32_t *states, const int32_t *proposals,
+                       int32_t num_proposed, int64_t ld_proposals, int32_t batch,
+                       int32_t *accepted, int32_t *final_state, void *stream);
+
+/*
+ * dv_spec_verify_workspace_bytes -- device workspace dv_spec_verify needs for
+ * `batch` rows of `num_proposed` proposals over `num_tokens` logits (the
+ * state of every position and the masked step's partial results).  Returns 0
+ * when a size is outside its limit.
+ */
+DV_API size_t dv_spec_verify_workspace_bytes(int32_t batch, int32_t num_proposed,
+                                             int32_t num_tokens);
+
+/*
+ * dv_spec_verify -- verification of proposed tokens with greedy decoding
+ * (Sec. 3.6: the model scores all proposed positions in one pass and the
+ * proposals it does not confirm are discarded; its choice at a position is
+ * the masked greedy decode of Algorithm 1).
+ *
+ * Row b proposes s = num_proposed tokens p_j = proposals[b*ld_proposals + j].
+ * The logits the model gives at position j (j = 0 .. s, after reading the
+ * first j proposals) are V elements at logits[b*ld_row + j*ld_pos].  With
+ * q_j the state after the first j proposals as defined by dv_spec_walk, and
+ * DV_DEAD once a proposal was not admitted:
+ *     token[b*(s+1) + j] = the masked greedy choice of dv_masked_step in
+ *                          state q_j for position j's logits (-1 when q_j is
+ *                          DV_DEAD or allows nothing);
+ *     accepted[b]        = the first j < s whose choice is -1 or differs from
+ *                          p_j, else s: the proposals p_0 .. p_{a-1} agree with
+ *                          the model and token[b][0 .. a] are the tokens
+ *                          plain greedy decoding emits (a + 1 of them, a if
+ *                          token[b][a] = -1);
+ *     new_state[b]       = next_state[q_a*V + token[b][a]], or DV_DEAD when
+ *                          token[b][a] = -1.
+ * The tokens emitted are exactly those of one-step-at-a-time decoding with
+ * dv_masked_step on the same logits; an end-of-sequence token among them
+ * ends the sequence at that point (the caller truncates there).
+ *
+ * Inputs (device, read only): next_state, allow, states as for
+ *   dv_masked_step; proposals [B][ld_proposals] int32 (ld_proposals >= s;
+ *   may be NULL when s = 0; ids outside [0, V) are never confirmed);
+ *   logits of `dtype`, any non-negative ld_row and ld_pos (a model's
+ *   [B][s+1][V] output is ld_row = (s+1)*V, ld_pos = V).
+ * Outputs (device): token [B][s+1], accepted [B], new_state [B] int32; they
+ *   must not overlap each other, an input or the workspace.
+ * Workspace: at least dv_spec_verify_workspace_bytes(B, s, V) bytes of
+ *   device memory, 256-byte aligned; contents on entry are ignored, on exit
+ *   undefined.  Calls that share a workspace must be ordered on one stream.
+ * B = 0 is valid and enqueues nothing.
+ * Errors: DV_ERR_INVALID_ARG, DV_ERR_SHAPE (S, V, B or s out of range,
+ *   B*(s+1) > DV_MAX_BATCH, ld_proposals < s, a negative or too large
+ *   stride), DV_ERR_DTYPE, DV_ERR_ALIAS, DV_ERR_WORKSPACE, DV_ERR_HIP.
+ */
+DV_API dv_status dv_spec_verify(const int32_t *next_state, const uint32_t *allow,
+                         int32_t num_states, int32_t num_tokens,
+                         const int32_t *states, const int32_t *proposals,
+                         int32_t num_proposed, int64_t ld_proposals,
+                         const void *logits, int32_t dtype, int64_t ld_row, int64_t ld_pos,
+                         int32_t batch, int32_t *token, int32_t *accepted, int32_t *new_state,
                          void *workspace, size_t workspace_bytes, void *stream);
 
 /* Static, human-readable name of a status code ("DV_OK", ...). */

@@ -309,3 +309,33 @@ def masked_chain(cache: RowCache, init_state: int, logits_rows, lib=None):
         s = DEAD if t == -1 else int(ns_row[t])
         sts[k + 1] = s
     return toks, sts
+
+
+def spec_verify_rows(cache: RowCache, state: int, proposals, pos_logits, lib=None):
+    """``spec_verify`` for one row of a workload whose full table is too large
+    for the CPU: the table rows it needs come from ``cache`` (same definition
+    as ``align``).  ``pos_logits`` is [s+1][V'] for that row.  Returns
+    (token[s+1], accepted, new_state)."""
+    lib = lib or cache.lib
+    proposals = np.asarray(proposals, np.int32)
+    s = proposals.shape[0]
+    S = cache.trans.shape[0]
+    V = cache.offsets.shape[0] - 1
+    toks = np.full(s + 1, -1, np.int32)
+    st = int(state) if 0 <= int(state) < S else DEAD
+    acc, new = None, DEAD
+    for j in range(s + 1):
+        if st != DEAD:
+            ns_row, al_row = cache.get(st)
+            toks[j] = masked_argmax(al_row, pos_logits[j][:V], lib=lib)
+        t = int(toks[j])
+        if acc is None and (j == s or t == -1 or t != proposals[j]):
+            acc, new = j, (DEAD if t == -1 else int(ns_row[t]))
+        if j < s:
+            p = int(proposals[j])
+            if st != DEAD and 0 <= p < V and (al_row[p // 32] >> np.uint32(p % 32)) & 1:
+                nx = int(ns_row[p])
+                st = nx if 0 <= nx < S else DEAD
+            else:
+                st = DEAD
+    return toks, acc, new

@@ -10,7 +10,8 @@ importing this package fails if the library is not built.
 
 ``align`` is the offline vocabulary alignment of the DOMINO paper (Sec. 3.3,
 Algorithm 2, walked to full depth as in Sec. 3.5) for a byte-level DFA;
-``masked_step`` is one step of its Algorithm 1 with greedy decoding.
+``masked_step`` is one step of its Algorithm 1 with greedy decoding;
+``spec_walk`` / ``spec_verify`` are the speculative chain check of Sec. 3.6.
 """
 from __future__ import annotations
 
@@ -19,8 +20,9 @@ import os
 
 import torch
 
-__all__ = ["align", "masked_step", "align_workspace_bytes", "masked_step_workspace_bytes",
-           "step_workspace", "DvError", "DEAD", "library_path", "lib"]
+__all__ = ["align", "masked_step", "spec_walk", "spec_verify", "align_workspace_bytes",
+           "masked_step_workspace_bytes", "spec_verify_workspace_bytes", "step_workspace",
+           "spec_workspace", "DvError", "DEAD", "library_path", "lib"]
 
 DEAD = -1
 DV_OK = 0
@@ -60,6 +62,13 @@ def _load():
     lib.dv_masked_step_workspace_bytes.argtypes = [i32, i32]
     lib.dv_masked_step.restype = ctypes.c_int
     lib.dv_masked_step.argtypes = [vp, vp, i32, i32, vp, vp, i32, i32, i64, vp, vp, vp, sz, vp]
+    lib.dv_spec_walk.restype = ctypes.c_int
+    lib.dv_spec_walk.argtypes = [vp, vp, i32, i32, vp, vp, i32, i64, i32, vp, vp, vp]
+    lib.dv_spec_verify_workspace_bytes.restype = sz
+    lib.dv_spec_verify_workspace_bytes.argtypes = [i32, i32, i32]
+    lib.dv_spec_verify.restype = ctypes.c_int
+    lib.dv_spec_verify.argtypes = [vp, vp, i32, i32, vp, vp, i32, i64, vp, i32, i64, i64, i32, vp, vp, vp,
+                                   vp, sz, vp]
     return lib
 
 
@@ -192,3 +201,96 @@ def masked_step(next_state, allow, states, logits, token=None, new_state=None, w
                             _stream(stream, dev))
     _check(st, "dv_masked_step")
     return token, new_state
+
+
+def _dtype_code(logits):
+    if logits.dtype == torch.float32:
+        return DV_F32
+    if logits.dtype == torch.bfloat16:
+        return DV_BF16
+    raise TypeError(f"logits must be float32 or bfloat16, got {logits.dtype}")
+
+
+def _proposals(proposals, B, dev):
+    if proposals.dtype != torch.int32 or not proposals.is_cuda or proposals.device != dev:
+        raise TypeError("proposals must be an int32 device tensor on the states' device")
+    if proposals.dim() != 2 or proposals.shape[0] != B:
+        raise ValueError(f"proposals must be [{B}][s]")
+    s = proposals.shape[1]
+    if B and s and proposals.stride(1) != 1:
+        raise ValueError("proposals must have unit stride along a row")
+    ld = proposals.stride(0) if B > 1 else s
+    return s, max(ld, s)
+
+
+def spec_walk(next_state, allow, states, proposals, accepted=None, final_state=None, stream=None):
+    """Speculative chain check: (accepted [B], final_state [B]) -- how many of
+    each row's proposals [B][s] the table admits in turn, and where they lead."""
+    dev = states.device
+    _want(next_state, "next_state", torch.int32, dev)
+    _want(allow, "allow", torch.int32, dev)
+    _want(states, "states", torch.int32, dev)
+    S, V = next_state.shape
+    B = states.shape[0]
+    s, ld = _proposals(proposals, B, dev)
+    if accepted is None:
+        accepted = torch.empty(B, dtype=torch.int32, device=dev)
+    if final_state is None:
+        final_state = torch.empty(B, dtype=torch.int32, device=dev)
+    st = lib.dv_spec_walk(_ptr(next_state), _ptr(allow), S, V, _ptr(states),
+                          _ptr(proposals) if proposals.numel() else None, s, ld, B, _ptr(accepted),
+                          _ptr(final_state), _stream(stream, dev))
+    _check(st, "dv_spec_walk")
+    return accepted, final_state
+
+
+def spec_verify_workspace_bytes(batch: int, num_proposed: int, num_tokens: int) -> int:
+    return int(lib.dv_spec_verify_workspace_bytes(batch, num_proposed, num_tokens))
+
+
+def spec_workspace(batch: int, num_proposed: int, num_tokens: int, device) -> torch.Tensor:
+    """A workspace for ``spec_verify`` (reusable by calls ordered on one stream)."""
+    n = spec_verify_workspace_bytes(batch, num_proposed, num_tokens)
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
+
+
+def spec_verify(next_state, allow, states, proposals, logits, token=None, accepted=None,
+                new_state=None, workspace=None, stream=None):
+    """Greedy verification of proposed tokens (Sec. 3.6).
+
+    proposals [B][s] int32; logits [B][s+1][V] fp32 or bf16 with any strides
+    except a unit one along the vocabulary (position j of row b: the model's
+    logits after the first j proposals).  Returns (token [B][s+1],
+    accepted [B], new_state [B]): the emitted tokens are token[b][:accepted[b]+1]."""
+    dev = states.device
+    _want(next_state, "next_state", torch.int32, dev)
+    _want(allow, "allow", torch.int32, dev)
+    _want(states, "states", torch.int32, dev)
+    dt = _dtype_code(logits)
+    S, V = next_state.shape
+    B = states.shape[0]
+    s, ld = _proposals(proposals, B, dev)
+    if not logits.is_cuda or logits.device != dev:
+        raise ValueError("logits must be on the same device as states")
+    if logits.dim() != 3 or logits.shape[0] != B or logits.shape[1] != s + 1 or logits.shape[2] != V:
+        raise ValueError(f"logits must be [{B}][{s + 1}][{V}] (wider strides are allowed)")
+    if B and logits.stride(2) != 1:
+        raise ValueError("logits must have unit stride along the vocabulary")
+    ld_row, ld_pos = logits.stride(0), logits.stride(1)
+    if token is None:
+        token = torch.empty((B, s + 1), dtype=torch.int32, device=dev)
+    if accepted is None:
+        accepted = torch.empty(B, dtype=torch.int32, device=dev)
+    if new_state is None:
+        new_state = torch.empty(B, dtype=torch.int32, device=dev)
+    _want(token, "token", torch.int32, dev)
+    if token.numel() != B * (s + 1):
+        raise ValueError("token must be [B][s+1]")
+    if workspace is None:
+        workspace = spec_workspace(B, s, V, dev)
+    st = lib.dv_spec_verify(_ptr(next_state), _ptr(allow), S, V, _ptr(states),
+                            _ptr(proposals) if proposals.numel() else None, s, ld, _ptr(logits), dt,
+                            ld_row, ld_pos, B, _ptr(token), _ptr(accepted), _ptr(new_state),
+                            _ptr(workspace), workspace.numel(), _stream(stream, dev))
+    _check(st, "dv_spec_verify")
+    return token, accepted, new_state

@@ -179,4 +179,120 @@ dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow, int32
                       "dv_masked_step launch");
 }
 
+static dv_status spec_shape_checks(const char *name, int32_t num_states, int32_t num_tokens, int32_t batch,
+                                   int32_t num_proposed, int64_t ld_proposals)
+{
+    if (num_states < 1 || num_states > DV_MAX_STATES)
+        return fail(DV_ERR_SHAPE, "%s: num_states=%d outside [1, %d]", name, num_states, DV_MAX_STATES);
+    if (num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
+        return fail(DV_ERR_SHAPE, "%s: num_tokens=%d outside [1, %d]", name, num_tokens, DV_MAX_TOKENS);
+    if (batch < 0 || batch > DV_MAX_BATCH)
+        return fail(DV_ERR_SHAPE, "%s: batch=%d outside [0, %d]", name, batch, DV_MAX_BATCH);
+    if (num_proposed < 0 || num_proposed > DV_MAX_PROPOSED)
+        return fail(DV_ERR_SHAPE, "%s: num_proposed=%d outside [0, %d]", name, num_proposed, DV_MAX_PROPOSED);
+    if ((int64_t)batch * (num_proposed + 1) > DV_MAX_BATCH)
+        return fail(DV_ERR_SHAPE, "%s: batch * (num_proposed + 1) = %lld exceeds %d", name,
+                    (long long)batch * (num_proposed + 1), DV_MAX_BATCH);
+    if (num_proposed > 0 && (ld_proposals < num_proposed || ld_proposals > ((int64_t)1 << 40)))
+        return fail(DV_ERR_SHAPE, "%s: ld_proposals=%lld must be >= num_proposed=%d", name,
+                    (long long)ld_proposals, num_proposed);
+    return DV_OK;
+}
+
+dv_status dv_spec_walk(const int32_t *next_state, const uint32_t *allow, int32_t num_states, int32_t num_tokens,
+                       const int32_t *states, const int32_t *proposals, int32_t num_proposed,
+                       int64_t ld_proposals, int32_t batch, int32_t *accepted, int32_t *final_state, void *stream)
+{
+    g_error[0] = '\0';
+    const char *name = "dv_spec_walk";
+    if (!next_state || !allow)
+        return fail(DV_ERR_INVALID_ARG, "%s: next_state and allow must be non-NULL", name);
+    if (batch > 0 && (!states || !accepted || !final_state || (num_proposed > 0 && !proposals)))
+        return fail(DV_ERR_INVALID_ARG, "%s: states, proposals, accepted and final_state must be non-NULL "
+                                        "when batch > 0", name);
+    const dv_status st = spec_shape_checks(name, num_states, num_tokens, batch, num_proposed, ld_proposals);
+    if (st != DV_OK)
+        return st;
+    if (batch == 0)
+        return DV_OK;
+    const size_t S = (size_t)num_states, V = (size_t)num_tokens, W = (V + 31) / 32, B = (size_t)batch;
+    const size_t np = (size_t)num_proposed;
+    const Range r_acc = range_of(accepted, B * 4), r_fin = range_of(final_state, B * 4);
+    const Range r_ns = range_of(next_state, S * V * 4), r_al = range_of(allow, S * W * 4);
+    const Range r_st = range_of(states, B * 4);
+    const Range r_pr = range_of(proposals, np ? ((B - 1) * (size_t)ld_proposals + np) * 4 : 0);
+    if (overlap(r_acc, r_fin))
+        return fail(DV_ERR_ALIAS, "%s: accepted and final_state overlap", name);
+    for (Range out : {r_acc, r_fin})
+        if (overlap(out, r_ns) || overlap(out, r_al) || overlap(out, r_st) || overlap(out, r_pr))
+            return fail(DV_ERR_ALIAS, "%s: an output overlaps an input", name);
+    return hip_status(dv::launch_spec_walk(next_state, allow, num_states, num_tokens, states, proposals,
+                                           num_proposed, num_proposed ? ld_proposals : 0, batch, accepted,
+                                           final_state, static_cast<hipStream_t>(stream)),
+                      "dv_spec_walk launch");
+}
+
+size_t dv_spec_verify_workspace_bytes(int32_t batch, int32_t num_proposed, int32_t num_tokens)
+{
+    if (batch < 0 || batch > DV_MAX_BATCH || num_proposed < 0 || num_proposed > DV_MAX_PROPOSED ||
+        (int64_t)batch * (num_proposed + 1) > DV_MAX_BATCH || num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
+        return 0;
+    return dv::spec_workspace_bytes(batch, num_proposed, num_tokens);
+}
+
+dv_status dv_spec_verify(const int32_t *next_state, const uint32_t *allow, int32_t num_states,
+                         int32_t num_tokens, const int32_t *states, const int32_t *proposals,
+                         int32_t num_proposed, int64_t ld_proposals, const void *logits, int32_t dtype,
+                         int64_t ld_row, int64_t ld_pos, int32_t batch, int32_t *token, int32_t *accepted,
+                         int32_t *new_state, void *workspace, size_t workspace_bytes, void *stream)
+{
+    g_error[0] = '\0';
+    const char *name = "dv_spec_verify";
+    if (!next_state || !allow)
+        return fail(DV_ERR_INVALID_ARG, "%s: next_state and allow must be non-NULL", name);
+    if (batch > 0 && (!states || !logits || !token || !accepted || !new_state || (num_proposed > 0 && !proposals)))
+        return fail(DV_ERR_INVALID_ARG, "%s: states, proposals, logits, token, accepted and new_state must be "
+                                        "non-NULL when batch > 0", name);
+    dv_status st = spec_shape_checks(name, num_states, num_tokens, batch, num_proposed, ld_proposals);
+    if (st != DV_OK)
+        return st;
+    const int64_t kMaxStride = (int64_t)1 << 40;
+    if (ld_row < 0 || ld_row > kMaxStride || ld_pos < 0 || ld_pos > kMaxStride)
+        return fail(DV_ERR_SHAPE, "%s: ld_row=%lld and ld_pos=%lld must be in [0, 2^40]", name,
+                    (long long)ld_row, (long long)ld_pos);
+    if (dtype != DV_F32 && dtype != DV_BF16)
+        return fail(DV_ERR_DTYPE, "%s: unknown dtype %d", name, dtype);
+    if (batch == 0)
+        return DV_OK;
+    const size_t S = (size_t)num_states, V = (size_t)num_tokens, W = (V + 31) / 32, B = (size_t)batch;
+    const size_t np = (size_t)num_proposed, P = np + 1;
+    const size_t elt = dtype == DV_F32 ? 4 : 2;
+    const Range r_tok = range_of(token, B * P * 4), r_acc = range_of(accepted, B * 4),
+                r_new = range_of(new_state, B * 4);
+    const Range r_ns = range_of(next_state, S * V * 4), r_al = range_of(allow, S * W * 4);
+    const Range r_st = range_of(states, B * 4);
+    const Range r_pr = range_of(proposals, np ? ((B - 1) * (size_t)ld_proposals + np) * 4 : 0);
+    const Range r_lg = range_of(logits, ((B - 1) * (size_t)ld_row + np * (size_t)ld_pos + V) * elt);
+    if (overlap(r_tok, r_acc) || overlap(r_tok, r_new) || overlap(r_acc, r_new))
+        return fail(DV_ERR_ALIAS, "%s: token, accepted and new_state overlap", name);
+    for (Range out : {r_tok, r_acc, r_new})
+        if (overlap(out, r_ns) || overlap(out, r_al) || overlap(out, r_st) || overlap(out, r_pr) ||
+            overlap(out, r_lg))
+            return fail(DV_ERR_ALIAS, "%s: an output overlaps an input", name);
+    const size_t need = dv::spec_workspace_bytes(batch, num_proposed, num_tokens);
+    if (!workspace || workspace_bytes < need)
+        return fail(DV_ERR_WORKSPACE, "%s: workspace of %zu bytes given, %zu needed", name, workspace_bytes, need);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255)
+        return fail(DV_ERR_WORKSPACE, "%s: workspace must be 256-byte aligned", name);
+    const Range r_ws = range_of(workspace, need);
+    for (Range r : {r_tok, r_acc, r_new, r_ns, r_al, r_st, r_pr, r_lg})
+        if (overlap(r_ws, r))
+            return fail(DV_ERR_ALIAS, "%s: workspace overlaps an input or output", name);
+    return hip_status(dv::launch_spec_verify(next_state, allow, num_states, num_tokens, states, proposals,
+                                             num_proposed, num_proposed ? ld_proposals : 0, logits, dtype, ld_row,
+                                             ld_pos, batch, token, accepted, new_state, workspace,
+                                             static_cast<hipStream_t>(stream)),
+                      "dv_spec_verify launch");
+}
+
 }  // extern "C"

@@ -69,4 +69,53 @@ hipError_t launch_masked_step(const int32_t *next_state, const uint32_t *allow, 
                               int64_t ld, int32_t *token, int32_t *new_state, void *workspace,
                               hipStream_t stream);
 
+// Where the logits of row r start, in elements: rows come in groups of `per`
+// (a sequence's positions); group g = r / per, position j = r % per, at
+// g * ld_row + j * ld_pos.  A plain batch is {ld, 0, 1}.
+struct RowMap {
+    int64_t ld_row;
+    int64_t ld_pos;
+    int per;
+    __host__ __device__ int64_t offset(int r) const
+    {
+        if (per == 1)  // a plain batch: no division ahead of the first loads
+            return (int64_t)r * ld_row;
+        const int g = r / per;
+        return (int64_t)g * ld_row + (int64_t)(r - g * per) * ld_pos;
+    }
+};
+
+// The masked step over R rows addressed through `map` (workspace as above,
+// for R rows).
+hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, int S, int V,
+                              const int32_t *states, const void *logits, int dtype, int R,
+                              RowMap map, int32_t *token, int32_t *new_state, void *workspace,
+                              hipStream_t stream);
+
+// ------------------------------------------------ speculative chain check
+//
+// Workspace of the verification, for B rows of s proposals (R = B (s + 1)
+// positions), 256-byte aligned parts:
+//   [0, ...)     int32 state of every position [B][s+1] (DEAD after a
+//                proposal that was not allowed)
+//   [pos_new..)  int32 state after each position's choice [B][s+1]
+//   [partial..)  the masked step's workspace for R rows
+inline size_t spec_positions(int B, int s) { return (size_t)B * (size_t)(s + 1); }
+inline size_t spec_pos_new_offset(int B, int s) { return align_up(spec_positions(B, s) * 4, 256); }
+inline size_t spec_partial_offset(int B, int s) { return 2 * spec_pos_new_offset(B, s); }
+inline size_t spec_workspace_bytes(int B, int s, int V)
+{
+    return spec_partial_offset(B, s) + step_workspace_bytes((int)spec_positions(B, s), V);
+}
+
+hipError_t launch_spec_walk(const int32_t *next_state, const uint32_t *allow, int S, int V,
+                            const int32_t *states, const int32_t *proposals, int s, int64_t ld_prop,
+                            int B, int32_t *accepted, int32_t *final_state, hipStream_t stream);
+
+hipError_t launch_spec_verify(const int32_t *next_state, const uint32_t *allow, int S, int V,
+                              const int32_t *states, const int32_t *proposals, int s, int64_t ld_prop,
+                              const void *logits, int dtype, int64_t ld_row, int64_t ld_pos, int B,
+                              int32_t *token, int32_t *accepted, int32_t *new_state, void *workspace,
+                              hipStream_t stream);
+
 }  // namespace dv

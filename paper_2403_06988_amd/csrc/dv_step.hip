@@ -235,7 +235,7 @@ __device__ __forceinline__ void scan_vectors(const char *row, const uint32_t *ar
 template <int DT, int THREADS, int U>
 __global__ __launch_bounds__(THREADS) void masked_step_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
-    const int32_t *__restrict__ states, const void *__restrict__ logits, int64_t ld, int chunk_vec,
+    const int32_t *__restrict__ states, const void *__restrict__ logits, RowMap map, int chunk_vec,
     int nchunks, int32_t *__restrict__ token, int32_t *__restrict__ new_state,
     uint64_t *__restrict__ partial)
 {
@@ -249,7 +249,7 @@ __global__ __launch_bounds__(THREADS) void masked_step_kernel(
     uint32_t best_key = 0;
     int best_idx = 0;
     if (live) {
-        const char *row = static_cast<const char *>(logits) + (size_t)b * (size_t)ld * E::kBytes;
+        const char *row = static_cast<const char *>(logits) + (size_t)map.offset(b) * E::kBytes;
         const uint32_t *arow = allow + (size_t)s * W;
         const int nvec = V / kVec;
         const int e0 = c * chunk_vec * kVec;
@@ -310,7 +310,7 @@ __device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v, bool is_max)
 template <int THREADS, int U>
 __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
-    const int32_t *__restrict__ states, const void *__restrict__ logits, int64_t ld, int chunk_vec,
+    const int32_t *__restrict__ states, const void *__restrict__ logits, RowMap map, int chunk_vec,
     int nchunks, int32_t *__restrict__ token, int32_t *__restrict__ new_state,
     uint64_t *__restrict__ partial)
 {
@@ -320,7 +320,7 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     const int tid = threadIdx.x;
     const int b = blockIdx.x / nchunks;
     const int c = blockIdx.x - b * nchunks;
-    const char *row = static_cast<const char *>(logits) + (size_t)b * (size_t)ld * 2;
+    const char *row = static_cast<const char *>(logits) + (size_t)map.offset(b) * 2;
     const int nvec = V / kVec;
     const int v0 = c * chunk_vec;
     const int v1 = min(nvec, v0 + chunk_vec);
@@ -539,9 +539,9 @@ StepGeometry step_geometry(int B, int V, int dtype)
     return {chunk_vec, nchunks, threads};
 }
 
-hipError_t launch_masked_step(const int32_t *next_state, const uint32_t *allow, int S, int V,
+hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, int S, int V,
                               const int32_t *states, const void *logits, int dtype, int B,
-                              int64_t ld, int32_t *token, int32_t *new_state, void *workspace,
+                              RowMap map, int32_t *token, int32_t *new_state, void *workspace,
                               hipStream_t stream)
 {
     const int W = (V + 31) / 32;
@@ -550,14 +550,23 @@ hipError_t launch_masked_step(const int32_t *next_state, const uint32_t *allow, 
     const unsigned grid = (unsigned)B * (unsigned)g.nchunks;
     if (dtype == 0)
         masked_step_kernel<0, kSmallThreads, kSmallU><<<grid, kSmallThreads, 0, stream>>>(
-            next_state, allow, S, V, W, states, logits, ld, g.chunk_vec, g.nchunks, token, new_state, partial);
+            next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial);
     else
         masked_step_bf16_kernel<kBigThreads, kBigU><<<grid, kBigThreads, 0, stream>>>(
-            next_state, allow, S, V, W, states, logits, ld, g.chunk_vec, g.nchunks, token, new_state, partial);
+            next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial);
     if (g.nchunks > 1)
         finalize_kernel<<<(B + kSmallThreads - 1) / kSmallThreads, kSmallThreads, 0, stream>>>(
             next_state, S, V, states, B, g.nchunks, partial, token, new_state);
     return hipGetLastError();
+}
+
+hipError_t launch_masked_step(const int32_t *next_state, const uint32_t *allow, int S, int V,
+                              const int32_t *states, const void *logits, int dtype, int B,
+                              int64_t ld, int32_t *token, int32_t *new_state, void *workspace,
+                              hipStream_t stream)
+{
+    return launch_masked_rows(next_state, allow, S, V, states, logits, dtype, B, RowMap{ld, 0, 1}, token,
+                              new_state, workspace, stream);
 }
 
 }  // namespace dv

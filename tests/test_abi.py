@@ -146,3 +146,73 @@ def test_align_eos_rejects_bad_token_before_launch():
     st = lib.dv_align_eos(P, 16, P + GB, P + 2 * GB, 1000, P + 3 * GB + 8, 3, P + 3 * GB, P + 4 * GB,
                           P + 5 * GB, ws_bytes, None)
     assert st == ALIAS
+
+
+def _walk(ns=P, allow=P + GB, S=16, V=1000, states=P + 2 * GB, props=P + 3 * GB, s=4, ld=4, B=8,
+          acc=P + 4 * GB, fin=P + 5 * GB):
+    return lib.dv_spec_walk(ns, allow, S, V, states, props, s, ld, B, acc, fin, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(ns=None), INVALID),
+    (dict(props=None), INVALID),
+    (dict(acc=None), INVALID),
+    (dict(S=0), SHAPE),
+    (dict(B=-1), SHAPE),
+    (dict(s=-1), SHAPE),
+    (dict(s=1025, ld=2000), SHAPE),
+    (dict(ld=3), SHAPE),
+    (dict(B=300000, s=4), SHAPE),                 # B * (s + 1) above the batch limit
+    (dict(fin=P + 4 * GB + 4), ALIAS),
+    (dict(acc=P + 3 * GB + 16), ALIAS),           # output inside the proposals
+    (dict(fin=P + 2 * GB), ALIAS),                # final state written over the states
+])
+def test_spec_walk_rejects_before_launch(kw, status):
+    assert _walk(**kw) == status
+    assert lib.dv_last_error().startswith(b"dv_spec_walk")
+
+
+def test_spec_walk_empty_and_no_proposals():
+    assert _walk(B=0, states=None, props=None, acc=None, fin=None) == OK
+    assert _walk(B=0, ns=None) == INVALID
+
+
+def _verify(ns=P, allow=P + GB, S=16, V=1000, states=P + 2 * GB, props=P + 3 * GB, s=4, ldp=4,
+            logits=P + 4 * GB, dtype=1, ld_row=5000, ld_pos=1000, B=8, tok=P + 5 * GB,
+            acc=P + 6 * GB, new=P + 7 * GB, ws=P + 8 * GB, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = lib.dv_spec_verify_workspace_bytes(max(B, 0), max(s, 0), max(V, 1))
+    return lib.dv_spec_verify(ns, allow, S, V, states, props, s, ldp, logits, dtype, ld_row, ld_pos, B,
+                              tok, acc, new, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(allow=None), INVALID),
+    (dict(logits=None), INVALID),
+    (dict(tok=None), INVALID),
+    (dict(new=None), INVALID),
+    (dict(V=0), SHAPE),
+    (dict(s=-2), SHAPE),
+    (dict(ldp=2), SHAPE),
+    (dict(ld_row=-1), SHAPE),
+    (dict(ld_pos=1 << 41), SHAPE),
+    (dict(B=(1 << 20) // 5 + 1), SHAPE),
+    (dict(dtype=7), DTYPE),
+    (dict(acc=P + 5 * GB + 8), ALIAS),            # accepted inside token [B][s+1]
+    (dict(tok=P + 4 * GB + 64), ALIAS),           # token inside the logits
+    (dict(new=P + 2 * GB), ALIAS),                # new state written over the states
+    (dict(ws=None), WORKSPACE),
+    (dict(ws_bytes=16), WORKSPACE),
+    (dict(ws=P + 8 * GB + 128), WORKSPACE),
+    (dict(ws=P + 3 * GB), ALIAS),
+])
+def test_spec_verify_rejects_before_launch(kw, status):
+    assert _verify(**kw) == status
+    assert lib.dv_last_error().startswith(b"dv_spec_verify")
+
+
+def test_spec_verify_workspace_and_empty_batch():
+    assert lib.dv_spec_verify_workspace_bytes(-1, 4, 10) == 0
+    assert lib.dv_spec_verify_workspace_bytes(8, 2000, 10) == 0
+    assert lib.dv_spec_verify_workspace_bytes(256, 8, 128256) >= 2 * 256 * 9 * 4
+    assert _verify(B=0, states=None, props=None, logits=None, tok=None, acc=None, new=None) == OK

@@ -479,3 +479,185 @@ def test_chain_stops_on_eos(dv):
         np.testing.assert_array_equal(t_o[live] == eos, acc[cur[live]].astype(bool))
         cur = n_o
     assert (toks == eos).any()
+
+
+# ------------------------------------------- speculative chain check (Sec. 3.6)
+
+def _perturb(rng, greedy, V, keep):
+    """Proposals that follow ``greedy`` with probability ``keep`` per position,
+    else a random id (possibly outside [0, V))."""
+    other = rng.integers(-2, V + 2, greedy.shape).astype(np.int32)
+    return np.where(rng.random(greedy.shape) < keep, greedy, other).astype(np.int32)
+
+
+def _greedy_proposals(ns_o, al_o, states, xs_pos, s):
+    """The oracle's greedy chain over the first s positions: [B][s]."""
+    out = np.empty((states.shape[0], s), np.int32)
+    cur = states
+    for j in range(s):
+        t, cur = oracle.masked_step(ns_o, al_o, cur, xs_pos[:, j])
+        out[:, j] = t
+    return out
+
+
+def _check_spec(dv, ns, al, ns_o, al_o, states, props, x_dev, label):
+    tok, acc, nst = dv.spec_verify(ns, al, _dev(states), _dev(props), x_dev)
+    a_w, f_w = dv.spec_walk(ns, al, _dev(states), _dev(props))
+    torch.cuda.synchronize()
+    xs = to_oracle(x_dev)
+    tok_o, acc_o, nst_o = oracle.spec_verify(ns_o, al_o, states, props, xs)
+    np.testing.assert_array_equal(tok.cpu().numpy(), tok_o, err_msg=label)
+    np.testing.assert_array_equal(acc.cpu().numpy(), acc_o, err_msg=label)
+    np.testing.assert_array_equal(nst.cpu().numpy(), nst_o, err_msg=label)
+    a_o, f_o = oracle.spec_walk(ns_o, al_o, states, props)
+    np.testing.assert_array_equal(a_w.cpu().numpy(), a_o, err_msg=label)
+    np.testing.assert_array_equal(f_w.cpu().numpy(), f_o, err_msg=label)
+    return acc_o
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_spec_paper_example(dv, dtype):
+    g = json.load(open(os.path.join(GOLDEN, "fig_nfa_int.json")))
+    e, sp = g["eos"], g["spec"]
+    trans = W.dfa_from_spec(len(g["states"]), g["moves"])
+    offsets, data = W.vocab_from_tokens([t.encode() for t in g["vocab"]] + [b"</s>"])
+    acc = np.array(e["accepting"], np.uint8)
+    ns, al = dv.align(_dev(trans), _dev(offsets), _dev(data), accepting=_dev(acc), eos_token=e["eos_token"])
+    lg = np.array([[[float(v) for v in r] for r in rows] for rows in sp["logits"]], np.float32)
+    x = _dev(lg).to(dtype)
+    states, props = np.array(sp["states"], np.int32), np.array(sp["proposals"], np.int32)
+    tok, a, nst = dv.spec_verify(ns, al, _dev(states), _dev(props), x)
+    a_w, f_w = dv.spec_walk(ns, al, _dev(states), _dev(props))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(tok.cpu().numpy(), sp["expected_token"])
+    np.testing.assert_array_equal(a.cpu().numpy(), sp["expected_accepted"])
+    np.testing.assert_array_equal(nst.cpu().numpy(), sp["expected_new_state"])
+    np.testing.assert_array_equal(a_w.cpu().numpy(), sp["expected_walk_accepted"])
+    np.testing.assert_array_equal(f_w.cpu().numpy(), sp["expected_walk_final_state"])
+
+
+@pytest.mark.parametrize("wid,s", [(1, 4), (2, 4), (2, 8), (3, 6)])
+@pytest.mark.parametrize("layout", ["rows", "steps"])
+def test_spec_workload_full(dv, wid, s, layout):
+    """Every row and position against the oracle.  ``rows``: the model's
+    [B][s+1][V] output; ``steps``: positions stored as [s+1][B][V] and passed
+    through strides."""
+    w = W.WORKLOADS[wid]
+    _say(f"spec verify workload {w.describe()} s={s} layout={layout}")
+    trans, offsets, data, ns, al = _workload_table(dv, wid)
+    ns_o, al_o = oracle.align(trans, offsets, data)
+    x = W.logits_all(wid, device=DEV, steps=s + 1)           # [s+1][B][V]
+    x_rows = x.transpose(0, 1)                                # [B][s+1][V] view
+    if layout == "rows":
+        x_rows = x_rows.contiguous()
+    states = W.init_states(wid)
+    states[::7] = -1
+    rng = np.random.default_rng(200 + wid * 10 + s)
+    greedy = _greedy_proposals(ns_o, al_o, states, to_oracle(x_rows), s)
+    props = _perturb(rng, greedy, w.V, 0.85)
+    acc = _check_spec(dv, ns, al, ns_o, al_o, states, props, x_rows, f"workload {wid} s={s} {layout}")
+    _say(f"  accepted histogram {np.bincount(acc, minlength=s + 1).tolist()}")
+
+
+@pytest.mark.parametrize("wid,s", [(4, 8), (5, 4)])
+def test_spec_workload_sampled(dv, wid, s):
+    """Full-size batch in the benchmark's layout; sampled rows against the
+    oracle (table rows on demand), properties over every row."""
+    w = W.WORKLOADS[wid]
+    _say(f"spec verify workload {w.describe()} s={s} (sampled rows)")
+    trans, offsets, data, ns, al = _workload_table(dv, wid)
+    x = W.logits_all(wid, device=DEV, steps=s + 1).transpose(0, 1).contiguous()  # [B][s+1][V]
+    init = W.init_states(wid)
+    rng = np.random.default_rng(300 + wid)
+    rows = np.unique(np.concatenate([[0, w.B - 1], rng.integers(0, w.B, 14)]))
+    cache = oracle.RowCache(trans, offsets, data)
+    xr = to_oracle(x[torch.from_numpy(rows.astype(np.int64)).to(DEV)])
+    props = rng.integers(-2, w.V + 2, (w.B, s)).astype(np.int32)
+    for i, b in enumerate(rows):
+        greedy, _ = oracle.masked_chain(cache, init[b], xr[i, :s])
+        props[b] = _perturb(rng, greedy, w.V, 0.85)
+    tok, acc, nst = dv.spec_verify(ns, al, _dev(init), _dev(props), x)
+    a_w, f_w = dv.spec_walk(ns, al, _dev(init), _dev(props))
+    torch.cuda.synchronize()
+    tok_h, acc_h, nst_h = tok.cpu().numpy(), acc.cpu().numpy(), nst.cpu().numpy()
+    for i, b in enumerate(rows):
+        t_o, a_o, n_o = oracle.spec_verify_rows(cache, init[b], props[b], xr[i])
+        np.testing.assert_array_equal(tok_h[b], t_o, err_msg=f"workload {wid} row {b}")
+        assert acc_h[b] == a_o and nst_h[b] == n_o, f"workload {wid} row {b}"
+    # every row: a verified prefix is admitted by the walk; emitted tokens are allowed
+    assert bool((acc <= a_w).all())
+    assert bool(((acc >= 0) & (acc <= s)).all())
+    first = tok.gather(1, acc.to(torch.int64)[:, None])[:, 0]
+    assert bool(((first == -1) == (nst == -1)).all())
+    _say(f"  {len(rows)} rows bit-exact; mean accepted {float(acc.float().mean()):.2f}")
+
+
+def test_spec_zero_proposals_is_a_step(dv):
+    w = W.WORKLOADS[3]
+    trans, offsets, data, ns, al = _workload_table(dv, 3)
+    x = W.logits(3, 0, device=DEV)                            # [B][V]
+    states = _dev(W.init_states(3))
+    tok, acc, nst = dv.spec_verify(ns, al, states, torch.empty((w.B, 0), dtype=torch.int32, device=DEV),
+                                   x[:, None, :])
+    t, n = dv.masked_step(ns, al, states, x)
+    a_w, f_w = dv.spec_walk(ns, al, states, torch.empty((w.B, 0), dtype=torch.int32, device=DEV))
+    torch.cuda.synchronize()
+    assert torch.equal(tok[:, 0], t) and torch.equal(nst, n)
+    assert int(acc.abs().sum()) == 0 and int(a_w.abs().sum()) == 0
+    assert torch.equal(f_w, torch.where((states >= 0) & (states < w.S), states, torch.full_like(states, -1)))
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("B,s,V,pad_prop,misalign", [
+    (1, 1, 1, 0, 0),            # a one-token vocabulary
+    (1, 64, 1000, 3, 0),        # one long row of proposals: positions split over chunks
+    (3, 5, 33, 0, 1),           # a ragged word; rows not 16-byte aligned (scalar path)
+    (40, 7, 4099, 2, 0),        # 320 positions: one block per position
+    (300, 2, 20000, 0, 1),      # many rows, odd position stride
+])
+def test_spec_shapes_strides_and_edges(dv, dtype, B, s, V, pad_prop, misalign):
+    rng = np.random.default_rng(B * 1000 + s * 10 + V)
+    S = 12
+    trans = rng.integers(-1, S + 1, (S, 256)).astype(np.int32)       # includes out-of-range targets
+    trans[:, rng.random(256) < 0.5] = -1
+    lens = rng.integers(1, 4, V)
+    offsets = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    data = rng.integers(0, 256, int(offsets[-1])).astype(np.uint8)
+    ns, al = _align(dv, trans, offsets, data)
+    ns_o, al_o = oracle.align(trans, offsets, data)
+    states = rng.integers(-2, S + 2, B).astype(np.int32)
+    ld_pos = V + misalign
+    buf = torch.randn(B * (s + 1) * ld_pos + 8, device=DEV).to(dtype)
+    x = buf.as_strided((B, s + 1, V), ((s + 1) * ld_pos, ld_pos, 1), misalign)
+    greedy = _greedy_proposals(ns_o, al_o, states, to_oracle(x), s)
+    props_full = np.zeros((B, s + pad_prop), np.int32)
+    props_full[:, :s] = _perturb(rng, greedy, V, 0.8)
+    props_full[:, :s][rng.random((B, s)) < 0.05] = np.int32(2 ** 31 - 1)
+    props_full[:, :s][rng.random((B, s)) < 0.05] = np.int32(-2 ** 31)
+    props_dev = _dev(props_full)[:, :s]                      # row stride s + pad_prop
+    tok, acc, nst = dv.spec_verify(ns, al, _dev(states), props_dev, x)
+    a_w, f_w = dv.spec_walk(ns, al, _dev(states), props_dev)
+    torch.cuda.synchronize()
+    props = props_full[:, :s]
+    tok_o, acc_o, nst_o = oracle.spec_verify(ns_o, al_o, states, props, to_oracle(x))
+    a_o, f_o = oracle.spec_walk(ns_o, al_o, states, props)
+    np.testing.assert_array_equal(tok.cpu().numpy(), tok_o)
+    np.testing.assert_array_equal(acc.cpu().numpy(), acc_o)
+    np.testing.assert_array_equal(nst.cpu().numpy(), nst_o)
+    np.testing.assert_array_equal(a_w.cpu().numpy(), a_o)
+    np.testing.assert_array_equal(f_w.cpu().numpy(), f_o)
+
+
+def test_spec_empty_batch_and_aliasing(dv):
+    trans, offsets, data, ns, al = _workload_table(dv, 1)
+    e = torch.empty((0,), dtype=torch.int32, device=DEV)
+    tok, acc, nst = dv.spec_verify(ns, al, e, torch.empty((0, 3), dtype=torch.int32, device=DEV),
+                                   torch.empty((0, 4, ns.shape[1]), device=DEV))
+    assert tok.shape == (0, 4) and acc.numel() == 0
+    states = _dev(np.zeros(2, np.int32))
+    props = _dev(np.zeros((2, 3), np.int32))
+    x = torch.randn((2, 4, ns.shape[1]), device=DEV)
+    with pytest.raises(dv.DvError):
+        dv.spec_verify(ns, al, states, props, x, new_state=states)
+    with pytest.raises(dv.DvError):
+        dv.spec_walk(ns, al, states, props, accepted=props[0])

@@ -596,3 +596,17 @@ def test_spec_perfect_draft_is_fully_accepted(tiny_table, oracle_lib):
     assert (acc[live] == s).all()
     np.testing.assert_array_equal(tok[live, s], bonus[live])
     np.testing.assert_array_equal(nst[live], after[live])
+
+
+def test_spec_verify_rows_matches_table_version(tiny_table, oracle_lib):
+    """The row-cache form used for full-size workloads agrees with the
+    whole-table form on a workload small enough for both."""
+    trans, offsets, data, ns, al = tiny_table
+    rng = np.random.default_rng(37)
+    states, props, lg = _spec_inputs(ns, al, rng, 20, 5, 0.7, oracle_lib, "bf16")
+    tok, acc, nst = oracle.spec_verify(ns, al, states, props, lg, lib=oracle_lib)
+    cache = oracle.RowCache(trans, offsets, data, lib=oracle_lib)
+    for b in range(20):
+        t, a, n = oracle.spec_verify_rows(cache, states[b], props[b], lg[b], lib=oracle_lib)
+        np.testing.assert_array_equal(t, tok[b])
+        assert a == acc[b] and n == nst[b]
