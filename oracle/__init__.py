@@ -16,6 +16,8 @@ Way"):
   update) with Algorithm 3's argmax over an admissible token set.
 * ``align_eos``: the same table with an end-of-sequence column (Algorithm 1
   stops on EOS; Sec. 3.2 makes EOS a terminal), allowed in accepting states.
+* ``masked_step_opportunistic``: opportunistic masking (Sec. 3.5, further
+  optimizations) -- the model's unconstrained choice is checked first.
 * ``spec_walk`` / ``spec_verify``: the speculative chain check of Sec. 3.6 --
   how many proposed tokens the constraint admits, and greedy verification of
   the proposals against the model's logits at every proposed position.
@@ -82,6 +84,11 @@ def _bind(lib):
                                        ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int,
                                        ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, _i32p, _i32p,
                                        _i32p]
+    lib.oracle_masked_step_opportunistic.restype = None
+    lib.oracle_masked_step_opportunistic.argtypes = [_i32p, _u32p, ctypes.c_int32, ctypes.c_int32,
+                                                     _i32p, ctypes.c_void_p, ctypes.c_int,
+                                                     ctypes.c_int32, ctypes.c_int64, _i32p, _i32p,
+                                                     ctypes.c_void_p]
     lib.oracle_walk_lookups.restype = ctypes.c_int64
     lib.oracle_walk_lookups.argtypes = [_i32p, ctypes.c_int32, _i32p, _u8p, ctypes.c_int32,
                                         _i32p, ctypes.c_int64]
@@ -204,6 +211,28 @@ def masked_step(next_state, allow, states, logits, num_tokens: int | None = None
         lib.oracle_masked_step(_p(next_state, _i32p), _p(allow, _u32p), S, V, _p(states, _i32p),
                                logits.ctypes.data, dt, B, ld, _p(tok, _i32p), _p(nst, _i32p))
     return tok, nst
+
+
+def masked_step_opportunistic(next_state, allow, states, logits, lib=None):
+    """Opportunistic masking (Sec. 3.5): the unconstrained choice first, the
+    mask only when it is not allowed.  Returns (token, new_state,
+    unconstrained_ok[B] bool)."""
+    lib = lib or load()
+    next_state = _c(next_state, np.int32)
+    allow = _c(allow, np.uint32)
+    states = _c(states, np.int32)
+    logits, dt = _logit_array(np.ascontiguousarray(logits))
+    S, V = next_state.shape
+    B = states.shape[0]
+    ld = logits.shape[1] if B else V
+    tok = np.empty(B, np.int32)
+    nst = np.empty(B, np.int32)
+    ok = np.zeros(B, np.uint8)
+    if B:
+        lib.oracle_masked_step_opportunistic(_p(next_state, _i32p), _p(allow, _u32p), S, V,
+                                             _p(states, _i32p), logits.ctypes.data, dt, B, ld,
+                                             _p(tok, _i32p), _p(nst, _i32p), ok.ctypes.data)
+    return tok, nst, ok.astype(bool)
 
 
 def spec_walk(next_state, allow, states, proposals, lib=None):

@@ -290,3 +290,45 @@ void oracle_spec_verify(const int32_t *next_state, const uint32_t *allow, int32_
         new_state[b] = ns;
     }
 }
+
+/* Opportunistic masking (Sec. 3.5, further optimizations): decode first
+ * without the constraint, check the model's own choice against the mask,
+ * and compute the masked choice only when that check fails.  The
+ * unconstrained choice follows the same value rules as the masked one
+ * (NaN ranks as -inf, ties to the lowest index). */
+void oracle_masked_step_opportunistic(const int32_t *next_state, const uint32_t *allow,
+                                      int32_t num_states, int32_t num_tokens,
+                                      const int32_t *states, const void *logits, int dtype,
+                                      int32_t batch, int64_t ld_logits, int32_t *token,
+                                      int32_t *new_state, uint8_t *unconstrained_ok)
+{
+    int64_t words = ((int64_t)num_tokens + 31) / 32;
+    size_t elt = dtype == 0 ? 4 : 2;
+    for (int32_t b = 0; b < batch; ++b) {
+        int32_t s = oracle_canon(states[b], num_states);
+        const void *row = (const char *)logits + (size_t)b * (size_t)ld_logits * elt;
+        int32_t tok = -1;
+        int ok = 0;
+        if (s != ORACLE_DEAD) {
+            /* the model's own greedy choice: argmax over every token */
+            int32_t free_tok = 0;
+            double best_v = 0.0;
+            for (int32_t i = 0; i < num_tokens; ++i) {
+                double v = oracle_logit(row, i, dtype);
+                if (isnan(v))
+                    v = -INFINITY;
+                if (i == 0 || v > best_v) {
+                    free_tok = i;
+                    best_v = v;
+                }
+            }
+            const uint32_t *arow = allow + (int64_t)s * words;
+            ok = (int)((arow[free_tok / 32] >> (free_tok % 32)) & 1u);
+            tok = ok ? free_tok : oracle_masked_argmax(arow, row, dtype, num_tokens);
+        }
+        token[b] = tok;
+        new_state[b] = tok == -1 ? ORACLE_DEAD : next_state[(int64_t)s * num_tokens + tok];
+        if (unconstrained_ok)
+            unconstrained_ok[b] = (uint8_t)ok;
+    }
+}

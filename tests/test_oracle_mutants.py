@@ -45,6 +45,9 @@ MUTANTS = {
         "ns = tok == -1 ? ORACLE_DEAD : next_state[(int64_t)oracle_canon(states[b], num_states) * num_tokens + tok];"),
     "spec position stride ignored": ("j * ld_pos", "j * (int64_t)num_tokens"),
     "spec stops one position late": ("a = j;\n", "a = j + (j < num_proposed);\n"),
+    "opportunistic skips the check": ("tok = ok ? free_tok :", "tok = 1 ? free_tok :"),
+    "opportunistic free ties to highest": ("if (i == 0 || v > best_v)", "if (i == 0 || v >= best_v)"),
+    "opportunistic free keeps nan": ("v = -INFINITY;\n                if (i == 0", "v = v;\n                if (i == 0"),
     "zero-length token dies": ("int32_t st = oracle_canon(s, num_states);\n    for",
                                "int32_t st = len ? oracle_canon(s, num_states) : ORACLE_DEAD;\n    for"),
 }
@@ -87,6 +90,9 @@ def _checks(lib):
         ("spec_legal", lambda: P.test_spec_verify_accepts_only_legal_prefixes(table, lib)),
         ("spec_zero", lambda: P.test_spec_zero_proposals_is_one_masked_step(table, lib)),
         ("spec_perfect", lambda: P.test_spec_perfect_draft_is_fully_accepted(table, lib)),
+        ("opportunistic", lambda: [P.test_opportunistic_equals_masked_step(a, d, table, lib)
+                                   for a in (0.0, 0.7, 1.0) for d in ("f32", "bf16")]),
+        ("opportunistic_tie", lambda: P.test_opportunistic_planted_tie_goes_to_lowest_allowed(lib)),
         ("ties_bf16", lambda: [P.test_planted_ties_and_specials_bf16(b, a, e, lib)
                                for b, a, e in [([0x8000, 0x0000, 0x0001], [0, 1, 2], 2),
                                                ([0x3F80, 0x3F80, 0x3F80], [1, 2], 1),

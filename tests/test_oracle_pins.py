@@ -610,3 +610,51 @@ def test_spec_verify_rows_matches_table_version(tiny_table, oracle_lib):
         t, a, n = oracle.spec_verify_rows(cache, states[b], props[b], lg[b], lib=oracle_lib)
         np.testing.assert_array_equal(t, tok[b])
         assert a == acc[b] and n == nst[b]
+
+
+# ------------------------------------- opportunistic masking (Sec. 3.5, optimizations)
+
+@pytest.mark.parametrize("adherent", [0.0, 0.7, 1.0])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_opportunistic_equals_masked_step(adherent, dtype, tiny_table, oracle_lib):
+    """Checking the model's own choice first never changes the result, and the
+    check succeeds exactly when numpy's argmax (NaN as -inf) is allowed."""
+    _, _, _, ns, al = tiny_table
+    S, V = ns.shape
+    rng = np.random.default_rng(41)
+    B = 64
+    states = rng.integers(0, S, B).astype(np.int32)
+    states[:3] = [-1, S, 0]
+    x = rng.standard_normal((B, V)).astype(np.float32)
+    x[5, rng.integers(0, V, 40)] = np.nan
+    x[6] = np.nan
+    t, _ = oracle.masked_step(ns, al, states, x, lib=oracle_lib)
+    adh = rng.random(B) < adherent
+    x[adh & (t >= 0), t[adh & (t >= 0)]] = 40.0   # the model wants the masked choice itself
+    lg = _bf16_bits(x) if dtype == "bf16" else x
+    tok, nst, ok = oracle.masked_step_opportunistic(ns, al, states, lg, lib=oracle_lib)
+    t2, n2 = oracle.masked_step(ns, al, states, lg, lib=oracle_lib)
+    np.testing.assert_array_equal(tok, t2)
+    np.testing.assert_array_equal(nst, n2)
+    xf = lg.astype(np.uint32) << 16 if dtype == "bf16" else lg
+    xf = xf.view(np.float32) if dtype == "bf16" else xf
+    free = np.argmax(np.where(np.isnan(xf), -np.inf, xf), axis=1)
+    live = (states >= 0) & (states < S)
+    allowed_free = np.array([ns[s, f] != -1 if l else False for s, f, l in zip(states, free, live)])
+    np.testing.assert_array_equal(ok, allowed_free)
+    if adherent == 1.0:
+        assert ok[live & (t >= 0)].all()
+
+
+def test_opportunistic_planted_tie_goes_to_lowest_allowed(oracle_lib):
+    V = 40
+    ns = np.full((1, V), -1, np.int32)
+    ns[0, [3, 7, 11]] = 0
+    al = _pack_allow(ns != -1)
+    x = np.zeros((1, V), np.float32)
+    x[0, [3, 7, 20]] = 5.0        # tie at 3 and 7 (allowed) and 20 (not allowed)
+    tok, _, ok = oracle.masked_step_opportunistic(ns, al, np.zeros(1, np.int32), x, lib=oracle_lib)
+    assert tok[0] == 3 and ok[0]
+    x[0, 1] = 5.0                 # now the lowest maximum (1) is not allowed
+    tok, _, ok = oracle.masked_step_opportunistic(ns, al, np.zeros(1, np.int32), x, lib=oracle_lib)
+    assert tok[0] == 3 and not ok[0]
