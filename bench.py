@@ -16,6 +16,8 @@ Reported (one JSON line):
                around the replay of the job's decode steps, captured once as
                a HIP graph, on the launch stream; divided by the step count)
   roofline_align  dv_align against the HBM write roofline (4.125 B / pair)
+  opportunistic  the decode chain with the model's own choice checked first
+               (Sec. 3.5), on the workload's logits and on adherent logits
   spec_verify  greedy verification of s = 8 proposed tokens per row (Sec. 3.6)
                over windows of the job's decode chain, with its own roofline
   cpu_baseline the CPU oracle on a bounded sample of the same workload
@@ -60,6 +62,7 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-probes", action="store_true", help="skip the roofline probes")
     ap.add_argument("--no-spec", action="store_true", help="skip the speculative-verification leg")
+    ap.add_argument("--no-opportunistic", action="store_true", help="skip the opportunistic-masking leg")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
 
@@ -284,6 +287,73 @@ def bench_spec(dv, w, ns, al, x, tokens_all, states_all, dev, s=8, keep=0.9, rep
     }
 
 
+def bench_opportunistic(dv, w, ns, al, x, tokens_all, states_all, dev, adherent=(0.9, 1.0), reps=3):
+    """Opportunistic masking (Sec. 3.5): the job's decode chain with the model's
+    own choice checked first, on the workload's logits and on copies in which
+    a fraction ``adherent`` of the row-steps favour the chain's own (allowed)
+    choice -- raising the chosen logit leaves the chain unchanged.  With every
+    row-step adherent no row is read twice: the time is that of the
+    unconstrained greedy pass alone.  Each chain
+    is captured as a HIP graph and replayed; the check's hit rate is the
+    fraction of live row-steps whose overall argmax is allowed."""
+    import numpy as np
+    import torch
+
+    steps = tokens_all.shape[0]
+    ws = dv.step_workspace(w.B, w.V, dev)
+    sts = torch.empty_like(states_all)
+    tks = torch.empty_like(tokens_all)
+    stream = torch.cuda.current_stream(dev)
+
+    def timed_chain(xv):
+        def launches():
+            for k in range(steps):
+                dv.masked_step(ns, al, sts[k], xv[k], token=tks[k], new_state=sts[k + 1], workspace=ws,
+                               opportunistic=True)
+        sts[0].copy_(states_all[0])
+        launches()
+        torch.cuda.synchronize()
+        same_eager = bool(torch.equal(tks, tokens_all))
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream(dev)
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            launches()
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            launches()
+        times = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            graph.replay()
+            b.record(stream)
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b) / 1e3 / steps)
+        same = same_eager and bool(torch.equal(tks, tokens_all))
+        free = torch.stack([xv[k].float().argmax(dim=1) for k in range(steps)]).to(torch.int64)
+        st = states_all[:-1].to(torch.int64)
+        live = st >= 0
+        word = al[st.clamp(min=0), free // 32].to(torch.int64) & 0xFFFFFFFF
+        hit = ((word >> (free % 32)) & 1).bool() & live
+        return {"us_per_step": float(np.median(times)) * 1e6, "matches_masked_step": same,
+                "check_hit_rate": float(hit.sum()) / max(int(live.sum()), 1)}
+
+    out = {"random_logits": timed_chain(x)}
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    u = torch.rand(tokens_all.shape, generator=g, device=dev)
+    for frac in adherent:
+        pick = (u < frac) & (tokens_all >= 0)
+        k_idx, b_idx = torch.nonzero(pick, as_tuple=True)
+        xa = x.clone()
+        xa[k_idx, b_idx, tokens_all[k_idx, b_idx].to(torch.int64)] = 30.0
+        out[f"adherent_{frac:g}"] = timed_chain(xa)
+        del xa
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -422,6 +492,10 @@ def main():
                            "traffic": traffic_record("align", wid)},
         "kernel_source_hash": {k: kernel_source_hash(k) for k in KERNEL_SOURCES},
     }
+    if not args.no_opportunistic and w.dtype == "bf16":
+        log("opportunistic masking")
+        out["opportunistic"] = bench_opportunistic(dv, w, ns, al, x, tokens_all, states_all, dev)
+        out["opportunistic"]["masked_us_per_step"] = mean_launch_s * 1e6
     if not args.no_spec:
         log("speculative verification")
         out["spec_verify"] = bench_spec(dv, w, ns, al, x, tokens_all, states_all, dev)

@@ -14,6 +14,9 @@
  *                   and advance the state with the chosen token.
  *   dv_align_eos    dv_align with an end-of-sequence token that is allowed
  *                   exactly in accepting states.
+ *   dv_masked_step_opportunistic
+ *                   dv_masked_step that checks the model's own choice first
+ *                   (opportunistic masking, Sec. 3.5).
  *   dv_spec_walk,   the speculative chain check of Sec. 3.6: how many
  *   dv_spec_verify  proposed tokens the constraint admits, and greedy
  *                   verification of the proposals against the model's logits
@@ -184,6 +187,28 @@ DV_API size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens);
  *   ld_logits < V), DV_ERR_DTYPE, DV_ERR_ALIAS, DV_ERR_WORKSPACE, DV_ERR_HIP.
  */
 DV_API dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow,
+                         int32_t num_states, int32_t num_tokens,
+                         const int32_t *states, const void *logits, int32_t dtype,
+                         int32_t batch, int64_t ld_logits,
+                         int32_t *token, int32_t *new_state,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * dv_masked_step_opportunistic -- dv_masked_step with opportunistic masking
+ * (Sec. 3.5, further optimizations): the model's own greedy choice over all
+ * V logits is found first, without reading the mask, and checked against
+ * the mask; only when it is not allowed is the masked choice computed.
+ *
+ * The outputs are exactly those of dv_masked_step (an allowed overall
+ * maximum at the lowest index is also the masked one), so the two are
+ * interchangeable; this one reads less memory when the model mostly picks
+ * allowed tokens and reads a row twice when it does not.  The check runs
+ * first for bf16 rows that one block covers (batch >= 256); other shapes take
+ * dv_masked_step's kernels.
+ * Arguments, workspace (dv_masked_step_workspace_bytes) and errors as
+ *   dv_masked_step.
+ */
+DV_API dv_status dv_masked_step_opportunistic(const int32_t *next_state, const uint32_t *allow,
                          int32_t num_states, int32_t num_tokens,
                          const int32_t *states, const void *logits, int32_t dtype,
                          int32_t batch, int64_t ld_logits,

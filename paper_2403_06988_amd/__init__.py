@@ -62,6 +62,9 @@ def _load():
     lib.dv_masked_step_workspace_bytes.argtypes = [i32, i32]
     lib.dv_masked_step.restype = ctypes.c_int
     lib.dv_masked_step.argtypes = [vp, vp, i32, i32, vp, vp, i32, i32, i64, vp, vp, vp, sz, vp]
+    lib.dv_masked_step_opportunistic.restype = ctypes.c_int
+    lib.dv_masked_step_opportunistic.argtypes = [vp, vp, i32, i32, vp, vp, i32, i32, i64, vp, vp, vp, sz,
+                                                 vp]
     lib.dv_spec_walk.restype = ctypes.c_int
     lib.dv_spec_walk.argtypes = [vp, vp, i32, i32, vp, vp, i32, i64, i32, vp, vp, vp]
     lib.dv_spec_verify_workspace_bytes.restype = sz
@@ -168,9 +171,11 @@ def step_workspace(batch: int, num_tokens: int, device) -> torch.Tensor:
 
 
 def masked_step(next_state, allow, states, logits, token=None, new_state=None, workspace=None,
-                stream=None):
+                stream=None, opportunistic=False):
     """One greedy masked decoding step.  logits [B][ld] (fp32 or bf16, unit
-    stride along the vocabulary).  Returns (token [B] int32, new_state [B] int32)."""
+    stride along the vocabulary).  Returns (token [B] int32, new_state [B] int32).
+    ``opportunistic``: check the model's own choice against the mask first
+    (dv_masked_step_opportunistic; same results)."""
     dev = states.device
     _want(next_state, "next_state", torch.int32, dev)
     _want(allow, "allow", torch.int32, dev)
@@ -196,10 +201,10 @@ def masked_step(next_state, allow, states, logits, token=None, new_state=None, w
         new_state = torch.empty(B, dtype=torch.int32, device=dev)
     if workspace is None:
         workspace = step_workspace(B, V, dev)
-    st = lib.dv_masked_step(_ptr(next_state), _ptr(allow), S, V, _ptr(states), _ptr(logits), dt, B,
-                            ld, _ptr(token), _ptr(new_state), _ptr(workspace), workspace.numel(),
-                            _stream(stream, dev))
-    _check(st, "dv_masked_step")
+    fn = lib.dv_masked_step_opportunistic if opportunistic else lib.dv_masked_step
+    st = fn(_ptr(next_state), _ptr(allow), S, V, _ptr(states), _ptr(logits), dt, B, ld, _ptr(token),
+            _ptr(new_state), _ptr(workspace), workspace.numel(), _stream(stream, dev))
+    _check(st, "dv_masked_step_opportunistic" if opportunistic else "dv_masked_step")
     return token, new_state
 
 

@@ -127,28 +127,28 @@ size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens)
     return dv::step_workspace_bytes(batch, num_tokens);
 }
 
-dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow, int32_t num_states,
-                         int32_t num_tokens, const int32_t *states, const void *logits, int32_t dtype,
-                         int32_t batch, int64_t ld_logits, int32_t *token, int32_t *new_state,
-                         void *workspace, size_t workspace_bytes, void *stream)
+static dv_status step_common(const char *name, bool opportunistic, const int32_t *next_state,
+                             const uint32_t *allow, int32_t num_states, int32_t num_tokens, const int32_t *states,
+                             const void *logits, int32_t dtype, int32_t batch, int64_t ld_logits, int32_t *token,
+                             int32_t *new_state, void *workspace, size_t workspace_bytes, void *stream)
 {
     g_error[0] = '\0';
     if (!next_state || !allow)
-        return fail(DV_ERR_INVALID_ARG, "dv_masked_step: next_state and allow must be non-NULL");
+        return fail(DV_ERR_INVALID_ARG, "%s: next_state and allow must be non-NULL", name);
     if (batch > 0 && (!states || !logits || !token || !new_state))
-        return fail(DV_ERR_INVALID_ARG, "dv_masked_step: states, logits, token and new_state must be "
-                                        "non-NULL when batch > 0");
+        return fail(DV_ERR_INVALID_ARG, "%s: states, logits, token and new_state must be "
+                                        "non-NULL when batch > 0", name);
     if (num_states < 1 || num_states > DV_MAX_STATES)
-        return fail(DV_ERR_SHAPE, "dv_masked_step: num_states=%d outside [1, %d]", num_states, DV_MAX_STATES);
+        return fail(DV_ERR_SHAPE, "%s: num_states=%d outside [1, %d]", name, num_states, DV_MAX_STATES);
     if (num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
-        return fail(DV_ERR_SHAPE, "dv_masked_step: num_tokens=%d outside [1, %d]", num_tokens, DV_MAX_TOKENS);
+        return fail(DV_ERR_SHAPE, "%s: num_tokens=%d outside [1, %d]", name, num_tokens, DV_MAX_TOKENS);
     if (batch < 0 || batch > DV_MAX_BATCH)
-        return fail(DV_ERR_SHAPE, "dv_masked_step: batch=%d outside [0, %d]", batch, DV_MAX_BATCH);
+        return fail(DV_ERR_SHAPE, "%s: batch=%d outside [0, %d]", name, batch, DV_MAX_BATCH);
     if (ld_logits < num_tokens || ld_logits > ((int64_t)1 << 40))
-        return fail(DV_ERR_SHAPE, "dv_masked_step: ld_logits=%lld must be >= num_tokens=%d",
+        return fail(DV_ERR_SHAPE, "%s: ld_logits=%lld must be >= num_tokens=%d", name,
                     (long long)ld_logits, num_tokens);
     if (dtype != DV_F32 && dtype != DV_BF16)
-        return fail(DV_ERR_DTYPE, "dv_masked_step: unknown dtype %d", dtype);
+        return fail(DV_ERR_DTYPE, "%s: unknown dtype %d", name, dtype);
     if (batch == 0)
         return DV_OK;
     const size_t S = (size_t)num_states, V = (size_t)num_tokens, W = (V + 31) / 32, B = (size_t)batch;
@@ -158,25 +158,48 @@ dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow, int32
     const Range r_st = range_of(states, B * 4);
     const Range r_lg = range_of(logits, ((B - 1) * (size_t)ld_logits + V) * elt);
     if (overlap(r_tok, r_new))
-        return fail(DV_ERR_ALIAS, "dv_masked_step: token and new_state overlap");
+        return fail(DV_ERR_ALIAS, "%s: token and new_state overlap", name);
     for (Range out : {r_tok, r_new})
         if (overlap(out, r_ns) || overlap(out, r_al) || overlap(out, r_st) || overlap(out, r_lg))
-            return fail(DV_ERR_ALIAS, "dv_masked_step: an output overlaps an input "
-                                      "(ping-pong two state buffers instead of updating in place)");
+            return fail(DV_ERR_ALIAS, "%s: an output overlaps an input "
+                                      "(ping-pong two state buffers instead of updating in place)", name);
     const size_t need = dv::step_workspace_bytes(batch, num_tokens);
     if (!workspace || workspace_bytes < need)
-        return fail(DV_ERR_WORKSPACE, "dv_masked_step: workspace of %zu bytes given, %zu needed",
-                    workspace_bytes, need);
+        return fail(DV_ERR_WORKSPACE, "%s: workspace of %zu bytes given, %zu needed", name, workspace_bytes,
+                    need);
     if (reinterpret_cast<uintptr_t>(workspace) & 255)
-        return fail(DV_ERR_WORKSPACE, "dv_masked_step: workspace must be 256-byte aligned");
+        return fail(DV_ERR_WORKSPACE, "%s: workspace must be 256-byte aligned", name);
     const Range r_ws = range_of(workspace, need);
     for (Range r : {r_tok, r_new, r_ns, r_al, r_st, r_lg})
         if (overlap(r_ws, r))
-            return fail(DV_ERR_ALIAS, "dv_masked_step: workspace overlaps an input or output");
-    return hip_status(dv::launch_masked_step(next_state, allow, num_states, num_tokens, states, logits,
-                                             dtype, batch, ld_logits, token, new_state, workspace,
-                                             static_cast<hipStream_t>(stream)),
-                      "dv_masked_step launch");
+            return fail(DV_ERR_ALIAS, "%s: workspace overlaps an input or output", name);
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    return hip_status(opportunistic
+                          ? dv::launch_masked_step_opportunistic(next_state, allow, num_states, num_tokens, states,
+                                                                 logits, dtype, batch, ld_logits, token, new_state,
+                                                                 workspace, st)
+                          : dv::launch_masked_step(next_state, allow, num_states, num_tokens, states, logits,
+                                                   dtype, batch, ld_logits, token, new_state, workspace, st),
+                      "launch");
+}
+
+dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow, int32_t num_states,
+                         int32_t num_tokens, const int32_t *states, const void *logits, int32_t dtype,
+                         int32_t batch, int64_t ld_logits, int32_t *token, int32_t *new_state,
+                         void *workspace, size_t workspace_bytes, void *stream)
+{
+    return step_common("dv_masked_step", false, next_state, allow, num_states, num_tokens, states, logits,
+                       dtype, batch, ld_logits, token, new_state, workspace, workspace_bytes, stream);
+}
+
+dv_status dv_masked_step_opportunistic(const int32_t *next_state, const uint32_t *allow, int32_t num_states,
+                                       int32_t num_tokens, const int32_t *states, const void *logits,
+                                       int32_t dtype, int32_t batch, int64_t ld_logits, int32_t *token,
+                                       int32_t *new_state, void *workspace, size_t workspace_bytes,
+                                       void *stream)
+{
+    return step_common("dv_masked_step_opportunistic", true, next_state, allow, num_states, num_tokens, states,
+                       logits, dtype, batch, ld_logits, token, new_state, workspace, workspace_bytes, stream);
 }
 
 static dv_status spec_shape_checks(const char *name, int32_t num_states, int32_t num_tokens, int32_t batch,

@@ -69,6 +69,13 @@ hipError_t launch_masked_step(const int32_t *next_state, const uint32_t *allow, 
                               int64_t ld, int32_t *token, int32_t *new_state, void *workspace,
                               hipStream_t stream);
 
+// Opportunistic masking: the same outputs as launch_masked_step (and the
+// same workspace).
+hipError_t launch_masked_step_opportunistic(const int32_t *next_state, const uint32_t *allow, int S, int V,
+                                            const int32_t *states, const void *logits, int dtype, int B,
+                                            int64_t ld, int32_t *token, int32_t *new_state,
+                                            void *workspace, hipStream_t stream);
+
 // Where the logits of row r start, in elements: rows come in groups of `per`
 // (a sequence's positions); group g = r / per, position j = r % per, at
 // g * ld_row + j * ld_pos.  A plain batch is {ld, 0, 1}.

@@ -216,3 +216,23 @@ def test_spec_verify_workspace_and_empty_batch():
     assert lib.dv_spec_verify_workspace_bytes(8, 2000, 10) == 0
     assert lib.dv_spec_verify_workspace_bytes(256, 8, 128256) >= 2 * 256 * 9 * 4
     assert _verify(B=0, states=None, props=None, logits=None, tok=None, acc=None, new=None) == OK
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(ns=None), INVALID),
+    (dict(ld=999), SHAPE),
+    (dict(dtype=2), DTYPE),
+    (dict(new=P + 2 * GB), ALIAS),
+    (dict(ws_bytes=8), WORKSPACE),
+])
+def test_opportunistic_step_rejects_before_launch(kw, status):
+    args = dict(ns=P, allow=P + GB, S=16, V=1000, states=P + 2 * GB, logits=P + 3 * GB, dtype=1, B=300,
+                ld=1000, tok=P + 4 * GB, new=P + 5 * GB, ws=P + 6 * GB, ws_bytes=None)
+    args.update(kw)
+    if args["ws_bytes"] is None:
+        args["ws_bytes"] = lib.dv_masked_step_workspace_bytes(300, 1000)
+    st = lib.dv_masked_step_opportunistic(args["ns"], args["allow"], args["S"], args["V"], args["states"],
+                                          args["logits"], args["dtype"], args["B"], args["ld"], args["tok"],
+                                          args["new"], args["ws"], args["ws_bytes"], None)
+    assert st == status
+    assert lib.dv_last_error().startswith(b"dv_masked_step_opportunistic")

@@ -661,3 +661,87 @@ def test_spec_empty_batch_and_aliasing(dv):
         dv.spec_verify(ns, al, states, props, x, new_state=states)
     with pytest.raises(dv.DvError):
         dv.spec_walk(ns, al, states, props, accepted=props[0])
+
+
+# ------------------------------------- opportunistic masking (Sec. 3.5, optimizations)
+
+OPP_BF16 = [  # (bits, allowed, expect): the free maximum allowed, not allowed, special keys on top
+    ([0x3F80, 0x4000, 0x3F80], [0, 1, 2], 1),
+    ([0x3F80, 0x4000, 0x3F80], [0, 2], 0),
+    ([0x7FC1, 0xC000, 0x7F80], [0, 1], 1),       # NaN first, +inf not allowed
+    ([0x7FC1, 0xC000, 0x7F80], [0, 1, 2], 2),
+    ([0x8000, 0x0000, 0xFFC1], [0, 1, 2], 0),    # -0.0 ties +0.0: lowest index
+    ([0xFFC1, 0xFF80, 0xFF7F], [0, 1], 0),       # -NaN and -inf tie at -inf
+    ([0x4000, 0x4000, 0x4000], [1, 2], 1),       # a tie whose lowest index is not allowed
+]
+
+
+@pytest.mark.parametrize("case", range(len(OPP_BF16)))
+@pytest.mark.parametrize("spread", [1, 9, 50021])
+def test_opportunistic_planted_specials_bf16(dv, case, spread):
+    """256 rows (one block per row, so the check-first kernel runs), the same
+    planted values in each, at indices that cross vector, wave and batch
+    boundaries; every other logit is -1.0 and not allowed."""
+    bits, allowed, expect = OPP_BF16[case]
+    V = len(bits) * spread + 3
+    B = 256
+    x = np.full((B, V), 0xBF80, np.uint16)
+    x[:, np.arange(len(bits)) * spread] = np.array(bits, np.uint16)
+    ns, al = _one_row_table(V, [a * spread for a in allowed])
+    xt = _dev(x.view(np.int16)).view(torch.bfloat16)
+    zeros = _dev(np.zeros(B, np.int32))
+    tok, new = dv.masked_step(_dev(ns), _dev(al.view(np.int32)), zeros, xt, opportunistic=True)
+    tok_o, new_o, _ = oracle.masked_step_opportunistic(ns, al, np.zeros(B, np.int32), x)
+    np.testing.assert_array_equal(tok.cpu().numpy(), tok_o)
+    np.testing.assert_array_equal(new.cpu().numpy(), new_o)
+    assert int(tok_o[0]) == expect * spread
+
+
+@pytest.mark.parametrize("allowed_last", [True, False])
+def test_opportunistic_tail_maximum(dv, allowed_last):
+    """The overall maximum in the scalar tail (V not a multiple of 8)."""
+    B, V = 300, 1003
+    rng = np.random.default_rng(7)
+    x = rng.standard_normal((B, V)).astype(np.float32)
+    x[:, V - 1] = 9.0
+    allowed = [3, 500, 1000] + ([V - 1] if allowed_last else [])
+    ns, al = _one_row_table(V, allowed)
+    xt = _dev(x).to(torch.bfloat16)
+    zeros = _dev(np.zeros(B, np.int32))
+    tok, _ = dv.masked_step(_dev(ns), _dev(al.view(np.int32)), zeros, xt, opportunistic=True)
+    tok_o, _, ok = oracle.masked_step_opportunistic(ns, al, np.zeros(B, np.int32), to_oracle(xt))
+    np.testing.assert_array_equal(tok.cpu().numpy(), tok_o)
+    assert bool(ok.all()) == allowed_last
+
+
+@pytest.mark.parametrize("wid", [3, 4, 5])
+@pytest.mark.parametrize("adherent", [0.0, 0.9])
+def test_opportunistic_workload(dv, wid, adherent):
+    """The benchmark's shapes: sampled rows against the oracle, every row
+    against dv_masked_step.  ``adherent``: the fraction of rows whose logits
+    favour an allowed token (chosen from the oracle's table row)."""
+    w = W.WORKLOADS[wid]
+    _say(f"opportunistic step workload {w.describe()} adherent={adherent}")
+    trans, offsets, data, ns, al = _workload_table(dv, wid)
+    cache = oracle.RowCache(trans, offsets, data)
+    init = W.init_states(wid)
+    x = W.logits(wid, 0, device=DEV)
+    rng = np.random.default_rng(400 + wid)
+    if adherent:
+        pick = np.nonzero(rng.random(w.B) < adherent)[0]
+        cols = []
+        for b in pick:
+            ns_row, _ = cache.get(int(init[b]))
+            ok = np.nonzero(ns_row != -1)[0]
+            cols.append(int(ok[rng.integers(0, ok.size)]) if ok.size else 0)
+        x[torch.from_numpy(pick).to(DEV), torch.from_numpy(np.array(cols, np.int64)).to(DEV)] = 30.0
+    states = _dev(init)
+    tok, new = dv.masked_step(ns, al, states, x, opportunistic=True)
+    t2, n2 = dv.masked_step(ns, al, states, x)
+    torch.cuda.synchronize()
+    assert torch.equal(tok, t2) and torch.equal(new, n2)
+    rows = np.unique(np.concatenate([[0, w.B - 1], rng.integers(0, w.B, 14)]))
+    xr = to_oracle(x[torch.from_numpy(rows.astype(np.int64)).to(DEV)])
+    for i, b in enumerate(rows):
+        t_o, _ = oracle.masked_chain(cache, init[b], xr[i][None])
+        assert int(tok[b]) == int(t_o[0]), f"workload {wid} row {b}"
