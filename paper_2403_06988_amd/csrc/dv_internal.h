@@ -76,13 +76,18 @@ hipError_t launch_masked_step_opportunistic(const int32_t *next_state, const uin
                                             int64_t ld, int32_t *token, int32_t *new_state,
                                             void *workspace, hipStream_t stream);
 
-// Where the logits of row r start, in elements: rows come in groups of `per`
-// (a sequence's positions); group g = r / per, position j = r % per, at
-// g * ld_row + j * ld_pos.  A plain batch is {ld, 0, 1}.
+// How the rows of a masked-step launch map to logits and states.  Rows come
+// in groups of `per` (a sequence's positions): row r is position j = r % per
+// of group g = r / per.  Its logits start at element g * ld_row + j * ld_pos;
+// its state is the group's state advanced by the group's first j proposals
+// prop[g * ld_prop + i] (DEAD once one is not allowed).  A plain batch is
+// {ld, 0, 1, nullptr, 0}: row r's state is states[r].
 struct RowMap {
     int64_t ld_row;
     int64_t ld_pos;
     int per;
+    const int32_t *prop;
+    int64_t ld_prop;
     __host__ __device__ int64_t offset(int r) const
     {
         if (per == 1)  // a plain batch: no division ahead of the first loads
@@ -91,6 +96,40 @@ struct RowMap {
         return (int64_t)g * ld_row + (int64_t)(r - g * per) * ld_pos;
     }
 };
+
+// One move of the speculative chain: the state after proposal t from state
+// st (-1 if st is DEAD, t is not a token id or its allow bit is clear; a
+// table entry outside [0, S) also reads as -1).  The mask word and the
+// table entry are loaded together at clamped addresses.
+__device__ __forceinline__ int spec_hop(const int32_t *next_state, const uint32_t *allow, int S, int V, int st,
+                                        int t, bool &legal)
+{
+    const bool ok = st >= 0 && (uint32_t)t < (uint32_t)V;
+    const size_t si = ok ? (size_t)st : 0, ti = ok ? (size_t)t : 0;
+    const size_t W = ((size_t)V + 31) / 32;
+    const uint32_t word = allow[si * W + (ti >> 5)];
+    const int nx = next_state[si * (size_t)V + ti];
+    legal = ok && ((word >> (ti & 31)) & 1u);
+    return legal && (uint32_t)nx < (uint32_t)S ? nx : -1;
+}
+
+// State of row r under `m` (for a plain batch the raw states[r]; the caller
+// treats anything outside [0, S) as DEAD).
+__device__ __forceinline__ int row_state(const int32_t *states, const RowMap &m, const int32_t *next_state,
+                                         const uint32_t *allow, int S, int V, int r)
+{
+    if (m.per == 1)
+        return states[r];
+    const int g = r / m.per, j = r - g * m.per;
+    int st = states[g];
+    st = (uint32_t)st < (uint32_t)S ? st : -1;
+    const int32_t *p = m.prop + (size_t)g * (size_t)m.ld_prop;
+    for (int i = 0; i < j; ++i) {
+        bool legal;
+        st = spec_hop(next_state, allow, S, V, st, p[i], legal);
+    }
+    return st;
+}
 
 // The masked step over R rows addressed through `map` (workspace as above,
 // for R rows).
@@ -103,13 +142,10 @@ hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, 
 //
 // Workspace of the verification, for B rows of s proposals (R = B (s + 1)
 // positions), 256-byte aligned parts:
-//   [0, ...)     int32 state of every position [B][s+1] (DEAD after a
-//                proposal that was not allowed)
-//   [pos_new..)  int32 state after each position's choice [B][s+1]
+//   [0, ...)     int32 state after each position's choice [B][s+1]
 //   [partial..)  the masked step's workspace for R rows
 inline size_t spec_positions(int B, int s) { return (size_t)B * (size_t)(s + 1); }
-inline size_t spec_pos_new_offset(int B, int s) { return align_up(spec_positions(B, s) * 4, 256); }
-inline size_t spec_partial_offset(int B, int s) { return 2 * spec_pos_new_offset(B, s); }
+inline size_t spec_partial_offset(int B, int s) { return align_up(spec_positions(B, s) * 4, 256); }
 inline size_t spec_workspace_bytes(int B, int s, int V)
 {
     return spec_partial_offset(B, s) + step_workspace_bytes((int)spec_positions(B, s), V);

@@ -6,12 +6,14 @@
 //     may follow, next_state where it leads.  Each hop's two loads (mask word
 //     and table entry) are issued together at clamped, always-valid
 //     addresses, so a hop costs one memory round trip.
-//   * Verification (dv_spec_verify): the same walk writes the state of every
-//     position (DEAD after a proposal that is not allowed), then the masked
-//     greedy step runs over all B (s + 1) positions at once as independent
-//     rows -- the HBM-bound part, with dead positions costing no logit
-//     reads -- and a last lane-per-row pass finds the first position whose
-//     choice differs from its proposal.
+//   * Verification (dv_spec_verify): the masked greedy step runs over all
+//     B (s + 1) positions at once as independent rows -- the HBM-bound part,
+//     with positions past a proposal that is not allowed costing no logit
+//     reads.  Each position's block walks its own j proposals after its
+//     first batch of logits is in flight, so the walk's round trips overlap
+//     other blocks' streaming instead of forming a serial kernel of their
+//     own.  A last lane-per-row pass finds the first position whose choice
+//     differs from its proposal.
 #include "dv_internal.h"
 
 namespace dv {
@@ -19,44 +21,34 @@ namespace {
 
 constexpr int kSpecThreads = 256;
 
-// One lane per row: walk the row's proposals.  Writes, when non-NULL, the
-// state of each position [B][s+1], the number of leading allowed proposals
-// and the table entry reached by the last of them.
+// One lane per row: walk the row's proposals.  Writes the number of leading
+// allowed proposals and the table entry reached by the last of them.
 __global__ __launch_bounds__(kSpecThreads) void spec_chain_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V,
     const int32_t *__restrict__ states, const int32_t *__restrict__ proposals, int s, int64_t ld_prop,
-    int B, int32_t *__restrict__ pos_state, int32_t *__restrict__ accepted, int32_t *__restrict__ final_state)
+    int B, int32_t *__restrict__ accepted, int32_t *__restrict__ final_state)
 {
     const int b = blockIdx.x * kSpecThreads + threadIdx.x;
     if (b >= B)
         return;
-    const size_t W = ((size_t)V + 31) / 32;
     const int32_t *prop = proposals + (size_t)b * (size_t)ld_prop;
-    int32_t *pos = pos_state ? pos_state + (size_t)b * (size_t)(s + 1) : nullptr;
     int st = states[b];
     st = (uint32_t)st < (uint32_t)S ? st : -1;
     int fin = st, a = 0;
+#pragma unroll 4
     for (int j = 0; j < s; ++j) {
-        if (pos)
-            pos[j] = st;
         const int t = prop[j];
-        const bool ok = st >= 0 && (uint32_t)t < (uint32_t)V;
-        const size_t si = ok ? (size_t)st : 0, ti = ok ? (size_t)t : 0;
-        const uint32_t word = allow[si * W + (ti >> 5)];
-        const int nx = next_state[si * (size_t)V + ti];
-        const bool legal = ok && ((word >> (ti & 31)) & 1u);
+        bool legal;
+        const int nx = spec_hop(next_state, allow, S, V, st, t, legal);
         if (legal) {
             ++a;
-            fin = nx;
+            // the table entry as stored (spec_hop maps entries outside [0, S) to -1)
+            fin = next_state[(size_t)st * (size_t)V + (size_t)t];
         }
-        st = legal && (uint32_t)nx < (uint32_t)S ? nx : -1;
+        st = nx;
     }
-    if (pos)
-        pos[s] = st;
-    if (accepted)
-        accepted[b] = a;
-    if (final_state)
-        final_state[b] = fin;
+    accepted[b] = a;
+    final_state[b] = fin;
 }
 
 // One lane per row: the first position whose choice is not its proposal (or
@@ -70,11 +62,21 @@ __global__ __launch_bounds__(kSpecThreads) void spec_accept_kernel(
         return;
     const int32_t *prop = proposals + (size_t)b * (size_t)ld_prop;
     const int32_t *tok = token + (size_t)b * (size_t)(s + 1);
-    int a = 0;
-    while (a < s && tok[a] != -1 && tok[a] == prop[a])
-        ++a;
+    const int32_t *pn = pos_new + (size_t)b * (size_t)(s + 1);
+    // no early exit, and every position's state read alongside its token:
+    // the loads of several positions are in flight together, in one round
+    // trip instead of one per position
+    int a = s, ns = pn[s];
+#pragma unroll 8
+    for (int j = 0; j < s; ++j) {
+        const int t = tok[j], p = prop[j], n = pn[j];
+        if (a == s && (t == -1 || t != p)) {
+            a = j;
+            ns = n;
+        }
+    }
     accepted[b] = a;
-    new_state[b] = pos_new[(size_t)b * (size_t)(s + 1) + a];
+    new_state[b] = ns;
 }
 
 unsigned lanes_grid(int B) { return (unsigned)((B + kSpecThreads - 1) / kSpecThreads); }
@@ -86,7 +88,7 @@ hipError_t launch_spec_walk(const int32_t *next_state, const uint32_t *allow, in
                             int B, int32_t *accepted, int32_t *final_state, hipStream_t stream)
 {
     spec_chain_kernel<<<lanes_grid(B), kSpecThreads, 0, stream>>>(next_state, allow, S, V, states, proposals, s,
-                                                                  ld_prop, B, nullptr, accepted, final_state);
+                                                                  ld_prop, B, accepted, final_state);
     return hipGetLastError();
 }
 
@@ -97,17 +99,12 @@ hipError_t launch_spec_verify(const int32_t *next_state, const uint32_t *allow, 
                               hipStream_t stream)
 {
     char *ws = static_cast<char *>(workspace);
-    int32_t *pos_state = reinterpret_cast<int32_t *>(ws);
-    int32_t *pos_new = reinterpret_cast<int32_t *>(ws + spec_pos_new_offset(B, s));
+    int32_t *pos_new = reinterpret_cast<int32_t *>(ws);
     void *partial = ws + spec_partial_offset(B, s);
     const int R = (int)spec_positions(B, s);
-    spec_chain_kernel<<<lanes_grid(B), kSpecThreads, 0, stream>>>(next_state, allow, S, V, states, proposals, s,
-                                                                  ld_prop, B, pos_state, nullptr, nullptr);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess)
-        return e;
-    e = launch_masked_rows(next_state, allow, S, V, pos_state, logits, dtype, R, RowMap{ld_row, ld_pos, s + 1},
-                           token, pos_new, partial, stream);
+    const RowMap map{ld_row, ld_pos, s + 1, proposals, ld_prop};
+    hipError_t e = launch_masked_rows(next_state, allow, S, V, states, logits, dtype, R, map, token, pos_new,
+                                      partial, stream);
     if (e != hipSuccess)
         return e;
     spec_accept_kernel<<<lanes_grid(B), kSpecThreads, 0, stream>>>(token, proposals, s, ld_prop, B, pos_new,

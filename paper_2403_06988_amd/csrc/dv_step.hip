@@ -244,7 +244,7 @@ __global__ __launch_bounds__(THREADS) void masked_step_kernel(
     constexpr int kVec = E::kVec;
     const int b = blockIdx.x / nchunks;
     const int c = blockIdx.x - b * nchunks;
-    const int s = states[b];
+    const int s = row_state(states, map, next_state, allow, S, V, b);
     const bool live = (uint32_t)s < (uint32_t)S;
 
     uint32_t best_key = 0;
@@ -504,7 +504,7 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     uint4 da[U];
     if (vector_path)
         load_batch_bf16<THREADS, U>(da, row, v0, v1);
-    const int s = states[b];
+    const int s = row_state(states, map, next_state, allow, S, V, b);
     const bool live = (uint32_t)s < (uint32_t)S;  // block-uniform
     uint64_t mine = 0;
     if (live) {
@@ -575,9 +575,10 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
 }
 
 // One lane per row: combine the row's chunk results and write the outputs.
-__global__ __launch_bounds__(kSmallThreads) void finalize_kernel(const int32_t *__restrict__ next_state, int S,
+__global__ __launch_bounds__(kSmallThreads) void finalize_kernel(const int32_t *__restrict__ next_state,
+                                                           const uint32_t *__restrict__ allow, int S,
                                                            int V, const int32_t *__restrict__ states,
-                                                           int B, int nchunks,
+                                                           RowMap map, int B, int nchunks,
                                                            const uint64_t *__restrict__ partial,
                                                            int32_t *__restrict__ token,
                                                            int32_t *__restrict__ new_state)
@@ -590,7 +591,7 @@ __global__ __launch_bounds__(kSmallThreads) void finalize_kernel(const int32_t *
         const uint64_t p = partial[(size_t)b * nchunks + c];
         best = p > best ? p : best;
     }
-    const int s = states[b];
+    const int s = row_state(states, map, next_state, allow, S, V, b);
     const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
     const bool found = tok >= 0 && tok < V && (uint32_t)s < (uint32_t)S;  // guards the read
     token[b] = found ? tok : -1;
@@ -639,7 +640,7 @@ hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, 
             next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial);
     if (g.nchunks > 1)
         finalize_kernel<<<(B + kSmallThreads - 1) / kSmallThreads, kSmallThreads, 0, stream>>>(
-            next_state, S, V, states, B, g.nchunks, partial, token, new_state);
+            next_state, allow, S, V, states, map, B, g.nchunks, partial, token, new_state);
     return hipGetLastError();
 }
 
@@ -654,10 +655,10 @@ hipError_t launch_masked_step_opportunistic(const int32_t *next_state, const uin
     // result.
     if (dtype == 1 && step_geometry(B, V, 1).nchunks == 1) {
         opportunistic_step_bf16_kernel<kBigThreads, kBigU><<<(unsigned)B, kBigThreads, 0, stream>>>(
-            next_state, allow, S, V, (V + 31) / 32, states, logits, RowMap{ld, 0, 1}, token, new_state);
+            next_state, allow, S, V, (V + 31) / 32, states, logits, RowMap{ld, 0, 1, nullptr, 0}, token, new_state);
         return hipGetLastError();
     }
-    return launch_masked_rows(next_state, allow, S, V, states, logits, dtype, B, RowMap{ld, 0, 1}, token,
+    return launch_masked_rows(next_state, allow, S, V, states, logits, dtype, B, RowMap{ld, 0, 1, nullptr, 0}, token,
                               new_state, workspace, stream);
 }
 
@@ -666,7 +667,7 @@ hipError_t launch_masked_step(const int32_t *next_state, const uint32_t *allow, 
                               int64_t ld, int32_t *token, int32_t *new_state, void *workspace,
                               hipStream_t stream)
 {
-    return launch_masked_rows(next_state, allow, S, V, states, logits, dtype, B, RowMap{ld, 0, 1}, token,
+    return launch_masked_rows(next_state, allow, S, V, states, logits, dtype, B, RowMap{ld, 0, 1, nullptr, 0}, token,
                               new_state, workspace, stream);
 }
 
