@@ -39,10 +39,12 @@ HBM_PEAK_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2403_06988_amd", "csrc")
 KERNEL_SOURCES = {"masked_step": ("dv_step.hip", "dv_internal.h"),
-                  "align": ("dv_align.hip", "dv_internal.h")}
+                  "align": ("dv_align.hip", "dv_internal.h"),
+                  "spec_verify": ("dv_step.hip", "dv_spec.hip", "dv_internal.h")}
 TRAFFIC_FILES = {
     "masked_step": "masked_step_bf16_kernel__grammar-lexer-union_S8192_V128256_B256.traffic.txt",
     "align": "walk_kernel__grammar-lexer-union_S8192_V128256.traffic.txt",
+    "spec_verify": "spec_verify__grammar-lexer-union_S8192_V128256_B256_s8.traffic.txt",
 }
 
 
@@ -214,7 +216,7 @@ def run_probes(dv, dev, table_bytes):
     return out
 
 
-def bench_spec(dv, w, ns, al, x, tokens_all, states_all, dev, s=8, keep=0.9, reps=3):
+def bench_spec(dv, w, wid, ns, al, x, tokens_all, states_all, dev, s=8, keep=0.9, reps=3):
     """Speculative verification (Sec. 3.6) over the job's decode chain: window
     k proposes the chain's tokens of steps k(s+1) .. k(s+1)+s-1, each kept with
     probability ``keep`` (else replaced by the next token id), and verifies
@@ -280,10 +282,11 @@ def bench_spec(dv, w, ns, al, x, tokens_all, states_all, dev, s=8, keep=0.9, rep
         "emitted_tokens_per_s": emitted / t, "positions_per_s": w.B * (s + 1) / t,
         "mean_accepted": float(acc.float().mean()), "live_positions_per_call": live_pos,
         "graph_matches_eager": same,
-        "roofline": {"kernel": "masked_step_bf16_kernel over B(s+1) positions + chain and accept kernels"
+        "roofline": {"kernel": "masked_step_bf16_kernel over B(s+1) positions + spec_accept_kernel"
                      if w.dtype == "bf16" else "masked_step_kernel over B(s+1) positions",
                      "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "bytes_per_launch": bytes_call},
+                     "frac": achieved / HBM_PEAK_GBS, "bytes_per_launch": bytes_call,
+                     "traffic": traffic_record("spec_verify", wid) if s == 8 else None},
     }
 
 
@@ -498,7 +501,7 @@ def main():
         out["opportunistic"]["masked_us_per_step"] = mean_launch_s * 1e6
     if not args.no_spec:
         log("speculative verification")
-        out["spec_verify"] = bench_spec(dv, w, ns, al, x, tokens_all, states_all, dev)
+        out["spec_verify"] = bench_spec(dv, w, wid, ns, al, x, tokens_all, states_all, dev)
     if not args.no_probes:
         log("roofline probes")
         out["probes"] = run_probes(dv, dev, w.S * 96 * 2)
