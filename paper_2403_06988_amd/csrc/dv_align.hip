@@ -5,8 +5,11 @@
 //
 // Pipeline (all on the caller's stream, no host synchronisation):
 //   1. live_columns: which byte columns have at least one live move.
-//   2. byte_classes: rank the live columns; dead columns get no storage.
-//   3. compact: uint16 table [S][Cp] over the live columns only (DEAD = 0xFFFF).
+//   2. byte_classes: rank the live columns; the bytes dead from every state
+//      share one extra class whose column is all DEAD (it exists only when
+//      some byte is dead, so the C <= 256 classes always fit in a byte).
+//   3. compact: uint16 table [S][Cp] over the live columns, then the DEAD
+//      column (DEAD = 0xFFFF).
 //      Random printable-ASCII DFAs keep ~95 of 256 columns, so the table is
 //      ~2.7x smaller than the int32 input and stays resident in each XCD's L2.
 //   4. token_info: each token's first 8 byte classes, length and offset.
@@ -106,17 +109,19 @@ __global__ __launch_bounds__(kThreads) void byte_classes_kernel(const uint32_t *
     }
     uint8_t *cls = ws + 256;
     uint8_t *byte_of = ws + 512;
-    cls[b] = live ? (uint8_t)rank : kDeadClass;
+    // a dead byte exists only when total < 256, so class `total` fits in a byte
+    cls[b] = (uint8_t)(live ? rank : total);
     if (live)
         byte_of[rank] = (uint8_t)b;
     if (b == 0) {
         int32_t *meta = reinterpret_cast<int32_t *>(ws);
         meta[0] = total;
-        meta[1] = (total + 1) & ~1;
+        meta[1] = total < 256 ? (total + 2) & ~1 : 256;  // room for the DEAD column, even
     }
 }
 
-// 3. compacted uint16 table [S][Cp]; padding columns are DEAD.
+// 3. compacted uint16 table [S][Cp]; columns C .. Cp-1 (the dead bytes'
+// class and padding) are DEAD.
 __global__ __launch_bounds__(kThreads) void compact_kernel(const int32_t *__restrict__ trans, int S,
                                                            const uint8_t *__restrict__ ws,
                                                            uint16_t *__restrict__ table)
@@ -222,9 +227,8 @@ __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
         const bool acc = accepting != nullptr && accepting[s] != 0;
 #pragma unroll
         for (int j = 0; j < kTokPerLane; ++j) {
-            const uint32_t c0 = c03[j] & 0xFFu;
-            const uint32_t v = row[c0 == kDeadClass ? 0u : c0];
-            uint32_t st = c0 == kDeadClass ? kDead16 : v;
+            const uint32_t c0 = c03[j] & 0xFFu;  // always a column of the table
+            uint32_t st = row[c0];
             if (len[j] <= 0) {
                 if (len[j] == 0)
                     st = (uint32_t)s;  // an empty token keeps the state
@@ -269,9 +273,8 @@ __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
                     c = ((h[j] < 4 ? c03[j] : c47[j]) >> (8 * (h[j] & 3))) & 0xFFu;
                 else
                     c = cls[bytes[off[j] + h[j]]];
-                const uint32_t idx = c == kDeadClass ? 0u : st[j] * (uint32_t)Cp + c;
-                const uint32_t v = WHOLE ? tab[idx] : table[idx];
-                st[j] = c == kDeadClass ? kDead16 : v;
+                const uint32_t idx = st[j] * (uint32_t)Cp + c;
+                st[j] = WHOLE ? tab[idx] : table[idx];
                 h[j] += 1;
                 if (st[j] == kDead16 || h[j] >= (uint32_t)len[j]) {
                     res[cur[j] * kTokTile + j * kThreads + tid] = (uint16_t)st[j];

@@ -14,8 +14,10 @@ constexpr int kWave = 64;
 //
 // Workspace of dv_align (all offsets 256-byte aligned):
 //   [0, 4)        int32  number of live byte columns C
-//   [4, 8)        int32  row stride Cp of the compacted table (C rounded up to 2)
-//   [256, 512)    uint8  class of each byte (0xFF: the byte is dead from every state)
+//   [4, 8)        int32  row stride Cp of the compacted table (C + 1 rounded up
+//                        to even; 256 when every byte is live)
+//   [256, 512)    uint8  class of each byte (the bytes dead from every state
+//                        share class C, whose table column is all DEAD)
 //   [512, 768)    uint8  byte of each class
 //   [1024, ...)   uint32 per-block live-column bit sets, 8 words per block
 //   [table, ...)  uint16 compacted table [S][Cp], DEAD = 0xFFFF
@@ -23,7 +25,6 @@ constexpr int kWave = 64;
 constexpr int kAlignMetaBytes = 1024;
 constexpr int kLiveRowsPerBlock = 16;
 constexpr uint16_t kDead16 = 0xFFFF;
-constexpr uint8_t kDeadClass = 0xFF;
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 

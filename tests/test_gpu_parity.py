@@ -116,14 +116,19 @@ def test_align_all_transitions_dead(dv):
     assert (ns.cpu().numpy() == -1).all() and (u32(al) == 0).all()
 
 
-def test_align_every_byte_value(dv):
-    # every byte 0x00..0xFF is a live column: Cp = 256, no compaction
+@pytest.mark.parametrize("dead_byte", [None, 0xFF, 0x00, 0x80])
+def test_align_every_byte_value(dv, dead_byte):
+    """All 256 bytes live (C = 256 classes, no spare class for dead bytes), or
+    all but one (C = 255: the dead byte's class is the last one).  Every
+    single-byte token and tokens through the dead byte are walked."""
     rng = np.random.default_rng(5)
     S = 50
     trans = rng.integers(0, S, size=(S, 256)).astype(np.int32)
-    trans[:, 0xFF] = -1
+    if dead_byte is not None:
+        trans[:, dead_byte] = -1
     toks = [bytes([b]) for b in range(256)] + [bytes(rng.integers(0, 256, 3).astype(np.uint8))
                                                for _ in range(700)]
+    toks += [bytes([0x41, b, 0x42]) for b in (0x00, 0x80, 0xFF)]
     offsets, data = W.vocab_from_tokens(toks)
     ns, al = _align(dv, trans, offsets, data)
     ns_o, al_o = oracle.align(trans, offsets, data)
@@ -157,7 +162,7 @@ def _workload_table(dv, wid):
     return _Cache.data
 
 
-@pytest.mark.parametrize("wid", [1, 2, 3])
+@pytest.mark.parametrize("wid", [1, 2, 3, 6, 7, 8])
 def test_align_workload_full(dv, wid):
     _say(f"align workload {W.WORKLOADS[wid].describe()}")
     trans, offsets, data, ns, al = _workload_table(dv, wid)
@@ -226,7 +231,7 @@ def _chain_check(dv, wid, sample_rows):
     assert bool(((tk == -1) == (sts[1:] == -1)).all())
 
 
-@pytest.mark.parametrize("wid", [1, 2, 3])
+@pytest.mark.parametrize("wid", [1, 2, 3, 6, 7, 8])
 def test_chain_workload_full(dv, wid):
     _say(f"chain workload {W.WORKLOADS[wid].describe()}")
     _chain_check(dv, wid, None)
@@ -426,7 +431,7 @@ def test_align_eos_paper_example(dv):
     np.testing.assert_array_equal(u32(al)[:, 0], np.array([int(x, 16) for x in e["expected_allow"]], np.uint32))
 
 
-@pytest.mark.parametrize("wid", [1, 2, 3])
+@pytest.mark.parametrize("wid", [1, 2, 3, 7, 8])
 @pytest.mark.parametrize("where", ["first", "middle", "last"])
 def test_align_eos_workloads(dv, wid, where):
     w = W.WORKLOADS[wid]
@@ -536,7 +541,7 @@ def test_spec_paper_example(dv, dtype):
     np.testing.assert_array_equal(f_w.cpu().numpy(), sp["expected_walk_final_state"])
 
 
-@pytest.mark.parametrize("wid,s", [(1, 4), (2, 4), (2, 8), (3, 6)])
+@pytest.mark.parametrize("wid,s", [(1, 4), (2, 4), (2, 8), (3, 6), (6, 8), (7, 8), (8, 8)])
 @pytest.mark.parametrize("layout", ["rows", "steps"])
 def test_spec_workload_full(dv, wid, s, layout):
     """Every row and position against the oracle.  ``rows``: the model's

@@ -11,7 +11,7 @@ def test_seeded_generators_are_deterministic():
     t2, a2 = W.dfa(1)
     assert W.sha256(t1) == W.sha256(t2) and W.sha256(a1) == W.sha256(a2)
     o1, d1 = W.vocab(1)
-    W.vocab.cache_clear()
+    W._vocab_of.cache_clear()
     o2, d2 = W.vocab(1)
     assert W.sha256(o1) == W.sha256(o2) and W.sha256(d1) == W.sha256(d2)
 

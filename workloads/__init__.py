@@ -17,7 +17,19 @@ these generators stand in for them with the shapes below.  Five workloads:
  3     llm-tokenizer-scale         1,024    128,256   64      512    bf16   N(0, 3)
  4     grammar-lexer-union         8,192    128,256   256     256    bf16   N(0, 3)
  5     large-vocab-high-batch      4,096    256,000   1,024   128    bf16   N(0, 3)
+ 6     json-scanner-bpe32k         22       32,000    64      256    bf16   N(0, 3)
+ 7     json-schema-bpe32k          83       32,000    64      256    bf16   N(0, 3)
+ 8     c-lexer-bpe32k              50       32,000    64      256    bf16   N(0, 3)
 ====  ==========================  =======  ========  ======  =====  =====  ===========
+
+Workloads 6-8 are real grammars' automata (``workloads.grammars``): the
+Sec. 3.2 scanner of JSON's lexical terminals, one JSON object shape as a
+single regular expression, and the scanner of C's lexical terminals, each
+compiled from regular expressions by ``workloads.regex_dfa`` (minimal,
+trimmed: every state can still reach acceptance).  They share one byte-level
+BPE vocabulary of 32,000 tokens trained on a seeded synthetic corpus (the
+size of the paper's two models' vocabularies); the accepting states are the
+automata's own.
 
 Readings of points the workload description leaves open:
 
@@ -83,7 +95,7 @@ class Workload:
     lengths: tuple         # ("uniform", lo, hi) or ("geometric", p, hi)
     p_printable: float
     init: str              # "zero" or "uniform"
-    kind: str = "random"   # "random" or "union"
+    kind: str = "random"   # "random", "union" or a grammar: "json-scanner", "json-schema", "c-lexer"
     vocab_from: int = 0    # reuse another workload's vocabulary stream
 
     @property
@@ -109,6 +121,12 @@ WORKLOADS = {
                 ("geometric", 0.2, 32), 0.90, "zero", kind="union", vocab_from=3),
     5: Workload(5, "large-vocab-high-batch", 4096, 256000, 1024, 128, "bf16", 3.0, (8, 96),
                 ("geometric", 0.2, 48), 0.90, "uniform"),
+    6: Workload(6, "json-scanner-bpe32k", 22, 32000, 64, 256, "bf16", 3.0, (0, 0), ("bpe",), 1.0, "zero",
+                kind="json-scanner"),
+    7: Workload(7, "json-schema-bpe32k", 83, 32000, 64, 256, "bf16", 3.0, (0, 0), ("bpe",), 1.0, "zero",
+                kind="json-schema", vocab_from=6),
+    8: Workload(8, "c-lexer-bpe32k", 50, 32000, 64, 256, "bf16", 3.0, (0, 0), ("bpe",), 1.0, "zero",
+                kind="c-lexer", vocab_from=6),
 }
 
 
@@ -237,20 +255,36 @@ def dfa(workload: int):
     rng = rng_for(workload, COMPONENT_DFA)
     if w.kind == "union":
         trans, acc = union_dfa(rng, 40, w.S, w.subset, LEXER_ALPHABET)
-    else:
+    elif w.kind == "random":
         trans, acc = random_dfa(rng, w.S, w.subset, PRINTABLE)
+    else:
+        from . import grammars
+
+        build = {"json-scanner": grammars.json_scanner, "json-schema": grammars.json_schema,
+                 "c-lexer": grammars.c_scanner}[w.kind]
+        trans, acc = (a.copy() for a in build())
+        if trans.shape[0] != w.S:
+            raise RuntimeError(f"{w.name}: automaton has {trans.shape[0]} states, {w.S} expected")
     trans.setflags(write=False)
     acc.setflags(write=False)
     return trans, acc
 
 
-@functools.lru_cache(maxsize=8)
 def vocab(workload: int):
     """(offsets[V+1] int32, bytes uint8) of a workload."""
     w = WORKLOADS[workload]
-    src = w.vocab_from or workload
+    return _vocab_of(w.vocab_from or workload)
+
+
+@functools.lru_cache(maxsize=8)
+def _vocab_of(src: int):
     ws = WORKLOADS[src]
-    offsets, data = random_vocab(rng_for(src, COMPONENT_VOCAB), ws.V, ws.lengths, ws.p_printable)
+    if ws.lengths[0] == "bpe":
+        from . import grammars
+
+        offsets, data = vocab_from_tokens(grammars.bpe_vocab(rng_for(src, COMPONENT_VOCAB), ws.V))
+    else:
+        offsets, data = random_vocab(rng_for(src, COMPONENT_VOCAB), ws.V, ws.lengths, ws.p_printable)
     offsets.setflags(write=False)
     data.setflags(write=False)
     return offsets, data
