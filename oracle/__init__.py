@@ -18,6 +18,9 @@ Way"):
   stops on EOS; Sec. 3.2 makes EOS a terminal), allowed in accepting states.
 * ``masked_step_opportunistic``: opportunistic masking (Sec. 3.5, further
   optimizations) -- the model's unconstrained choice is checked first.
+* ``masked_sample`` (with ``philox4x32_10``, ``ln_f32``, ``gumbel``): the
+  sampled decode of Algorithm 1 at temperature T (Sec. 4 samples at T = 1)
+  as a Gumbel-max draw over the allowed tokens, with counter-based noise.
 * ``spec_walk`` / ``spec_verify``: the speculative chain check of Sec. 3.6 --
   how many proposed tokens the constraint admits, and greedy verification of
   the proposals against the model's logits at every proposed position.
@@ -89,6 +92,16 @@ def _bind(lib):
                                                      _i32p, ctypes.c_void_p, ctypes.c_int,
                                                      ctypes.c_int32, ctypes.c_int64, _i32p, _i32p,
                                                      ctypes.c_void_p]
+    lib.oracle_philox4x32_10.restype = None
+    lib.oracle_philox4x32_10.argtypes = [_u32p, _u32p, _u32p]
+    lib.oracle_ln_f32.restype = ctypes.c_float
+    lib.oracle_ln_f32.argtypes = [ctypes.c_float]
+    lib.oracle_gumbel.restype = ctypes.c_float
+    lib.oracle_gumbel.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32]
+    lib.oracle_masked_sample.restype = None
+    lib.oracle_masked_sample.argtypes = [_i32p, _u32p, ctypes.c_int32, ctypes.c_int32, _i32p,
+                                         ctypes.c_void_p, ctypes.c_int, ctypes.c_int32, ctypes.c_int64,
+                                         ctypes.c_float, ctypes.c_uint64, ctypes.c_uint64, _i32p, _i32p]
     lib.oracle_walk_lookups.restype = ctypes.c_int64
     lib.oracle_walk_lookups.argtypes = [_i32p, ctypes.c_int32, _i32p, _u8p, ctypes.c_int32,
                                         _i32p, ctypes.c_int64]
@@ -233,6 +246,46 @@ def masked_step_opportunistic(next_state, allow, states, logits, lib=None):
                                              _p(states, _i32p), logits.ctypes.data, dt, B, ld,
                                              _p(tok, _i32p), _p(nst, _i32p), ok.ctypes.data)
     return tok, nst, ok.astype(bool)
+
+
+def philox4x32_10(ctr, key, lib=None):
+    """Philox4x32-10 of a 4-word counter and a 2-word key -> 4 words."""
+    lib = lib or load()
+    c = np.ascontiguousarray(ctr, np.uint32)
+    k = np.ascontiguousarray(key, np.uint32)
+    out = np.empty(4, np.uint32)
+    lib.oracle_philox4x32_10(_p(c, _u32p), _p(k, _u32p), _p(out, _u32p))
+    return out
+
+
+def ln_f32(x, lib=None) -> float:
+    lib = lib or load()
+    return float(np.float32(lib.oracle_ln_f32(float(np.float32(x)))))
+
+
+def gumbel(seed: int, offset: int, row: int, token: int, lib=None) -> float:
+    lib = lib or load()
+    return float(np.float32(lib.oracle_gumbel(seed, offset, row, token)))
+
+
+def masked_sample(next_state, allow, states, logits, inv_temperature: float, seed: int, offset: int,
+                  lib=None):
+    """One sampled masked step (Gumbel-max over the allowed tokens)."""
+    lib = lib or load()
+    next_state = _c(next_state, np.int32)
+    allow = _c(allow, np.uint32)
+    states = _c(states, np.int32)
+    logits, dt = _logit_array(np.ascontiguousarray(logits))
+    S, V = next_state.shape
+    B = states.shape[0]
+    ld = logits.shape[1] if B else V
+    tok = np.empty(B, np.int32)
+    nst = np.empty(B, np.int32)
+    if B:
+        lib.oracle_masked_sample(_p(next_state, _i32p), _p(allow, _u32p), S, V, _p(states, _i32p),
+                                 logits.ctypes.data, dt, B, ld, float(np.float32(inv_temperature)),
+                                 int(seed), int(offset), _p(tok, _i32p), _p(nst, _i32p))
+    return tok, nst
 
 
 def spec_walk(next_state, allow, states, proposals, lib=None):

@@ -332,3 +332,139 @@ void oracle_masked_step_opportunistic(const int32_t *next_state, const uint32_t 
             unconstrained_ok[b] = (uint8_t)ok;
     }
 }
+
+/* ------------------------------------------------------------------------
+ * Masked sampling.  The paper samples at temperature 1.0 (Sec. 4, setup) and
+ * Algorithm 1's decode may be "argmax or sample".  The sampled token is the
+ * Gumbel-max choice over the admissible set:
+ *     token = argmax over allowed i of  x_i / T + G_i,   G_i ~ Gumbel(0, 1),
+ * which draws i with probability softmax(x / T) restricted to the allowed
+ * tokens.  G_i = -ln(-ln U_i) with U_i from a counter-based generator, so the
+ * draw is reproducible and the same on every device:
+ *   - Philox4x32-10 (Salmon, Moraes, Dror and Shaw, "Parallel random
+ *     numbers: as easy as 1, 2, 3", SC 2011), key = (seed low, seed high),
+ *     counter = (i / 4, row, offset low, offset high), word i % 4 -> w;
+ *   - U = (2 (w >> 9) + 1) 2^-24, exactly, strictly inside (0, 1);
+ *   - ln in binary32 by fixed steps that every IEEE implementation rounds
+ *     alike (no library log, no division):  x = m 2^e with m in
+ *     [sqrt(1/2), sqrt(2)); f = m - 1; r = 1 / (2 + f) by four Newton steps
+ *     from 1/2 (each t = fma(-d, r, 1), r = fma(r, t, r)); z = f r;
+ *     ln m = 2 (z + z^3 (1/3 + w (1/5 + w (1/7 + w / 9)))), w = z^2, with
+ *     the polynomial by fused multiply-adds; ln x = fma(e, ln 2, ln m);
+ *   - the key is fma(x_i, 1/T, G_i) in binary32, NaN ranks as -infinity,
+ *     ties go to the lowest index.
+ * ------------------------------------------------------------------------ */
+
+void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {            /* the key is bumped between rounds */
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+        uint32_t n1 = (uint32_t)p1;
+        uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        uint32_t n3 = (uint32_t)p0;
+        c0 = n0;
+        c1 = n1;
+        c2 = n2;
+        c3 = n3;
+    }
+    out[0] = c0;
+    out[1] = c1;
+    out[2] = c2;
+    out[3] = c3;
+}
+
+static float oracle_bits_f32(uint32_t u)
+{
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+static uint32_t oracle_f32_bits(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    return u;
+}
+
+/* Natural log of a positive normal binary32 by the fixed steps above. */
+float oracle_ln_f32(float x)
+{
+    uint32_t bits = oracle_f32_bits(x);
+    int32_t e = (int32_t)(bits >> 23) - 127;
+    uint32_t mb = (bits & 0x007FFFFFu) | 0x3F800000u;
+    if (mb > 0x3FB504F3u) {         /* m above sqrt(2): halve it */
+        mb -= 0x00800000u;
+        e += 1;
+    }
+    float f = oracle_bits_f32(mb) - 1.0f;
+    float d = f + 2.0f;
+    float r = 0.5f;
+    for (int it = 0; it < 4; ++it) {
+        float t = fmaf(-d, r, 1.0f);
+        r = fmaf(r, t, r);
+    }
+    float z = f * r;
+    float w = z * z;
+    float p = fmaf(w, 0x1.c71c72p-4f, 0x1.24924ap-3f);  /* 1/9, 1/7 */
+    p = fmaf(w, p, 0x1.99999ap-3f);                       /* 1/5 */
+    p = fmaf(w, p, 0x1.555556p-2f);                       /* 1/3 */
+    float zw = z * w;
+    float half = fmaf(zw, p, z);
+    float lnm = half + half;
+    return fmaf((float)e, 0x1.62e430p-1f, lnm);           /* ln 2 */
+}
+
+/* The Gumbel noise of (seed, offset, row, token). */
+float oracle_gumbel(uint64_t seed, uint64_t offset, uint32_t row, uint32_t token)
+{
+    uint32_t ctr[4] = {token / 4u, row, (uint32_t)offset, (uint32_t)(offset >> 32)};
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t out[4];
+    oracle_philox4x32_10(ctr, key, out);
+    uint32_t w = out[token % 4u];
+    float u = (float)(2u * (w >> 9) + 1u) * 0x1p-24f;
+    return -oracle_ln_f32(-oracle_ln_f32(u));
+}
+
+/* One sampled masked step: as oracle_masked_step with the Gumbel-max draw
+ * in place of the argmax.  inv_temperature = 1 / T > 0. */
+void oracle_masked_sample(const int32_t *next_state, const uint32_t *allow, int32_t num_states,
+                          int32_t num_tokens, const int32_t *states, const void *logits, int dtype,
+                          int32_t batch, int64_t ld_logits, float inv_temperature, uint64_t seed,
+                          uint64_t offset, int32_t *token, int32_t *new_state)
+{
+    int64_t words = ((int64_t)num_tokens + 31) / 32;
+    size_t elt = dtype == 0 ? 4 : 2;
+    for (int32_t b = 0; b < batch; ++b) {
+        int32_t s = oracle_canon(states[b], num_states);
+        int32_t best = -1;
+        float best_key = 0.0f;
+        if (s != ORACLE_DEAD) {
+            const void *row = (const char *)logits + (size_t)b * (size_t)ld_logits * elt;
+            const uint32_t *arow = allow + (int64_t)s * words;
+            for (int32_t i = 0; i < num_tokens; ++i) {
+                if (((arow[i / 32] >> (i % 32)) & 1u) == 0)
+                    continue;
+                float x = (float)oracle_logit(row, i, dtype);   /* exact: the logit is binary32 or bf16 */
+                float key = fmaf(x, inv_temperature, oracle_gumbel(seed, offset, (uint32_t)b, (uint32_t)i));
+                if (isnan(key))
+                    key = -INFINITY;
+                if (best == -1 || key > best_key) {
+                    best = i;
+                    best_key = key;
+                }
+            }
+        }
+        token[b] = best;
+        new_state[b] = best == -1 ? ORACLE_DEAD : next_state[(int64_t)s * num_tokens + best];
+    }
+}

@@ -48,6 +48,14 @@ MUTANTS = {
     "opportunistic skips the check": ("tok = ok ? free_tok :", "tok = 1 ? free_tok :"),
     "opportunistic free ties to highest": ("if (i == 0 || v > best_v)", "if (i == 0 || v >= best_v)"),
     "opportunistic free keeps nan": ("v = -INFINITY;\n                if (i == 0", "v = v;\n                if (i == 0"),
+    "sample noise sign flipped": ("fmaf(x, inv_temperature, oracle_gumbel(", "fmaf(x, inv_temperature, -oracle_gumbel("),
+    "sample temperature ignored": ("float key = fmaf(x, inv_temperature,", "float key = fmaf(x, 1.0f,"),
+    "sample takes the next philox word": ("uint32_t w = out[token % 4u];", "uint32_t w = out[(token + 1u) % 4u];"),
+    "sample counter fields swapped": ("{token / 4u, row, (uint32_t)offset,", "{row, token / 4u, (uint32_t)offset,"),
+    "ln without the exponent": ("return fmaf((float)e, 0x1.62e430p-1f, lnm);", "return lnm;"),
+    "philox key not bumped": ("k1 += 0xBB67AE85u;", "k1 += 0u;"),
+    "sample ignores the mask": ("            for (int32_t i = 0; i < num_tokens; ++i) {\n                if (((arow[i / 32] >> (i % 32)) & 1u) == 0)\n                    continue;\n                float x",
+                                "            for (int32_t i = 0; i < num_tokens; ++i) {\n                float x"),
     "zero-length token dies": ("int32_t st = oracle_canon(s, num_states);\n    for",
                                "int32_t st = len ? oracle_canon(s, num_states) : ORACLE_DEAD;\n    for"),
 }
@@ -93,6 +101,14 @@ def _checks(lib):
         ("opportunistic", lambda: [P.test_opportunistic_equals_masked_step(a, d, table, lib)
                                    for a in (0.0, 0.7, 1.0) for d in ("f32", "bf16")]),
         ("opportunistic_tie", lambda: P.test_opportunistic_planted_tie_goes_to_lowest_allowed(lib)),
+        ("philox_kat", lambda: [P.test_philox_known_answers(c, k, o, lib) for c, k, o in P.PHILOX_KAT]),
+        ("gumbel_words", lambda: [P.test_gumbel_noise_from_published_philox_words(k, lib) for k in (0, 2)]),
+        ("ln_f32", lambda: P.test_ln_f32_accuracy(lib)),
+        ("gumbel_ks", lambda: P.test_gumbel_noise_is_gumbel_distributed(lib)),
+        ("sample_softmax", lambda: [P.test_sample_frequencies_follow_masked_softmax(t, d, lib)
+                                    for t in (1.0, 2.0) for d in ("f32", "bf16")]),
+        ("sample_greedy", lambda: P.test_sample_at_low_temperature_is_the_masked_argmax(table, lib)),
+        ("sample_inv", lambda: P.test_sample_invariants(table, lib)),
         ("ties_bf16", lambda: [P.test_planted_ties_and_specials_bf16(b, a, e, lib)
                                for b, a, e in [([0x8000, 0x0000, 0x0001], [0, 1, 2], 2),
                                                ([0x3F80, 0x3F80, 0x3F80], [1, 2], 1),

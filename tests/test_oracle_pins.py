@@ -658,3 +658,134 @@ def test_opportunistic_planted_tie_goes_to_lowest_allowed(oracle_lib):
     x[0, 1] = 5.0                 # now the lowest maximum (1) is not allowed
     tok, _, ok = oracle.masked_step_opportunistic(ns, al, np.zeros(1, np.int32), x, lib=oracle_lib)
     assert tok[0] == 3 and not ok[0]
+
+
+# ---------------------------------------- masked sampling (Sec. 4 samples at T = 1)
+
+# Known-answer vectors of Philox4x32-10 published with the generator
+# (Salmon et al., SC 2011; the Random123 distribution's test vectors).
+PHILOX_KAT = [
+    ((0, 0, 0, 0), (0, 0), (0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8)),
+    ((0xFFFFFFFF,) * 4, (0xFFFFFFFF,) * 2, (0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD)),
+    ((0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344), (0xA4093822, 0x299F31D0),
+     (0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1)),
+]
+
+
+@pytest.mark.parametrize("ctr,key,out", PHILOX_KAT)
+def test_philox_known_answers(ctr, key, out, oracle_lib):
+    assert tuple(int(x) for x in oracle.philox4x32_10(ctr, key, lib=oracle_lib)) == out
+
+
+def _gumbel_from_words(w):
+    u = (2.0 * (np.uint64(w) >> np.uint64(9)) + 1.0) * 2.0 ** -24
+    return -np.log(-np.log(u))
+
+
+@pytest.mark.parametrize("k", [0, 2])
+def test_gumbel_noise_from_published_philox_words(k, oracle_lib):
+    """The noise of the tokens whose counters are the published inputs equals
+    -ln(-ln u) of the published outputs (float64 reference): pins the counter
+    layout (token / 4, row, offset) and the word each token takes."""
+    ctr, key, out = PHILOX_KAT[k]
+    seed = key[0] | (key[1] << 32)
+    offset = ctr[2] | (ctr[3] << 32)
+    for j in range(4):
+        g = oracle.gumbel(seed, offset, ctr[1], 4 * ctr[0] + j, lib=oracle_lib)
+        ref = _gumbel_from_words(out[j])
+        assert abs(g - ref) <= 4e-6 * max(1.0, abs(ref)), (j, g, ref)
+
+
+def test_ln_f32_accuracy(oracle_lib):
+    rng = np.random.default_rng(51)
+    xs = np.concatenate([rng.uniform(2.0 ** -24, 1.0, 4000), rng.uniform(5.9e-8, 20.0, 4000),
+                         2.0 ** rng.uniform(-24, 5, 2000), [1.0, 2.0, 0.5, np.sqrt(2.0), 0.70710678]])
+    worst = 0.0
+    for x in xs.astype(np.float32):
+        ref = np.log(np.float64(x))
+        got = oracle.ln_f32(x, lib=oracle_lib)
+        ulp = np.spacing(np.float32(max(abs(ref), 2.0 ** -24)))
+        worst = max(worst, abs(got - ref) / ulp)
+    assert worst <= 2.5
+    assert oracle.ln_f32(1.0, lib=oracle_lib) == 0.0
+
+
+def test_gumbel_noise_is_gumbel_distributed(oracle_lib):
+    """Kolmogorov-Smirnov distance to the Gumbel CDF exp(-exp(-g))."""
+    n = 40000
+    g = np.array([oracle.gumbel(7, 3, r, t, lib=oracle_lib) for r in range(4) for t in range(n // 4)])
+    g.sort()
+    cdf = np.exp(-np.exp(-g))
+    emp = np.arange(1, n + 1) / n
+    ks = max(np.abs(cdf - emp).max(), np.abs(cdf - (emp - 1.0 / n)).max())
+    assert ks < 1.63 / np.sqrt(n) * 1.5   # well inside the 1 % critical value's range
+    assert abs(g.mean() - 0.5772) < 0.02  # Euler-Mascheroni constant
+
+
+def _one_state_table(V, allowed):
+    ns = np.full((1, V), -1, np.int32)
+    ns[0, allowed] = 0
+    return ns, _pack_allow(ns != -1)
+
+
+@pytest.mark.parametrize("inv_t", [1.0, 2.0])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_sample_frequencies_follow_masked_softmax(inv_t, dtype, oracle_lib):
+    """Many draws (different offsets) of one row: chi-square of the counts
+    against softmax(x / T) over the allowed tokens; disallowed never drawn."""
+    V = 40
+    allowed = [1, 5, 6, 17, 30, 39]
+    ns, al = _one_state_table(V, allowed)
+    x = np.linspace(-1.5, 1.2, V).astype(np.float32)
+    x[[5, 30]] = 0.3                            # a tie in value
+    lg = _bf16_bits(x[None]) if dtype == "bf16" else x[None]
+    xv = (lg.astype(np.uint32) << 16).view(np.float32)[0] if dtype == "bf16" else x
+    n = 6000
+    B = 8                                         # rows of one call draw independently
+    counts = np.zeros(V)
+    for off in range(n // B):
+        tok, _ = oracle.masked_sample(ns, al, np.zeros(B, np.int32), np.repeat(lg, B, 0), inv_t, 11, off,
+                                      lib=oracle_lib)
+        np.add.at(counts, tok, 1)
+    p = np.exp(xv[allowed].astype(np.float64) * inv_t)
+    p /= p.sum()
+    exp = p * n
+    chi2 = ((counts[allowed] - exp) ** 2 / exp).sum()
+    assert counts.sum() == n and counts[np.setdiff1d(np.arange(V), allowed)].sum() == 0
+    assert chi2 < 25.7                            # 5 degrees of freedom, p = 1e-4
+
+
+def test_sample_at_low_temperature_is_the_masked_argmax(tiny_table, oracle_lib):
+    """With 1/T = 10^4 and logits at least 0.01 apart the noise (range < 20)
+    cannot reorder them: the draw is the masked greedy choice."""
+    _, _, _, ns, al = tiny_table
+    S, V = ns.shape
+    rng = np.random.default_rng(52)
+    B = 32
+    x = np.stack([rng.permutation(V).astype(np.float32) * 0.01 for _ in range(B)])
+    x[3, :5] = np.nan
+    states = rng.integers(0, S, B).astype(np.int32)
+    states[:2] = [-1, S]
+    t_s, n_s = oracle.masked_sample(ns, al, states, x, 1e4, 5, 9, lib=oracle_lib)
+    t_g, n_g = oracle.masked_step(ns, al, states, x, lib=oracle_lib)
+    np.testing.assert_array_equal(t_s, t_g)
+    np.testing.assert_array_equal(n_s, n_g)
+
+
+def test_sample_invariants(tiny_table, oracle_lib):
+    trans, _, _, ns, al = tiny_table
+    S, V = ns.shape
+    rng = np.random.default_rng(53)
+    B = 48
+    x = rng.standard_normal((B, V)).astype(np.float32) * 3
+    states = rng.integers(0, S, B).astype(np.int32)
+    states[:3] = [-1, S, 2 ** 30]
+    t1, n1 = oracle.masked_sample(ns, al, states, x, 1.0, 99, 0, lib=oracle_lib)
+    t2, n2 = oracle.masked_sample(ns, al, states, x, 1.0, 99, 0, lib=oracle_lib)
+    t3, _ = oracle.masked_sample(ns, al, states, x, 1.0, 99, 1, lib=oracle_lib)
+    np.testing.assert_array_equal(t1, t2)        # reproducible
+    assert (t1 != t3).sum() > B // 4              # another offset draws anew
+    assert (t1[:3] == -1).all() and (n1[:3] == -1).all()
+    live = t1 >= 0
+    assert (ns[states[live], t1[live]] != -1).all()  # always an allowed token
+    np.testing.assert_array_equal(n1[live], ns[states[live], t1[live]])
