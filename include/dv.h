@@ -17,6 +17,9 @@
  *   dv_masked_step_opportunistic
  *                   dv_masked_step that checks the model's own choice first
  *                   (opportunistic masking, Sec. 3.5).
+ *   dv_masked_sample
+ *                   the sampled decode at temperature T over the allowed
+ *                   tokens, reproducible from a seed and an offset.
  *   dv_spec_walk,   the speculative chain check of Sec. 3.6: how many
  *   dv_spec_verify  proposed tokens the constraint admits, and greedy
  *                   verification of the proposals against the model's logits
@@ -212,6 +215,49 @@ DV_API dv_status dv_masked_step_opportunistic(const int32_t *next_state, const u
                          int32_t num_states, int32_t num_tokens,
                          const int32_t *states, const void *logits, int32_t dtype,
                          int32_t batch, int64_t ld_logits,
+                         int32_t *token, int32_t *new_state,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * dv_masked_sample_workspace_bytes -- device workspace dv_masked_sample needs
+ * for `batch` rows of `num_tokens` logits.  Returns 0 when a size is outside
+ * its limit.
+ */
+DV_API size_t dv_masked_sample_workspace_bytes(int32_t batch, int32_t num_tokens);
+
+/*
+ * dv_masked_sample -- one sampled constrained decoding step (Algorithm 1's
+ * decode "argmax or sample"; the paper samples at temperature 1.0, Sec. 4).
+ *
+ * For every row b with a live state s (as dv_masked_step), the token is
+ * drawn from softmax(logits / T) restricted to the allowed tokens, as the
+ * Gumbel-max choice
+ *     token[b] = argmax over allowed i of  fma(x_i, inv_temperature, G_i)
+ * in binary32 (x_i the logit, widened exactly from bf16), NaN ranking as
+ * -infinity and ties going to the lowest index, with the noise
+ *     G_i = -ln(-ln U_i),  U_i = (2 (w >> 9) + 1) 2^-24,
+ *     w = word (i mod 4) of Philox4x32-10 (Salmon et al., SC 2011) with
+ *         key (seed mod 2^32, seed >> 32) and
+ *         counter (i / 4, b, offset mod 2^32, offset >> 32),
+ * and ln evaluated in binary32 by fixed IEEE steps (x = m 2^e with m in
+ * [sqrt(1/2), sqrt(2)); z = (m - 1) r, r = 1/(m + 1) by four Newton steps
+ * t = fma(-d, r, 1), r = fma(r, t, r) from r = 1/2; ln m = 2 h with
+ * h = fma(z^3, p, z), p = 1/3 + w (1/5 + w (1/7 + w/9)) by fused
+ * multiply-adds, w = z^2; ln x = fma(e, ln 2, ln m)), so the draw is the
+ * same on every device.  new_state[b] = next_state[s*V + token[b]]; a dead
+ * row or a row with nothing allowed gives token -1 and DV_DEAD.  Rows are
+ * independent draws; use a different `offset` for every step (the pair
+ * (seed, offset) names one draw of the whole batch).
+ *
+ * inv_temperature = 1/T, finite and > 0 (T -> 0 approaches dv_masked_step).
+ * Other arguments and errors as dv_masked_step (DV_ERR_SHAPE also for a
+ * bad inv_temperature); workspace: dv_masked_sample_workspace_bytes(B, V).
+ */
+DV_API dv_status dv_masked_sample(const int32_t *next_state, const uint32_t *allow,
+                         int32_t num_states, int32_t num_tokens,
+                         const int32_t *states, const void *logits, int32_t dtype,
+                         int32_t batch, int64_t ld_logits, float inv_temperature,
+                         uint64_t seed, uint64_t offset,
                          int32_t *token, int32_t *new_state,
                          void *workspace, size_t workspace_bytes, void *stream);
 

@@ -20,9 +20,9 @@ import os
 
 import torch
 
-__all__ = ["align", "masked_step", "spec_walk", "spec_verify", "align_workspace_bytes",
-           "masked_step_workspace_bytes", "spec_verify_workspace_bytes", "step_workspace",
-           "spec_workspace", "DvError", "DEAD", "library_path", "lib"]
+__all__ = ["align", "masked_step", "masked_sample", "spec_walk", "spec_verify", "align_workspace_bytes",
+           "masked_step_workspace_bytes", "masked_sample_workspace_bytes", "spec_verify_workspace_bytes",
+           "step_workspace", "sample_workspace", "spec_workspace", "DvError", "DEAD", "library_path", "lib"]
 
 DEAD = -1
 DV_OK = 0
@@ -65,6 +65,11 @@ def _load():
     lib.dv_masked_step_opportunistic.restype = ctypes.c_int
     lib.dv_masked_step_opportunistic.argtypes = [vp, vp, i32, i32, vp, vp, i32, i32, i64, vp, vp, vp, sz,
                                                  vp]
+    lib.dv_masked_sample_workspace_bytes.restype = sz
+    lib.dv_masked_sample_workspace_bytes.argtypes = [i32, i32]
+    lib.dv_masked_sample.restype = ctypes.c_int
+    lib.dv_masked_sample.argtypes = [vp, vp, i32, i32, vp, vp, i32, i32, i64, ctypes.c_float, ctypes.c_uint64,
+                                     ctypes.c_uint64, vp, vp, vp, sz, vp]
     lib.dv_spec_walk.restype = ctypes.c_int
     lib.dv_spec_walk.argtypes = [vp, vp, i32, i32, vp, vp, i32, i64, i32, vp, vp, vp]
     lib.dv_spec_verify_workspace_bytes.restype = sz
@@ -205,6 +210,48 @@ def masked_step(next_state, allow, states, logits, token=None, new_state=None, w
     st = fn(_ptr(next_state), _ptr(allow), S, V, _ptr(states), _ptr(logits), dt, B, ld, _ptr(token),
             _ptr(new_state), _ptr(workspace), workspace.numel(), _stream(stream, dev))
     _check(st, "dv_masked_step_opportunistic" if opportunistic else "dv_masked_step")
+    return token, new_state
+
+
+def masked_sample_workspace_bytes(batch: int, num_tokens: int) -> int:
+    return int(lib.dv_masked_sample_workspace_bytes(batch, num_tokens))
+
+
+def sample_workspace(batch: int, num_tokens: int, device) -> torch.Tensor:
+    """A workspace for ``masked_sample`` (reusable by calls ordered on one stream)."""
+    n = masked_sample_workspace_bytes(batch, num_tokens)
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
+
+
+def masked_sample(next_state, allow, states, logits, seed: int, offset: int, inv_temperature: float = 1.0,
+                  token=None, new_state=None, workspace=None, stream=None):
+    """One sampled masked decoding step: each row draws from softmax(logits *
+    inv_temperature) over its allowed tokens (Gumbel-max with Philox noise of
+    (seed, offset, row, token); use a new offset for every step).  logits
+    [B][ld] fp32 or bf16.  Returns (token [B], new_state [B])."""
+    dev = states.device
+    _want(next_state, "next_state", torch.int32, dev)
+    _want(allow, "allow", torch.int32, dev)
+    _want(states, "states", torch.int32, dev)
+    dt = _dtype_code(logits)
+    S, V = next_state.shape
+    B = states.shape[0]
+    if logits.dim() != 2 or logits.shape[0] != B or logits.shape[1] != V or not logits.is_cuda:
+        raise ValueError(f"logits must be a [{B}][{V}] device tensor (a wider row stride is allowed)")
+    if B and logits.stride(1) != 1:
+        raise ValueError("logits must have unit stride along the vocabulary")
+    ld = logits.stride(0) if B > 1 else max(V, logits.stride(0))
+    if token is None:
+        token = torch.empty(B, dtype=torch.int32, device=dev)
+    if new_state is None:
+        new_state = torch.empty(B, dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = sample_workspace(B, V, dev)
+    st = lib.dv_masked_sample(_ptr(next_state), _ptr(allow), S, V, _ptr(states), _ptr(logits), dt, B, ld,
+                              float(inv_temperature), int(seed) & (2**64 - 1), int(offset) & (2**64 - 1),
+                              _ptr(token), _ptr(new_state), _ptr(workspace), workspace.numel(),
+                              _stream(stream, dev))
+    _check(st, "dv_masked_sample")
     return token, new_state
 
 

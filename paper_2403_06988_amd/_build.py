@@ -8,7 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["dv_api.hip", "dv_align.hip", "dv_step.hip", "dv_spec.hip", "dv_probes.hip"]
+SOURCES = ["dv_api.hip", "dv_align.hip", "dv_step.hip", "dv_spec.hip", "dv_sample.hip", "dv_probes.hip"]
 LIB = os.path.join(HERE, "libdv.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

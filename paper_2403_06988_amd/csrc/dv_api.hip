@@ -6,6 +6,7 @@
 
 #include "../../include/dv.h"
 #include "dv_internal.h"
+#include "dv_sample.h"
 
 namespace {
 
@@ -127,7 +128,14 @@ size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens)
     return dv::step_workspace_bytes(batch, num_tokens);
 }
 
-static dv_status step_common(const char *name, bool opportunistic, const int32_t *next_state,
+// How a step call decodes: greedy, greedy with the check first, or sampled.
+struct StepMode {
+    int kind;  // 0 greedy, 1 opportunistic, 2 sampled
+    float inv_temperature;
+    uint64_t seed, offset;
+};
+
+static dv_status step_common(const char *name, StepMode mode, const int32_t *next_state,
                              const uint32_t *allow, int32_t num_states, int32_t num_tokens, const int32_t *states,
                              const void *logits, int32_t dtype, int32_t batch, int64_t ld_logits, int32_t *token,
                              int32_t *new_state, void *workspace, size_t workspace_bytes, void *stream)
@@ -149,6 +157,9 @@ static dv_status step_common(const char *name, bool opportunistic, const int32_t
                     (long long)ld_logits, num_tokens);
     if (dtype != DV_F32 && dtype != DV_BF16)
         return fail(DV_ERR_DTYPE, "%s: unknown dtype %d", name, dtype);
+    if (mode.kind == 2 && !(mode.inv_temperature > 0.0f && mode.inv_temperature <= 3.0e38f))
+        return fail(DV_ERR_SHAPE, "%s: inv_temperature=%g must be finite and > 0", name,
+                    (double)mode.inv_temperature);
     if (batch == 0)
         return DV_OK;
     const size_t S = (size_t)num_states, V = (size_t)num_tokens, W = (V + 31) / 32, B = (size_t)batch;
@@ -163,7 +174,8 @@ static dv_status step_common(const char *name, bool opportunistic, const int32_t
         if (overlap(out, r_ns) || overlap(out, r_al) || overlap(out, r_st) || overlap(out, r_lg))
             return fail(DV_ERR_ALIAS, "%s: an output overlaps an input "
                                       "(ping-pong two state buffers instead of updating in place)", name);
-    const size_t need = dv::step_workspace_bytes(batch, num_tokens);
+    const size_t need = mode.kind == 2 ? dv::sample_workspace_bytes(batch, num_tokens)
+                                       : dv::step_workspace_bytes(batch, num_tokens);
     if (!workspace || workspace_bytes < need)
         return fail(DV_ERR_WORKSPACE, "%s: workspace of %zu bytes given, %zu needed", name, workspace_bytes,
                     need);
@@ -174,13 +186,18 @@ static dv_status step_common(const char *name, bool opportunistic, const int32_t
         if (overlap(r_ws, r))
             return fail(DV_ERR_ALIAS, "%s: workspace overlaps an input or output", name);
     const hipStream_t st = static_cast<hipStream_t>(stream);
-    return hip_status(opportunistic
-                          ? dv::launch_masked_step_opportunistic(next_state, allow, num_states, num_tokens, states,
-                                                                 logits, dtype, batch, ld_logits, token, new_state,
-                                                                 workspace, st)
-                          : dv::launch_masked_step(next_state, allow, num_states, num_tokens, states, logits,
-                                                   dtype, batch, ld_logits, token, new_state, workspace, st),
-                      "launch");
+    hipError_t e;
+    if (mode.kind == 2)
+        e = dv::launch_masked_sample(next_state, allow, num_states, num_tokens, states, logits, dtype, batch,
+                                     ld_logits, mode.inv_temperature, mode.seed, mode.offset, token, new_state,
+                                     workspace, st);
+    else if (mode.kind == 1)
+        e = dv::launch_masked_step_opportunistic(next_state, allow, num_states, num_tokens, states, logits, dtype,
+                                                 batch, ld_logits, token, new_state, workspace, st);
+    else
+        e = dv::launch_masked_step(next_state, allow, num_states, num_tokens, states, logits, dtype, batch,
+                                   ld_logits, token, new_state, workspace, st);
+    return hip_status(e, "launch");
 }
 
 dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow, int32_t num_states,
@@ -188,7 +205,7 @@ dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow, int32
                          int32_t batch, int64_t ld_logits, int32_t *token, int32_t *new_state,
                          void *workspace, size_t workspace_bytes, void *stream)
 {
-    return step_common("dv_masked_step", false, next_state, allow, num_states, num_tokens, states, logits,
+    return step_common("dv_masked_step", StepMode{0, 1.0f, 0, 0}, next_state, allow, num_states, num_tokens, states, logits,
                        dtype, batch, ld_logits, token, new_state, workspace, workspace_bytes, stream);
 }
 
@@ -198,8 +215,26 @@ dv_status dv_masked_step_opportunistic(const int32_t *next_state, const uint32_t
                                        int32_t *new_state, void *workspace, size_t workspace_bytes,
                                        void *stream)
 {
-    return step_common("dv_masked_step_opportunistic", true, next_state, allow, num_states, num_tokens, states,
+    return step_common("dv_masked_step_opportunistic", StepMode{1, 1.0f, 0, 0}, next_state, allow, num_states, num_tokens, states,
                        logits, dtype, batch, ld_logits, token, new_state, workspace, workspace_bytes, stream);
+}
+
+size_t dv_masked_sample_workspace_bytes(int32_t batch, int32_t num_tokens)
+{
+    if (batch < 0 || batch > DV_MAX_BATCH || num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
+        return 0;
+    return dv::sample_workspace_bytes(batch, num_tokens);
+}
+
+dv_status dv_masked_sample(const int32_t *next_state, const uint32_t *allow, int32_t num_states, int32_t num_tokens,
+                           const int32_t *states, const void *logits, int32_t dtype, int32_t batch,
+                           int64_t ld_logits, float inv_temperature, uint64_t seed, uint64_t offset,
+                           int32_t *token, int32_t *new_state, void *workspace, size_t workspace_bytes,
+                           void *stream)
+{
+    return step_common("dv_masked_sample", StepMode{2, inv_temperature, seed, offset}, next_state, allow,
+                       num_states, num_tokens, states, logits, dtype, batch, ld_logits, token, new_state, workspace,
+                       workspace_bytes, stream);
 }
 
 static dv_status spec_shape_checks(const char *name, int32_t num_states, int32_t num_tokens, int32_t batch,

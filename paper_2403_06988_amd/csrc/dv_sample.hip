@@ -1,0 +1,262 @@
+// Masked sampling on CDNA4 (gfx950): the sampled decode of Algorithm 1 (the
+// paper samples at temperature 1.0, Sec. 4) as a Gumbel-max draw over each
+// row's admissible tokens:
+//     token = argmax over allowed i of  fma(x_i, 1/T, G_i),  G_i = -ln(-ln U_i),
+// with U_i from Philox4x32-10 (Salmon et al., SC 2011) keyed by the seed and
+// counted by (i / 4, row, offset), and ln in binary32 by fixed steps that
+// round alike on every IEEE implementation (no library log, no division), so
+// the draw is reproducible bit for bit.
+//
+// The cost is arithmetic, not memory: a Philox call (ten rounds of two
+// 32x32->64 multiplies) per 4 tokens and two logarithms per token.  Only
+// admissible tokens need noise, so each wave compacts its 4-token groups
+// that hold at least one allowed token into an LDS queue (one allow word of
+// 32 tokens per lane, a shuffle prefix sum for the queue offsets), then every
+// lane takes one queued group: one Philox call per group, a logarithm pair
+// per allowed token.  Sparse masks then cost in proportion to their allowed
+// groups and dense ones keep every lane busy.  Lanes combine exact
+// (order-preserving fp32 key << 32 | ~index) maxima, so ties go to the lowest
+// index and the result does not depend on the order of the work.
+#include "dv_sample.h"
+
+namespace dv {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kTokPerIter = kThreads * 32;  // one allow word per lane per iteration
+constexpr int kTargetBlocks = 2048;
+constexpr int kMaxChunks = 64;
+
+struct SampleGeometry {
+    int chunk_tok;  // a multiple of kTokPerIter
+    int nchunks;
+};
+
+SampleGeometry sample_geometry(int B, int V)
+{
+    const int iters = (V + kTokPerIter - 1) / kTokPerIter;
+    int want = (kTargetBlocks + (B > 0 ? B : 1) - 1) / (B > 0 ? B : 1);
+    want = want > iters ? iters : want;
+    want = want > kMaxChunks ? kMaxChunks : want;
+    want = want < 1 ? 1 : want;
+    const int per = (iters + want - 1) / want;
+    return {per * kTokPerIter, (iters + per - 1) / per};
+}
+
+__device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                               uint32_t k1)
+{
+#pragma unroll
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        c1 = (uint32_t)p1;
+        c3 = (uint32_t)p0;
+        c0 = n0;
+        c2 = n2;
+    }
+    return make_uint4(c0, c1, c2, c3);
+}
+
+// ln of a positive normal binary32: x = m 2^e, m in [sqrt(1/2), sqrt(2));
+// z = (m - 1) / (m + 1) with the reciprocal by four Newton steps from 1/2;
+// ln m = 2 (z + z^3 (1/3 + w (1/5 + w (1/7 + w / 9)))), w = z^2;
+// ln x = fma(e, ln 2, ln m).  Every operation is a rounded IEEE add,
+// multiply or fused multiply-add, written out (no contraction).
+__device__ __forceinline__ float ln_f32(float x)
+{
+#pragma clang fp contract(off)
+    const uint32_t bits = __float_as_uint(x);
+    int e = (int)(bits >> 23) - 127;
+    uint32_t mb = (bits & 0x007FFFFFu) | 0x3F800000u;
+    if (mb > 0x3FB504F3u) {
+        mb -= 0x00800000u;
+        e += 1;
+    }
+    const float f = __uint_as_float(mb) - 1.0f;
+    const float d = f + 2.0f;
+    float r = 0.5f;
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const float t = __builtin_fmaf(-d, r, 1.0f);
+        r = __builtin_fmaf(r, t, r);
+    }
+    const float z = f * r;
+    const float w = z * z;
+    float p = __builtin_fmaf(w, 0x1.c71c72p-4f, 0x1.24924ap-3f);
+    p = __builtin_fmaf(w, p, 0x1.99999ap-3f);
+    p = __builtin_fmaf(w, p, 0x1.555556p-2f);
+    const float zw = z * w;
+    const float half = __builtin_fmaf(zw, p, z);
+    const float lnm = half + half;
+    return __builtin_fmaf((float)e, 0x1.62e430p-1f, lnm);
+}
+
+__device__ __forceinline__ float gumbel_of_word(uint32_t w)
+{
+#pragma clang fp contract(off)
+    const float u = (float)(2u * (w >> 9) + 1u) * 0x1p-24f;  // exact, strictly inside (0, 1)
+    return -ln_f32(-ln_f32(u));
+}
+
+// Order-preserving key of an fp32 bit pattern: NaN ranks as -inf, -0.0 as
+// +0.0; every value's key is > 0, so 0 stands for "nothing yet".
+__device__ __forceinline__ uint32_t order_key(uint32_t u)
+{
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u)
+        u = 0xFF800000u;
+    if (u == 0x80000000u)
+        u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+template <int DT>
+__device__ __forceinline__ float logit_at(const char *row, int i)
+{
+    if constexpr (DT == 0)
+        return reinterpret_cast<const float *>(row)[i];
+    else
+        return __uint_as_float((uint32_t)reinterpret_cast<const uint16_t *>(row)[i] << 16);
+}
+
+template <int DT>
+__global__ __launch_bounds__(kThreads) void masked_sample_kernel(
+    const uint32_t *__restrict__ allow, int S, int V, int W, const int32_t *__restrict__ states,
+    const void *__restrict__ logits, int64_t ld, float inv_t, uint32_t seed_lo, uint32_t seed_hi, uint32_t off_lo,
+    uint32_t off_hi, int chunk_tok, int nchunks, uint64_t *__restrict__ partial)
+{
+#pragma clang fp contract(off)
+    __shared__ uint32_t queue[kWaves][kWave * 8];  // up to 8 groups per lane per iteration
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int b = blockIdx.x / nchunks;
+    const int c = blockIdx.x - b * nchunks;
+    const int s = states[b];
+    const bool live = (uint32_t)s < (uint32_t)S;  // block-uniform
+    uint64_t best = 0;
+    if (live) {
+        const char *row = static_cast<const char *>(logits) + (size_t)b * (size_t)ld * (DT == 0 ? 4 : 2);
+        const uint32_t *arow = allow + (size_t)s * W;
+        const int t0 = c * chunk_tok;
+        const int t1 = min(V, t0 + chunk_tok);
+        for (int base = t0; base < t1; base += kTokPerIter) {  // block-uniform trip count
+            const int tok0 = base + tid * 32;
+            uint32_t word = tok0 < t1 ? arow[tok0 >> 5] : 0u;
+            if (tok0 < t1 && t1 - tok0 < 32)
+                word &= (1u << (t1 - tok0)) - 1u;  // a chunk ends inside this word only at V
+            // groups (4 tokens) holding an allowed token: bit 4k of `nz`
+            uint32_t nz = (word | (word >> 1) | (word >> 2) | (word >> 3)) & 0x11111111u;
+            const int cnt = __popc(nz);
+            int incl = cnt;
+#pragma unroll
+            for (int d = 1; d < kWave; d <<= 1) {
+                const int y = __shfl_up(incl, d);
+                if (lane >= d)
+                    incl += y;
+            }
+            const int total = __shfl(incl, kWave - 1);
+            int pos = incl - cnt;
+            while (nz) {
+                const int k = __builtin_ctz(nz) >> 2;
+                nz &= nz - 1u;
+                // token group index (token / 4) and its 4 mask bits
+                queue[wave][pos++] = ((uint32_t)((tok0 >> 2) + k) << 4) | ((word >> (4 * k)) & 0xFu);
+            }
+            __syncthreads();
+            for (int q = lane; q < total; q += kWave) {
+                const uint32_t entry = queue[wave][q];
+                const uint32_t g = entry >> 4;
+                uint32_t bitsg = entry & 0xFu;
+                const uint4 rnd = philox4x32_10(g, (uint32_t)b, off_lo, off_hi, seed_lo, seed_hi);
+                while (bitsg) {
+                    const int e = __builtin_ctz(bitsg);
+                    bitsg &= bitsg - 1u;
+                    const uint32_t w = e == 0 ? rnd.x : e == 1 ? rnd.y : e == 2 ? rnd.z : rnd.w;
+                    const int i = (int)(g * 4u) + e;
+                    const float key = __builtin_fmaf(logit_at<DT>(row, i), inv_t, gumbel_of_word(w));
+                    const uint64_t packed =
+                        ((uint64_t)order_key(__float_as_uint(key)) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i);
+                    best = max_u64(best, packed);
+                }
+            }
+            __syncthreads();
+        }
+    }
+    // block-wide maximum
+    __shared__ uint64_t red[kWaves];
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1)
+        best = max_u64(best, __shfl_xor(best, d));
+    if (lane == 0)
+        red[wave] = best;
+    __syncthreads();
+    if (tid == 0) {
+        for (int w = 1; w < kWaves; ++w)
+            best = max_u64(best, red[w]);
+        partial[blockIdx.x] = best;
+    }
+}
+
+// One lane per row: combine the row's chunk maxima and write the outputs.
+__global__ __launch_bounds__(kThreads) void sample_finalize_kernel(const int32_t *__restrict__ next_state, int S,
+                                                                  int V, const int32_t *__restrict__ states, int B,
+                                                                  int nchunks,
+                                                                  const uint64_t *__restrict__ partial,
+                                                                  int32_t *__restrict__ token,
+                                                                  int32_t *__restrict__ new_state)
+{
+    const int b = blockIdx.x * kThreads + threadIdx.x;
+    if (b >= B)
+        return;
+    uint64_t best = 0;
+    for (int c = 0; c < nchunks; ++c)
+        best = max_u64(best, partial[(size_t)b * nchunks + c]);
+    const int s = states[b];
+    const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
+    const bool found = tok >= 0 && tok < V && (uint32_t)s < (uint32_t)S;  // guards the read
+    token[b] = found ? tok : -1;
+    new_state[b] = found ? next_state[(size_t)s * V + tok] : -1;
+}
+
+}  // namespace
+
+size_t sample_workspace_bytes(int B, int V)
+{
+    const SampleGeometry g = sample_geometry(B, V);
+    return align_up((size_t)(B > 0 ? B : 1) * (size_t)g.nchunks * sizeof(uint64_t), 256);
+}
+
+hipError_t launch_masked_sample(const int32_t *next_state, const uint32_t *allow, int S, int V,
+                                const int32_t *states, const void *logits, int dtype, int B, int64_t ld,
+                                float inv_temperature, uint64_t seed, uint64_t offset, int32_t *token,
+                                int32_t *new_state, void *workspace, hipStream_t stream)
+{
+    const int W = (V + 31) / 32;
+    const SampleGeometry g = sample_geometry(B, V);
+    uint64_t *partial = static_cast<uint64_t *>(workspace);
+    const unsigned grid = (unsigned)B * (unsigned)g.nchunks;
+    const uint32_t s_lo = (uint32_t)seed, s_hi = (uint32_t)(seed >> 32);
+    const uint32_t o_lo = (uint32_t)offset, o_hi = (uint32_t)(offset >> 32);
+    if (dtype == 0)
+        masked_sample_kernel<0><<<grid, kThreads, 0, stream>>>(allow, S, V, W, states, logits, ld, inv_temperature,
+                                                               s_lo, s_hi, o_lo, o_hi, g.chunk_tok, g.nchunks,
+                                                               partial);
+    else
+        masked_sample_kernel<1><<<grid, kThreads, 0, stream>>>(allow, S, V, W, states, logits, ld, inv_temperature,
+                                                               s_lo, s_hi, o_lo, o_hi, g.chunk_tok, g.nchunks,
+                                                               partial);
+    sample_finalize_kernel<<<(B + kThreads - 1) / kThreads, kThreads, 0, stream>>>(next_state, S, V, states, B,
+                                                                                  g.nchunks, partial, token,
+                                                                                  new_state);
+    return hipGetLastError();
+}
+
+}  // namespace dv

@@ -236,3 +236,33 @@ def test_opportunistic_step_rejects_before_launch(kw, status):
                                           args["new"], args["ws"], args["ws_bytes"], None)
     assert st == status
     assert lib.dv_last_error().startswith(b"dv_masked_step_opportunistic")
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(ns=None), INVALID),
+    (dict(ld=999), SHAPE),
+    (dict(inv_t=0.0), SHAPE),
+    (dict(inv_t=-1.0), SHAPE),
+    (dict(inv_t=float("nan")), SHAPE),
+    (dict(inv_t=float("inf")), SHAPE),
+    (dict(dtype=5), DTYPE),
+    (dict(new=P + 2 * GB), ALIAS),
+    (dict(ws_bytes=8), WORKSPACE),
+    (dict(ws=P + 6 * GB + 8), WORKSPACE),
+])
+def test_masked_sample_rejects_before_launch(kw, status):
+    args = dict(ns=P, allow=P + GB, S=16, V=1000, states=P + 2 * GB, logits=P + 3 * GB, dtype=1, B=8,
+                ld=1000, inv_t=1.0, tok=P + 4 * GB, new=P + 5 * GB, ws=P + 6 * GB, ws_bytes=None)
+    args.update(kw)
+    if args["ws_bytes"] is None:
+        args["ws_bytes"] = lib.dv_masked_sample_workspace_bytes(8, 1000)
+    st = lib.dv_masked_sample(args["ns"], args["allow"], args["S"], args["V"], args["states"], args["logits"],
+                              args["dtype"], args["B"], args["ld"], args["inv_t"], 1, 2, args["tok"], args["new"],
+                              args["ws"], args["ws_bytes"], None)
+    assert st == status
+    assert lib.dv_last_error().startswith(b"dv_masked_sample")
+
+
+def test_masked_sample_workspace_query():
+    assert lib.dv_masked_sample_workspace_bytes(-1, 10) == 0
+    assert lib.dv_masked_sample_workspace_bytes(256, 128256) >= 256 * 8

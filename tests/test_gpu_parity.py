@@ -750,3 +750,143 @@ def test_opportunistic_workload(dv, wid, adherent):
     for i, b in enumerate(rows):
         t_o, _ = oracle.masked_chain(cache, init[b], xr[i][None])
         assert int(tok[b]) == int(t_o[0]), f"workload {wid} row {b}"
+
+
+# ----------------------------------------------- masked sampling (Sec. 4: T = 1.0)
+
+SEED = 0x5EED_0000_0000_2403
+
+
+def _sample_chain(dv, ns, al, init_states, x, seed, inv_t, ws):
+    """Sampled decoding on the device: step k draws with offset k."""
+    steps, B = x.shape[0], x.shape[1]
+    sts = torch.empty((steps + 1, B), dtype=torch.int32, device=DEV)
+    tks = torch.empty((steps, B), dtype=torch.int32, device=DEV)
+    sts[0].copy_(init_states)
+    for k in range(steps):
+        dv.masked_sample(ns, al, sts[k], x[k], seed, k, inv_temperature=inv_t, token=tks[k],
+                         new_state=sts[k + 1], workspace=ws)
+    return tks, sts
+
+
+@pytest.mark.parametrize("wid,steps,inv_t", [(1, 64, 1.0), (2, 64, 1.0), (2, 16, 0.5), (3, 16, 1.0),
+                                             (6, 32, 1.0), (7, 32, 2.0), (8, 32, 1.0)])
+def test_sample_chain_workload_full(dv, wid, steps, inv_t):
+    """Every row and step against the oracle's own sampled chain (its own
+    table, its own previous states)."""
+    w = W.WORKLOADS[wid]
+    _say(f"sampled chain workload {w.describe()} steps={steps} 1/T={inv_t}")
+    trans, offsets, data, ns, al = _workload_table(dv, wid)
+    ns_o, al_o = oracle.align(trans, offsets, data)
+    init = W.init_states(wid)
+    x = W.logits_all(wid, device=DEV, steps=steps)
+    ws = dv.sample_workspace(w.B, w.V, DEV)
+    tks, sts = _sample_chain(dv, ns, al, _dev(init), x, SEED + wid, inv_t, ws)
+    torch.cuda.synchronize()
+    xs = to_oracle(x)
+    cur = init
+    for k in range(steps):
+        t_o, n_o = oracle.masked_sample(ns_o, al_o, cur, xs[k], inv_t, SEED + wid, k)
+        np.testing.assert_array_equal(tks[k].cpu().numpy(), t_o, err_msg=f"workload {wid} step {k}")
+        np.testing.assert_array_equal(sts[k + 1].cpu().numpy(), n_o, err_msg=f"workload {wid} step {k}")
+        cur = n_o
+    # a sampled chain differs from the greedy one (it is a draw, not the argmax)
+    g_t, _ = oracle.masked_step(ns_o, al_o, init, xs[0])
+    assert (tks[0].cpu().numpy() != g_t).any() or w.B == 1
+
+
+def _one_row_of(cache, s, b):
+    """Oracle inputs that give row b state s through a one-state table: rows
+    0..b-1 are dead, so the noise counter of row b is the device's."""
+    ns_row, al_row = cache.get(int(s))
+    states = np.full(b + 1, -1, np.int32)
+    states[b] = 0
+    return ns_row[None], al_row[None], states
+
+
+@pytest.mark.parametrize("wid", [4, 5])
+def test_sample_step_workload_sampled(dv, wid):
+    """The benchmark's shapes, one sampled step: sampled rows against the
+    oracle; every row's draw is allowed and its new state follows it."""
+    w = W.WORKLOADS[wid]
+    _say(f"sampled step workload {w.describe()} (sampled rows)")
+    trans, offsets, data, ns, al = _workload_table(dv, wid)
+    cache = oracle.RowCache(trans, offsets, data)
+    init = W.init_states(wid)
+    x = W.logits(wid, 3, device=DEV)
+    tok, new = dv.masked_sample(ns, al, _dev(init), x, SEED, 3)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(500 + wid)
+    rows = np.unique(np.concatenate([[0, w.B - 1], rng.integers(0, w.B, 10)]))
+    xr = to_oracle(x[torch.from_numpy(rows.astype(np.int64)).to(DEV)])
+    for i, b in enumerate(rows):
+        ns1, al1, st1 = _one_row_of(cache, init[b], int(b))
+        lg = np.zeros((b + 1, xr.shape[1]), xr.dtype)
+        lg[b] = xr[i]
+        t_o, n_o = oracle.masked_sample(ns1, al1, st1, lg, 1.0, SEED, 3)
+        assert int(tok[b]) == int(t_o[b]) and int(new[b]) == int(n_o[b]), f"workload {wid} row {b}"
+    st = _dev(init).to(torch.int64)
+    tk = tok.to(torch.int64)
+    assert bool((tk >= 0).all())
+    word = al[st, tk // 32].to(torch.int64) & 0xFFFFFFFF
+    assert bool((((word >> (tk % 32)) & 1) == 1).all())
+    assert torch.equal(new, ns[st, tk])
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("inv_t", [1.0, 0.25, 3.0, 1e4])
+def test_sample_planted_and_random_rows(dv, dtype, inv_t):
+    """Random tables (dead and out-of-range states), NaN, +-inf and tied
+    logits, ragged V, rows that are not 16-byte aligned."""
+    rng = np.random.default_rng(int(inv_t * 100) + (dtype == torch.float32))
+    S, V, B = 11, 4099, 300
+    alive = rng.random((S, V)) < rng.choice([0.0, 0.003, 0.1, 0.6, 1.0], size=(S, 1))
+    ns = np.where(alive, rng.integers(0, S, (S, V)), -1).astype(np.int32)
+    Wd = (V + 31) // 32
+    pad = np.zeros((S, Wd * 32), bool)
+    pad[:, :V] = alive
+    al = np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(S, Wd)
+    states = rng.integers(-2, S + 2, B).astype(np.int32)
+    buf = torch.from_numpy((rng.standard_normal(B * (V + 1) + 8) * 3).astype(np.float32)).to(dtype)
+    buf[torch.from_numpy(rng.integers(0, buf.numel(), 200))] = float("nan")
+    buf[torch.from_numpy(rng.integers(0, buf.numel(), 20))] = float("inf")
+    buf[torch.from_numpy(rng.integers(0, buf.numel(), 20))] = -float("inf")
+    buf[: 5 * (V + 1)] = 1.5                                  # rows 0-4: every logit tied
+    x_h = buf[1:1 + B * (V + 1)].view(B, V + 1)[:, :V]        # row stride V + 1, offset 1
+    x = buf.to(DEV)[1:1 + B * (V + 1)].view(B, V + 1)[:, :V]
+    tok, new = dv.masked_sample(_dev(ns), _dev(al.view(np.int32)), _dev(states), x, 77, 5, inv_temperature=inv_t)
+    t_o, n_o = oracle.masked_sample(ns, al, states, to_oracle(x_h.contiguous()), inv_t, 77, 5)
+    np.testing.assert_array_equal(tok.cpu().numpy(), t_o)
+    np.testing.assert_array_equal(new.cpu().numpy(), n_o)
+
+
+def test_sample_is_reproducible_and_graph_safe(dv):
+    w = W.WORKLOADS[3]
+    trans, offsets, data, ns, al = _workload_table(dv, 3)
+    x = W.logits(3, 0, device=DEV)
+    st = _dev(W.init_states(3))
+    ws = dv.sample_workspace(w.B, w.V, DEV)
+    t1, n1 = dv.masked_sample(ns, al, st, x, 123, 0, workspace=ws)
+    t2, _ = dv.masked_sample(ns, al, st, x, 123, 0, workspace=ws)
+    t3, _ = dv.masked_sample(ns, al, st, x, 123, 1, workspace=ws)
+    t4, _ = dv.masked_sample(ns, al, st, x, 124, 0, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(t1, t2)
+    assert (t1 != t3).sum() > w.B // 4 and (t1 != t4).sum() > w.B // 4
+    tk = torch.empty_like(t1)
+    nw = torch.empty_like(n1)
+    side = torch.cuda.Stream(DEV)
+    side.wait_stream(torch.cuda.current_stream(DEV))
+    with torch.cuda.stream(side):
+        dv.masked_sample(ns, al, st, x, 123, 0, token=tk, new_state=nw, workspace=ws)
+    torch.cuda.current_stream(DEV).wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        dv.masked_sample(ns, al, st, x, 123, 0, token=tk, new_state=nw, workspace=ws)
+    for rep in range(3):
+        tk.fill_(-7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(tk, t1) and torch.equal(nw, n1), f"replay {rep}"
