@@ -18,6 +18,7 @@ Reported (one JSON line):
   roofline_align  dv_align against the HBM write roofline (4.125 B / pair)
   opportunistic  the decode chain with the model's own choice checked first
                (Sec. 3.5), on the workload's logits and on adherent logits
+  sample       the decode chain sampled at temperature 1 (Sec. 4), ALU roofline
   spec_verify  greedy verification of s = 8 proposed tokens per row (Sec. 3.6)
                over windows of the job's decode chain, with its own roofline
   cpu_baseline the CPU oracle on a bounded sample of the same workload
@@ -65,6 +66,7 @@ def parse():
     ap.add_argument("--no-probes", action="store_true", help="skip the roofline probes")
     ap.add_argument("--no-spec", action="store_true", help="skip the speculative-verification leg")
     ap.add_argument("--no-opportunistic", action="store_true", help="skip the opportunistic-masking leg")
+    ap.add_argument("--no-sample", action="store_true", help="skip the masked-sampling leg")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
 
@@ -357,6 +359,80 @@ def bench_opportunistic(dv, w, ns, al, x, tokens_all, states_all, dev, adherent=
     return out
 
 
+# Algorithmic VALU work of a sampled step, in full-rate lane-op slots: a
+# Gumbel-noised allowed token costs two binary32 logarithms (25 each: the
+# exponent split, a four-step Newton reciprocal, the series, the final fma),
+# the uniform (4) and the key (3); a Philox4x32-10 call, per 4-token group
+# with an allowed token, costs 10 rounds of two 32x32->64 multiplies (quarter
+# rate: 4 slots each) and 4 other operations.
+SAMPLE_OPS_PER_TOKEN = 57
+SAMPLE_OPS_PER_GROUP = 120
+VALU_PEAK_OPS = 256 * 64 * 2.4e9   # CUs x lanes per clock x clock (no packed math)
+
+
+def bench_sample(dv, w, ns, al, x, init_d, dev, seed=2024, reps=3):
+    """Masked sampling at temperature 1 (Sec. 4): the job's decode chain with
+    dv_masked_sample in place of the greedy step (step k uses offset k),
+    captured as a HIP graph and replayed."""
+    import numpy as np
+    import torch
+
+    steps = x.shape[0]
+    ws = dv.sample_workspace(w.B, w.V, dev)
+    sts = torch.empty((steps + 1, w.B), dtype=torch.int32, device=dev)
+    tks = torch.empty((steps, w.B), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def launches():
+        for k in range(steps):
+            dv.masked_sample(ns, al, sts[k], x[k], seed, k, token=tks[k], new_state=sts[k + 1], workspace=ws)
+
+    sts[0].copy_(init_d)
+    launches()
+    torch.cuda.synchronize()
+    ref = (tks.clone(), sts.clone())
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        launches()
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        launches()
+    times = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        graph.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b) / 1e3 / steps)
+    same = bool(torch.equal(tks, ref[0]) and torch.equal(sts, ref[1]))
+    t = float(np.median(times))
+    # work along the chain: allowed tokens and 4-token groups holding one
+    pop8 = torch.tensor([bin(i).count("1") for i in range(256)], dtype=torch.int64, device=dev)
+    allowed = groups = 0
+    for k in range(steps):
+        st = sts[k].to(torch.int64)
+        rows = al[st.clamp(min=0)][st >= 0].to(torch.int64) & 0xFFFFFFFF
+        for sh in (0, 8, 16, 24):
+            allowed += int(pop8[(rows >> sh) & 0xFF].sum())
+        nz = (rows | (rows >> 1) | (rows >> 2) | (rows >> 3)) & 0x11111111
+        for sh in (0, 8, 16, 24):
+            groups += int(pop8[(nz >> sh) & 0xFF].sum())
+    ops = (allowed * SAMPLE_OPS_PER_TOKEN + groups * SAMPLE_OPS_PER_GROUP) / steps
+    achieved = ops / t
+    return {"us_per_step": t * 1e6, "steps_per_s": 1.0 / t, "temperature": 1.0,
+            "allowed_tokens_per_step": allowed / steps, "groups_per_step": groups / steps,
+            "graph_matches_eager": same,
+            "roofline": {"kernel": "masked_sample_kernel + sample_finalize_kernel", "bound": "alu",
+                         "achieved": achieved / 1e9, "peak": VALU_PEAK_OPS / 1e9, "unit": "Gop/s",
+                         "frac": achieved / VALU_PEAK_OPS, "ops_per_launch": ops,
+                         "note": f"{SAMPLE_OPS_PER_TOKEN} ops per noised token + {SAMPLE_OPS_PER_GROUP} per "
+                                 "Philox call, full-rate lane-op slots; peak = 256 CUs x 64 lanes x 2.4 GHz"}}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -499,6 +575,9 @@ def main():
         log("opportunistic masking")
         out["opportunistic"] = bench_opportunistic(dv, w, ns, al, x, tokens_all, states_all, dev)
         out["opportunistic"]["masked_us_per_step"] = mean_launch_s * 1e6
+    if not args.no_sample:
+        log("masked sampling")
+        out["sample"] = bench_sample(dv, w, ns, al, x, init_d, dev)
     if not args.no_spec:
         log("speculative verification")
         out["spec_verify"] = bench_spec(dv, w, wid, ns, al, x, tokens_all, states_all, dev)

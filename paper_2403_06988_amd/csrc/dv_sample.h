@@ -5,7 +5,7 @@
 
 namespace dv {
 
-// Workspace: [B][nchunks] uint64 partial maxima (always written).
+// Workspace: [B][nchunks] uint64 partial maxima (rows split over blocks).
 size_t sample_workspace_bytes(int B, int V);
 
 hipError_t launch_masked_sample(const int32_t *next_state, const uint32_t *allow, int S, int V,

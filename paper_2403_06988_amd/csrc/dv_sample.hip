@@ -22,26 +22,37 @@
 namespace dv {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / kWave;
-constexpr int kTokPerIter = kThreads * 32;  // one allow word per lane per iteration
+constexpr int kThreads = 256;       // split rows: several blocks per row, then a combining pass
+constexpr int kRowThreads = 1024;   // one block per row once B >= kOneBlockRows: no combining pass
+                                    // (below that, split rows keep more waves per CU, which this
+                                    // latency-laden arithmetic needs more than it saves a launch)
+#ifndef DV_SAMPLE_ONE_BLOCK_ROWS
+#define DV_SAMPLE_ONE_BLOCK_ROWS 1024  // four or more rows per CU keep enough waves resident
+#endif
+constexpr int kOneBlockRows = DV_SAMPLE_ONE_BLOCK_ROWS;
 constexpr int kTargetBlocks = 2048;
 constexpr int kMaxChunks = 64;
 
 struct SampleGeometry {
-    int chunk_tok;  // a multiple of kTokPerIter
+    int threads;
+    int chunk_tok;  // a multiple of threads * 32 tokens (one allow word per lane per iteration)
     int nchunks;
 };
 
 SampleGeometry sample_geometry(int B, int V)
 {
-    const int iters = (V + kTokPerIter - 1) / kTokPerIter;
+    if (B >= kOneBlockRows) {
+        const int per_iter = kRowThreads * 32;
+        return {kRowThreads, (V + per_iter - 1) / per_iter * per_iter, 1};
+    }
+    const int per_iter = kThreads * 32;
+    const int iters = (V + per_iter - 1) / per_iter;
     int want = (kTargetBlocks + (B > 0 ? B : 1) - 1) / (B > 0 ? B : 1);
     want = want > iters ? iters : want;
     want = want > kMaxChunks ? kMaxChunks : want;
     want = want < 1 ? 1 : want;
     const int per = (iters + want - 1) / want;
-    return {per * kTokPerIter, (iters + per - 1) / per};
+    return {kThreads, per * per_iter, (iters + per - 1) / per};
 }
 
 __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
@@ -128,13 +139,53 @@ __device__ __forceinline__ float logit_at(const char *row, int i)
         return __uint_as_float((uint32_t)reinterpret_cast<const uint16_t *>(row)[i] << 16);
 }
 
+// The 4 logits of group g (tokens 4g .. 4g+3) as binary32 bit patterns: one
+// vector load when the row is aligned to a group and the group lies inside
+// the row, else element loads of the allowed tokens only (the last group
+// may run past V).
 template <int DT>
-__global__ __launch_bounds__(kThreads) void masked_sample_kernel(
-    const uint32_t *__restrict__ allow, int S, int V, int W, const int32_t *__restrict__ states,
-    const void *__restrict__ logits, int64_t ld, float inv_t, uint32_t seed_lo, uint32_t seed_hi, uint32_t off_lo,
-    uint32_t off_hi, int chunk_tok, int nchunks, uint64_t *__restrict__ partial)
+__device__ __forceinline__ uint4 group_logits(const char *row, bool aligned, uint32_t g, uint32_t bits, int V)
+{
+    const int i0 = (int)(g * 4u);
+    if (aligned && i0 + 3 < V) {
+        if constexpr (DT == 0) {
+            return reinterpret_cast<const uint4 *>(row)[g];
+        } else {
+            const uint2 h = reinterpret_cast<const uint2 *>(row)[g];
+            return make_uint4(h.x << 16, h.x & 0xFFFF0000u, h.y << 16, h.y & 0xFFFF0000u);
+        }
+    }
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (bits & 1u)
+        v.x = __float_as_uint(logit_at<DT>(row, i0));
+    if (bits & 2u)
+        v.y = __float_as_uint(logit_at<DT>(row, i0 + 1));
+    if (bits & 4u)
+        v.z = __float_as_uint(logit_at<DT>(row, i0 + 2));
+    if (bits & 8u)
+        v.w = __float_as_uint(logit_at<DT>(row, i0 + 3));
+    return v;
+}
+
+__device__ __forceinline__ uint32_t pick(uint4 v, int e)
+{
+    uint32_t r = v.x;
+    r = e == 1 ? v.y : r;
+    r = e == 2 ? v.z : r;
+    r = e == 3 ? v.w : r;
+    return r;
+}
+
+template <int DT, int THREADS>
+__global__ __launch_bounds__(THREADS) void masked_sample_kernel(
+    const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
+    const int32_t *__restrict__ states, const void *__restrict__ logits, int64_t ld, float inv_t, uint32_t seed_lo,
+    uint32_t seed_hi, uint32_t off_lo, uint32_t off_hi, int chunk_tok, int nchunks, uint64_t *__restrict__ partial,
+    int32_t *__restrict__ token, int32_t *__restrict__ new_state)
 {
 #pragma clang fp contract(off)
+    constexpr int kWaves = THREADS / kWave;
+    constexpr int kTokPerIter = THREADS * 32;  // one allow word per lane per iteration
     __shared__ uint32_t queue[kWaves][kWave * 8];  // up to 8 groups per lane per iteration
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int b = blockIdx.x / nchunks;
@@ -144,6 +195,7 @@ __global__ __launch_bounds__(kThreads) void masked_sample_kernel(
     uint64_t best = 0;
     if (live) {
         const char *row = static_cast<const char *>(logits) + (size_t)b * (size_t)ld * (DT == 0 ? 4 : 2);
+        const bool aligned = (reinterpret_cast<uintptr_t>(row) & (DT == 0 ? 15 : 7)) == 0;  // block-uniform
         const uint32_t *arow = allow + (size_t)s * W;
         const int t0 = c * chunk_tok;
         const int t1 = min(V, t0 + chunk_tok);
@@ -175,13 +227,15 @@ __global__ __launch_bounds__(kThreads) void masked_sample_kernel(
                 const uint32_t entry = queue[wave][q];
                 const uint32_t g = entry >> 4;
                 uint32_t bitsg = entry & 0xFu;
+                // the logits first: their load is in flight during the Philox rounds
+                const uint4 xs = group_logits<DT>(row, aligned, g, bitsg, V);
                 const uint4 rnd = philox4x32_10(g, (uint32_t)b, off_lo, off_hi, seed_lo, seed_hi);
                 while (bitsg) {
                     const int e = __builtin_ctz(bitsg);
                     bitsg &= bitsg - 1u;
-                    const uint32_t w = e == 0 ? rnd.x : e == 1 ? rnd.y : e == 2 ? rnd.z : rnd.w;
                     const int i = (int)(g * 4u) + e;
-                    const float key = __builtin_fmaf(logit_at<DT>(row, i), inv_t, gumbel_of_word(w));
+                    const float key =
+                        __builtin_fmaf(__uint_as_float(pick(xs, e)), inv_t, gumbel_of_word(pick(rnd, e)));
                     const uint64_t packed =
                         ((uint64_t)order_key(__float_as_uint(key)) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i);
                     best = max_u64(best, packed);
@@ -191,7 +245,7 @@ __global__ __launch_bounds__(kThreads) void masked_sample_kernel(
         }
     }
     // block-wide maximum
-    __shared__ uint64_t red[kWaves];
+    __shared__ uint64_t red[THREADS / kWave];
 #pragma unroll
     for (int d = kWave / 2; d > 0; d >>= 1)
         best = max_u64(best, __shfl_xor(best, d));
@@ -201,11 +255,19 @@ __global__ __launch_bounds__(kThreads) void masked_sample_kernel(
     if (tid == 0) {
         for (int w = 1; w < kWaves; ++w)
             best = max_u64(best, red[w]);
-        partial[blockIdx.x] = best;
+        if (nchunks > 1) {
+            partial[blockIdx.x] = best;
+        } else {
+            const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
+            const bool found = live && tok >= 0 && tok < V;  // guards the read
+            token[b] = found ? tok : -1;
+            new_state[b] = found ? next_state[(size_t)s * V + tok] : -1;
+        }
     }
 }
 
-// One lane per row: combine the row's chunk maxima and write the outputs.
+// One lane per row: combine the row's chunk maxima and write the outputs
+// (rows split over several blocks only).
 __global__ __launch_bounds__(kThreads) void sample_finalize_kernel(const int32_t *__restrict__ next_state, int S,
                                                                   int V, const int32_t *__restrict__ states, int B,
                                                                   int nchunks,
@@ -245,17 +307,26 @@ hipError_t launch_masked_sample(const int32_t *next_state, const uint32_t *allow
     const unsigned grid = (unsigned)B * (unsigned)g.nchunks;
     const uint32_t s_lo = (uint32_t)seed, s_hi = (uint32_t)(seed >> 32);
     const uint32_t o_lo = (uint32_t)offset, o_hi = (uint32_t)(offset >> 32);
-    if (dtype == 0)
-        masked_sample_kernel<0><<<grid, kThreads, 0, stream>>>(allow, S, V, W, states, logits, ld, inv_temperature,
-                                                               s_lo, s_hi, o_lo, o_hi, g.chunk_tok, g.nchunks,
-                                                               partial);
-    else
-        masked_sample_kernel<1><<<grid, kThreads, 0, stream>>>(allow, S, V, W, states, logits, ld, inv_temperature,
-                                                               s_lo, s_hi, o_lo, o_hi, g.chunk_tok, g.nchunks,
-                                                               partial);
-    sample_finalize_kernel<<<(B + kThreads - 1) / kThreads, kThreads, 0, stream>>>(next_state, S, V, states, B,
-                                                                                  g.nchunks, partial, token,
-                                                                                  new_state);
+#define DV_SAMPLE_LAUNCH(DT, T)                                                                                  \
+    masked_sample_kernel<DT, T><<<grid, T, 0, stream>>>(next_state, allow, S, V, W, states, logits, ld,          \
+                                                        inv_temperature, s_lo, s_hi, o_lo, o_hi, g.chunk_tok,    \
+                                                        g.nchunks, partial, token, new_state)
+    if (g.threads == kRowThreads) {
+        if (dtype == 0)
+            DV_SAMPLE_LAUNCH(0, kRowThreads);
+        else
+            DV_SAMPLE_LAUNCH(1, kRowThreads);
+    } else {
+        if (dtype == 0)
+            DV_SAMPLE_LAUNCH(0, kThreads);
+        else
+            DV_SAMPLE_LAUNCH(1, kThreads);
+    }
+#undef DV_SAMPLE_LAUNCH
+    if (g.nchunks > 1)
+        sample_finalize_kernel<<<(B + kThreads - 1) / kThreads, kThreads, 0, stream>>>(next_state, S, V, states, B,
+                                                                                      g.nchunks, partial, token,
+                                                                                      new_state);
     return hipGetLastError();
 }
 

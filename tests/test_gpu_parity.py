@@ -835,11 +835,16 @@ def test_sample_step_workload_sampled(dv, wid):
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("inv_t", [1.0, 0.25, 3.0, 1e4])
-def test_sample_planted_and_random_rows(dv, dtype, inv_t):
+@pytest.mark.parametrize("B,layout", [(300, "misaligned"), (300, "aligned"), (100, "misaligned"),
+                                      (100, "aligned")])
+def test_sample_planted_and_random_rows(dv, dtype, inv_t, B, layout):
     """Random tables (dead and out-of-range states), NaN, +-inf and tied
-    logits, ragged V, rows that are not 16-byte aligned."""
-    rng = np.random.default_rng(int(inv_t * 100) + (dtype == torch.float32))
-    S, V, B = 11, 4099, 300
+    logits, V = 4099 (a last group of 3 tokens), rows of stride V + 1 that
+    start aligned to a 4-token group or one element off it; B = 300 takes one
+    block per row, B = 100 splits rows over blocks."""
+    rng = np.random.default_rng(int(inv_t * 100) + (dtype == torch.float32) + B)
+    S, V = 11, 4099
+    off = 1 if layout == "misaligned" else 0
     alive = rng.random((S, V)) < rng.choice([0.0, 0.003, 0.1, 0.6, 1.0], size=(S, 1))
     ns = np.where(alive, rng.integers(0, S, (S, V)), -1).astype(np.int32)
     Wd = (V + 31) // 32
@@ -852,8 +857,8 @@ def test_sample_planted_and_random_rows(dv, dtype, inv_t):
     buf[torch.from_numpy(rng.integers(0, buf.numel(), 20))] = float("inf")
     buf[torch.from_numpy(rng.integers(0, buf.numel(), 20))] = -float("inf")
     buf[: 5 * (V + 1)] = 1.5                                  # rows 0-4: every logit tied
-    x_h = buf[1:1 + B * (V + 1)].view(B, V + 1)[:, :V]        # row stride V + 1, offset 1
-    x = buf.to(DEV)[1:1 + B * (V + 1)].view(B, V + 1)[:, :V]
+    x_h = buf[off:off + B * (V + 1)].view(B, V + 1)[:, :V]    # row stride V + 1
+    x = buf.to(DEV)[off:off + B * (V + 1)].view(B, V + 1)[:, :V]
     tok, new = dv.masked_sample(_dev(ns), _dev(al.view(np.int32)), _dev(states), x, 77, 5, inv_temperature=inv_t)
     t_o, n_o = oracle.masked_sample(ns, al, states, to_oracle(x_h.contiguous()), inv_t, 77, 5)
     np.testing.assert_array_equal(tok.cpu().numpy(), t_o)
