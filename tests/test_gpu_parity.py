@@ -835,12 +835,12 @@ def test_sample_step_workload_sampled(dv, wid):
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("inv_t", [1.0, 0.25, 3.0, 1e4])
-@pytest.mark.parametrize("B,layout", [(300, "misaligned"), (300, "aligned"), (100, "misaligned"),
+@pytest.mark.parametrize("B,layout", [(1030, "misaligned"), (1030, "aligned"), (100, "misaligned"),
                                       (100, "aligned")])
 def test_sample_planted_and_random_rows(dv, dtype, inv_t, B, layout):
     """Random tables (dead and out-of-range states), NaN, +-inf and tied
     logits, V = 4099 (a last group of 3 tokens), rows of stride V + 1 that
-    start aligned to a 4-token group or one element off it; B = 300 takes one
+    start aligned to a 4-token group or one element off it; B = 1030 takes one
     block per row, B = 100 splits rows over blocks."""
     rng = np.random.default_rng(int(inv_t * 100) + (dtype == torch.float32) + B)
     S, V = 11, 4099
