@@ -99,6 +99,29 @@ def test_align_edge_shapes(dv, S, V, max_len, p_empty):
     np.testing.assert_array_equal(u32(al), al_o)
 
 
+@pytest.mark.parametrize("S,V,max_len,p_empty,alphabet,eos", [
+    (513, 2100, 12, 0.02, 48, None),      # odd S: the last state tile has one state
+    (1025, 1500, 9, 0.0, 256, None),      # every byte live: Cp = 256
+    (700, 4097, 40, 0.05, 100, 17),       # long tokens (bytes past the eighth), EOS column
+    (600, 999, 2, 0.3, 126, 998),         # Cp = 128 (126 live classes + the dead class)
+])
+def test_align_large_dfa(dv, S, V, max_len, p_empty, alphabet, eos):
+    """DFAs above 512 states: the walk stages only its row tile in LDS and
+    reads later moves from the L2-resident table."""
+    _say(f"align large S={S} V={V} max_len={max_len} alphabet={alphabet} eos={eos}")
+    trans, offsets, data = _random_case(S * 7 + V, S, V, max_len, p_empty, alphabet=np.arange(alphabet))
+    if eos is None:
+        ns, al = _align(dv, trans, offsets, data)
+        ns_o, al_o = oracle.align(trans, offsets, data)
+    else:
+        acc = (np.random.default_rng(S).random(S) < 0.3).astype(np.uint8)
+        ns, al = dv.align(_dev(trans), _dev(offsets), _dev(data), accepting=_dev(acc), eos_token=eos)
+        torch.cuda.synchronize()
+        ns_o, al_o = oracle.align_eos(trans, offsets, data, acc, eos)
+    np.testing.assert_array_equal(ns.cpu().numpy(), ns_o)
+    np.testing.assert_array_equal(u32(al), al_o)
+
+
 def test_align_all_tokens_empty(dv):
     trans = np.zeros((4, 256), np.int32)
     offsets = np.zeros(70, np.int32)
