@@ -176,9 +176,11 @@ DV_API size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens);
  *              is read from it as is).
  *   states     [B] int32.
  *   logits     [B][ld_logits] of `dtype` (dv_dtype), row stride ld_logits
- *              elements (ld_logits >= V).  Rows whose address is 16-byte
- *              aligned take a vector path; others a scalar path with the
- *              same results.
+ *              elements (ld_logits >= V); the pointer must be aligned to
+ *              the element size.  bf16 rows of any such alignment take the
+ *              vector path (up to 7 elements before the row's first 16-byte
+ *              boundary are read one by one); fp32 rows not 16-byte aligned
+ *              take a scalar path with the same results.
  * Outputs (device): token [B] int32, new_state [B] int32.  They must not
  *   overlap each other or any input (callers ping-pong two state buffers).
  * Workspace: at least dv_masked_step_workspace_bytes(B, V) bytes of device
@@ -186,8 +188,9 @@ DV_API size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens);
  *   undefined.  Calls that share a workspace must be ordered on one stream.
  * B = 0 is valid and enqueues nothing; states, logits, token and new_state
  *   may then be NULL (the pointers of empty tensors).
- * Errors: DV_ERR_INVALID_ARG, DV_ERR_SHAPE (S, V, B out of range or
- *   ld_logits < V), DV_ERR_DTYPE, DV_ERR_ALIAS, DV_ERR_WORKSPACE, DV_ERR_HIP.
+ * Errors: DV_ERR_INVALID_ARG (also for logits not aligned to the element
+ *   size), DV_ERR_SHAPE (S, V, B out of range or ld_logits < V),
+ *   DV_ERR_DTYPE, DV_ERR_ALIAS, DV_ERR_WORKSPACE, DV_ERR_HIP.
  */
 DV_API dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow,
                          int32_t num_states, int32_t num_tokens,
@@ -206,8 +209,8 @@ DV_API dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow
  * maximum at the lowest index is also the masked one), so the two are
  * interchangeable; this one reads less memory when the model mostly picks
  * allowed tokens and reads a row twice when it does not.  The check runs
- * first for bf16 rows that one block covers (batch >= 256); other shapes take
- * dv_masked_step's kernels.
+ * first for bf16 rows that one block covers (batch >= 256, or rows of at
+ * most 32768 tokens); other shapes take dv_masked_step's kernels.
  * Arguments, workspace (dv_masked_step_workspace_bytes) and errors as
  *   dv_masked_step.
  */
@@ -328,17 +331,19 @@ DV_API size_t dv_spec_verify_workspace_bytes(int32_t batch, int32_t num_proposed
  * Inputs (device, read only): next_state, allow, states as for
  *   dv_masked_step; proposals [B][ld_proposals] int32 (ld_proposals >= s;
  *   may be NULL when s = 0; ids outside [0, V) are never confirmed);
- *   logits of `dtype`, any non-negative ld_row and ld_pos (a model's
- *   [B][s+1][V] output is ld_row = (s+1)*V, ld_pos = V).
+ *   logits of `dtype`, aligned to the element size, any non-negative
+ *   ld_row and ld_pos (a model's [B][s+1][V] output is ld_row = (s+1)*V,
+ *   ld_pos = V).
  * Outputs (device): token [B][s+1], accepted [B], new_state [B] int32; they
  *   must not overlap each other, an input or the workspace.
  * Workspace: at least dv_spec_verify_workspace_bytes(B, s, V) bytes of
  *   device memory, 256-byte aligned; contents on entry are ignored, on exit
  *   undefined.  Calls that share a workspace must be ordered on one stream.
  * B = 0 is valid and enqueues nothing.
- * Errors: DV_ERR_INVALID_ARG, DV_ERR_SHAPE (S, V, B or s out of range,
- *   B*(s+1) > DV_MAX_BATCH, ld_proposals < s, a negative or too large
- *   stride), DV_ERR_DTYPE, DV_ERR_ALIAS, DV_ERR_WORKSPACE, DV_ERR_HIP.
+ * Errors: DV_ERR_INVALID_ARG (also for misaligned logits), DV_ERR_SHAPE
+ *   (S, V, B or s out of range, B*(s+1) > DV_MAX_BATCH, ld_proposals < s,
+ *   a negative or too large stride), DV_ERR_DTYPE, DV_ERR_ALIAS,
+ *   DV_ERR_WORKSPACE, DV_ERR_HIP.
  */
 DV_API dv_status dv_spec_verify(const int32_t *next_state, const uint32_t *allow,
                          int32_t num_states, int32_t num_tokens,

@@ -164,6 +164,8 @@ static dv_status step_common(const char *name, StepMode mode, const int32_t *nex
         return DV_OK;
     const size_t S = (size_t)num_states, V = (size_t)num_tokens, W = (V + 31) / 32, B = (size_t)batch;
     const size_t elt = dtype == DV_F32 ? 4 : 2;
+    if (reinterpret_cast<uintptr_t>(logits) % elt)
+        return fail(DV_ERR_INVALID_ARG, "%s: logits must be aligned to their element size (%zu bytes)", name, elt);
     const Range r_tok = range_of(token, B * 4), r_new = range_of(new_state, B * 4);
     const Range r_ns = range_of(next_state, S * V * 4), r_al = range_of(allow, S * W * 4);
     const Range r_st = range_of(states, B * 4);
@@ -325,6 +327,8 @@ dv_status dv_spec_verify(const int32_t *next_state, const uint32_t *allow, int32
     const size_t S = (size_t)num_states, V = (size_t)num_tokens, W = (V + 31) / 32, B = (size_t)batch;
     const size_t np = (size_t)num_proposed, P = np + 1;
     const size_t elt = dtype == DV_F32 ? 4 : 2;
+    if (reinterpret_cast<uintptr_t>(logits) % elt)
+        return fail(DV_ERR_INVALID_ARG, "%s: logits must be aligned to their element size (%zu bytes)", name, elt);
     const Range r_tok = range_of(token, B * P * 4), r_acc = range_of(accepted, B * 4),
                 r_new = range_of(new_state, B * 4);
     const Range r_ns = range_of(next_state, S * V * 4), r_al = range_of(allow, S * W * 4);

@@ -5,7 +5,9 @@
 // the design is about keeping enough bytes in flight and spending few ALU
 // operations per element.
 //   * Launch shape (bf16).  A row is one 512-lane block once B >= 256
-//     (every CU gets at least one row), so no second pass is needed.  Each
+//     (every CU gets at least one row), or when it holds at most 32768
+//     logits (a second pass would cost more than the split saves), so no
+//     second pass is needed.  Each
 //     lane streams batches of 4 independent non-temporal 16-byte loads with
 //     a register double buffer: batch i + 1 is in flight while batch i is
 //     reduced.  Each batch loads its allow-mask
@@ -23,6 +25,9 @@
 //     differs from the exact ordering only for NaN (which must rank as -inf)
 //     and -0.0 (which must tie with +0.0); a batch whose maximum is one of
 //     those few key values is redone with exact keys.
+//   * A bf16 row need not be 16-byte aligned (any row stride): the elements
+//     before its first 16-byte boundary are read one by one and the mask
+//     bits of each vector are taken from two mask bytes, shifted.
 //   * fp32 rows (small workloads) use 256-lane blocks and exact keys with the
 //     index tracked per element.
 //   * Lanes combine (exact 32-bit key << 32 | ~index) as one 64-bit maximum:
@@ -295,7 +300,7 @@ __device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v, bool is_max)
     return v;  // in every lane of the wave
 }
 
-// bf16 rows, 16-byte aligned.  Per batch of U vectors per lane:
+// bf16 rows.  Per batch of U vectors per lane:
 //   pass 1: packed 16-bit fast keys, masked through an LDS table that turns
 //           a mask byte into four 32-bit lane masks, folded with
 //           v_pk_max_u16 -- two VALU operations per logit;
@@ -348,31 +353,59 @@ __device__ __forceinline__ void load_batch_bf16(uint4 (&d)[U], const char *row, 
     }
 }
 
+// A row is read as a head of `head` < 8 elements (its first 16-byte
+// boundary), then 16-byte vectors from element `head` on, then a tail of
+// fewer than 8 elements.  Vector v holds elements head + 8v .. head + 8v + 7,
+// whose mask bits are bits head .. head + 7 of allow bytes v and v + 1 (just
+// byte v when head = 0).  Rows of any alignment (any row stride) thus take
+// the vector path; the head and the tail are scanned element by element.
+struct RowSplit {
+    int head;  // elements before the first 16-byte boundary (< 8)
+    int nvec;  // 16-byte vectors after the head
+};
+
+__device__ __forceinline__ RowSplit split_row(const char *row, int V)
+{
+    const int head = min(V, (int)(((16u - (uint32_t)(reinterpret_cast<uintptr_t>(row) & 15u)) & 15u) >> 1));
+    return {head, (V - head) / 8};
+}
+
 // This lane's packed best (exact key << 32 | ~index, 0 if none) over the
-// chunk of 16-byte vectors [v0, v1) of `row` -- on the vector path -- plus,
-// when `last`, the scalar tail [nvec * 8, V); off the vector path, the
-// scalar scan of elements [v0 * 8, e1).  On the vector path `da` holds the
-// chunk's first batch (loaded by the caller, so it can be in flight before
-// the row's state is known).
-template <int THREADS, int U, bool MASKED>
-__device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *arow, int v0, int v1,
-                                              bool vector_path, bool last, int nvec, int V, int e1,
-                                              const uint4 *lut, uint4 (&da)[U])
+// vectors [v0, v1) of `row` past its head, plus the head when `first` and
+// the tail when `last`.  `da` holds the first batch (loaded by the caller,
+// so it can be in flight before the row's state is known).  SHIFTED: the
+// head is not empty, so mask bits straddle two bytes.
+template <int THREADS, int U, bool MASKED, bool SHIFTED>
+__device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *arow, RowSplit rs, int v0,
+                                              int v1, bool first, bool last, int V, const uint4 *lut,
+                                              uint4 (&da)[U])
 {
     constexpr int kVec = 8;
     constexpr int kStep = THREADS * U;  // vectors per batch
     const int tid = threadIdx.x;
+    const int head = SHIFTED ? rs.head : 0;
+    const char *vrow = row + 2 * head;  // 16-byte aligned
     uint32_t best_key = 0;  // exact key of the wave's best vector-path element, wave-uniform
     int best_idx = 0;
-    uint32_t lane_key = 0;  // exact key of this lane's tail / misaligned elements
+    uint32_t lane_key = 0;  // exact key of this lane's head / tail elements
     int lane_idx = 0;
-    if (vector_path) {
-        // byte v of the allow row holds the mask bits of vector v (8 tokens)
+    if (v0 < v1) {
         const uint8_t *abytes = reinterpret_cast<const uint8_t *>(arow);
+        const int last_byte = (V - 1) >> 3;
+        auto mask_of = [&](int v) -> uint32_t {
+            if constexpr (!MASKED) {
+                return 0xFFu;
+            } else if constexpr (!SHIFTED) {
+                return abytes[v];
+            } else {
+                const uint32_t b0 = abytes[v], b1 = abytes[min(v + 1, last_byte)];
+                return ((b0 | (b1 << 8)) >> head) & 0xFFu;
+            }
+        };
         auto load_masks = [&](uint32_t (&m)[U], int vb) {
 #pragma unroll
             for (int u = 0; u < U; ++u)
-                m[u] = MASKED ? (uint32_t)abytes[min(vb + u * THREADS + tid, v1 - 1)] : 0xFFu;
+                m[u] = mask_of(min(vb + u * THREADS + tid, v1 - 1));
         };
         // One batch: U vectors per lane.  Loads are issued a batch ahead
         // (logits, then their mask bytes), so while batch i is reduced,
@@ -421,9 +454,9 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
 #pragma unroll
                         for (int k = 3; k >= 0; --k) {
                             if ((w[k] >> 16) == h && ((mk[u] >> (2 * k + 1)) & 1u))
-                                pos = v * kVec + 2 * k + 1;
+                                pos = head + v * kVec + 2 * k + 1;
                             if ((w[k] & 0xFFFFu) == h && ((mk[u] >> (2 * k)) & 1u))
-                                pos = v * kVec + 2 * k;
+                                pos = head + v * kVec + 2 * k;
                         }
                     }
                 }
@@ -442,10 +475,11 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
 #pragma unroll 1
                     for (int e = 0; e < kVec; ++e) {
                         if ((mb >> e) & 1u) {
-                            const uint32_t key = f32_key(Elt<1>::bits(row, (int64_t)v * kVec + e));
+                            const int i = head + v * kVec + e;
+                            const uint32_t key = f32_key(Elt<1>::bits(row, i));
                             if (key > bk) {
                                 bk = key;
-                                bi = v * kVec + e;
+                                bi = i;
                             }
                         }
                     }
@@ -463,22 +497,33 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
         uint32_t ma[U], mb[U];
         load_masks(ma, v0);
         for (int vb = v0; vb < v1; vb += 2 * kStep) {
-            load_batch_bf16<THREADS, U>(db, row, vb + kStep, v1);
+            load_batch_bf16<THREADS, U>(db, vrow, vb + kStep, v1);
             load_masks(mb, vb + kStep);
             process_batch(da, ma, vb);
-            load_batch_bf16<THREADS, U>(da, row, vb + 2 * kStep, v1);
+            load_batch_bf16<THREADS, U>(da, vrow, vb + 2 * kStep, v1);
             load_masks(ma, vb + 2 * kStep);
             if (vb + kStep < v1)  // block-uniform
                 process_batch(db, mb, vb + kStep);
         }
-        if (last)
-            scan_exact<1, THREADS, MASKED>(row, arow, nvec * kVec, V, lane_key, lane_idx);
-    } else {
-        scan_exact<1, THREADS, MASKED>(row, arow, v0 * kVec, e1, lane_key, lane_idx);
     }
+    if (first)
+        scan_exact<1, THREADS, MASKED>(row, arow, 0, rs.head, lane_key, lane_idx);
+    if (last)
+        scan_exact<1, THREADS, MASKED>(row, arow, rs.head + rs.nvec * kVec, V, lane_key, lane_idx);
     const uint64_t mine = pack(lane_key, lane_idx);
     const uint64_t vec_best = pack(best_key, best_idx);
     return vec_best > mine ? vec_best : mine;
+}
+
+// The scan of a row's chunk with the right mask alignment (block-uniform).
+template <int THREADS, int U, bool MASKED>
+__device__ __forceinline__ uint64_t scan_chunk_bf16(const char *row, const uint32_t *arow, RowSplit rs, int v0,
+                                                    int v1, bool first, bool last, int V, const uint4 *lut,
+                                                    uint4 (&da)[U])
+{
+    if (rs.head == 0)
+        return scan_bf16<THREADS, U, MASKED, false>(row, arow, rs, v0, v1, first, last, V, lut, da);
+    return scan_bf16<THREADS, U, MASKED, true>(row, arow, rs, v0, v1, first, last, V, lut, da);
 }
 
 template <int THREADS, int U>
@@ -492,26 +537,23 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     const int b = blockIdx.x / nchunks;
     const int c = blockIdx.x - b * nchunks;
     const char *row = static_cast<const char *>(logits) + (size_t)map.offset(b) * 2;
-    const int nvec = V / 8;
+    const RowSplit rs = split_row(row, V);  // block-uniform
     const int v0 = c * chunk_vec;
-    const int v1 = min(nvec, v0 + chunk_vec);
-    const bool vector_path = (reinterpret_cast<uintptr_t>(row) & 15) == 0 && v0 < v1;  // block-uniform
+    const int v1 = min(rs.nvec, v0 + chunk_vec);
     fill_lut(lut);
     __syncthreads();
 
     // The first batch of logits does not depend on the row's state: it is in
     // flight before the state lookup returns.
     uint4 da[U];
-    if (vector_path)
-        load_batch_bf16<THREADS, U>(da, row, v0, v1);
+    if (v0 < v1)
+        load_batch_bf16<THREADS, U>(da, row + 2 * rs.head, v0, v1);
     const int s = row_state(states, map, next_state, allow, S, V, b);
     const bool live = (uint32_t)s < (uint32_t)S;  // block-uniform
     uint64_t mine = 0;
-    if (live) {
-        const int e1 = c == nchunks - 1 ? V : min(V, (c + 1) * chunk_vec * 8);
-        mine = scan_bf16<THREADS, U, true>(row, allow + (size_t)s * W, v0, v1, vector_path, c == nchunks - 1,
-                                           nvec, V, e1, lut, da);
-    }
+    if (live)
+        mine = scan_chunk_bf16<THREADS, U, true>(row, allow + (size_t)s * W, rs, v0, v1, c == 0, c == nchunks - 1,
+                                                 V, lut, da);
     const uint64_t best = block_max<THREADS>(mine);
     if (threadIdx.x != 0)
         return;
@@ -539,20 +581,19 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     __shared__ int miss;
     const int b = blockIdx.x;
     const char *row = static_cast<const char *>(logits) + (size_t)map.offset(b) * 2;
-    const int nvec = V / 8;
-    const bool vector_path = (reinterpret_cast<uintptr_t>(row) & 15) == 0 && nvec > 0;  // block-uniform
+    const RowSplit rs = split_row(row, V);  // block-uniform
     fill_lut(lut);
     __syncthreads();
 
     uint4 da[U];
-    if (vector_path)
-        load_batch_bf16<THREADS, U>(da, row, 0, nvec);
+    if (rs.nvec > 0)
+        load_batch_bf16<THREADS, U>(da, row + 2 * rs.head, 0, rs.nvec);
     const int s = states[b];
     const bool live = (uint32_t)s < (uint32_t)S;  // block-uniform
     const uint32_t *arow = allow + (size_t)(live ? s : 0) * W;
     uint64_t mine = 0;
     if (live)
-        mine = scan_bf16<THREADS, U, false>(row, arow, 0, nvec, vector_path, true, nvec, V, V, lut, da);
+        mine = scan_chunk_bf16<THREADS, U, false>(row, arow, rs, 0, rs.nvec, true, true, V, lut, da);
     uint64_t best = block_max<THREADS>(mine);
     if (threadIdx.x == 0) {
         const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
@@ -561,9 +602,9 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     }
     __syncthreads();
     if (miss) {  // block-uniform
-        if (vector_path)
-            load_batch_bf16<THREADS, U>(da, row, 0, nvec);
-        mine = scan_bf16<THREADS, U, true>(row, arow, 0, nvec, vector_path, true, nvec, V, V, lut, da);
+        if (rs.nvec > 0)
+            load_batch_bf16<THREADS, U>(da, row + 2 * rs.head, 0, rs.nvec);
+        mine = scan_chunk_bf16<THREADS, U, true>(row, arow, rs, 0, rs.nvec, true, true, V, lut, da);
         best = block_max<THREADS>(mine);
     }
     if (threadIdx.x != 0)
@@ -600,11 +641,22 @@ __global__ __launch_bounds__(kSmallThreads) void finalize_kernel(const int32_t *
 
 }  // namespace
 
+#ifndef DV_STEP_SINGLE_BLOCK_ROW_BYTES
+#define DV_STEP_SINGLE_BLOCK_ROW_BYTES 65536
+#endif
+
 StepGeometry step_geometry(int B, int V, int dtype)
 {
     const int vec = dtype == 0 ? Elt<0>::kVec : Elt<1>::kVec;
     const bool bf16 = dtype == 1;
     const int threads = bf16 ? kBigThreads : kSmallThreads;
+    // A bf16 row this short is read by one block in a batch or two: splitting
+    // it would cost a second launch (about 4 us) to save less than that.
+    if (bf16 && (int64_t)V * 2 <= DV_STEP_SINGLE_BLOCK_ROW_BYTES) {
+        const int nvec = V / vec;
+        int chunk_vec = (nvec + threads - 1) / threads * threads;
+        return {chunk_vec > 0 ? chunk_vec : threads, 1, threads};
+    }
     const int target = bf16 ? kStepOneBlockRows : kStepTargetBlocks;
     const int nvec = V / vec;
     // about `target` blocks, at least one vector per lane per chunk

@@ -111,6 +111,8 @@ def _step(ns=P, allow=P + GB, S=16, V=1000, states=P + 2 * GB, logits=P + 3 * GB
     (dict(ws_bytes=8), WORKSPACE),
     (dict(ws=P + 6 * GB + 64), WORKSPACE),
     (dict(ws=P + 2 * GB), ALIAS),
+    (dict(logits=P + 3 * GB + 2), INVALID),       # fp32 logits not 4-byte aligned
+    (dict(logits=P + 3 * GB + 1, dtype=1), INVALID),  # bf16 logits at an odd address
 ])
 def test_masked_step_rejects_before_launch(kw, status):
     assert _step(**kw) == status
@@ -205,6 +207,7 @@ def _verify(ns=P, allow=P + GB, S=16, V=1000, states=P + 2 * GB, props=P + 3 * G
     (dict(ws_bytes=16), WORKSPACE),
     (dict(ws=P + 8 * GB + 128), WORKSPACE),
     (dict(ws=P + 3 * GB), ALIAS),
+    (dict(logits=P + 4 * GB + 3), INVALID),       # bf16 logits at an odd address
 ])
 def test_spec_verify_rejects_before_launch(kw, status):
     assert _verify(**kw) == status
@@ -249,6 +252,7 @@ def test_opportunistic_step_rejects_before_launch(kw, status):
     (dict(new=P + 2 * GB), ALIAS),
     (dict(ws_bytes=8), WORKSPACE),
     (dict(ws=P + 6 * GB + 8), WORKSPACE),
+    (dict(logits=P + 3 * GB + 1), INVALID),
 ])
 def test_masked_sample_rejects_before_launch(kw, status):
     args = dict(ns=P, allow=P + GB, S=16, V=1000, states=P + 2 * GB, logits=P + 3 * GB, dtype=1, B=8,

@@ -366,6 +366,47 @@ def test_step_shapes_ld_and_alignment(dv, dtype, B, V, extra_ld, offset):
     np.testing.assert_array_equal(new.cpu().numpy(), new_o)
 
 
+@pytest.mark.parametrize("B,V,extra_ld", [
+    (1, 5, 0), (2, 13, 1), (3, 4100, 3), (2, 70001, 0), (1, 70001, 5), (260, 1030, 1), (64, 50257, 0),
+])
+@pytest.mark.parametrize("head", range(8))
+def test_step_bf16_every_row_alignment(dv, B, V, extra_ld, head):
+    """bf16 rows starting at every 2-byte offset within 16 bytes: the first
+    row's head (elements before its first 16-byte boundary) is `head`, later
+    rows vary with the row stride.  Few distinct values (many ties across
+    the head, vector and tail regions), planted NaN and signed zeros, random
+    masks of every density; greedy and opportunistic steps both checked."""
+    _say(f"step bf16 alignment B={B} V={V} ld=V+{extra_ld} head={head}")
+    rng = np.random.default_rng(1000 * head + V + B)
+    S = 7
+    alive = rng.random((S, V)) < rng.choice([0.002, 0.05, 0.5, 0.97, 1.0], size=(S, 1))
+    ns = np.where(alive, rng.integers(0, S, (S, V)), -1).astype(np.int32)
+    Wd = (V + 31) // 32
+    pad = np.zeros((S, Wd * 32), bool)
+    pad[:, :V] = alive
+    al = np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(S, Wd)
+    states = rng.integers(-1, S, B).astype(np.int32)
+    ld = V + extra_ld
+    offset = (8 - head) % 8          # elements from a 16-byte boundary
+    vals = rng.integers(-2, 3, B * ld + offset + 8).astype(np.float32)
+    buf = torch.from_numpy(vals).to(torch.bfloat16)
+    special = torch.tensor([float("nan"), -0.0, 0.0, 2.0], dtype=torch.bfloat16)
+    pos = torch.from_numpy(rng.integers(0, buf.numel(), 40))
+    buf[pos] = special[torch.from_numpy(rng.integers(0, 4, 40))]
+    base = torch.empty(buf.numel() + 64, dtype=torch.bfloat16, device=DEV)
+    shift = (-(base.data_ptr() // 2)) % 8    # first 16-byte boundary of base
+    buf_d = base[shift:shift + buf.numel()]
+    buf_d.copy_(buf.to(DEV))
+    x = buf_d[offset:offset + B * ld].view(B, ld)[:, :V]
+    assert (x.data_ptr() // 2 + head) % 8 == 0
+    xo = to_oracle(buf[offset:offset + B * ld].view(B, ld))
+    tok_o, new_o = oracle.masked_step(ns, al, states, xo)
+    for opp in (False, True):
+        tok, new = dv.masked_step(_dev(ns), _dev(al.view(np.int32)), _dev(states), x, opportunistic=opp)
+        np.testing.assert_array_equal(tok.cpu().numpy(), tok_o)
+        np.testing.assert_array_equal(new.cpu().numpy(), new_o)
+
+
 def test_step_empty_batch(dv):
     ns = torch.zeros((2, 10), dtype=torch.int32, device=DEV)
     al = torch.full((2, 1), 0x3FF, dtype=torch.int32, device=DEV)
