@@ -10,6 +10,65 @@ namespace dv {
 
 constexpr int kWave = 64;
 
+// ---------------------------------------------------------- wave reductions
+//
+// Maximum or minimum over the 64 lanes of a wave, the same value returned in
+// every lane: inside each 16-lane row by DPP moves (swap neighbours in a
+// quad, swap quad pairs, mirror each half-row, mirror the row: no LDS traffic
+// and no waits), then across the four rows by reading lanes 0, 16, 32 and
+// 48.  Every lane of the wave must be active.
+constexpr int kDppQuadSwap1 = 0xB1;       // quad_perm [1, 0, 3, 2]
+constexpr int kDppQuadSwap2 = 0x4E;       // quad_perm [2, 3, 0, 1]
+constexpr int kDppRowHalfMirror = 0x141;  // lane i of each 8 reads lane 7 - i
+constexpr int kDppRowMirror = 0x140;      // lane i of each 16 reads lane 15 - i
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_move(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+template <bool MAX, typename T>
+__device__ __forceinline__ T pick(T a, T b)
+{
+    return MAX ? (a > b ? a : b) : (a < b ? a : b);
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_move64(uint64_t v)
+{
+    return (uint64_t)dpp_move<CTRL>((uint32_t)(v >> 32)) << 32 | dpp_move<CTRL>((uint32_t)v);
+}
+
+__device__ __forceinline__ uint32_t lane_value(uint32_t v, int lane)
+{
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
+}
+
+__device__ __forceinline__ uint64_t lane_value(uint64_t v, int lane)
+{
+    return (uint64_t)lane_value((uint32_t)(v >> 32), lane) << 32 | lane_value((uint32_t)v, lane);
+}
+
+template <bool MAX, typename T>
+__device__ __forceinline__ T wave_reduce(T v)
+{
+    static_assert(sizeof(T) == 4 || sizeof(T) == 8, "32- or 64-bit lanes");
+    if constexpr (sizeof(T) == 4) {
+        v = pick<MAX>(v, (T)dpp_move<kDppQuadSwap1>(v));
+        v = pick<MAX>(v, (T)dpp_move<kDppQuadSwap2>(v));
+        v = pick<MAX>(v, (T)dpp_move<kDppRowHalfMirror>(v));
+        v = pick<MAX>(v, (T)dpp_move<kDppRowMirror>(v));
+    } else {
+        v = pick<MAX>(v, (T)dpp_move64<kDppQuadSwap1>(v));
+        v = pick<MAX>(v, (T)dpp_move64<kDppQuadSwap2>(v));
+        v = pick<MAX>(v, (T)dpp_move64<kDppRowHalfMirror>(v));
+        v = pick<MAX>(v, (T)dpp_move64<kDppRowMirror>(v));
+    }
+    return pick<MAX>(pick<MAX>((T)lane_value(v, 0), (T)lane_value(v, 16)),
+                     pick<MAX>((T)lane_value(v, 32), (T)lane_value(v, 48)));
+}
+
 // ---------------------------------------------------------------- alignment
 //
 // Workspace of dv_align (all offsets 256-byte aligned):
@@ -95,6 +154,12 @@ struct RowMap {
             return (int64_t)r * ld_row;
         const int g = r / per;
         return (int64_t)g * ld_row + (int64_t)(r - g * per) * ld_pos;
+    }
+    // Every row of `base` starts on a 16-byte boundary.
+    bool rows_aligned(const void *base, int elt) const
+    {
+        return reinterpret_cast<uintptr_t>(base) % 16 == 0 && (ld_row * elt) % 16 == 0 &&
+               (per == 1 || (ld_pos * elt) % 16 == 0);
     }
 };
 

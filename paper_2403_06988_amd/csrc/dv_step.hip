@@ -28,7 +28,8 @@
 //   * A bf16 row need not be 16-byte aligned (any row stride): the elements
 //     before its first 16-byte boundary are read one by one and the mask
 //     bits of each vector are taken from two mask bytes, shifted.
-//   * fp32 rows (small workloads) use 256-lane blocks and exact keys with the
+//   * fp32 rows (small workloads) use 256-lane blocks, the same head, vector
+//     and tail split (4 elements per vector) and exact keys with the
 //     index tracked per element.
 //   * Lanes combine (exact 32-bit key << 32 | ~index) as one 64-bit maximum:
 //     a larger key wins, on equal keys the smaller index wins.  The result
@@ -78,26 +79,12 @@ __device__ __forceinline__ uint32_t fast_key2(uint32_t w)
     return w ^ (__builtin_bit_cast(uint32_t, sign) | 0x80008000u);
 }
 
-// All-ones if bit j of m is set, else zero.
-__device__ __forceinline__ uint32_t bit_mask(uint32_t m, int j)
-{
-    return (uint32_t)(((int32_t)(m << (31 - j))) >> 31);
-}
-
 __device__ __forceinline__ uint64_t pack(uint32_t key, int idx)
 {
     return key ? ((uint64_t)key << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)idx) : 0ull;
 }
 
-__device__ __forceinline__ uint64_t wave_max(uint64_t v)
-{
-#pragma unroll
-    for (int d = kWave / 2; d > 0; d >>= 1) {
-        const uint64_t o = __shfl_xor(v, d);
-        v = o > v ? o : v;
-    }
-    return v;
-}
+__device__ __forceinline__ uint64_t wave_max(uint64_t v) { return wave_reduce<true>(v); }
 
 template <int THREADS>
 __device__ __forceinline__ uint64_t block_max(uint64_t v)
@@ -115,10 +102,40 @@ __device__ __forceinline__ uint64_t block_max(uint64_t v)
     return v;  // valid in thread 0
 }
 
+// "next state not loaded yet": the winner was not a vector-path best.
+constexpr int kNsUnknown = INT_MIN;
+
+// block_max, also returning (in thread 0) the next state of the winner when
+// its wave had already loaded it: `vec_pack` is the wave's vector-path best
+// (wave-uniform) and `vec_ns` its next state.
+template <int THREADS>
+__device__ __forceinline__ uint64_t block_max_ns(uint64_t v, uint64_t vec_pack, int vec_ns, int &ns)
+{
+    __shared__ uint64_t red[THREADS / kWave];
+    __shared__ int red_ns[THREADS / kWave];
+    v = wave_max(v);
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    if (lane == 0) {
+        red[wave] = v;
+        red_ns[wave] = v != 0 && v == vec_pack ? vec_ns : kNsUnknown;
+    }
+    __syncthreads();
+    ns = kNsUnknown;
+    if (threadIdx.x == 0) {
+        ns = red_ns[0];
+        for (int w = 1; w < THREADS / kWave; ++w) {
+            if (red[w] > v) {
+                v = red[w];
+                ns = red_ns[w];
+            }
+        }
+    }
+    return v;  // valid in thread 0
+}
+
 template <int DT> struct Elt;
 template <> struct Elt<0> {  // fp32
     static constexpr int kVec = 4;
-    static constexpr int kBytes = 4;
     __device__ static uint32_t bits(const char *row, int64_t i)
     {
         return reinterpret_cast<const uint32_t *>(row)[i];
@@ -149,104 +166,67 @@ __device__ __forceinline__ void scan_exact(const char *row, const uint32_t *arow
     }
 }
 
-// Vector path over the full vectors [v0, v1) of a 16-byte aligned row; each
-// lane takes U vectors per batch, strided by THREADS so loads coalesce.
-template <int DT, int THREADS, int U>
-__device__ __forceinline__ void scan_vectors(const char *row, const uint32_t *arow, int v0, int v1,
-                                             uint32_t &best_key, int &best_idx)
+// fp32 rows are read as a head of `head` < 4 elements (up to the row's first
+// 16-byte boundary), 16-byte vectors from element `head` on, and a tail of
+// fewer than 4 elements.  Vector v holds elements i = head + 4v .. i + 3,
+// whose mask bits straddle two mask words when i mod 32 > 28.
+__device__ __forceinline__ int f32_head(const char *row, int V)
 {
-    using E = Elt<DT>;
-    constexpr int kVec = E::kVec;
-    constexpr int kU = U;
-    constexpr int kThreads = THREADS;
+    return min(V, (int)(((16u - (uint32_t)(reinterpret_cast<uintptr_t>(row) & 15u)) & 15u) >> 2));
+}
+
+// Vector path over vectors [v0, v1) past the head; each lane takes U vectors
+// per batch, strided by THREADS so loads coalesce.  Per lane, elements are
+// visited in increasing index order and only a strictly larger key replaces
+// the lane's best, so the lane keeps the lowest index of its maximum.
+template <int THREADS, int U>
+__device__ __forceinline__ void scan_vectors_f32(const char *row, const uint32_t *arow, int head, int v0, int v1,
+                                                 uint32_t &best_key, int &best_idx)
+{
+    const char *vrow = row + 4 * head;  // 16-byte aligned
     const int tid = threadIdx.x;
-    for (int vb = v0; vb < v1; vb += kThreads * kU) {
-        uint4 d[kU];
-        uint32_t m[kU];
+    for (int vb = v0; vb < v1; vb += THREADS * U) {
+        uint4 d[U];
+        uint32_t m[U];
 #pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const int v = vb + u * kThreads + tid;
+        for (int u = 0; u < U; ++u) {
+            const int v = vb + u * THREADS + tid;
             if (v < v1) {
-                d[u] = *reinterpret_cast<const uint4 *>(row + (size_t)v * 16);
-                m[u] = (arow[(v * kVec) >> 5] >> ((v * kVec) & 31)) & ((1u << kVec) - 1u);
+                d[u] = *reinterpret_cast<const uint4 *>(vrow + (size_t)v * 16);
+                const int i = head + 4 * v, w = i >> 5, sh = i & 31;
+                uint32_t bits = arow[w] >> sh;
+                if (sh > 28)  // element i + 3 < V, so word w + 1 is in the row
+                    bits |= arow[w + 1] << (32 - sh);
+                m[u] = bits & 0xFu;
             } else {
                 d[u] = make_uint4(0, 0, 0, 0);
                 m[u] = 0;
             }
         }
-        if constexpr (DT == 1) {
-            constexpr int kLast = kU * 8 - 1;  // positions 0..kLast in the lane's batch
-            // fast packed keys: (key16 << 16 | last - position) masked by the allow bit
-            uint32_t bmax = 0, any = 0;
 #pragma unroll
-            for (int u = 0; u < kU; ++u) {
-                any |= m[u];
-                const uint32_t w[4] = {d[u].x, d[u].y, d[u].z, d[u].w};
+        for (int u = 0; u < U; ++u) {
+            const int i = head + 4 * (vb + u * THREADS + tid);
+            const uint32_t w[4] = {d[u].x, d[u].y, d[u].z, d[u].w};
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const uint32_t key = fast_key2(w[k]);
-                    const int p = u * 8 + 2 * k;
-                    const uint32_t lo = ((key << 16) | (uint32_t)(kLast - p)) & bit_mask(m[u], 2 * k);
-                    const uint32_t hi = ((key & 0xFFFF0000u) | (uint32_t)(kLast - 1 - p)) & bit_mask(m[u], 2 * k + 1);
-                    bmax = max(bmax, max(lo, hi));
-                }
-            }
-            if (any) {
-                const uint32_t k16 = bmax >> 16;
-                const bool special = k16 <= 0x007Fu || k16 == 0x7FFFu || k16 == 0x8000u || k16 > 0xFF80u;
-                if (!special) {
-                    const int p = kLast - (int)(bmax & 0xFFFFu);
-                    const int v = vb + (p >> 3) * kThreads + tid;
-                    const uint32_t h = (k16 & 0x8000u) ? (k16 & 0x7FFFu) : (~k16 & 0xFFFFu);
-                    const uint32_t key = f32_key(h << 16);
-                    if (key > best_key) {
-                        best_key = key;
-                        best_idx = v * kVec + (p & 7);
-                    }
-                } else {
-                    // exact recompute of this lane's batch (NaN or signed zero at the top)
-#pragma unroll 1
-                    for (int u = 0; u < kU; ++u) {
-                        const int v = vb + u * kThreads + tid;
-                        for (int e = 0; e < kVec; ++e) {
-                            if ((m[u] >> e) & 1u) {
-                                const uint32_t key = f32_key(E::bits(row, (int64_t)v * kVec + e));
-                                if (key > best_key) {
-                                    best_key = key;
-                                    best_idx = v * kVec + e;
-                                }
-                            }
-                        }
-                    }
-                }
-            }
-        } else {
-#pragma unroll
-            for (int u = 0; u < kU; ++u) {
-                const int v = vb + u * kThreads + tid;
-                const uint32_t w[4] = {d[u].x, d[u].y, d[u].z, d[u].w};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint32_t key = ((m[u] >> e) & 1u) ? f32_key(w[e]) : 0u;
-                    if (key > best_key) {
-                        best_key = key;
-                        best_idx = v * kVec + e;
-                    }
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t key = ((m[u] >> e) & 1u) ? f32_key(w[e]) : 0u;
+                if (key > best_key) {
+                    best_key = key;
+                    best_idx = i + e;
                 }
             }
         }
     }
 }
 
-template <int DT, int THREADS, int U>
+// fp32 rows, 256-lane blocks, exact keys.
+template <int THREADS, int U>
 __global__ __launch_bounds__(THREADS) void masked_step_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
     const int32_t *__restrict__ states, const void *__restrict__ logits, RowMap map, int chunk_vec,
     int nchunks, int32_t *__restrict__ token, int32_t *__restrict__ new_state,
     uint64_t *__restrict__ partial)
 {
-    using E = Elt<DT>;
-    constexpr int kVec = E::kVec;
     const int b = blockIdx.x / nchunks;
     const int c = blockIdx.x - b * nchunks;
     const int s = row_state(states, map, next_state, allow, S, V, b);
@@ -255,19 +235,17 @@ __global__ __launch_bounds__(THREADS) void masked_step_kernel(
     uint32_t best_key = 0;
     int best_idx = 0;
     if (live) {
-        const char *row = static_cast<const char *>(logits) + (size_t)map.offset(b) * E::kBytes;
+        const char *row = static_cast<const char *>(logits) + (size_t)map.offset(b) * 4;
         const uint32_t *arow = allow + (size_t)s * W;
-        const int nvec = V / kVec;
-        const int e0 = c * chunk_vec * kVec;
-        const int e1 = c == nchunks - 1 ? V : min(V, (c + 1) * chunk_vec * kVec);
-        if ((reinterpret_cast<uintptr_t>(row) & 15) == 0) {
-            scan_vectors<DT, THREADS, U>(row, arow, c * chunk_vec, min(nvec, (c + 1) * chunk_vec), best_key,
-                                         best_idx);
-            if (c == nchunks - 1)
-                scan_exact<DT, THREADS>(row, arow, nvec * kVec, V, best_key, best_idx);
-        } else {
-            scan_exact<DT, THREADS>(row, arow, e0, e1, best_key, best_idx);
-        }
+        const int head = f32_head(row, V);
+        const int nvec = (V - head) / 4;
+        // increasing index order per lane: head, vectors, tail
+        if (c == 0)
+            scan_exact<0, THREADS>(row, arow, 0, head, best_key, best_idx);
+        scan_vectors_f32<THREADS, U>(row, arow, head, c * chunk_vec, min(nvec, (c + 1) * chunk_vec), best_key,
+                                     best_idx);
+        if (c == nchunks - 1)
+            scan_exact<0, THREADS>(row, arow, head + nvec * 4, V, best_key, best_idx);
     }
     const uint64_t best = block_max<THREADS>(pack(best_key, best_idx));
     if (threadIdx.x != 0)
@@ -292,12 +270,7 @@ __device__ __forceinline__ uint32_t pk_max_u16(uint32_t a, uint32_t b)
 
 __device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v, bool is_max)
 {
-#pragma unroll
-    for (int d = kWave / 2; d > 0; d >>= 1) {
-        const uint32_t o = __shfl_xor(v, d);
-        v = is_max ? max(v, o) : min(v, o);
-    }
-    return v;  // in every lane of the wave
+    return is_max ? wave_reduce<true>(v) : wave_reduce<false>(v);  // in every lane of the wave
 }
 
 // bf16 rows.  Per batch of U vectors per lane:
@@ -374,11 +347,15 @@ __device__ __forceinline__ RowSplit split_row(const char *row, int V)
 // vectors [v0, v1) of `row` past its head, plus the head when `first` and
 // the tail when `last`.  `da` holds the first batch (loaded by the caller,
 // so it can be in flight before the row's state is known).  SHIFTED: the
-// head is not empty, so mask bits straddle two bytes.
+// head is not empty, so mask bits straddle two bytes.  Whenever the wave's
+// vector-path best improves, its entry of `ns_row` (the row state's
+// next-state row) is loaded at once, so the final gather is in flight long
+// before the block's maximum is known: `vec_pack` and `vec_ns` return that
+// best and its next state (wave-uniform).
 template <int THREADS, int U, bool MASKED, bool SHIFTED>
-__device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *arow, RowSplit rs, int v0,
-                                              int v1, bool first, bool last, int V, const uint4 *lut,
-                                              uint4 (&da)[U])
+__device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *arow, const int32_t *ns_row,
+                                              RowSplit rs, int v0, int v1, bool first, bool last, int V,
+                                              const uint4 *lut, uint4 (&da)[U], uint64_t &vec_pack, int &vec_ns)
 {
     constexpr int kVec = 8;
     constexpr int kStep = THREADS * U;  // vectors per batch
@@ -387,6 +364,7 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
     const char *vrow = row + 2 * head;  // 16-byte aligned
     uint32_t best_key = 0;  // exact key of the wave's best vector-path element, wave-uniform
     int best_idx = 0;
+    int best_ns = kNsUnknown;
     uint32_t lane_key = 0;  // exact key of this lane's head / tail elements
     int lane_idx = 0;
     if (v0 < v1) {
@@ -504,6 +482,10 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
             load_masks(ma, vb + 2 * kStep);
             if (vb + kStep < v1)  // block-uniform
                 process_batch(db, mb, vb + kStep);
+            // the best so far's next state, loaded outside any branch (a load
+            // under a branch would make the compiler wait for every load in
+            // flight where the branches join)
+            best_ns = ns_row[best_idx];
         }
     }
     if (first)
@@ -512,21 +494,29 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
         scan_exact<1, THREADS, MASKED>(row, arow, rs.head + rs.nvec * kVec, V, lane_key, lane_idx);
     const uint64_t mine = pack(lane_key, lane_idx);
     const uint64_t vec_best = pack(best_key, best_idx);
+    vec_pack = vec_best;
+    vec_ns = best_ns;
     return vec_best > mine ? vec_best : mine;
 }
 
 // The scan of a row's chunk with the right mask alignment (block-uniform).
-template <int THREADS, int U, bool MASKED>
-__device__ __forceinline__ uint64_t scan_chunk_bf16(const char *row, const uint32_t *arow, RowSplit rs, int v0,
-                                                    int v1, bool first, bool last, int V, const uint4 *lut,
-                                                    uint4 (&da)[U])
+// ANY_ALIGN false: the caller has checked that every row is 16-byte aligned,
+// so only the aligned scan is compiled (fewer registers: more resident
+// blocks where several share a CU).
+template <int THREADS, int U, bool MASKED, bool ANY_ALIGN>
+__device__ __forceinline__ uint64_t scan_chunk_bf16(const char *row, const uint32_t *arow, const int32_t *ns_row,
+                                                    RowSplit rs, int v0, int v1, bool first, bool last, int V,
+                                                    const uint4 *lut, uint4 (&da)[U], uint64_t &vec_pack,
+                                                    int &vec_ns)
 {
-    if (rs.head == 0)
-        return scan_bf16<THREADS, U, MASKED, false>(row, arow, rs, v0, v1, first, last, V, lut, da);
-    return scan_bf16<THREADS, U, MASKED, true>(row, arow, rs, v0, v1, first, last, V, lut, da);
+    if (!ANY_ALIGN || rs.head == 0)
+        return scan_bf16<THREADS, U, MASKED, false>(row, arow, ns_row, rs, v0, v1, first, last, V, lut, da, vec_pack,
+                                                    vec_ns);
+    return scan_bf16<THREADS, U, MASKED, true>(row, arow, ns_row, rs, v0, v1, first, last, V, lut, da, vec_pack,
+                                               vec_ns);
 }
 
-template <int THREADS, int U>
+template <int THREADS, int U, bool ANY_ALIGN>
 __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
     const int32_t *__restrict__ states, const void *__restrict__ logits, RowMap map, int chunk_vec,
@@ -550,11 +540,13 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
         load_batch_bf16<THREADS, U>(da, row + 2 * rs.head, v0, v1);
     const int s = row_state(states, map, next_state, allow, S, V, b);
     const bool live = (uint32_t)s < (uint32_t)S;  // block-uniform
-    uint64_t mine = 0;
+    uint64_t mine = 0, vec_pack = 0;
+    int vec_ns = kNsUnknown;
     if (live)
-        mine = scan_chunk_bf16<THREADS, U, true>(row, allow + (size_t)s * W, rs, v0, v1, c == 0, c == nchunks - 1,
-                                                 V, lut, da);
-    const uint64_t best = block_max<THREADS>(mine);
+        mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN>(row, allow + (size_t)s * W, next_state + (size_t)s * V, rs, v0, v1,
+                                                 c == 0, c == nchunks - 1, V, lut, da, vec_pack, vec_ns);
+    int ns;
+    const uint64_t best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
     if (threadIdx.x != 0)
         return;
     if (nchunks > 1) {
@@ -564,14 +556,14 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
     const bool found = tok >= 0 && tok < V;  // always true for a found token; guards the read
     token[b] = found ? tok : -1;
-    new_state[b] = found ? next_state[(size_t)s * V + tok] : -1;
+    new_state[b] = !found ? -1 : ns != kNsUnknown ? ns : next_state[(size_t)s * V + tok];
 }
 
 // Opportunistic masking (Sec. 3.5, further optimizations), one block per
 // row: the model's own choice over the whole row is found first, without
 // reading the mask; only when the mask does not allow it is the row scanned
 // again with the mask.  Same result as masked_step_bf16_kernel.
-template <int THREADS, int U>
+template <int THREADS, int U, bool ANY_ALIGN>
 __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
     const int32_t *__restrict__ states, const void *__restrict__ logits, RowMap map,
@@ -591,10 +583,13 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     const int s = states[b];
     const bool live = (uint32_t)s < (uint32_t)S;  // block-uniform
     const uint32_t *arow = allow + (size_t)(live ? s : 0) * W;
-    uint64_t mine = 0;
+    const int32_t *ns_row = next_state + (size_t)(live ? s : 0) * V;
+    uint64_t mine = 0, vec_pack = 0;
+    int vec_ns = kNsUnknown, ns;
     if (live)
-        mine = scan_chunk_bf16<THREADS, U, false>(row, arow, rs, 0, rs.nvec, true, true, V, lut, da);
-    uint64_t best = block_max<THREADS>(mine);
+        mine = scan_chunk_bf16<THREADS, U, false, ANY_ALIGN>(row, arow, ns_row, rs, 0, rs.nvec, true, true, V, lut, da, vec_pack,
+                                                  vec_ns);
+    uint64_t best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
     if (threadIdx.x == 0) {
         const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
         const bool ok = tok >= 0 && tok < V && ((arow[tok >> 5] >> (tok & 31)) & 1u);
@@ -604,15 +599,16 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     if (miss) {  // block-uniform
         if (rs.nvec > 0)
             load_batch_bf16<THREADS, U>(da, row + 2 * rs.head, 0, rs.nvec);
-        mine = scan_chunk_bf16<THREADS, U, true>(row, arow, rs, 0, rs.nvec, true, true, V, lut, da);
-        best = block_max<THREADS>(mine);
+        mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN>(row, arow, ns_row, rs, 0, rs.nvec, true, true, V, lut, da, vec_pack,
+                                                 vec_ns);
+        best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
     }
     if (threadIdx.x != 0)
         return;
     const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
     const bool found = live && tok >= 0 && tok < V;  // guards the read
     token[b] = found ? tok : -1;
-    new_state[b] = found ? next_state[(size_t)s * V + tok] : -1;
+    new_state[b] = !found ? -1 : ns != kNsUnknown ? ns : next_state[(size_t)s * V + tok];
 }
 
 // One lane per row: combine the row's chunk results and write the outputs.
@@ -685,10 +681,13 @@ hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, 
     uint64_t *partial = static_cast<uint64_t *>(workspace);
     const unsigned grid = (unsigned)B * (unsigned)g.nchunks;
     if (dtype == 0)
-        masked_step_kernel<0, kSmallThreads, kSmallU><<<grid, kSmallThreads, 0, stream>>>(
+        masked_step_kernel<kSmallThreads, kSmallU><<<grid, kSmallThreads, 0, stream>>>(
+            next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial);
+    else if (map.rows_aligned(logits, 2))
+        masked_step_bf16_kernel<kBigThreads, kBigU, false><<<grid, kBigThreads, 0, stream>>>(
             next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial);
     else
-        masked_step_bf16_kernel<kBigThreads, kBigU><<<grid, kBigThreads, 0, stream>>>(
+        masked_step_bf16_kernel<kBigThreads, kBigU, true><<<grid, kBigThreads, 0, stream>>>(
             next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial);
     if (g.nchunks > 1)
         finalize_kernel<<<(B + kSmallThreads - 1) / kSmallThreads, kSmallThreads, 0, stream>>>(
@@ -706,8 +705,13 @@ hipError_t launch_masked_step_opportunistic(const int32_t *next_state, const uin
     // an extra pass over the chunks) the plain masked step gives the same
     // result.
     if (dtype == 1 && step_geometry(B, V, 1).nchunks == 1) {
-        opportunistic_step_bf16_kernel<kBigThreads, kBigU><<<(unsigned)B, kBigThreads, 0, stream>>>(
-            next_state, allow, S, V, (V + 31) / 32, states, logits, RowMap{ld, 0, 1, nullptr, 0}, token, new_state);
+        const RowMap map{ld, 0, 1, nullptr, 0};
+        if (map.rows_aligned(logits, 2))
+            opportunistic_step_bf16_kernel<kBigThreads, kBigU, false><<<(unsigned)B, kBigThreads, 0, stream>>>(
+                next_state, allow, S, V, (V + 31) / 32, states, logits, map, token, new_state);
+        else
+            opportunistic_step_bf16_kernel<kBigThreads, kBigU, true><<<(unsigned)B, kBigThreads, 0, stream>>>(
+                next_state, allow, S, V, (V + 31) / 32, states, logits, map, token, new_state);
         return hipGetLastError();
     }
     return launch_masked_rows(next_state, allow, S, V, states, logits, dtype, B, RowMap{ld, 0, 1, nullptr, 0}, token,

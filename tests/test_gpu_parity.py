@@ -369,14 +369,15 @@ def test_step_shapes_ld_and_alignment(dv, dtype, B, V, extra_ld, offset):
 @pytest.mark.parametrize("B,V,extra_ld", [
     (1, 5, 0), (2, 13, 1), (3, 4100, 3), (2, 70001, 0), (1, 70001, 5), (260, 1030, 1), (64, 50257, 0),
 ])
-@pytest.mark.parametrize("head", range(8))
-def test_step_bf16_every_row_alignment(dv, B, V, extra_ld, head):
-    """bf16 rows starting at every 2-byte offset within 16 bytes: the first
+@pytest.mark.parametrize("dtype,head", [(torch.bfloat16, h) for h in range(8)] +
+                         [(torch.float32, h) for h in range(4)])
+def test_step_every_row_alignment(dv, B, V, extra_ld, dtype, head):
+    """Rows starting at every element offset within 16 bytes: the first
     row's head (elements before its first 16-byte boundary) is `head`, later
     rows vary with the row stride.  Few distinct values (many ties across
     the head, vector and tail regions), planted NaN and signed zeros, random
     masks of every density; greedy and opportunistic steps both checked."""
-    _say(f"step bf16 alignment B={B} V={V} ld=V+{extra_ld} head={head}")
+    _say(f"step alignment {dtype} B={B} V={V} ld=V+{extra_ld} head={head}")
     rng = np.random.default_rng(1000 * head + V + B)
     S = 7
     alive = rng.random((S, V)) < rng.choice([0.002, 0.05, 0.5, 0.97, 1.0], size=(S, 1))
@@ -387,18 +388,20 @@ def test_step_bf16_every_row_alignment(dv, B, V, extra_ld, head):
     al = np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(S, Wd)
     states = rng.integers(-1, S, B).astype(np.int32)
     ld = V + extra_ld
-    offset = (8 - head) % 8          # elements from a 16-byte boundary
+    esz = 2 if dtype == torch.bfloat16 else 4
+    per = 16 // esz                  # elements per 16-byte vector
+    offset = (per - head) % per      # elements from a 16-byte boundary
     vals = rng.integers(-2, 3, B * ld + offset + 8).astype(np.float32)
-    buf = torch.from_numpy(vals).to(torch.bfloat16)
-    special = torch.tensor([float("nan"), -0.0, 0.0, 2.0], dtype=torch.bfloat16)
+    buf = torch.from_numpy(vals).to(dtype)
+    special = torch.tensor([float("nan"), -0.0, 0.0, 2.0], dtype=dtype)
     pos = torch.from_numpy(rng.integers(0, buf.numel(), 40))
     buf[pos] = special[torch.from_numpy(rng.integers(0, 4, 40))]
-    base = torch.empty(buf.numel() + 64, dtype=torch.bfloat16, device=DEV)
-    shift = (-(base.data_ptr() // 2)) % 8    # first 16-byte boundary of base
+    base = torch.empty(buf.numel() + 64, dtype=dtype, device=DEV)
+    shift = (-(base.data_ptr() // esz)) % per    # first 16-byte boundary of base
     buf_d = base[shift:shift + buf.numel()]
     buf_d.copy_(buf.to(DEV))
     x = buf_d[offset:offset + B * ld].view(B, ld)[:, :V]
-    assert (x.data_ptr() // 2 + head) % 8 == 0
+    assert (x.data_ptr() // esz + head) % per == 0
     xo = to_oracle(buf[offset:offset + B * ld].view(B, ld))
     tok_o, new_o = oracle.masked_step(ns, al, states, xo)
     for opp in (False, True):
