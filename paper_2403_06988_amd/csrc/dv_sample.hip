@@ -176,6 +176,34 @@ __device__ __forceinline__ uint32_t pick(uint4 v, int e)
     return r;
 }
 
+// Exclusive prefix sum over the wave of a count in [0, 15], and the wave's
+// total, from four ballots of the count's bits (no LDS, no waits).
+__device__ __forceinline__ int wave_prefix_small(int cnt, int &total)
+{
+    int excl = 0, tot = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const uint64_t m = __ballot((cnt >> j) & 1);
+        const int below = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        excl += below << j;
+        tot += __popcll(m) << j;
+    }
+    total = tot;
+    return excl;
+}
+
+// Lanes of one wave hand data to each other through LDS: the wave's LDS
+// operations run in order, so a compiler barrier with wavefront-scope
+// ordering is all that is needed (no block barrier: waves do not wait for
+// each other).
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <int DT, int THREADS>
 __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
@@ -206,23 +234,15 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
                 word &= (1u << (t1 - tok0)) - 1u;  // a chunk ends inside this word only at V
             // groups (4 tokens) holding an allowed token: bit 4k of `nz`
             uint32_t nz = (word | (word >> 1) | (word >> 2) | (word >> 3)) & 0x11111111u;
-            const int cnt = __popc(nz);
-            int incl = cnt;
-#pragma unroll
-            for (int d = 1; d < kWave; d <<= 1) {
-                const int y = __shfl_up(incl, d);
-                if (lane >= d)
-                    incl += y;
-            }
-            const int total = __shfl(incl, kWave - 1);
-            int pos = incl - cnt;
+            int total;
+            int pos = wave_prefix_small(__popc(nz), total);  // at most 8 groups per lane
             while (nz) {
                 const int k = __builtin_ctz(nz) >> 2;
                 nz &= nz - 1u;
                 // token group index (token / 4) and its 4 mask bits
                 queue[wave][pos++] = ((uint32_t)((tok0 >> 2) + k) << 4) | ((word >> (4 * k)) & 0xFu);
             }
-            __syncthreads();
+            wave_lds_sync();
             for (int q = lane; q < total; q += kWave) {
                 const uint32_t entry = queue[wave][q];
                 const uint32_t g = entry >> 4;
@@ -241,14 +261,12 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
                     best = max_u64(best, packed);
                 }
             }
-            __syncthreads();
+            wave_lds_sync();  // every lane has read its entries before the next iteration writes
         }
     }
     // block-wide maximum
     __shared__ uint64_t red[THREADS / kWave];
-#pragma unroll
-    for (int d = kWave / 2; d > 0; d >>= 1)
-        best = max_u64(best, __shfl_xor(best, d));
+    best = wave_reduce<true>(best);
     if (lane == 0)
         red[wave] = best;
     __syncthreads();
