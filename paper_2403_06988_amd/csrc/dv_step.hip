@@ -8,7 +8,7 @@
 //     (every CU gets at least one row), or when it holds at most 32768
 //     logits (a second pass would cost more than the split saves), so no
 //     second pass is needed.  Each
-//     lane streams batches of 4 independent non-temporal 16-byte loads with
+//     lane streams batches of 2 independent non-temporal 16-byte loads with
 //     a register double buffer: batch i + 1 is in flight while batch i is
 //     reduced.  Each batch loads its allow-mask
 //     bytes (one byte per 8 logits) right behind its logits.  Smaller
@@ -45,7 +45,7 @@ constexpr int kSmallU = 8;          // 16-byte vectors per lane per batch
 #define DV_STEP_BF16_THREADS 512
 #endif
 #ifndef DV_STEP_BF16_U
-#define DV_STEP_BF16_U 4
+#define DV_STEP_BF16_U 2
 #endif
 constexpr int kBigThreads = DV_STEP_BF16_THREADS;  // lanes per bf16 block
 constexpr int kBigU = DV_STEP_BF16_U;              // vectors per lane per batch (x2: double-buffered)
@@ -290,6 +290,14 @@ __device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v, bool is_max)
 // masking) every element of the chunk counts as allowed and no mask byte is
 // read.
 
+// Block barrier ordering LDS only: global loads in flight stay in flight.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // mask byte -> two 16-bit lane masks per 32-bit word of logits
 __device__ __forceinline__ void fill_lut(uint4 *lut)
 {
@@ -530,15 +538,16 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     const RowSplit rs = split_row(row, V);  // block-uniform
     const int v0 = c * chunk_vec;
     const int v1 = min(rs.nvec, v0 + chunk_vec);
-    fill_lut(lut);
-    __syncthreads();
 
     // The first batch of logits does not depend on the row's state: it is in
-    // flight before the state lookup returns.
+    // flight before the state lookup returns, and the mask table is built
+    // meanwhile.
     uint4 da[U];
     if (v0 < v1)
         load_batch_bf16<THREADS, U>(da, row + 2 * rs.head, v0, v1);
     const int s = row_state(states, map, next_state, allow, S, V, b);
+    fill_lut(lut);
+    lds_barrier();
     const bool live = (uint32_t)s < (uint32_t)S;  // block-uniform
     uint64_t mine = 0, vec_pack = 0;
     int vec_ns = kNsUnknown;
@@ -574,13 +583,13 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     const int b = blockIdx.x;
     const char *row = static_cast<const char *>(logits) + (size_t)map.offset(b) * 2;
     const RowSplit rs = split_row(row, V);  // block-uniform
-    fill_lut(lut);
-    __syncthreads();
 
     uint4 da[U];
     if (rs.nvec > 0)
         load_batch_bf16<THREADS, U>(da, row + 2 * rs.head, 0, rs.nvec);
     const int s = states[b];
+    fill_lut(lut);
+    lds_barrier();
     const bool live = (uint32_t)s < (uint32_t)S;  // block-uniform
     const uint32_t *arow = allow + (size_t)(live ? s : 0) * W;
     const int32_t *ns_row = next_state + (size_t)(live ? s : 0) * V;
