@@ -75,12 +75,40 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def step_bytes(w, live_rows, B):
-    """Algorithmic HBM bytes of one masked step: each live row streams its
-    logits (V elements) and its allow row (4 * ceil(V/32) B) and gathers one
-    next_state entry; every row reads its state and writes token and new state."""
-    per_live = w.V * w.elt + 4 * w.words + 4
-    return live_rows * per_live + 12 * B
+LINE = 128  # bytes the memory system fetches at a time
+
+
+def touched_line_bytes(al, states, base_ptr, ld, V, elt):
+    """Logit bytes a masked step must read: the 128-byte lines that hold at
+    least one allowed token, over the rows whose state is live (a line with
+    no allowed token cannot change the result).  Row r (state states[r])
+    starts at byte base_ptr + r * ld * elt; lines are aligned in memory, so a
+    row that does not start on a line boundary counts the lines it touches."""
+    import torch
+
+    rows = torch.nonzero(states >= 0)[:, 0]
+    if rows.numel() == 0:
+        return 0
+    tpl = LINE // elt
+    total = 0
+    for part in torch.split(rows, max(1, (1 << 26) // max(V, 1))):   # bounded temporaries
+        words = al[states[part].long()]                                  # [m, W] int32
+        shift = torch.arange(32, device=words.device, dtype=torch.int32)
+        bits = ((words[..., None] >> shift) & 1).reshape(part.numel(), -1)[:, :V]
+        off = ((base_ptr + part.long() * ld * elt) % LINE) // elt          # [m]
+        lid = (off[:, None] + torch.arange(V, device=words.device)) // tpl
+        hit = torch.zeros((part.numel(), (V + tpl - 1) // tpl + 1), dtype=torch.int32, device=words.device)
+        hit.scatter_reduce_(1, lid, bits, reduce="amax")
+        total += int(hit.sum())
+    return total * LINE
+
+
+def step_bytes(w, logit_bytes, live_rows, B):
+    """Algorithmic HBM bytes of one masked step: the logit lines the live rows
+    must read (touched_line_bytes), each live row's allow row (4 ceil(V/32) B)
+    and one gathered next_state entry; every row reads its state and writes
+    token and new state."""
+    return logit_bytes + live_rows * (4 * w.words + 4) + 12 * B
 
 
 def traffic_record(which, workload_id):
@@ -274,10 +302,24 @@ def bench_spec(dv, w, wid, ns, al, x, tokens_all, states_all, dev, s=8, keep=0.9
         times.append(a.elapsed_time(b) / 1e3 / n_win)
     same = bool(torch.equal(tok, ref[0]) and torch.equal(acc, ref[1]) and torch.equal(nst, ref[2]))
     t = float(np.median(times))
-    live_pos = int((tok != -1).sum()) / n_win
     emitted = float((acc + (tok.gather(2, acc.to(torch.int64)[..., None])[..., 0] != -1)).sum()) / n_win
-    per_live = w.V * w.elt + 4 * w.words + 4
-    bytes_call = live_pos * per_live + w.B * (s * 12 + (s + 1) * 4 + 12)
+    # each position's state: the window's start advanced by its first j
+    # proposals (DEAD after an illegal one); live positions read logits
+    logit_bytes, live = 0, 0
+    for k in range(n_win):
+        st = starts[k].clone()
+        k0 = k * (s + 1)
+        for j in range(s + 1):
+            logit_bytes += touched_line_bytes(al, st, x[k0 + j].data_ptr(), w.V, w.V, w.elt)
+            live += int((st >= 0).sum())
+            if j < s:
+                p = props[k][:, j].long()
+                ok = (st >= 0) & (p >= 0) & (p < w.V)
+                nxt = ns[st.clamp(min=0).long(), p.clamp(0, w.V - 1)]
+                st = torch.where(ok, nxt, torch.full_like(st, -1))
+    live_pos = live / n_win
+    bytes_call = (logit_bytes / n_win + live_pos * (4 * w.words + 4)
+                  + w.B * (s * 12 + (s + 1) * 4 + 12))
     achieved = bytes_call / t / 1e9
     return {
         "proposed_per_row": s, "keep_probability": keep, "calls": n_win,
@@ -532,7 +574,11 @@ def main():
     pairs = w.S * w.V
     align_s = float(np.mean(align_ms)) / 1e3
     dec_s = float(np.mean(decode_ms)) / 1e3
-    bytes_per_launch = float(np.mean([step_bytes(w, int(n), w.B) for n in live_per_step]))
+    logit_bytes = [touched_line_bytes(al.view(torch.int32), states_all[k], x[k].data_ptr(), w.V, w.V, w.elt)
+                   for k in range(w.steps)]
+    bytes_per_launch = float(np.mean([step_bytes(w, lb, int(n), w.B)
+                                      for lb, n in zip(logit_bytes, live_per_step)]))
+    whole_rows = float(np.mean(live_per_step)) * w.V * w.elt
     mean_launch_s = dec_s / w.steps
     achieved = bytes_per_launch / mean_launch_s / 1e9
     align_bytes = pairs * 4.125
@@ -565,6 +611,7 @@ def main():
                      "bound": "hbm", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "bytes_per_launch": bytes_per_launch,
+                     "logit_lines_read_fraction": float(np.mean(logit_bytes)) / whole_rows if whole_rows else None,
                      "traffic": traffic_record("masked_step", wid)},
         "roofline_align": {"kernel": "dv_align (walk_kernel + 3 small prep kernels)", "bound": "hbm",
                            "achieved": align_achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",

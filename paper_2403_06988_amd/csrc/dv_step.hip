@@ -34,12 +34,15 @@
 //   * Lanes combine (exact 32-bit key << 32 | ~index) as one 64-bit maximum:
 //     a larger key wins, on equal keys the smaller index wins.  The result
 //     does not depend on block or lane order, so the step is deterministic.
+#include <atomic>
+
 #include "dv_internal.h"
 
 namespace dv {
 namespace {
 
 constexpr int kSmallThreads = 256;  // split rows and fp32 rows
+constexpr int kMaxDevices = 64;
 constexpr int kSmallU = 8;          // 16-byte vectors per lane per batch
 #ifndef DV_STEP_BF16_THREADS
 #define DV_STEP_BF16_THREADS 512
@@ -334,6 +337,32 @@ __device__ __forceinline__ void load_batch_bf16(uint4 (&d)[U], const char *row, 
     }
 }
 
+// Read in place of a vector with no allowed token: every block reads the
+// same 16 bytes, so they stay in cache.
+__device__ uint4 g_unread_vector;
+
+// load_batch_bf16, except that a vector whose mask byte `sel[u]` is 0 (no
+// allowed token) is read from g_unread_vector: its logits are never used,
+// and a 128-byte line none of whose vectors is needed is not fetched.  The
+// address is selected, not branched on, so the loads stay branch-free.
+template <int THREADS, int U>
+__device__ __forceinline__ void load_batch_bf16_sel(uint4 (&d)[U], const char *row, int vb, int v1,
+                                                    const uint32_t (&sel)[U])
+{
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int v = min(vb + u * THREADS + tid, v1 - 1);
+        const char *p = sel[u] ? row + (size_t)v * 16 : reinterpret_cast<const char *>(&g_unread_vector);
+#if DV_STEP_NT_LOADS
+        const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+        d[u] = make_uint4(x[0], x[1], x[2], x[3]);
+#else
+        d[u] = *reinterpret_cast<const uint4 *>(p);
+#endif
+    }
+}
+
 // A row is read as a head of `head` < 8 elements (its first 16-byte
 // boundary), then 16-byte vectors from element `head` on, then a tail of
 // fewer than 8 elements.  Vector v holds elements head + 8v .. head + 8v + 7,
@@ -359,8 +388,9 @@ __device__ __forceinline__ RowSplit split_row(const char *row, int V)
 // vector-path best improves, its entry of `ns_row` (the row state's
 // next-state row) is loaded at once, so the final gather is in flight long
 // before the block's maximum is known: `vec_pack` and `vec_ns` return that
-// best and its next state (wave-uniform).
-template <int THREADS, int U, bool MASKED, bool SHIFTED>
+// best and its next state (wave-uniform).  SELECT: vectors with no allowed
+// token are not read (see load_batch_bf16_sel).
+template <int THREADS, int U, bool MASKED, bool SHIFTED, bool SELECT>
 __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *arow, const int32_t *ns_row,
                                               RowSplit rs, int v0, int v1, bool first, bool last, int V,
                                               const uint4 *lut, uint4 (&da)[U], uint64_t &vec_pack, int &vec_ns)
@@ -481,19 +511,53 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
         // they are harmless reloads, masked out when reduced).
         uint4 db[U];
         uint32_t ma[U], mb[U];
-        load_masks(ma, v0);
-        for (int vb = v0; vb < v1; vb += 2 * kStep) {
-            load_batch_bf16<THREADS, U>(db, vrow, vb + kStep, v1);
-            load_masks(mb, vb + kStep);
-            process_batch(da, ma, vb);
-            load_batch_bf16<THREADS, U>(da, vrow, vb + 2 * kStep, v1);
-            load_masks(ma, vb + 2 * kStep);
-            if (vb + kStep < v1)  // block-uniform
-                process_batch(db, mb, vb + kStep);
-            // the best so far's next state, loaded outside any branch (a load
-            // under a branch would make the compiler wait for every load in
-            // flight where the branches join)
-            best_ns = ns_row[best_idx];
+        if constexpr (SELECT && MASKED && !SHIFTED) {
+            // From the third batch on, a vector with no allowed token is not
+            // read (load_batch_bf16_sel), so a 128-byte line with no allowed
+            // token is never fetched.  Choosing the addresses needs the
+            // batch's mask bytes first: they are issued one batch ahead of
+            // the logits (sc, sd), so with the in-order load counter waiting
+            // for them never waits for the previous batch's logits, which
+            // stay in flight while a batch is reduced.
+            // (The scheduling barriers keep that issue order: the compiler
+            // would otherwise issue the logits first.  The prologue issues
+            // sc ahead of the second batch as the loop does, so the waits
+            // the compiler merges at the loop head are those of the loop.)
+            uint32_t sc[U], sd[U];
+            load_masks(ma, v0);
+            load_masks(sc, v0 + 2 * kStep);
+            __builtin_amdgcn_sched_barrier(0);
+            load_batch_bf16<THREADS, U>(db, vrow, v0 + kStep, v1);
+            load_masks(mb, v0 + kStep);
+            for (int vb = v0; vb < v1; vb += 2 * kStep) {
+                process_batch(da, ma, vb);
+                load_masks(sd, vb + 3 * kStep);
+                __builtin_amdgcn_sched_barrier(0);
+                load_batch_bf16_sel<THREADS, U>(da, vrow, vb + 2 * kStep, v1, sc);
+                load_masks(ma, vb + 2 * kStep);
+                if (vb + kStep < v1)  // block-uniform
+                    process_batch(db, mb, vb + kStep);
+                load_masks(sc, vb + 4 * kStep);
+                __builtin_amdgcn_sched_barrier(0);
+                load_batch_bf16_sel<THREADS, U>(db, vrow, vb + 3 * kStep, v1, sd);
+                load_masks(mb, vb + 3 * kStep);
+                best_ns = ns_row[best_idx];  // as below
+            }
+        } else {
+            load_masks(ma, v0);
+            for (int vb = v0; vb < v1; vb += 2 * kStep) {
+                load_batch_bf16<THREADS, U>(db, vrow, vb + kStep, v1);
+                load_masks(mb, vb + kStep);
+                process_batch(da, ma, vb);
+                load_batch_bf16<THREADS, U>(da, vrow, vb + 2 * kStep, v1);
+                load_masks(ma, vb + 2 * kStep);
+                if (vb + kStep < v1)  // block-uniform
+                    process_batch(db, mb, vb + kStep);
+                // the best so far's next state, loaded outside any branch (a
+                // load under a branch would make the compiler wait for every
+                // load in flight where the branches join)
+                best_ns = ns_row[best_idx];
+            }
         }
     }
     if (first)
@@ -511,20 +575,20 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
 // ANY_ALIGN false: the caller has checked that every row is 16-byte aligned,
 // so only the aligned scan is compiled (fewer registers: more resident
 // blocks where several share a CU).
-template <int THREADS, int U, bool MASKED, bool ANY_ALIGN>
+template <int THREADS, int U, bool MASKED, bool ANY_ALIGN, bool SELECT>
 __device__ __forceinline__ uint64_t scan_chunk_bf16(const char *row, const uint32_t *arow, const int32_t *ns_row,
                                                     RowSplit rs, int v0, int v1, bool first, bool last, int V,
                                                     const uint4 *lut, uint4 (&da)[U], uint64_t &vec_pack,
                                                     int &vec_ns)
 {
     if (!ANY_ALIGN || rs.head == 0)
-        return scan_bf16<THREADS, U, MASKED, false>(row, arow, ns_row, rs, v0, v1, first, last, V, lut, da, vec_pack,
-                                                    vec_ns);
-    return scan_bf16<THREADS, U, MASKED, true>(row, arow, ns_row, rs, v0, v1, first, last, V, lut, da, vec_pack,
-                                               vec_ns);
+        return scan_bf16<THREADS, U, MASKED, false, SELECT>(row, arow, ns_row, rs, v0, v1, first, last, V, lut, da,
+                                                            vec_pack, vec_ns);
+    return scan_bf16<THREADS, U, MASKED, true, SELECT>(row, arow, ns_row, rs, v0, v1, first, last, V, lut, da,
+                                                       vec_pack, vec_ns);
 }
 
-template <int THREADS, int U, bool ANY_ALIGN>
+template <int THREADS, int U, bool ANY_ALIGN, bool SELECT>
 __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
     const int32_t *__restrict__ states, const void *__restrict__ logits, RowMap map, int chunk_vec,
@@ -552,7 +616,7 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     uint64_t mine = 0, vec_pack = 0;
     int vec_ns = kNsUnknown;
     if (live)
-        mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN>(row, allow + (size_t)s * W, next_state + (size_t)s * V, rs, v0, v1,
+        mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN, SELECT>(row, allow + (size_t)s * W, next_state + (size_t)s * V, rs, v0, v1,
                                                  c == 0, c == nchunks - 1, V, lut, da, vec_pack, vec_ns);
     int ns;
     const uint64_t best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
@@ -572,7 +636,7 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
 // row: the model's own choice over the whole row is found first, without
 // reading the mask; only when the mask does not allow it is the row scanned
 // again with the mask.  Same result as masked_step_bf16_kernel.
-template <int THREADS, int U, bool ANY_ALIGN>
+template <int THREADS, int U, bool ANY_ALIGN, bool SELECT>
 __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
     const int32_t *__restrict__ states, const void *__restrict__ logits, RowMap map,
@@ -596,7 +660,7 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     uint64_t mine = 0, vec_pack = 0;
     int vec_ns = kNsUnknown, ns;
     if (live)
-        mine = scan_chunk_bf16<THREADS, U, false, ANY_ALIGN>(row, arow, ns_row, rs, 0, rs.nvec, true, true, V, lut, da, vec_pack,
+        mine = scan_chunk_bf16<THREADS, U, false, ANY_ALIGN, false>(row, arow, ns_row, rs, 0, rs.nvec, true, true, V, lut, da, vec_pack,
                                                   vec_ns);
     uint64_t best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
     if (threadIdx.x == 0) {
@@ -608,7 +672,7 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     if (miss) {  // block-uniform
         if (rs.nvec > 0)
             load_batch_bf16<THREADS, U>(da, row + 2 * rs.head, 0, rs.nvec);
-        mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN>(row, arow, ns_row, rs, 0, rs.nvec, true, true, V, lut, da, vec_pack,
+        mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN, SELECT>(row, arow, ns_row, rs, 0, rs.nvec, true, true, V, lut, da, vec_pack,
                                                  vec_ns);
         best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
     }
@@ -680,6 +744,27 @@ StepGeometry step_geometry(int B, int V, int dtype)
     return {chunk_vec, nchunks, threads};
 }
 
+// Whether a bf16 launch of `blocks` blocks skips lines with no allowed
+// token.  Choosing addresses from the mask adds a dependent trip ahead of
+// each batch's logits; with two or more blocks per compute unit other
+// blocks hide it and the saved bytes win (B = 1024 x V = 256000: 82 against
+// 87 us per step), with one block per unit it shows (B = 256 x V = 128256:
+// 14.5 against 13.9 us).
+static bool skip_unread_lines(unsigned blocks)
+{
+    static std::atomic<int> cus[kMaxDevices];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return false;
+    int n = cus[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = -1;  // unknown: never skip
+        cus[dev].store(n, std::memory_order_relaxed);
+    }
+    return n > 0 && blocks >= 2u * (unsigned)n;
+}
+
 hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, int S, int V,
                               const int32_t *states, const void *logits, int dtype, int B,
                               RowMap map, int32_t *token, int32_t *new_state, void *workspace,
@@ -692,12 +777,21 @@ hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, 
     if (dtype == 0)
         masked_step_kernel<kSmallThreads, kSmallU><<<grid, kSmallThreads, 0, stream>>>(
             next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial);
-    else if (map.rows_aligned(logits, 2))
-        masked_step_bf16_kernel<kBigThreads, kBigU, false><<<grid, kBigThreads, 0, stream>>>(
-            next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial);
-    else
-        masked_step_bf16_kernel<kBigThreads, kBigU, true><<<grid, kBigThreads, 0, stream>>>(
-            next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial);
+    else {
+        const bool aligned = map.rows_aligned(logits, 2), select = skip_unread_lines(grid);
+#define DV_STEP_BF16(A, SEL)                                                                                   \
+    masked_step_bf16_kernel<kBigThreads, kBigU, A, SEL><<<grid, kBigThreads, 0, stream>>>(                    \
+        next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial)
+        if (aligned && select)
+            DV_STEP_BF16(false, true);
+        else if (aligned)
+            DV_STEP_BF16(false, false);
+        else if (select)
+            DV_STEP_BF16(true, true);
+        else
+            DV_STEP_BF16(true, false);
+#undef DV_STEP_BF16
+    }
     if (g.nchunks > 1)
         finalize_kernel<<<(B + kSmallThreads - 1) / kSmallThreads, kSmallThreads, 0, stream>>>(
             next_state, allow, S, V, states, map, B, g.nchunks, partial, token, new_state);
@@ -715,12 +809,19 @@ hipError_t launch_masked_step_opportunistic(const int32_t *next_state, const uin
     // result.
     if (dtype == 1 && step_geometry(B, V, 1).nchunks == 1) {
         const RowMap map{ld, 0, 1, nullptr, 0};
-        if (map.rows_aligned(logits, 2))
-            opportunistic_step_bf16_kernel<kBigThreads, kBigU, false><<<(unsigned)B, kBigThreads, 0, stream>>>(
-                next_state, allow, S, V, (V + 31) / 32, states, logits, map, token, new_state);
+        const bool aligned = map.rows_aligned(logits, 2), select = skip_unread_lines((unsigned)B);
+#define DV_OPP_BF16(A, SEL)                                                                                    \
+    opportunistic_step_bf16_kernel<kBigThreads, kBigU, A, SEL><<<(unsigned)B, kBigThreads, 0, stream>>>(      \
+        next_state, allow, S, V, (V + 31) / 32, states, logits, map, token, new_state)
+        if (aligned && select)
+            DV_OPP_BF16(false, true);
+        else if (aligned)
+            DV_OPP_BF16(false, false);
+        else if (select)
+            DV_OPP_BF16(true, true);
         else
-            opportunistic_step_bf16_kernel<kBigThreads, kBigU, true><<<(unsigned)B, kBigThreads, 0, stream>>>(
-                next_state, allow, S, V, (V + 31) / 32, states, logits, map, token, new_state);
+            DV_OPP_BF16(true, false);
+#undef DV_OPP_BF16
         return hipGetLastError();
     }
     return launch_masked_rows(next_state, allow, S, V, states, logits, dtype, B, RowMap{ld, 0, 1, nullptr, 0}, token,

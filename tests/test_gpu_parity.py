@@ -410,6 +410,45 @@ def test_step_every_row_alignment(dv, B, V, extra_ld, dtype, head):
         np.testing.assert_array_equal(new.cpu().numpy(), new_o)
 
 
+@pytest.mark.parametrize("B,V,offset,extra_ld", [(600, 40000, 0, 0), (520, 30011, 0, 1), (530, 33333, 3, 2),
+                                                 (1030, 24577, 0, 7)])
+def test_step_skips_lines_without_allowed_tokens(dv, B, V, offset, extra_ld):
+    """Launches of two or more blocks per compute unit do not read vectors
+    whose 8 tokens are all disallowed (from the third batch of a row on).
+    Sparse masks (whole runs of disallowed vectors), few distinct values,
+    planted NaN and signed zeros, aligned and misaligned rows; greedy and
+    opportunistic steps against the oracle."""
+    _say(f"step line skipping B={B} V={V} offset={offset} ld=V+{extra_ld}")
+    rng = np.random.default_rng(B + V)
+    S = 9
+    dens = np.array([0.0005, 0.003, 0.02, 0.1, 0.5, 0.9, 1.0, 0.01, 0.05])[:, None]
+    alive = rng.random((S, V)) < dens
+    alive[7, : V // 2] = False                    # long empty runs, then dense
+    alive[7, V // 2:] = True
+    alive[8] = False
+    alive[8, ::4099] = True                       # isolated allowed tokens
+    ns = np.where(alive, rng.integers(0, S, (S, V)), -1).astype(np.int32)
+    Wd = (V + 31) // 32
+    pad = np.zeros((S, Wd * 32), bool)
+    pad[:, :V] = alive
+    al = np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(S, Wd)
+    states = rng.integers(-1, S, B).astype(np.int32)
+    ld = V + extra_ld
+    vals = rng.integers(-3, 4, B * ld + offset + 8).astype(np.float32)
+    buf = torch.from_numpy(vals).to(torch.bfloat16)
+    special = torch.tensor([float("nan"), -0.0, 0.0, 3.0], dtype=torch.bfloat16)
+    pos = torch.from_numpy(rng.integers(0, buf.numel(), 4000))
+    buf[pos] = special[torch.from_numpy(rng.integers(0, 4, 4000))]
+    buf_d = buf.to(DEV)
+    x = buf_d[offset:offset + B * ld].view(B, ld)[:, :V]
+    xo = to_oracle(buf[offset:offset + B * ld].view(B, ld))
+    tok_o, new_o = oracle.masked_step(ns, al, states, xo)
+    for opp in (False, True):
+        tok, new = dv.masked_step(_dev(ns), _dev(al.view(np.int32)), _dev(states), x, opportunistic=opp)
+        np.testing.assert_array_equal(tok.cpu().numpy(), tok_o)
+        np.testing.assert_array_equal(new.cpu().numpy(), new_o)
+
+
 def test_step_empty_batch(dv):
     ns = torch.zeros((2, 10), dtype=torch.int32, device=DEV)
     al = torch.full((2, 1), 0x3FF, dtype=torch.int32, device=DEV)
