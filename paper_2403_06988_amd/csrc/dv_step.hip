@@ -388,13 +388,19 @@ __device__ __forceinline__ RowSplit split_row(const char *row, int V)
 // vector-path best improves, its entry of `ns_row` (the row state's
 // next-state row) is loaded at once, so the final gather is in flight long
 // before the block's maximum is known: `vec_pack` and `vec_ns` return that
-// best and its next state (wave-uniform).  SELECT: vectors with no allowed
-// token are not read (see load_batch_bf16_sel).
-template <int THREADS, int U, bool MASKED, bool SHIFTED, bool SELECT>
-__device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *arow, const int32_t *ns_row,
-                                              RowSplit rs, int v0, int v1, bool first, bool last, int V,
-                                              const uint4 *lut, uint4 (&da)[U], uint64_t &vec_pack, int &vec_ns)
+// best and its next state (wave-uniform).  The mask byte of vector v (bits
+// 8v .. 8v + 7 of the allow row) is mbytes[v - moff]: the allow row itself
+// (moff = 0) or the chunk's bytes staged in LDS.  `db` holds the second
+// batch when STAGED (issued by the caller before the staging finished).
+// SELECT (STAGED only): vectors with no allowed token are not read (see
+// load_batch_bf16_sel).
+template <int THREADS, int U, bool MASKED, bool SHIFTED, bool STAGED, bool SELECT>
+__device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *arow, const uint8_t *mbytes,
+                                              int moff, const int32_t *ns_row, RowSplit rs, int v0, int v1,
+                                              bool first, bool last, int V, const uint4 *lut, uint4 (&da)[U],
+                                              uint4 (&db)[U], uint64_t &vec_pack, int &vec_ns)
 {
+    static_assert(!SELECT || STAGED, "selection reads the staged mask bytes");
     constexpr int kVec = 8;
     constexpr int kStep = THREADS * U;  // vectors per batch
     const int tid = threadIdx.x;
@@ -406,15 +412,14 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
     uint32_t lane_key = 0;  // exact key of this lane's head / tail elements
     int lane_idx = 0;
     if (v0 < v1) {
-        const uint8_t *abytes = reinterpret_cast<const uint8_t *>(arow);
         const int last_byte = (V - 1) >> 3;
         auto mask_of = [&](int v) -> uint32_t {
             if constexpr (!MASKED) {
                 return 0xFFu;
             } else if constexpr (!SHIFTED) {
-                return abytes[v];
+                return mbytes[v - moff];
             } else {
-                const uint32_t b0 = abytes[v], b1 = abytes[min(v + 1, last_byte)];
+                const uint32_t b0 = mbytes[v - moff], b1 = mbytes[min(v + 1, last_byte) - moff];
                 return ((b0 | (b1 << 8)) >> head) & 0xFFu;
             }
         };
@@ -509,39 +514,34 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
         };
         // The next batch's loads are issued unconditionally (past the chunk
         // they are harmless reloads, masked out when reduced).
-        uint4 db[U];
         uint32_t ma[U], mb[U];
-        if constexpr (SELECT && MASKED && !SHIFTED) {
-            // From the third batch on, a vector with no allowed token is not
-            // read (load_batch_bf16_sel), so a 128-byte line with no allowed
-            // token is never fetched.  Choosing the addresses needs the
-            // batch's mask bytes first: they are issued one batch ahead of
-            // the logits (sc, sd), so with the in-order load counter waiting
-            // for them never waits for the previous batch's logits, which
-            // stay in flight while a batch is reduced.
-            // (The scheduling barriers keep that issue order: the compiler
-            // would otherwise issue the logits first.  The prologue issues
-            // sc ahead of the second batch as the loop does, so the waits
-            // the compiler merges at the loop head are those of the loop.)
-            uint32_t sc[U], sd[U];
-            load_masks(ma, v0);
-            load_masks(sc, v0 + 2 * kStep);
-            __builtin_amdgcn_sched_barrier(0);
-            load_batch_bf16<THREADS, U>(db, vrow, v0 + kStep, v1);
-            load_masks(mb, v0 + kStep);
+        if constexpr (STAGED) {
+            // Both first batches are in flight (issued by the caller) and the
+            // mask bytes are in LDS: reading them costs no memory trip, so
+            // with SELECT every later batch's addresses are chosen from them
+            // just before its logits are issued.
+            auto issue = [&](uint4 (&d)[U], int vb) {
+                if constexpr (SELECT && MASKED && !SHIFTED) {
+                    uint32_t sel[U];
+                    load_masks(sel, vb);
+                    load_batch_bf16_sel<THREADS, U>(d, vrow, vb, v1, sel);
+                } else {
+                    load_batch_bf16<THREADS, U>(d, vrow, vb, v1);
+                }
+            };
             for (int vb = v0; vb < v1; vb += 2 * kStep) {
+                load_masks(ma, vb);
                 process_batch(da, ma, vb);
-                load_masks(sd, vb + 3 * kStep);
-                __builtin_amdgcn_sched_barrier(0);
-                load_batch_bf16_sel<THREADS, U>(da, vrow, vb + 2 * kStep, v1, sc);
-                load_masks(ma, vb + 2 * kStep);
-                if (vb + kStep < v1)  // block-uniform
+                issue(da, vb + 2 * kStep);
+                if (vb + kStep < v1) {  // block-uniform
+                    load_masks(mb, vb + kStep);
                     process_batch(db, mb, vb + kStep);
-                load_masks(sc, vb + 4 * kStep);
-                __builtin_amdgcn_sched_barrier(0);
-                load_batch_bf16_sel<THREADS, U>(db, vrow, vb + 3 * kStep, v1, sd);
-                load_masks(mb, vb + 3 * kStep);
-                best_ns = ns_row[best_idx];  // as below
+                }
+                issue(db, vb + 3 * kStep);
+                // the best so far's next state, loaded outside any branch (a
+                // load under a branch would make the compiler wait for every
+                // load in flight where the branches join)
+                best_ns = ns_row[best_idx];
             }
         } else {
             load_masks(ma, v0);
@@ -553,10 +553,7 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
                 load_masks(ma, vb + 2 * kStep);
                 if (vb + kStep < v1)  // block-uniform
                     process_batch(db, mb, vb + kStep);
-                // the best so far's next state, loaded outside any branch (a
-                // load under a branch would make the compiler wait for every
-                // load in flight where the branches join)
-                best_ns = ns_row[best_idx];
+                best_ns = ns_row[best_idx];  // as above
             }
         }
     }
@@ -575,18 +572,50 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
 // ANY_ALIGN false: the caller has checked that every row is 16-byte aligned,
 // so only the aligned scan is compiled (fewer registers: more resident
 // blocks where several share a CU).
-template <int THREADS, int U, bool MASKED, bool ANY_ALIGN, bool SELECT>
-__device__ __forceinline__ uint64_t scan_chunk_bf16(const char *row, const uint32_t *arow, const int32_t *ns_row,
-                                                    RowSplit rs, int v0, int v1, bool first, bool last, int V,
-                                                    const uint4 *lut, uint4 (&da)[U], uint64_t &vec_pack,
-                                                    int &vec_ns)
+template <int THREADS, int U, bool MASKED, bool ANY_ALIGN, bool STAGED, bool SELECT>
+__device__ __forceinline__ uint64_t scan_chunk_bf16(const char *row, const uint32_t *arow, const uint8_t *mbytes,
+                                                    int moff, const int32_t *ns_row, RowSplit rs, int v0, int v1,
+                                                    bool first, bool last, int V, const uint4 *lut, uint4 (&da)[U],
+                                                    uint4 (&db)[U], uint64_t &vec_pack, int &vec_ns)
 {
     if (!ANY_ALIGN || rs.head == 0)
-        return scan_bf16<THREADS, U, MASKED, false, SELECT>(row, arow, ns_row, rs, v0, v1, first, last, V, lut, da,
-                                                            vec_pack, vec_ns);
-    return scan_bf16<THREADS, U, MASKED, true, SELECT>(row, arow, ns_row, rs, v0, v1, first, last, V, lut, da,
-                                                       vec_pack, vec_ns);
+        return scan_bf16<THREADS, U, MASKED, false, STAGED, SELECT>(row, arow, mbytes, moff, ns_row, rs, v0, v1,
+                                                                    first, last, V, lut, da, db, vec_pack, vec_ns);
+    return scan_bf16<THREADS, U, MASKED, true, STAGED, SELECT>(row, arow, mbytes, moff, ns_row, rs, v0, v1, first,
+                                                               last, V, lut, da, db, vec_pack, vec_ns);
 }
+
+// Mask words staged per block: the chunk's mask bytes (one per vector, plus
+// one for a shifted head) in at most kStageWords words, so chunks are capped
+// at kMaxChunkVec vectors.
+constexpr int kStageWords = 8192;
+constexpr int kMaxChunkVec = (kStageWords - 1) * 4 / 512 * 512;
+
+// Copies allow-row words [w0, w0 + nwords) (nwords <= kStageWords) of `arow`
+// (a row of W words) into LDS: every lane's loads first (clamped into the
+// row, branch-free), then `between` (loads that must not queue behind the
+// LDS writes' waits), then the writes.
+template <int THREADS, typename F>
+__device__ __forceinline__ void stage_mask_words(uint32_t *lds, const uint32_t *arow, int w0, int nwords, int W,
+                                                 F between)
+{
+    constexpr int kPerLane = kStageWords / THREADS;
+    static_assert(kPerLane * THREADS == kStageWords, "whole words per lane");
+    uint32_t t[kPerLane];
+#pragma unroll
+    for (int k = 0; k < kPerLane; ++k)
+        t[k] = arow[min(w0 + min(k * THREADS + (int)threadIdx.x, nwords - 1), W - 1)];
+    between();
+#pragma unroll
+    for (int k = 0; k < kPerLane; ++k) {
+        const int i = k * THREADS + (int)threadIdx.x;
+        if (i < nwords)
+            lds[i] = t[k];
+    }
+}
+
+// LDS bytes of a launch's staged mask words (chunks of chunk_vec vectors).
+inline size_t staged_mask_bytes(int chunk_vec) { return ((size_t)chunk_vec / 4 + 1) * 4; }
 
 template <int THREADS, int U, bool ANY_ALIGN, bool SELECT>
 __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
@@ -595,29 +624,61 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     int nchunks, int32_t *__restrict__ token, int32_t *__restrict__ new_state,
     uint64_t *__restrict__ partial)
 {
+    extern __shared__ uint32_t staged[];  // the chunk's mask words
     __shared__ uint4 lut[256];
     const int b = blockIdx.x / nchunks;
     const int c = blockIdx.x - b * nchunks;
     const char *row = static_cast<const char *>(logits) + (size_t)map.offset(b) * 2;
     const RowSplit rs = split_row(row, V);  // block-uniform
-    const int v0 = c * chunk_vec;
+    const int v0 = c * chunk_vec;            // a multiple of 4: staging starts at word v0 / 4
     const int v1 = min(rs.nvec, v0 + chunk_vec);
+    const char *vrow = row + 2 * rs.head;
 
     // The first batch of logits does not depend on the row's state: it is in
-    // flight before the state lookup returns, and the mask table is built
-    // meanwhile.
-    uint4 da[U];
+    // flight before the state lookup returns.  With SELECT the chunk's mask
+    // bytes are then staged in LDS (their loads issued ahead of the second
+    // batch, so waiting for them does not wait for it) and vectors with no
+    // allowed token are not read; without, mask bytes stream beside their
+    // logits.  Either way the mask table is built meanwhile.
+    uint4 da[U], db[U];
     if (v0 < v1)
-        load_batch_bf16<THREADS, U>(da, row + 2 * rs.head, v0, v1);
+        load_batch_bf16<THREADS, U>(da, vrow, v0, v1);
     const int s = row_state(states, map, next_state, allow, S, V, b);
-    fill_lut(lut);
-    lds_barrier();
     const bool live = (uint32_t)s < (uint32_t)S;  // block-uniform
+    const uint32_t *arow = allow + (size_t)(live ? s : 0) * W;
     uint64_t mine = 0, vec_pack = 0;
     int vec_ns = kNsUnknown;
-    if (live)
-        mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN, SELECT>(row, allow + (size_t)s * W, next_state + (size_t)s * V, rs, v0, v1,
-                                                 c == 0, c == nchunks - 1, V, lut, da, vec_pack, vec_ns);
+    if constexpr (SELECT) {
+        // The streaming scan is reached only on this path, so the loads the
+        // compiler sees in flight at its loop head are the two batches'.
+        if (live && v0 < v1) {
+            const int w0 = v0 >> 2, nwords = min(W, (v1 >> 2) + 1) - w0;  // bytes v0 .. v1
+            stage_mask_words<THREADS>(staged, arow, w0, nwords, W,
+                                      [&] { load_batch_bf16<THREADS, U>(db, vrow, v0 + THREADS * U, v1); });
+            fill_lut(lut);
+            lds_barrier();
+            mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN, true, true>(
+                row, arow, reinterpret_cast<const uint8_t *>(staged), v0, next_state + (size_t)s * V, rs, v0, v1,
+                c == 0, c == nchunks - 1, V, lut, da, db, vec_pack, vec_ns);
+        } else if (live) {  // no whole vector in this chunk: the head and tail elements only
+            uint32_t key = 0;
+            int idx = 0;
+            if (c == 0)
+                scan_exact<1, THREADS>(row, arow, 0, rs.head, key, idx);
+            if (c == nchunks - 1)
+                scan_exact<1, THREADS>(row, arow, rs.head + rs.nvec * 8, V, key, idx);
+            mine = pack(key, idx);
+        }
+    } else {
+        // Mask bytes read from the allow row batch by batch, right behind
+        // their logits: nothing to wait for before the first batch.
+        fill_lut(lut);
+        lds_barrier();
+        if (live)
+            mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN, false, false>(
+                row, arow, reinterpret_cast<const uint8_t *>(arow), 0, next_state + (size_t)s * V, rs, v0, v1,
+                c == 0, c == nchunks - 1, V, lut, da, db, vec_pack, vec_ns);
+    }
     int ns;
     const uint64_t best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
     if (threadIdx.x != 0)
@@ -636,7 +697,7 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
 // row: the model's own choice over the whole row is found first, without
 // reading the mask; only when the mask does not allow it is the row scanned
 // again with the mask.  Same result as masked_step_bf16_kernel.
-template <int THREADS, int U, bool ANY_ALIGN, bool SELECT>
+template <int THREADS, int U, bool ANY_ALIGN>
 __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
     const int32_t *__restrict__ states, const void *__restrict__ logits, RowMap map,
@@ -648,7 +709,7 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     const char *row = static_cast<const char *>(logits) + (size_t)map.offset(b) * 2;
     const RowSplit rs = split_row(row, V);  // block-uniform
 
-    uint4 da[U];
+    uint4 da[U], db[U];  // db: scratch of the scan
     if (rs.nvec > 0)
         load_batch_bf16<THREADS, U>(da, row + 2 * rs.head, 0, rs.nvec);
     const int s = states[b];
@@ -660,8 +721,9 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     uint64_t mine = 0, vec_pack = 0;
     int vec_ns = kNsUnknown, ns;
     if (live)
-        mine = scan_chunk_bf16<THREADS, U, false, ANY_ALIGN, false>(row, arow, ns_row, rs, 0, rs.nvec, true, true, V, lut, da, vec_pack,
-                                                  vec_ns);
+        mine = scan_chunk_bf16<THREADS, U, false, ANY_ALIGN, false, false>(
+            row, arow, reinterpret_cast<const uint8_t *>(arow), 0, ns_row, rs, 0, rs.nvec, true, true, V, lut, da, db,
+            vec_pack, vec_ns);
     uint64_t best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
     if (threadIdx.x == 0) {
         const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
@@ -672,8 +734,9 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     if (miss) {  // block-uniform
         if (rs.nvec > 0)
             load_batch_bf16<THREADS, U>(da, row + 2 * rs.head, 0, rs.nvec);
-        mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN, SELECT>(row, arow, ns_row, rs, 0, rs.nvec, true, true, V, lut, da, vec_pack,
-                                                 vec_ns);
+        mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN, false, false>(
+            row, arow, reinterpret_cast<const uint8_t *>(arow), 0, ns_row, rs, 0, rs.nvec, true, true, V, lut, da, db,
+            vec_pack, vec_ns);
         best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
     }
     if (threadIdx.x != 0)
@@ -726,6 +789,7 @@ StepGeometry step_geometry(int B, int V, int dtype)
         int chunk_vec = (nvec + threads - 1) / threads * threads;
         return {chunk_vec > 0 ? chunk_vec : threads, 1, threads};
     }
+    static_assert(kMaxChunkVec % kBigThreads == 0, "chunks are whole batches of lanes");
     const int target = bf16 ? kStepOneBlockRows : kStepTargetBlocks;
     const int nvec = V / vec;
     // about `target` blocks, at least one vector per lane per chunk
@@ -738,18 +802,20 @@ StepGeometry step_geometry(int B, int V, int dtype)
     chunk_vec = (chunk_vec + threads - 1) / threads * threads;
     if (chunk_vec == 0)
         chunk_vec = threads;
+    if (bf16 && chunk_vec > kMaxChunkVec)  // the staged mask bytes must fit
+        chunk_vec = kMaxChunkVec;
     nchunks = (nvec + chunk_vec - 1) / chunk_vec;
     if (nchunks < 1)
         nchunks = 1;
     return {chunk_vec, nchunks, threads};
 }
 
-// Whether a bf16 launch of `blocks` blocks skips lines with no allowed
-// token.  Choosing addresses from the mask adds a dependent trip ahead of
-// each batch's logits; with two or more blocks per compute unit other
-// blocks hide it and the saved bytes win (B = 1024 x V = 256000: 82 against
-// 87 us per step), with one block per unit it shows (B = 256 x V = 128256:
-// 14.5 against 13.9 us).
+// Whether a bf16 launch of `blocks` blocks stages its mask bytes in LDS and
+// skips lines with no allowed token.  Staging puts the whole chunk's mask
+// row ahead of the first reduction; with two or more blocks per compute
+// unit other blocks hide that and the saved bytes win (B = 1024 x V =
+// 256000: 82 against 85 us per step), with one block per unit it shows
+// (B = 256 x V = 128256: 15.0 against 13.9 us).
 static bool skip_unread_lines(unsigned blocks)
 {
     static std::atomic<int> cus[kMaxDevices];
@@ -779,8 +845,9 @@ hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, 
             next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial);
     else {
         const bool aligned = map.rows_aligned(logits, 2), select = skip_unread_lines(grid);
+        const size_t lds = select ? staged_mask_bytes(g.chunk_vec) : 0;
 #define DV_STEP_BF16(A, SEL)                                                                                   \
-    masked_step_bf16_kernel<kBigThreads, kBigU, A, SEL><<<grid, kBigThreads, 0, stream>>>(                    \
+    masked_step_bf16_kernel<kBigThreads, kBigU, A, SEL><<<grid, kBigThreads, lds, stream>>>(                  \
         next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial)
         if (aligned && select)
             DV_STEP_BF16(false, true);
@@ -809,19 +876,12 @@ hipError_t launch_masked_step_opportunistic(const int32_t *next_state, const uin
     // result.
     if (dtype == 1 && step_geometry(B, V, 1).nchunks == 1) {
         const RowMap map{ld, 0, 1, nullptr, 0};
-        const bool aligned = map.rows_aligned(logits, 2), select = skip_unread_lines((unsigned)B);
-#define DV_OPP_BF16(A, SEL)                                                                                    \
-    opportunistic_step_bf16_kernel<kBigThreads, kBigU, A, SEL><<<(unsigned)B, kBigThreads, 0, stream>>>(      \
-        next_state, allow, S, V, (V + 31) / 32, states, logits, map, token, new_state)
-        if (aligned && select)
-            DV_OPP_BF16(false, true);
-        else if (aligned)
-            DV_OPP_BF16(false, false);
-        else if (select)
-            DV_OPP_BF16(true, true);
+        if (map.rows_aligned(logits, 2))
+            opportunistic_step_bf16_kernel<kBigThreads, kBigU, false><<<(unsigned)B, kBigThreads, 0, stream>>>(
+                next_state, allow, S, V, (V + 31) / 32, states, logits, map, token, new_state);
         else
-            DV_OPP_BF16(true, false);
-#undef DV_OPP_BF16
+            opportunistic_step_bf16_kernel<kBigThreads, kBigU, true><<<(unsigned)B, kBigThreads, 0, stream>>>(
+                next_state, allow, S, V, (V + 31) / 32, states, logits, map, token, new_state);
         return hipGetLastError();
     }
     return launch_masked_rows(next_state, allow, S, V, states, logits, dtype, B, RowMap{ld, 0, 1, nullptr, 0}, token,
