@@ -178,6 +178,7 @@ def cpu_baseline(w, wid, trans, offsets, data, init, x_dev, budget_s):
     # workload statistic for the alignment's L2 roofline: table moves per pair
     srows = rng.integers(0, w.S, 8).astype(np.int32)
     moves = oracle.walk_lookups(trans, offsets, data, srows, lib=lib) / (len(srows) * w.V)
+    every = all_cores(w, lib, cache, init, x_dev, done_steps, trans, offsets, data, budget_s / 3)
     return {
         "value": dec_steps_per_s, "unit": "steps/s", "cores": 1, "kind": "oracle",
         "moves_per_pair": moves,
@@ -186,7 +187,71 @@ def cpu_baseline(w, wid, trans, offsets, data, init, x_dev, budget_s):
         "align_value": pairs / t_al, "align_unit": "alignments/s",
         "align_sample": f"{pairs} (state, token) pairs in whole table rows",
         "seconds": round(t_dec + t_al, 2),
+        "all_cores": every,
+        "cpu_model": cpu_model(),
+        "oracle_build": " ".join(oracle.BUILD_FLAGS),
     }
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def all_cores(w, lib, cache, init, x_dev, steps, trans, offsets, data, budget_s):
+    """The same oracle calls spread over the process's CPU share (at most 16
+    threads; the C calls run without the interpreter lock): the first
+    ``steps`` steps of the greedy chain with the rows of each step split over
+    the threads, then whole table rows of the alignment, one call per thread
+    at a time."""
+    import concurrent.futures as cf
+
+    import numpy as np
+
+    import oracle
+    from tests.gpu_common import to_oracle
+
+    n = max(1, min(16, len(os.sched_getaffinity(0))))
+    parts = [list(range(i, w.B, n)) for i in range(n)]
+    cur = [int(s) for s in init]
+    t_dec, row_steps = 0.0, 0
+    with cf.ThreadPoolExecutor(n) as pool:
+        for k in range(steps):
+            xs = to_oracle(x_dev[k])
+            rows = [cache.get(s) if s >= 0 else None for s in cur]   # untimed (built by the 1-thread leg)
+
+            def run(part):
+                out = []
+                for b in part:
+                    if rows[b] is None:
+                        continue
+                    tok = oracle.masked_argmax(rows[b][1], xs[b], lib=lib)
+                    out.append((b, -1 if tok < 0 else int(rows[b][0][tok])))
+                return out
+
+            t0 = time.perf_counter()
+            results = list(pool.map(run, parts))
+            t_dec += time.perf_counter() - t0
+            for out in results:
+                for b, nxt in out:
+                    cur[b] = nxt
+                    row_steps += 1
+        rng = np.random.default_rng(1)
+        pairs, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < budget_s:
+            batches = [rng.integers(0, w.S, 2).astype(np.int32) for _ in range(n)]
+            list(pool.map(lambda r: oracle.align_rows(trans, offsets, data, r, lib=lib), batches))
+            pairs += sum(len(r) for r in batches) * w.V
+        t_al = time.perf_counter() - t0
+    return {"cores": n, "value": (row_steps / w.B) / t_dec if t_dec > 0 else None, "unit": "steps/s",
+            "align_value": pairs / t_al, "align_unit": "alignments/s",
+            "sample": f"{row_steps} row-steps over {steps} steps, then {pairs} (state, token) pairs",
+            "seconds": round(t_dec + t_al, 2)}
 
 
 def run_probes(dv, dev, table_bytes):

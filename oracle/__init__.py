@@ -44,13 +44,14 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "dv_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "libdv_oracle.so")
 _lib = None
+BUILD_FLAGS = ("-O2", "-std=c11")
 
 
 def build(force: bool = False, out: str | None = None, defines: tuple = ()) -> str:
     """Compile ``dv_oracle.c`` with gcc into a shared library; returns its path."""
     out = out or _LIB_PATH
     if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(_SRC):
-        cmd = ["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-o", out, _SRC, "-lm"]
+        cmd = ["gcc", *BUILD_FLAGS, "-shared", "-fPIC", "-o", out, _SRC, "-lm"]
         cmd += [f"-D{d}" for d in defines]
         subprocess.run(cmd, check=True)
     return out
