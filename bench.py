@@ -176,7 +176,7 @@ def cpu_baseline(w, wid, trans, offsets, data, init, x_dev, budget_s):
         t_al += time.perf_counter() - t0
         pairs += len(rows) * w.V
     # workload statistic for the alignment's L2 roofline: table moves per pair
-    srows = rng.integers(0, w.S, 8).astype(np.int32)
+    srows = rng.integers(0, w.S, 32).astype(np.int32)
     moves = oracle.walk_lookups(trans, offsets, data, srows, lib=lib) / (len(srows) * w.V)
     every = all_cores(w, lib, cache, init, x_dev, done_steps, trans, offsets, data, budget_s / 3)
     return {
