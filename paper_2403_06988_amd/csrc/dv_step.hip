@@ -6,25 +6,32 @@
 // operations per element.
 //   * Launch shape (bf16).  A row is one 512-lane block once B >= 256
 //     (every CU gets at least one row), or when it holds at most 32768
-//     logits (a second pass would cost more than the split saves), so no
-//     second pass is needed.  Each
-//     lane streams batches of 2 independent non-temporal 16-byte loads with
-//     a register double buffer: batch i + 1 is in flight while batch i is
-//     reduced.  Each batch loads its allow-mask
-//     bytes (one byte per 8 logits) right behind its logits.  Smaller
+//     logits (a second pass would cost more than the split saves).  Smaller
 //     batches split each row into chunks, one block each, and a tiny second
 //     kernel (one lane per row) combines the chunks -- no atomics and no
 //     device-wide fences in the streaming kernel (a release fence at device
 //     scope writes back and invalidates the XCD's L2 on gfx950).
+//   * Each lane streams batches of 2 independent non-temporal 16-byte loads
+//     with a register double buffer: batch i + 1 is in flight while batch i
+//     is reduced.  Loads are branch-free and in a fixed order, because the
+//     load counter is in order: waiting for one load waits for every earlier
+//     one.  The first batch is issued before the row's state is known.
+//   * Mask bytes (one per 8 logits).  With one block per compute unit they
+//     are loaded beside their batch's logits.  With two or more, the block
+//     first copies its chunk's mask bytes into LDS; each later batch's
+//     addresses are then chosen from them, and a vector with no allowed
+//     token is read from one cached location instead, so a 128-byte line
+//     with no allowed token is never fetched.
 //   * bf16 arithmetic, two VALU operations per logit: per 32-bit word (two
 //     logits) one v_pk_ashrrev_i16 and one bit operation give
 //     order-preserving 16-bit keys, an AND with two 16-bit lane masks (from
 //     an LDS table indexed by the mask byte) drops the disallowed ones, and
-//     v_pk_max_u16 folds them.  One block-wide max per batch; only the
-//     wave(s) holding the maximum look up its lowest index.  The fast key
-//     differs from the exact ordering only for NaN (which must rank as -inf)
-//     and -0.0 (which must tie with +0.0); a batch whose maximum is one of
-//     those few key values is redone with exact keys.
+//     v_pk_max_u16 folds them.  One wave-wide max per batch (DPP moves, no
+//     LDS and no barrier); only the wave(s) holding the maximum look up its
+//     lowest index.  The fast key differs from the exact ordering only for
+//     NaN (which must rank as -inf) and -0.0 (which must tie with +0.0); a
+//     batch whose maximum is one of those few key values is redone with
+//     exact keys.
 //   * A bf16 row need not be 16-byte aligned (any row stride): the elements
 //     before its first 16-byte boundary are read one by one and the mask
 //     bits of each vector are taken from two mask bytes, shifted.
