@@ -156,7 +156,7 @@ int32_t oracle_masked_argmax(const uint32_t *allow_row, const void *logits_row,
 }
 
 /* One masked decode step for a batch (Algorithm 1: mask, apply, decode,
- * then update the checker's state with the chosen token). */
+ * then update the constraint state with the chosen token). */
 void oracle_masked_step(const int32_t *next_state, const uint32_t *allow,
                         int32_t num_states, int32_t num_tokens,
                         const int32_t *states, const void *logits, int dtype,
