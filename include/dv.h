@@ -151,9 +151,11 @@ DV_API dv_status dv_align_eos(const int32_t *trans, int32_t num_states,
 
 /*
  * dv_masked_step_workspace_bytes -- device workspace dv_masked_step needs for
- * `batch` rows of `num_tokens` logits (per-chunk partial results when a row
- * is split over several blocks), for either dtype.  Returns 0 when a size is
- * outside its limit.
+ * `batch` rows of `num_tokens` logits, for either dtype: where a row is
+ * split over several blocks, they meet there (a running maximum and an
+ * arrival count per row; the last block to arrive writes the row's outputs
+ * and puts its entries back to zero).  Returns 0 when a size is outside its
+ * limit.
  */
 DV_API size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens);
 
@@ -184,8 +186,10 @@ DV_API size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens);
  * Outputs (device): token [B] int32, new_state [B] int32.  They must not
  *   overlap each other or any input (callers ping-pong two state buffers).
  * Workspace: at least dv_masked_step_workspace_bytes(B, V) bytes of device
- *   memory, 256-byte aligned; contents on entry are ignored, on exit
- *   undefined.  Calls that share a workspace must be ordered on one stream.
+ *   memory, 256-byte aligned, all zero before its first use (clear it once,
+ *   e.g. with hipMemset); every call leaves it all zero again, so it can be
+ *   reused by any later call of any size without clearing.  Calls that share
+ *   a workspace must be ordered on one stream.
  * B = 0 is valid and enqueues nothing; states, logits, token and new_state
  *   may then be NULL (the pointers of empty tensors).
  * Errors: DV_ERR_INVALID_ARG (also for logits not aligned to the element
@@ -254,7 +258,8 @@ DV_API size_t dv_masked_sample_workspace_bytes(int32_t batch, int32_t num_tokens
  *
  * inv_temperature = 1/T, finite and > 0 (T -> 0 approaches dv_masked_step).
  * Other arguments and errors as dv_masked_step (DV_ERR_SHAPE also for a
- * bad inv_temperature); workspace: dv_masked_sample_workspace_bytes(B, V).
+ * bad inv_temperature); workspace: dv_masked_sample_workspace_bytes(B, V),
+ * zero before its first use and left zero, as for dv_masked_step.
  */
 DV_API dv_status dv_masked_sample(const int32_t *next_state, const uint32_t *allow,
                          int32_t num_states, int32_t num_tokens,
@@ -297,7 +302,7 @@ DV_API dv_status dv_spec_walk(const int32_t *next_state, const uint32_t *allow,
 /*
  * dv_spec_verify_workspace_bytes -- device workspace dv_spec_verify needs for
  * `batch` rows of `num_proposed` proposals over `num_tokens` logits (the
- * state of every position and the masked step's partial results).  Returns 0
+ * state of every position and the masked step's meeting entries).  Returns 0
  * when a size is outside its limit.
  */
 DV_API size_t dv_spec_verify_workspace_bytes(int32_t batch, int32_t num_proposed,
@@ -337,8 +342,9 @@ DV_API size_t dv_spec_verify_workspace_bytes(int32_t batch, int32_t num_proposed
  * Outputs (device): token [B][s+1], accepted [B], new_state [B] int32; they
  *   must not overlap each other, an input or the workspace.
  * Workspace: at least dv_spec_verify_workspace_bytes(B, s, V) bytes of
- *   device memory, 256-byte aligned; contents on entry are ignored, on exit
- *   undefined.  Calls that share a workspace must be ordered on one stream.
+ *   device memory, 256-byte aligned, all zero before its first use and left
+ *   all zero by every call (as for dv_masked_step).  Calls that share a
+ *   workspace must be ordered on one stream.
  * B = 0 is valid and enqueues nothing.
  * Errors: DV_ERR_INVALID_ARG (also for misaligned logits), DV_ERR_SHAPE
  *   (S, V, B or s out of range, B*(s+1) > DV_MAX_BATCH, ld_proposals < s,

@@ -169,10 +169,10 @@ def align(trans, offsets, tok_bytes, next_state=None, allow=None, workspace=None
 
 
 def step_workspace(batch: int, num_tokens: int, device) -> torch.Tensor:
-    """A workspace for ``masked_step`` with up to ``batch`` rows (reusable by
-    calls ordered on one stream)."""
+    """A zero-filled workspace for ``masked_step`` with up to ``batch`` rows;
+    every call leaves it zero, so calls ordered on one stream can reuse it."""
     n = masked_step_workspace_bytes(batch, num_tokens)
-    return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
+    return torch.zeros(max(n, 1), dtype=torch.uint8, device=device)
 
 
 def masked_step(next_state, allow, states, logits, token=None, new_state=None, workspace=None,
@@ -218,9 +218,10 @@ def masked_sample_workspace_bytes(batch: int, num_tokens: int) -> int:
 
 
 def sample_workspace(batch: int, num_tokens: int, device) -> torch.Tensor:
-    """A workspace for ``masked_sample`` (reusable by calls ordered on one stream)."""
+    """A zero-filled workspace for ``masked_sample`` (left zero by every call;
+    reusable by calls ordered on one stream)."""
     n = masked_sample_workspace_bytes(batch, num_tokens)
-    return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
+    return torch.zeros(max(n, 1), dtype=torch.uint8, device=device)
 
 
 def masked_sample(next_state, allow, states, logits, seed: int, offset: int, inv_temperature: float = 1.0,
@@ -301,9 +302,10 @@ def spec_verify_workspace_bytes(batch: int, num_proposed: int, num_tokens: int) 
 
 
 def spec_workspace(batch: int, num_proposed: int, num_tokens: int, device) -> torch.Tensor:
-    """A workspace for ``spec_verify`` (reusable by calls ordered on one stream)."""
+    """A zero-filled workspace for ``spec_verify`` (left zero by every call;
+    reusable by calls ordered on one stream)."""
     n = spec_verify_workspace_bytes(batch, num_proposed, num_tokens)
-    return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
+    return torch.zeros(max(n, 1), dtype=torch.uint8, device=device)
 
 
 def spec_verify(next_state, allow, states, proposals, logits, token=None, accepted=None,

@@ -98,14 +98,55 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
                         int V, const uint8_t *accepting, int eos_token, int32_t *next_state,
                         uint32_t *allow, void *workspace, hipStream_t stream);
 
+// ----------------------------------------------------- split rows meet here
+//
+// When a row is split over several blocks, the blocks meet in the
+// workspace: per row a 64-bit maximum of (key << 32 | ~index) and a 32-bit
+// count of the blocks that have arrived, both zero between calls.  Each
+// block folds its best into the maximum and then counts itself; the block
+// that arrives last reads the maximum, puts both back to zero and writes the
+// row's outputs -- one kernel, no second pass, no waiting on other blocks.
+// Layout: best [B] uint64 at 0, arrived [B] uint32 at row_meet_count_offset.
+inline size_t row_meet_count_offset(int B) { return align_up((size_t)(B > 0 ? B : 1) * 8, 256); }
+inline size_t row_meet_bytes(int B) { return row_meet_count_offset(B) + align_up((size_t)(B > 0 ? B : 1) * 4, 256); }
+
+struct RowMeet {
+    uint64_t *best;
+    uint32_t *arrived;
+};
+
+inline RowMeet row_meet(void *workspace, int B)
+{
+    char *w = static_cast<char *>(workspace);
+    return {reinterpret_cast<uint64_t *>(w), reinterpret_cast<uint32_t *>(w + row_meet_count_offset(B))};
+}
+
+// Called by one lane of each of the `nchunks` blocks of row b.  Both
+// updates are device-scope atomics (performed where every XCD sees them).
+// The arrival is counted only once the maximum has been performed: its
+// operand depends on the value the maximum returned.  Returns true in the
+// block that arrives last, with the row's maximum in `fin` and the row's
+// entries back at zero.
+__device__ __forceinline__ bool meet_row(RowMeet m, int b, int nchunks, uint64_t best, uint64_t &fin)
+{
+    const uint64_t before = __hip_atomic_fetch_max(m.best + b, best, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t one = 1u;
+    asm volatile("" : "+v"(one) : "v"(before) : "memory");
+    const uint32_t n = __hip_atomic_fetch_add(m.arrived + b, one, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (n != (uint32_t)nchunks - 1u)
+        return false;
+    fin = __hip_atomic_exchange(m.best + b, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    (void)__hip_atomic_exchange(m.arrived + b, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return true;
+}
+
 // ------------------------------------------------------------- masked step
 //
 // A row of V logits is split into `nchunks` chunks of `chunk_vec` 16-byte
-// vectors, one block of `threads` lanes each.  With more than one chunk,
-// each block writes its best (key << 32 | ~index) to the workspace,
-// [B][nchunks] uint64, and a second kernel combines the chunks of each row.
-// bf16 rows use 512-lane blocks and aim for kStepOneBlockRows blocks per
-// launch (one block per row once B >= 256).
+// vectors, one block of `threads` lanes each; with more than one chunk the
+// blocks meet in the workspace (above).  bf16 rows use 512-lane blocks and
+// aim for kStepOneBlockRows blocks per launch (one block per row once
+// B >= 256).
 constexpr int kStepTargetBlocks = 2048;
 constexpr int kStepMaxChunks = 64;
 constexpr int kStepOneBlockRows = 256;
@@ -119,9 +160,8 @@ StepGeometry step_geometry(int B, int V, int dtype);
 
 inline size_t step_workspace_bytes(int B, int V)
 {
-    const StepGeometry a = step_geometry(B, V, 0), b = step_geometry(B, V, 1);
-    const int n = a.nchunks > b.nchunks ? a.nchunks : b.nchunks;
-    return align_up((size_t)(B > 0 ? B : 1) * (size_t)n * sizeof(uint64_t), 256);
+    (void)V;
+    return row_meet_bytes(B);
 }
 
 hipError_t launch_masked_step(const int32_t *next_state, const uint32_t *allow, int S, int V,
@@ -209,7 +249,7 @@ hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, 
 // Workspace of the verification, for B rows of s proposals (R = B (s + 1)
 // positions), 256-byte aligned parts:
 //   [0, ...)     int32 state after each position's choice [B][s+1]
-//   [partial..)  the masked step's workspace for R rows
+//   [meet..)     the masked step's workspace for R rows (zero between calls)
 inline size_t spec_positions(int B, int s) { return (size_t)B * (size_t)(s + 1); }
 inline size_t spec_partial_offset(int B, int s) { return align_up(spec_positions(B, s) * 4, 256); }
 inline size_t spec_workspace_bytes(int B, int s, int V)

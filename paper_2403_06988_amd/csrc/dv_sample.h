@@ -5,7 +5,8 @@
 
 namespace dv {
 
-// Workspace: [B][nchunks] uint64 partial maxima (rows split over blocks).
+// Workspace: the meeting slots of rows split over blocks (row_meet_bytes;
+// zero before the first call, left zero by every call).
 size_t sample_workspace_bytes(int B, int V);
 
 hipError_t launch_masked_sample(const int32_t *next_state, const uint32_t *allow, int S, int V,

@@ -22,8 +22,8 @@
 namespace dv {
 namespace {
 
-constexpr int kThreads = 256;       // split rows: several blocks per row, then a combining pass
-constexpr int kRowThreads = 1024;   // one block per row once B >= kOneBlockRows: no combining pass
+constexpr int kThreads = 256;       // split rows: several blocks per row, meeting in the workspace
+constexpr int kRowThreads = 1024;   // one block per row once B >= kOneBlockRows
                                     // (below that, split rows keep more waves per CU, which this
                                     // latency-laden arithmetic needs more than it saves a launch)
 #ifndef DV_SAMPLE_ONE_BLOCK_ROWS
@@ -208,7 +208,7 @@ template <int DT, int THREADS>
 __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
     const int32_t *__restrict__ states, const void *__restrict__ logits, int64_t ld, float inv_t, uint32_t seed_lo,
-    uint32_t seed_hi, uint32_t off_lo, uint32_t off_hi, int chunk_tok, int nchunks, uint64_t *__restrict__ partial,
+    uint32_t seed_hi, uint32_t off_lo, uint32_t off_hi, int chunk_tok, int nchunks, RowMeet meet,
     int32_t *__restrict__ token, int32_t *__restrict__ new_state)
 {
 #pragma clang fp contract(off)
@@ -273,9 +273,7 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
     if (tid == 0) {
         for (int w = 1; w < kWaves; ++w)
             best = max_u64(best, red[w]);
-        if (nchunks > 1) {
-            partial[blockIdx.x] = best;
-        } else {
+        if (nchunks == 1 || meet_row(meet, b, nchunks, best, best)) {  // else another block finishes the row
             const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
             const bool found = live && tok >= 0 && tok < V;  // guards the read
             token[b] = found ? tok : -1;
@@ -284,34 +282,13 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
     }
 }
 
-// One lane per row: combine the row's chunk maxima and write the outputs
-// (rows split over several blocks only).
-__global__ __launch_bounds__(kThreads) void sample_finalize_kernel(const int32_t *__restrict__ next_state, int S,
-                                                                  int V, const int32_t *__restrict__ states, int B,
-                                                                  int nchunks,
-                                                                  const uint64_t *__restrict__ partial,
-                                                                  int32_t *__restrict__ token,
-                                                                  int32_t *__restrict__ new_state)
-{
-    const int b = blockIdx.x * kThreads + threadIdx.x;
-    if (b >= B)
-        return;
-    uint64_t best = 0;
-    for (int c = 0; c < nchunks; ++c)
-        best = max_u64(best, partial[(size_t)b * nchunks + c]);
-    const int s = states[b];
-    const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
-    const bool found = tok >= 0 && tok < V && (uint32_t)s < (uint32_t)S;  // guards the read
-    token[b] = found ? tok : -1;
-    new_state[b] = found ? next_state[(size_t)s * V + tok] : -1;
-}
 
 }  // namespace
 
 size_t sample_workspace_bytes(int B, int V)
 {
-    const SampleGeometry g = sample_geometry(B, V);
-    return align_up((size_t)(B > 0 ? B : 1) * (size_t)g.nchunks * sizeof(uint64_t), 256);
+    (void)V;
+    return row_meet_bytes(B);
 }
 
 hipError_t launch_masked_sample(const int32_t *next_state, const uint32_t *allow, int S, int V,
@@ -321,14 +298,14 @@ hipError_t launch_masked_sample(const int32_t *next_state, const uint32_t *allow
 {
     const int W = (V + 31) / 32;
     const SampleGeometry g = sample_geometry(B, V);
-    uint64_t *partial = static_cast<uint64_t *>(workspace);
+    const RowMeet meet = row_meet(workspace, B);
     const unsigned grid = (unsigned)B * (unsigned)g.nchunks;
     const uint32_t s_lo = (uint32_t)seed, s_hi = (uint32_t)(seed >> 32);
     const uint32_t o_lo = (uint32_t)offset, o_hi = (uint32_t)(offset >> 32);
 #define DV_SAMPLE_LAUNCH(DT, T)                                                                                  \
     masked_sample_kernel<DT, T><<<grid, T, 0, stream>>>(next_state, allow, S, V, W, states, logits, ld,          \
                                                         inv_temperature, s_lo, s_hi, o_lo, o_hi, g.chunk_tok,    \
-                                                        g.nchunks, partial, token, new_state)
+                                                        g.nchunks, meet, token, new_state)
     if (g.threads == kRowThreads) {
         if (dtype == 0)
             DV_SAMPLE_LAUNCH(0, kRowThreads);
@@ -341,10 +318,6 @@ hipError_t launch_masked_sample(const int32_t *next_state, const uint32_t *allow
             DV_SAMPLE_LAUNCH(1, kThreads);
     }
 #undef DV_SAMPLE_LAUNCH
-    if (g.nchunks > 1)
-        sample_finalize_kernel<<<(B + kThreads - 1) / kThreads, kThreads, 0, stream>>>(next_state, S, V, states, B,
-                                                                                      g.nchunks, partial, token,
-                                                                                      new_state);
     return hipGetLastError();
 }
 

@@ -55,14 +55,14 @@ __global__ __launch_bounds__(kSpecThreads) void spec_chain_kernel(
 // is -1) ends the row; its choice is the model's own token.
 __global__ __launch_bounds__(kSpecThreads) void spec_accept_kernel(
     const int32_t *__restrict__ token, const int32_t *__restrict__ proposals, int s, int64_t ld_prop, int B,
-    const int32_t *__restrict__ pos_new, int32_t *__restrict__ accepted, int32_t *__restrict__ new_state)
+    int32_t *__restrict__ pos_new, int32_t *__restrict__ accepted, int32_t *__restrict__ new_state)
 {
     const int b = blockIdx.x * kSpecThreads + threadIdx.x;
     if (b >= B)
         return;
     const int32_t *prop = proposals + (size_t)b * (size_t)ld_prop;
     const int32_t *tok = token + (size_t)b * (size_t)(s + 1);
-    const int32_t *pn = pos_new + (size_t)b * (size_t)(s + 1);
+    int32_t *pn = pos_new + (size_t)b * (size_t)(s + 1);
     // no early exit, and every position's state read alongside its token:
     // the loads of several positions are in flight together, in one round
     // trip instead of one per position
@@ -77,6 +77,10 @@ __global__ __launch_bounds__(kSpecThreads) void spec_accept_kernel(
     }
     accepted[b] = a;
     new_state[b] = ns;
+    // the workspace is handed back all zero, like the step's part of it
+#pragma unroll 8
+    for (int j = 0; j <= s; ++j)
+        pn[j] = 0;
 }
 
 unsigned lanes_grid(int B) { return (unsigned)((B + kSpecThreads - 1) / kSpecThreads); }
@@ -100,11 +104,11 @@ hipError_t launch_spec_verify(const int32_t *next_state, const uint32_t *allow, 
 {
     char *ws = static_cast<char *>(workspace);
     int32_t *pos_new = reinterpret_cast<int32_t *>(ws);
-    void *partial = ws + spec_partial_offset(B, s);
+    void *meet = ws + spec_partial_offset(B, s);  // the step's meeting slots for R rows
     const int R = (int)spec_positions(B, s);
     const RowMap map{ld_row, ld_pos, s + 1, proposals, ld_prop};
     hipError_t e = launch_masked_rows(next_state, allow, S, V, states, logits, dtype, R, map, token, pos_new,
-                                      partial, stream);
+                                      meet, stream);
     if (e != hipSuccess)
         return e;
     spec_accept_kernel<<<lanes_grid(B), kSpecThreads, 0, stream>>>(token, proposals, s, ld_prop, B, pos_new,

@@ -234,8 +234,7 @@ template <int THREADS, int U>
 __global__ __launch_bounds__(THREADS) void masked_step_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
     const int32_t *__restrict__ states, const void *__restrict__ logits, RowMap map, int chunk_vec,
-    int nchunks, int32_t *__restrict__ token, int32_t *__restrict__ new_state,
-    uint64_t *__restrict__ partial)
+    int nchunks, int32_t *__restrict__ token, int32_t *__restrict__ new_state, RowMeet meet)
 {
     const int b = blockIdx.x / nchunks;
     const int c = blockIdx.x - b * nchunks;
@@ -257,13 +256,11 @@ __global__ __launch_bounds__(THREADS) void masked_step_kernel(
         if (c == nchunks - 1)
             scan_exact<0, THREADS>(row, arow, head + nvec * 4, V, best_key, best_idx);
     }
-    const uint64_t best = block_max<THREADS>(pack(best_key, best_idx));
+    uint64_t best = block_max<THREADS>(pack(best_key, best_idx));
     if (threadIdx.x != 0)
         return;
-    if (nchunks > 1) {
-        partial[blockIdx.x] = best;
-        return;
-    }
+    if (nchunks > 1 && !meet_row(meet, b, nchunks, best, best))
+        return;  // another block of the row finishes it
     const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
     const bool found = tok >= 0 && tok < V;  // always true for a found token; guards the read
     token[b] = found ? tok : -1;
@@ -628,8 +625,7 @@ template <int THREADS, int U, bool ANY_ALIGN, bool SELECT>
 __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
     const int32_t *__restrict__ states, const void *__restrict__ logits, RowMap map, int chunk_vec,
-    int nchunks, int32_t *__restrict__ token, int32_t *__restrict__ new_state,
-    uint64_t *__restrict__ partial)
+    int nchunks, int32_t *__restrict__ token, int32_t *__restrict__ new_state, RowMeet meet)
 {
     extern __shared__ uint32_t staged[];  // the chunk's mask words
     __shared__ uint4 lut[256];
@@ -687,12 +683,15 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
                 c == 0, c == nchunks - 1, V, lut, da, db, vec_pack, vec_ns);
     }
     int ns;
-    const uint64_t best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
+    uint64_t best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
     if (threadIdx.x != 0)
         return;
     if (nchunks > 1) {
-        partial[blockIdx.x] = best;
-        return;
+        const uint64_t own = best;
+        if (!meet_row(meet, b, nchunks, own, best))
+            return;  // another block of the row finishes it
+        if (best != own)
+            ns = kNsUnknown;  // another block's token: its next state is read below
     }
     const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
     const bool found = tok >= 0 && tok < V;  // always true for a found token; guards the read
@@ -752,30 +751,6 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
     const bool found = live && tok >= 0 && tok < V;  // guards the read
     token[b] = found ? tok : -1;
     new_state[b] = !found ? -1 : ns != kNsUnknown ? ns : next_state[(size_t)s * V + tok];
-}
-
-// One lane per row: combine the row's chunk results and write the outputs.
-__global__ __launch_bounds__(kSmallThreads) void finalize_kernel(const int32_t *__restrict__ next_state,
-                                                           const uint32_t *__restrict__ allow, int S,
-                                                           int V, const int32_t *__restrict__ states,
-                                                           RowMap map, int B, int nchunks,
-                                                           const uint64_t *__restrict__ partial,
-                                                           int32_t *__restrict__ token,
-                                                           int32_t *__restrict__ new_state)
-{
-    const int b = blockIdx.x * kSmallThreads + threadIdx.x;
-    if (b >= B)
-        return;
-    uint64_t best = 0;
-    for (int c = 0; c < nchunks; ++c) {
-        const uint64_t p = partial[(size_t)b * nchunks + c];
-        best = p > best ? p : best;
-    }
-    const int s = row_state(states, map, next_state, allow, S, V, b);
-    const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
-    const bool found = tok >= 0 && tok < V && (uint32_t)s < (uint32_t)S;  // guards the read
-    token[b] = found ? tok : -1;
-    new_state[b] = found ? next_state[(size_t)s * V + tok] : -1;
 }
 
 }  // namespace
@@ -845,17 +820,17 @@ hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, 
 {
     const int W = (V + 31) / 32;
     const StepGeometry g = step_geometry(B, V, dtype);
-    uint64_t *partial = static_cast<uint64_t *>(workspace);
+    const RowMeet meet = row_meet(workspace, B);
     const unsigned grid = (unsigned)B * (unsigned)g.nchunks;
     if (dtype == 0)
         masked_step_kernel<kSmallThreads, kSmallU><<<grid, kSmallThreads, 0, stream>>>(
-            next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial);
+            next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, meet);
     else {
         const bool aligned = map.rows_aligned(logits, 2), select = skip_unread_lines(grid);
         const size_t lds = select ? staged_mask_bytes(g.chunk_vec) : 0;
 #define DV_STEP_BF16(A, SEL)                                                                                   \
     masked_step_bf16_kernel<kBigThreads, kBigU, A, SEL><<<grid, kBigThreads, lds, stream>>>(                  \
-        next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, partial)
+        next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, meet)
         if (aligned && select)
             DV_STEP_BF16(false, true);
         else if (aligned)
@@ -866,9 +841,6 @@ hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, 
             DV_STEP_BF16(true, false);
 #undef DV_STEP_BF16
     }
-    if (g.nchunks > 1)
-        finalize_kernel<<<(B + kSmallThreads - 1) / kSmallThreads, kSmallThreads, 0, stream>>>(
-            next_state, allow, S, V, states, map, B, g.nchunks, partial, token, new_state);
     return hipGetLastError();
 }
 

@@ -475,6 +475,48 @@ def test_step_workspace_reuse_and_determinism(dv):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_split_rows_leave_the_workspace_zero(dv, dtype):
+    """Rows split over several blocks meet in the workspace; the block that
+    arrives last puts the row's entries back to zero.  After split-row calls
+    of every kind (greedy, sampled, speculative, all sizes) the shared
+    workspace is all zero again, and each call matches the oracle."""
+    rng = np.random.default_rng(5)
+    S, Vmax = 6, 70001
+    ws = torch.zeros(max(dv.spec_verify_workspace_bytes(64, 4, Vmax), dv.masked_step_workspace_bytes(64, Vmax),
+                         dv.masked_sample_workspace_bytes(64, Vmax)), dtype=torch.uint8, device=DEV)
+    for B, V in ((1, 70001), (7, 40000), (64, 4099), (3, 70001)):
+        _say(f"split rows B={B} V={V} {dtype}")
+        alive = rng.random((S, V)) < np.array([0.001, 0.02, 0.3, 1.0, 0.5, 0.0])[:, None]
+        ns = np.where(alive, rng.integers(0, S, (S, V)), -1).astype(np.int32)
+        Wd = (V + 31) // 32
+        pad = np.zeros((S, Wd * 32), bool)
+        pad[:, :V] = alive
+        al = np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(S, Wd)
+        states = rng.integers(-1, S, B).astype(np.int32)
+        x = torch.from_numpy(rng.integers(-4, 5, (B, V)).astype(np.float32)).to(dtype).to(DEV)
+        xo = to_oracle(x)
+        nsd, ald = _dev(ns), _dev(al.view(np.int32))
+        tok, new = dv.masked_step(nsd, ald, _dev(states), x, workspace=ws)
+        t_o, n_o = oracle.masked_step(ns, al, states, xo)
+        np.testing.assert_array_equal(tok.cpu().numpy(), t_o)
+        np.testing.assert_array_equal(new.cpu().numpy(), n_o)
+        assert int(ws.count_nonzero()) == 0
+        tok, new = dv.masked_sample(nsd, ald, _dev(states), x, 11, B, workspace=ws)
+        t_o, n_o = oracle.masked_sample(ns, al, states, xo, 1.0, 11, B)
+        np.testing.assert_array_equal(tok.cpu().numpy(), t_o)
+        np.testing.assert_array_equal(new.cpu().numpy(), n_o)
+        assert int(ws.count_nonzero()) == 0
+        props = rng.integers(0, V, (B, 4)).astype(np.int32)
+        lg = torch.from_numpy(rng.integers(-4, 5, (B, 5, V)).astype(np.float32)).to(dtype).to(DEV)
+        t, a, n = dv.spec_verify(nsd, ald, _dev(states), _dev(props), lg, workspace=ws)
+        t_o, a_o, n_o = oracle.spec_verify(ns, al, states, props, to_oracle(lg))
+        np.testing.assert_array_equal(t.cpu().numpy(), t_o)
+        np.testing.assert_array_equal(a.cpu().numpy(), a_o)
+        np.testing.assert_array_equal(n.cpu().numpy(), n_o)
+        assert int(ws.count_nonzero()) == 0
+
+
 def test_step_rejects_in_place_update(dv):
     ns = torch.zeros((2, 10), dtype=torch.int32, device=DEV)
     al = torch.zeros((2, 1), dtype=torch.int32, device=DEV)
