@@ -144,11 +144,9 @@ __device__ __forceinline__ bool meet_row(RowMeet m, int b, int nchunks, uint64_t
 //
 // A row of V logits is split into `nchunks` chunks of `chunk_vec` 16-byte
 // vectors, one block of `threads` lanes each; with more than one chunk the
-// blocks meet in the workspace (above).  bf16 rows use 512-lane blocks and
-// aim for kStepOneBlockRows blocks per launch (one block per row once
-// B >= 256).
-constexpr int kStepTargetBlocks = 2048;
-constexpr int kStepMaxChunks = 64;
+// blocks meet in the workspace (above).  bf16 rows use 512-lane blocks, one
+// per row once B >= kStepOneBlockRows; below that, about 32 / sqrt(B) chunks
+// per row (step_geometry).
 constexpr int kStepOneBlockRows = 256;
 
 struct StepGeometry {

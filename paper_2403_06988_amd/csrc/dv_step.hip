@@ -764,29 +764,36 @@ StepGeometry step_geometry(int B, int V, int dtype)
     const int vec = dtype == 0 ? Elt<0>::kVec : Elt<1>::kVec;
     const bool bf16 = dtype == 1;
     const int threads = bf16 ? kBigThreads : kSmallThreads;
-    // A bf16 row this short is read by one block in a batch or two: splitting
-    // it would cost a second launch (about 4 us) to save less than that.
-    if (bf16 && (int64_t)V * 2 <= DV_STEP_SINGLE_BLOCK_ROW_BYTES) {
-        const int nvec = V / vec;
-        int chunk_vec = (nvec + threads - 1) / threads * threads;
-        return {chunk_vec > 0 ? chunk_vec : threads, 1, threads};
-    }
-    static_assert(kMaxChunkVec % kBigThreads == 0, "chunks are whole batches of lanes");
-    const int target = bf16 ? kStepOneBlockRows : kStepTargetBlocks;
     const int nvec = V / vec;
-    // about `target` blocks, at least one vector per lane per chunk
-    const int max_chunks = (nvec + threads - 1) / threads;
-    int want = (target + B - 1) / (B > 0 ? B : 1);
+    static_assert(kMaxChunkVec % kBigThreads == 0, "chunks are whole batches of lanes");
+    int want;
+    if (bf16 && B >= kStepOneBlockRows) {
+        want = 1;  // a block per compute unit already
+    } else if (bf16 && B >= 64 && (int64_t)V * 2 <= DV_STEP_SINGLE_BLOCK_ROW_BYTES) {
+        want = 1;  // short rows: a second block per row buys nothing at this batch
+    } else {
+        // Chunks per row ~ 32 / sqrt(B): about 32 sqrt(B) blocks per launch
+        // (at most 256).  Since split rows meet in the workspace instead of a
+        // second kernel, this is what measures fastest from B = 1 to 128 at
+        // V = 32000 .. 256000: fewer blocks leave bandwidth unused, more
+        // make each block's stream too short for its fixed start-up cost.
+        int r = 1;
+        while (r * r < B)
+            ++r;  // ceil(sqrt(B))
+        const int blocks = 32 * r < 256 ? 32 * r : 256;
+        want = (blocks + B / 2) / (B > 0 ? B : 1);
+    }
+    // at least one vector per lane per chunk
+    const int max_chunks = nvec / threads > 1 ? nvec / threads : 1;
     want = want > max_chunks ? max_chunks : want;
-    want = want > kStepMaxChunks ? kStepMaxChunks : want;
-    int nchunks = want < 1 ? 1 : want;
-    int chunk_vec = (nvec + nchunks - 1) / nchunks;
+    want = want < 1 ? 1 : want;
+    int chunk_vec = (nvec + want - 1) / want;
     chunk_vec = (chunk_vec + threads - 1) / threads * threads;
     if (chunk_vec == 0)
         chunk_vec = threads;
     if (bf16 && chunk_vec > kMaxChunkVec)  // the staged mask bytes must fit
         chunk_vec = kMaxChunkVec;
-    nchunks = (nvec + chunk_vec - 1) / chunk_vec;
+    int nchunks = (nvec + chunk_vec - 1) / chunk_vec;
     if (nchunks < 1)
         nchunks = 1;
     return {chunk_vec, nchunks, threads};
