@@ -517,6 +517,41 @@ def test_split_rows_leave_the_workspace_zero(dv, dtype):
         assert int(ws.count_nonzero()) == 0
 
 
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_step_and_sample_at_the_largest_vocabulary(dv, dtype):
+    """V = 2^24 (the largest vocabulary the library accepts): rows split into
+    more chunks than at any workload (the chunk size cap for the staged mask
+    bytes applies), so many blocks meet on one row.  Greedy and sampled
+    steps against the oracle; one planted maximum near the end of the row."""
+    V, B, S = 1 << 24, 2, 2
+    _say(f"largest vocabulary V={V} B={B} {dtype}")
+    rng = np.random.default_rng(24)
+    Wd = V // 32
+    al = np.zeros((S, Wd), np.uint32)
+    al[0] = rng.integers(0, 1 << 32, Wd, dtype=np.uint64).astype(np.uint32) & 0x01010101   # sparse
+    al[1] = 0xFFFFFFFF
+    alive = np.unpackbits(al.view(np.uint8), axis=1, bitorder="little").astype(bool)
+    ns = np.where(alive, (np.arange(V) % S)[None, :], -1).astype(np.int32)
+    del alive
+    states = np.array([0, 1], np.int32)
+    x = torch.from_numpy(rng.integers(-8, 9, (B, V)).astype(np.float32))
+    x[0, V - 9] = 100.0   # allowed in state 0 or not: the oracle decides
+    x[1, V - 3] = 100.0   # state 1 allows every token: this one wins
+    x = x.to(dtype)
+    xd = x.to(DEV)
+    xo = to_oracle(x)
+    nsd, ald = _dev(ns), _dev(al.view(np.int32))
+    tok, new = dv.masked_step(nsd, ald, _dev(states), xd)
+    t_o, n_o = oracle.masked_step(ns, al, states, xo)
+    np.testing.assert_array_equal(tok.cpu().numpy(), t_o)
+    np.testing.assert_array_equal(new.cpu().numpy(), n_o)
+    assert int(t_o[1]) == V - 3
+    tok, new = dv.masked_sample(nsd, ald, _dev(states), xd, 3, 9)
+    t_o, n_o = oracle.masked_sample(ns, al, states, xo, 1.0, 3, 9)
+    np.testing.assert_array_equal(tok.cpu().numpy(), t_o)
+    np.testing.assert_array_equal(new.cpu().numpy(), n_o)
+
+
 def test_step_rejects_in_place_update(dv):
     ns = torch.zeros((2, 10), dtype=torch.int32, device=DEV)
     al = torch.zeros((2, 1), dtype=torch.int32, device=DEV)
