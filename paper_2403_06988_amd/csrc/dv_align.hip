@@ -13,17 +13,19 @@
 //      Random printable-ASCII DFAs keep ~95 of 256 columns, so the table is
 //      ~2.7x smaller than the int32 input and stays resident in each XCD's L2.
 //   4. token_info: each token's first 8 byte classes, length and offset.
-//   5. walk: one lane per (state, token) pair.  A block owns a tile of 32
-//      states x 1024 tokens (4 tokens per lane).  The byte classes of each
-//      token's first 8 bytes are looked up once per block and kept in
-//      registers, so a move costs one table read.  The table lives in LDS:
-//      the whole table when it fits, otherwise the block's 32 rows, which
-//      serve every walk's first move (every pair takes one); later moves
-//      (about half the pairs survive each byte) read the L2-resident table
-//      with 32-bit offsets.  A lane's 4 walks advance in lock-step for
-//      memory-level parallelism and the wave stops as soon as every walk in
-//      it has ended.  Stores are coalesced along tokens; the allow words come
-//      from a wave ballot (64 tokens -> 2 words).
+//   5. walk: one lane per token, over a tile of 16 states x 256 tokens per
+//      block.  The byte classes of each token's first 8 bytes are looked up
+//      once per block and kept in registers, so a move costs one table
+//      read.  The table lives in LDS: the whole table when it fits,
+//      otherwise the block's 16 rows, which serve every walk's first move
+//      (every pair takes one); later moves (about one per pair) read the
+//      cache-resident table with 32-bit offsets, each lane walking its
+//      token's pending states one after the other, and the wave stops as
+//      soon as every walk in it has ended.  One token per lane keeps the
+//      block's LDS small (more resident blocks hide the gathers' latency
+//      better than a second token per lane does).  Stores are coalesced
+//      along tokens; the allow words come from a wave ballot (64 tokens ->
+//      2 words).
 #include "dv_internal.h"
 
 namespace dv {
@@ -33,7 +35,7 @@ namespace {
 #define DV_ALIGN_STATE_TILE 16
 #endif
 #ifndef DV_ALIGN_TOK_PER_LANE
-#define DV_ALIGN_TOK_PER_LANE 2
+#define DV_ALIGN_TOK_PER_LANE 1
 #endif
 
 constexpr int kThreads = 256;
