@@ -60,6 +60,7 @@ def build(force: bool = False, out: str | None = None, defines: tuple = ()) -> s
 _i32p = ctypes.POINTER(ctypes.c_int32)
 _u32p = ctypes.POINTER(ctypes.c_uint32)
 _u8p = ctypes.POINTER(ctypes.c_uint8)
+_i64p = ctypes.POINTER(ctypes.c_int64)
 
 
 def _bind(lib):
@@ -106,6 +107,9 @@ def _bind(lib):
     lib.oracle_walk_lookups.restype = ctypes.c_int64
     lib.oracle_walk_lookups.argtypes = [_i32p, ctypes.c_int32, _i32p, _u8p, ctypes.c_int32,
                                         _i32p, ctypes.c_int64]
+    lib.oracle_walk_length_hist.restype = None
+    lib.oracle_walk_length_hist.argtypes = [_i32p, ctypes.c_int32, _i32p, _u8p, ctypes.c_int32,
+                                            _i32p, ctypes.c_int64, _i64p, ctypes.c_int32]
     return lib
 
 
@@ -350,6 +354,21 @@ def walk_lookups(trans, offsets, tok_bytes, rows, lib=None) -> int:
     return int(lib.oracle_walk_lookups(_p(trans, _i32p), trans.shape[0], _p(offsets, _i32p),
                                        _p(tok_bytes, _u8p), offsets.shape[0] - 1,
                                        _p(rows, _i32p), rows.shape[0]))
+
+
+def walk_length_hist(trans, offsets, tok_bytes, rows, lib=None) -> np.ndarray:
+    """hist[k] = number of (row state, token) walks taking exactly k DFA
+    transitions before they end or die; k runs to the longest token."""
+    lib = lib or load()
+    trans = _c(trans, np.int32)
+    offsets = _c(offsets, np.int32)
+    tok_bytes = _c(tok_bytes if len(tok_bytes) else np.zeros(1, np.uint8), np.uint8)
+    rows = _c(rows, np.int32)
+    max_len = int(np.diff(offsets).max()) if offsets.shape[0] > 1 else 0
+    hist = np.zeros(max_len + 1, np.int64)
+    lib.oracle_walk_length_hist(_p(trans, _i32p), trans.shape[0], _p(offsets, _i32p), _p(tok_bytes, _u8p),
+                                offsets.shape[0] - 1, _p(rows, _i32p), rows.shape[0], _p(hist, _i64p), max_len)
+    return hist
 
 
 class RowCache:

@@ -199,6 +199,32 @@ int64_t oracle_walk_lookups(const int32_t *trans, int32_t num_states,
     return total;
 }
 
+/* Histogram of walk lengths: hist[k] counts the (row state, token) walks
+ * that take exactly k transitions before they end or die (k >= max_len
+ * counts in hist[max_len]).  From it, the lookups past a given depth d are
+ * the sum over k of hist[k] * max(k - d, 0). */
+void oracle_walk_length_hist(const int32_t *trans, int32_t num_states,
+                             const int32_t *offsets, const uint8_t *bytes,
+                             int32_t num_tokens, const int32_t *rows, int64_t nrows,
+                             int64_t *hist, int32_t max_len)
+{
+    for (int32_t k = 0; k <= max_len; ++k)
+        hist[k] = 0;
+    for (int64_t r = 0; r < nrows; ++r) {
+        for (int32_t t = 0; t < num_tokens; ++t) {
+            int32_t st = oracle_canon(rows[r], num_states);
+            int64_t n = 0;
+            for (int64_t i = offsets[t]; i < offsets[t + 1]; ++i) {
+                if (st == ORACLE_DEAD)
+                    break;
+                st = oracle_canon(trans[(int64_t)st * 256 + bytes[i]], num_states);
+                ++n;
+            }
+            hist[n < max_len ? n : max_len] += 1;
+        }
+    }
+}
+
 /* Whether proposal t may follow state s (a live state, t a token id whose
  * allow bit is set): the mask of Algorithm 1 applied to a proposed token. */
 static int oracle_legal(const uint32_t *allow, int32_t num_states, int32_t num_tokens,

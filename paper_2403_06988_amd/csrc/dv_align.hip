@@ -13,7 +13,10 @@
 //      Random printable-ASCII DFAs keep ~95 of 256 columns, so the table is
 //      ~2.7x smaller than the int32 input and stays resident in each XCD's L2.
 //   4. token_info: each token's first 8 byte classes, length and offset.
-//   5. walk: one lane per token, over a tile of 16 states x 256 tokens per
+//   5. walk (tables of at most 98 columns that do not fit in LDS whole, e.g.
+//      random printable-ASCII DFAs of more than ~330 states): the prefix-table
+//      walk, kernel 6 below.  Otherwise:
+//      one lane per token, over a tile of 16 states x 256 tokens per
 //      block.  The byte classes of each token's first 8 bytes are looked up
 //      once per block and kept in registers, so a move costs one table
 //      read.  The table lives in LDS: the whole table when it fits,
@@ -48,6 +51,35 @@ constexpr int kResLds = kStateTile * kTokTile * 2;
 constexpr int kWholeLdsMax = 64 * 1024;           // LDS budget for a whole table
 static_assert(kStateTile >= 1 && kStateTile <= 32, "pending set is 32 bits");
 constexpr int kLiveRows = kLiveRowsPerBlock;
+
+// the prefix-table walk: states per block, tokens per lane and chunk, block
+// size, and the largest column count whose per-state table [Cp][Cp] uint16
+// (19.2 KB at 98 columns: printable ASCII, tab, newline and the dead class)
+// it takes.  Three states (57 KB of LDS) leave room for two 1024-lane blocks
+// per compute unit; measured against two and four states, and against two
+// tokens per lane.
+#ifndef DV_ALIGN_PREFIX_R
+#define DV_ALIGN_PREFIX_R 3
+#endif
+#ifndef DV_ALIGN_PREFIX_K
+#define DV_ALIGN_PREFIX_K 1
+#endif
+#ifndef DV_ALIGN_PREFIX_THREADS
+#define DV_ALIGN_PREFIX_THREADS 1024
+#endif
+constexpr int kPrefR = DV_ALIGN_PREFIX_R;
+constexpr int kPrefK = DV_ALIGN_PREFIX_K;
+constexpr int kPrefThreads = DV_ALIGN_PREFIX_THREADS;
+#ifndef DV_ALIGN_PREFIX_MAX_CP
+#define DV_ALIGN_PREFIX_MAX_CP 98
+#endif
+constexpr int kPrefixMaxCp = DV_ALIGN_PREFIX_MAX_CP;
+constexpr int kPrefStride = kPrefixMaxCp * kPrefixMaxCp + kPrefixMaxCp;  // entries per state
+constexpr int kPrefLds = 256 + kPrefR * kPrefStride * 2;
+constexpr int kPrefTargetBlocks = 2048;  // four rounds of two resident blocks per compute unit
+constexpr int kTileDeferGrid = 8192;
+static_assert(kPrefR >= 1 && 2 * kPrefLds <= 160 * 1024, "two blocks per compute unit");
+static_assert(kPrefThreads >= 256, "one byte class per thread in the first 256");
 
 // token lengths with a special meaning in the walk
 constexpr int kPastEnd = -1;  // a lane slot past the last token: never stored
@@ -312,7 +344,7 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
                                                         const uint16_t *__restrict__ table, int S,
                                                         const uint4 *__restrict__ tokinfo,
                                                         const uint8_t *__restrict__ bytes, int V,
-                                                        int W, int lds_table_bytes,
+                                                        int W, int lds_table_bytes, int defer,
                                                         const uint8_t *__restrict__ accepting,
                                                         int32_t *__restrict__ next_state,
                                                         uint32_t *__restrict__ allow)
@@ -324,27 +356,200 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
 
     const int tid = threadIdx.x;
     const int Cp = reinterpret_cast<const int32_t *>(ws)[1];
-    const int s0 = blockIdx.y * kStateTile;
-    const int nS = min(kStateTile, S - s0);
-    const int t_base = blockIdx.x * kTokTile;
     const bool whole = (size_t)S * Cp * 2 <= (size_t)lds_table_bytes;
+    if (defer && !whole && Cp <= kPrefixMaxCp)
+        return;  // the prefix-table walk owns this table
+    const int ntx = (V + kTokTile - 1) / kTokTile;
+    const int ntiles = ntx * ((S + kStateTile - 1) / kStateTile);
 
     cls[tid] = ws[256 + tid];
-    {
-        const int n32 = (whole ? S : nS) * Cp / 2;  // Cp is even
-        const uint32_t *src = reinterpret_cast<const uint32_t *>(whole ? table : table + (size_t)s0 * Cp);
+    if (whole) {
+        const int n32 = S * Cp / 2;  // Cp is even
+        const uint32_t *src = reinterpret_cast<const uint32_t *>(table);
         uint32_t *dst = reinterpret_cast<uint32_t *>(tab);
         for (int i = tid; i < n32; i += kThreads)
             dst[i] = src[i];
     }
+    // a grid smaller than the tile count (launched beside the prefix-table
+    // walk, so that it exits cheaply when that one owns the table) strides
+    for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int s0 = (tile / ntx) * kStateTile;
+        const int nS = min(kStateTile, S - s0);
+        const int t_base = (tile % ntx) * kTokTile;
+        if (!whole) {
+            if (tile != (int)blockIdx.x)
+                __syncthreads();  // the previous tile's rows are no longer read
+            const int n32 = nS * Cp / 2;
+            const uint32_t *src = reinterpret_cast<const uint32_t *>(table + (size_t)s0 * Cp);
+            uint32_t *dst = reinterpret_cast<uint32_t *>(tab);
+            for (int i = tid; i < n32; i += kThreads)
+                dst[i] = src[i];
+        }
+        __syncthreads();
+        if (whole)
+            walk_tile<true>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state,
+                            allow);
+        else
+            walk_tile<false>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state,
+                             allow);
+    }
+}
+
+// 6. the prefix-table walk, for tables of at most kPrefixMaxCp columns that
+// do not fit in LDS whole.  A block owns kPrefR states and a range of tokens.
+// It first builds, per state s, the table P_s[c0][c1] = state after the byte
+// classes c0 c1 from s (the rows of the states one move from s, copied from
+// the compacted table: coalesced reads) followed by s's own row, so that the
+// first two moves of every pair are one LDS read; only walks still live
+// after two bytes (about a fifth of the pairs for random printable DFAs)
+// read the cache-resident table.  The walk is bound by instruction issue
+// and L1 accesses, so the later moves run in lockstep: a lane walks its
+// token from all the block's states at once, one byte per iteration; the
+// byte class, doubled to a byte offset, is shifted out of a 64-bit register
+// and shared by the states; each live state costs one compare, one
+// multiply-add and one table read at a 32-bit offset, and a dead one skips
+// its read under the exec mask (reading an all-DEAD row instead costs an L1
+// access per lane); the lane stops when every state is dead or the token
+// ends.  Tokens take turns wave-wide (kPrefK per lane per chunk, strided by
+// the block size), so the results stay in registers until the chunk's
+// coalesced stores; a compare per result gives both the stored value and,
+// as a wave mask, the allow bits.
+__global__ __launch_bounds__(kPrefThreads) void walk_prefix_kernel(
+    const uint8_t *__restrict__ ws, const uint16_t *__restrict__ table, int S, const uint4 *__restrict__ tokinfo,
+    const uint8_t *__restrict__ bytes, int V, int W, int lds_table_bytes, int range,
+    const uint8_t *__restrict__ accepting, int32_t *__restrict__ next_state, uint32_t *__restrict__ allow)
+{
+    extern __shared__ __align__(16) uint8_t smem[];
+    const int Cp = reinterpret_cast<const int32_t *>(ws)[1];
+    if (Cp > kPrefixMaxCp || (size_t)S * Cp * 2 <= (size_t)lds_table_bytes)
+        return;  // the tile walk owns this table
+    uint8_t *cls = smem;                                     // [256]
+    uint16_t *pt = reinterpret_cast<uint16_t *>(smem + 256);  // [kPrefR][kPrefStride]: P_s, then s's row
+    const int CC = Cp * Cp;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1), wave = tid / kWave;
+    const int s0 = blockIdx.y * kPrefR;
+    const int nS = min(kPrefR, S - s0);
+    const int t_lo = blockIdx.x * range;
+    const int t_hi = min(V, t_lo + range);
+
+    if (tid < 256)
+        cls[tid] = ws[256 + tid];
+    for (int i = tid; i < kPrefR * Cp; i += kPrefThreads) {
+        const int si = i / Cp, c = i - si * Cp;
+        pt[si * kPrefStride + CC + c] = si < nS ? table[(size_t)(s0 + si) * Cp + c] : kDead16;
+    }
+    __syncthreads();
+    for (int row = wave; row < kPrefR * Cp; row += kPrefThreads / kWave) {
+        const int si = row / Cp, c0 = row - si * Cp;
+        const uint32_t f = pt[si * kPrefStride + CC + c0];
+        const bool live = f != kDead16;
+        uint16_t *dst = pt + si * kPrefStride + c0 * Cp;
+        const uint16_t *src = table + (size_t)(live ? f : 0u) * Cp;  // row 0 stands in for DEAD
+        for (int c = lane; c < Cp; c += kWave) {
+            const uint16_t v = src[c];
+            dst[c] = live ? v : kDead16;
+        }
+    }
     __syncthreads();
 
-    if (whole)
-        walk_tile<true>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state,
-                        allow);
-    else
-        walk_tile<false>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state,
-                         allow);
+    uint32_t acc_bits = 0;  // accepting flags of the block's states
+#pragma unroll
+    for (int si = 0; si < kPrefR; ++si)
+        if (si < nS && accepting != nullptr && accepting[s0 + si] != 0)
+            acc_bits |= 1u << si;
+    const char *tab_bytes = reinterpret_cast<const char *>(table);
+    const uint32_t Cp2 = 2u * (uint32_t)Cp;  // row stride in bytes
+
+    for (int base = t_lo; base < t_hi; base += kPrefThreads * kPrefK) {
+        uint32_t tx[kPrefK], ty[kPrefK], off[kPrefK];
+        int len[kPrefK];
+        uint32_t st[kPrefR][kPrefK];
+        bool special = false;
+#pragma unroll
+        for (int j = 0; j < kPrefK; ++j) {
+            const int t = base + j * kPrefThreads + tid;
+            const uint4 ti = t < t_hi ? tokinfo[t] : make_uint4(0, 0, (uint32_t)kPastEnd, 0);
+            tx[j] = ti.x;
+            ty[j] = ti.y;
+            len[j] = (int)ti.z;
+            off[j] = ti.w;
+            special |= len[j] <= 0;
+            const uint32_t c0 = ti.x & 0xFFu, c1 = (ti.x >> 8) & 0xFFu;
+            const uint32_t idx = len[j] >= 2 ? c0 * (uint32_t)Cp + c1 : (uint32_t)CC + c0;
+            // the first two moves of every pair: one LDS read
+#pragma unroll
+            for (int si = 0; si < kPrefR; ++si)
+                st[si][j] = pt[si * kPrefStride + idx];
+        }
+        if (__any(special)) {  // empty, EOS and past-the-end tokens
+#pragma unroll
+            for (int j = 0; j < kPrefK; ++j)
+#pragma unroll
+                for (int si = 0; si < kPrefR; ++si)
+                    if (len[j] <= 0) {
+                        const bool keep = si < nS && (len[j] == 0 || (len[j] == kEosLen && ((acc_bits >> si) & 1u)));
+                        st[si][j] = keep ? (uint32_t)(s0 + si) : kDead16;  // EOS: where the scanner may stop
+                    }
+        }
+
+        // the later moves, token by token, every state in lockstep
+#pragma unroll
+        for (int j = 0; j < kPrefK; ++j) {
+            uint32_t m = st[0][j];
+#pragma unroll
+            for (int si = 1; si < kPrefR; ++si)
+                m = min(m, st[si][j]);
+            bool go = m != kDead16 && len[j] > 2;
+            if (!__any(go))
+                continue;
+            uint64_t crem = (((uint64_t)ty[j] << 16) | (tx[j] >> 16)) << 1;  // classes 2..7, doubled
+            uint32_t h = 2;
+            while (go) {
+                uint32_t c2;
+                if (h < (uint32_t)kRegBytes) {
+                    c2 = (uint32_t)crem & 0xFFu;
+                    crem >>= 8;
+                } else {
+                    c2 = 2u * cls[bytes[off[j] + h]];
+                }
+#pragma unroll
+                for (int si = 0; si < kPrefR; ++si)
+                    if (st[si][j] != kDead16) {
+                        const uint32_t boff = __umul24(st[si][j], Cp2) + c2;  // < 2^24: S <= 65535, Cp <= 98
+                        st[si][j] = *reinterpret_cast<const uint16_t *>(tab_bytes + boff);
+                    }
+                h += 1;
+                m = st[0][j];
+#pragma unroll
+                for (int si = 1; si < kPrefR; ++si)
+                    m = min(m, st[si][j]);
+                go = m != kDead16 && h < (uint32_t)len[j];
+            }
+        }
+
+        // coalesced stores; the alive compare is also the wave's allow mask
+#pragma unroll
+        for (int j = 0; j < kPrefK; ++j) {
+            const int t = base + j * kPrefThreads + tid;
+            const bool in = t < t_hi;
+            const int t0 = base + j * kPrefThreads + wave * kWave;  // a multiple of 64
+            const int w = t0 / 32 + lane;
+#pragma unroll
+            for (int si = 0; si < kPrefR; ++si) {
+                if (si >= nS)
+                    break;
+                const uint32_t v = st[si][j];
+                const bool alive = v != kDead16;  // past-the-end slots are DEAD
+                if (in)
+                    next_state[(size_t)(s0 + si) * V + t] = alive ? (int32_t)v : -1;
+                const uint64_t m = __ballot(alive);
+                if (lane < 2 && t0 < t_hi && w < W)
+                    allow[(size_t)(s0 + si) * W + w] = (uint32_t)(m >> (32 * lane));
+            }
+        }
+    }
 }
 
 }  // namespace
@@ -379,15 +584,37 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
         256 + kWholeLdsMax + kResLds);
     if (lds_attr != hipSuccess)
         return lds_attr;
+    static const hipError_t prefix_lds_attr = hipFuncSetAttribute(
+        reinterpret_cast<const void *>(walk_prefix_kernel), hipFuncAttributeMaxDynamicSharedMemorySize, kPrefLds);
+    if (prefix_lds_attr != hipSuccess)
+        return prefix_lds_attr;
 
     live_columns_kernel<<<nblk, kThreads, 0, stream>>>(trans, S, partial);
     byte_classes_kernel<<<1, kThreads, 0, stream>>>(partial, nblk, ws);
     compact_kernel<<<(S + 15) / 16, kThreads, 0, stream>>>(trans, S, ws, table);
     token_info_kernel<<<(V + kThreads - 1) / kThreads, kThreads, 0, stream>>>(offsets, bytes, V, eos_token, ws,
                                                                               tokinfo);
-    dim3 grid((V + kTokTile - 1) / kTokTile, (S + kStateTile - 1) / kStateTile);
+    // Tables of at most kPrefixMaxCp columns that are not staged whole go to
+    // the prefix-table walk; the column count is known only on the device,
+    // so when such a table is possible both walks are launched and each
+    // block of the one that does not own the table exits at once (the tile
+    // walk then runs a strided grid of at most kTileDeferGrid blocks).
+    const bool prefix = (size_t)S * kPrefixMaxCp * 2 > (size_t)lds_table;
+    if (prefix) {
+        const int rows = (S + kPrefR - 1) / kPrefR;
+        const int chunk = kPrefThreads * kPrefK;
+        int nr = (kPrefTargetBlocks + rows - 1) / rows;
+        nr = max(1, min(nr, (V + chunk - 1) / chunk));
+        const int range = (int)align_up((size_t)((V + nr - 1) / nr), 64);  // whole allow-word pairs
+        nr = (V + range - 1) / range;
+        walk_prefix_kernel<<<dim3(nr, rows), kPrefThreads, kPrefLds, stream>>>(
+            ws, table, S, tokinfo, bytes, V, W, lds_table, range, accepting, next_state, allow);
+    }
+    const long long ntiles = (long long)((V + kTokTile - 1) / kTokTile) * ((S + kStateTile - 1) / kStateTile);
+    const int grid = (int)(prefix && ntiles > kTileDeferGrid ? kTileDeferGrid : ntiles);
     walk_kernel<<<grid, kThreads, 256 + lds_table + kResLds, stream>>>(ws, table, S, tokinfo, bytes, V, W,
-                                                                       lds_table, accepting, next_state, allow);
+                                                                       lds_table, prefix ? 1 : 0, accepting,
+                                                                       next_state, allow);
     return hipGetLastError();
 }
 

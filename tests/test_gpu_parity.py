@@ -104,10 +104,20 @@ def test_align_edge_shapes(dv, S, V, max_len, p_empty):
     (1025, 1500, 9, 0.0, 256, None),      # every byte live: Cp = 256
     (700, 4097, 40, 0.05, 100, 17),       # long tokens (bytes past the eighth), EOS column
     (600, 999, 2, 0.3, 126, 998),         # Cp = 128 (126 live classes + the dead class)
+    (700, 4097, 40, 0.05, 90, 17),        # prefix-table walk: long tokens, empty tokens, EOS
+    (900, 3000, 10, 0.01, 97, None),      # Cp = 98, the largest prefix table
+    (900, 3000, 10, 0.01, 98, 5),         # Cp = 100: the tile walk, beside an idle prefix walk
+    (600, 70000, 6, 0.0, 200, None),      # tile walk on a strided grid (more tiles than blocks)
+    (400, 140000, 5, 0.0, 30, None),      # whole table in LDS, strided grid
+    (400, 5000, 8, 0.0, 94, 4999),        # S <= 512 but too large whole: prefix walk, 3 token ranges
+    (65535, 300, 12, 0.02, 90, 7),        # the largest state count: prefix walk, sentinel row 0xFFFF
+    (65535, 300, 12, 0.0, 200, None),     # the largest state count: tile walk
 ])
 def test_align_large_dfa(dv, S, V, max_len, p_empty, alphabet, eos):
-    """DFAs above 512 states: the walk stages only its row tile in LDS and
-    reads later moves from the L2-resident table."""
+    """DFAs too large to stage whole in LDS: the prefix-table walk (tables of
+    at most 98 columns: the states two byte classes away come from LDS) or
+    the tile walk (its row tile in LDS), both reading later moves from the
+    L2-resident table; and the whole-table walk on a strided grid."""
     _say(f"align large S={S} V={V} max_len={max_len} alphabet={alphabet} eos={eos}")
     trans, offsets, data = _random_case(S * 7 + V, S, V, max_len, p_empty, alphabet=np.arange(alphabet))
     if eos is None:

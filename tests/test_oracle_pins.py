@@ -227,6 +227,42 @@ def test_walk_lookup_count_small_case(oracle_lib):
     assert oracle.walk_lookups(trans, offsets, data, np.array([0], np.int32), lib=oracle_lib) == 11
 
 
+def test_walk_length_histogram_small_case(oracle_lib):
+    g = _golden("fig_nfa_int.json")
+    trans = W.dfa_from_spec(len(g["states"]), g["moves"])
+    offsets, data = W.vocab_from_tokens([t.encode() for t in g["vocab"]])
+    hist = oracle.walk_length_hist(trans, offsets, data, np.array([0], np.int32), lib=oracle_lib)
+    # from state 0: 0 1 2 ) ( + one move each, +1 one (dies at '+'): seven
+    # walks of length 1; 12 and '1 (' two each
+    assert hist.tolist() == [0, 7, 2, 0]  # up to the longest token (3 bytes)
+    assert int((np.arange(len(hist)) * hist).sum()) == 11  # the lookup count above
+
+
+def test_walk_length_histogram_brute_force(oracle_lib):
+    rng = np.random.default_rng(21)
+    S = 9
+    trans = np.where(rng.random((S, 256)) < 0.5, rng.integers(0, S, (S, 256)), -1).astype(np.int32)
+    trans[:, :3] = rng.integers(-2, S + 2, (S, 3))  # out-of-range entries read as DEAD
+    toks = [bytes(rng.integers(0, 4, int(rng.integers(0, 7))).astype(np.uint8)) for _ in range(60)]
+    offsets, data = W.vocab_from_tokens(toks)
+    rows = np.array([0, 3, 8, 3], np.int32)
+    expect = np.zeros(7, np.int64)
+    for r in rows:
+        for tok in toks:
+            st, n = int(r), 0
+            for byte in tok:
+                if st == -1:
+                    break
+                nxt = int(trans[st, byte])
+                st = nxt if 0 <= nxt < S else -1
+                n += 1
+            expect[n] += 1
+    hist = oracle.walk_length_hist(trans, offsets, data, rows, lib=oracle_lib)
+    assert hist.tolist() == expect[:len(hist)].tolist() and expect[len(hist):].sum() == 0
+    assert int((np.arange(len(hist)) * hist).sum()) == oracle.walk_lookups(trans, offsets, data, rows,
+                                                                            lib=oracle_lib)
+
+
 # ------------------------------------------------------- P4 reductions to library calls
 
 def _reference_choice(x_f32, allowed):
