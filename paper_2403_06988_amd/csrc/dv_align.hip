@@ -52,30 +52,28 @@ constexpr int kWholeLdsMax = 64 * 1024;           // LDS budget for a whole tabl
 static_assert(kStateTile >= 1 && kStateTile <= 32, "pending set is 32 bits");
 constexpr int kLiveRows = kLiveRowsPerBlock;
 
-// the prefix-table walk: states per block, tokens per lane and chunk, block
-// size, and the largest column count whose per-state table [Cp][Cp] uint16
+// the prefix-table walk: states per block, block size, and the largest
+// column count whose per-state table [Cp][Cp] uint16
 // (19.2 KB at 98 columns: printable ASCII, tab, newline and the dead class)
 // it takes.  Three states (57 KB of LDS) leave room for two 1024-lane blocks
 // per compute unit; measured against two and four states, and against two
-// tokens per lane.
+// tokens per lane per round.
 #ifndef DV_ALIGN_PREFIX_R
 #define DV_ALIGN_PREFIX_R 3
-#endif
-#ifndef DV_ALIGN_PREFIX_K
-#define DV_ALIGN_PREFIX_K 1
 #endif
 #ifndef DV_ALIGN_PREFIX_THREADS
 #define DV_ALIGN_PREFIX_THREADS 1024
 #endif
 constexpr int kPrefR = DV_ALIGN_PREFIX_R;
-constexpr int kPrefK = DV_ALIGN_PREFIX_K;
 constexpr int kPrefThreads = DV_ALIGN_PREFIX_THREADS;
 #ifndef DV_ALIGN_PREFIX_MAX_CP
 #define DV_ALIGN_PREFIX_MAX_CP 98
 #endif
 constexpr int kPrefixMaxCp = DV_ALIGN_PREFIX_MAX_CP;
 constexpr int kPrefStride = kPrefixMaxCp * kPrefixMaxCp + kPrefixMaxCp;  // entries per state
-constexpr int kPrefLds = 256 + kPrefR * kPrefStride * 2;
+constexpr int kPrefWaveSpan = 1024;  // tokens per wave between allow-word writes: 32 words per state
+constexpr int kPrefWordsOffset = 256 + kPrefR * kPrefStride * 2;  // 4-byte aligned: the stride is even
+constexpr int kPrefLds = kPrefWordsOffset + kPrefThreads / 64 * kPrefR * 32 * 4;
 constexpr int kPrefTargetBlocks = 2048;  // four rounds of two resident blocks per compute unit
 constexpr int kTileDeferGrid = 8192;
 static_assert(kPrefR >= 1 && 2 * kPrefLds <= 160 * 1024, "two blocks per compute unit");
@@ -410,10 +408,11 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
 // multiply-add and one table read at a 32-bit offset, and a dead one skips
 // its read under the exec mask (reading an all-DEAD row instead costs an L1
 // access per lane); the lane stops when every state is dead or the token
-// ends.  Tokens take turns wave-wide (kPrefK per lane per chunk, strided by
-// the block size), so the results stay in registers until the chunk's
-// coalesced stores; a compare per result gives both the stored value and,
-// as a wave mask, the allow bits.
+// ends.  A wave takes 64 consecutive tokens per round, one per lane, over a
+// run of kPrefWaveSpan tokens; the results stay in registers until the
+// round's coalesced stores, and the alive compare gives both the stored
+// value and, as a wave mask, the allow bits, which wait in LDS until the
+// run's words are written together.
 __global__ __launch_bounds__(kPrefThreads) void walk_prefix_kernel(
     const uint8_t *__restrict__ ws, const uint16_t *__restrict__ table, int S, const uint4 *__restrict__ tokinfo,
     const uint8_t *__restrict__ bytes, int V, int W, int lds_table_bytes, int range,
@@ -462,93 +461,90 @@ __global__ __launch_bounds__(kPrefThreads) void walk_prefix_kernel(
     const char *tab_bytes = reinterpret_cast<const char *>(table);
     const uint32_t Cp2 = 2u * (uint32_t)Cp;  // row stride in bytes
 
-    for (int base = t_lo; base < t_hi; base += kPrefThreads * kPrefK) {
-        uint32_t tx[kPrefK], ty[kPrefK], off[kPrefK];
-        int len[kPrefK];
-        uint32_t st[kPrefR][kPrefK];
-        bool special = false;
-#pragma unroll
-        for (int j = 0; j < kPrefK; ++j) {
-            const int t = base + j * kPrefThreads + tid;
-            const uint4 ti = t < t_hi ? tokinfo[t] : make_uint4(0, 0, (uint32_t)kPastEnd, 0);
-            tx[j] = ti.x;
-            ty[j] = ti.y;
-            len[j] = (int)ti.z;
-            off[j] = ti.w;
-            special |= len[j] <= 0;
+    // Each wave walks kPrefWaveSpan consecutive tokens, 64 per round, and
+    // then writes its allow words for them as runs of 32 words (128 bytes)
+    // per state from LDS: whole L2 lines where the row is aligned, instead
+    // of 8-byte pieces from every wave of the block.
+    uint32_t *words = reinterpret_cast<uint32_t *>(smem + kPrefWordsOffset) + wave * (kPrefR * 32);
+    for (int sc = t_lo; sc < t_hi; sc += kPrefThreads / kWave * kPrefWaveSpan) {
+        const int wb = sc + wave * kPrefWaveSpan;  // a multiple of kPrefWaveSpan
+        if (wb >= t_hi)
+            continue;
+        const int we = min(t_hi, wb + kPrefWaveSpan);
+        for (int t0 = wb; t0 < we; t0 += kWave) {
+            const int t = t0 + lane;
+            const uint4 ti = t < we ? tokinfo[t] : make_uint4(0, 0, (uint32_t)kPastEnd, 0);
+            const int len = (int)ti.z;
             const uint32_t c0 = ti.x & 0xFFu, c1 = (ti.x >> 8) & 0xFFu;
-            const uint32_t idx = len[j] >= 2 ? c0 * (uint32_t)Cp + c1 : (uint32_t)CC + c0;
+            const uint32_t idx = len >= 2 ? c0 * (uint32_t)Cp + c1 : (uint32_t)CC + c0;
             // the first two moves of every pair: one LDS read
+            uint32_t st[kPrefR];
 #pragma unroll
             for (int si = 0; si < kPrefR; ++si)
-                st[si][j] = pt[si * kPrefStride + idx];
-        }
-        if (__any(special)) {  // empty, EOS and past-the-end tokens
-#pragma unroll
-            for (int j = 0; j < kPrefK; ++j)
+                st[si] = pt[si * kPrefStride + idx];
+            if (__any(len <= 0)) {  // empty, EOS and past-the-end tokens
 #pragma unroll
                 for (int si = 0; si < kPrefR; ++si)
-                    if (len[j] <= 0) {
-                        const bool keep = si < nS && (len[j] == 0 || (len[j] == kEosLen && ((acc_bits >> si) & 1u)));
-                        st[si][j] = keep ? (uint32_t)(s0 + si) : kDead16;  // EOS: where the scanner may stop
+                    if (len <= 0) {
+                        const bool keep = si < nS && (len == 0 || (len == kEosLen && ((acc_bits >> si) & 1u)));
+                        st[si] = keep ? (uint32_t)(s0 + si) : kDead16;  // EOS: where the scanner may stop
                     }
-        }
+            }
 
-        // the later moves, token by token, every state in lockstep
-#pragma unroll
-        for (int j = 0; j < kPrefK; ++j) {
-            uint32_t m = st[0][j];
+            // the later moves, every state in lockstep
+            uint32_t m = st[0];
 #pragma unroll
             for (int si = 1; si < kPrefR; ++si)
-                m = min(m, st[si][j]);
-            bool go = m != kDead16 && len[j] > 2;
-            if (!__any(go))
-                continue;
-            uint64_t crem = (((uint64_t)ty[j] << 16) | (tx[j] >> 16)) << 1;  // classes 2..7, doubled
-            uint32_t h = 2;
-            while (go) {
-                uint32_t c2;
-                if (h < (uint32_t)kRegBytes) {
-                    c2 = (uint32_t)crem & 0xFFu;
-                    crem >>= 8;
-                } else {
-                    c2 = 2u * cls[bytes[off[j] + h]];
-                }
-#pragma unroll
-                for (int si = 0; si < kPrefR; ++si)
-                    if (st[si][j] != kDead16) {
-                        const uint32_t boff = __umul24(st[si][j], Cp2) + c2;  // < 2^24: S <= 65535, Cp <= 98
-                        st[si][j] = *reinterpret_cast<const uint16_t *>(tab_bytes + boff);
+                m = min(m, st[si]);
+            bool go = m != kDead16 && len > 2;
+            if (__any(go)) {
+                uint64_t crem = (((uint64_t)ti.y << 16) | (ti.x >> 16)) << 1;  // classes 2..7, doubled
+                uint32_t h = 2;
+                while (go) {
+                    uint32_t c2;
+                    if (h < (uint32_t)kRegBytes) {
+                        c2 = (uint32_t)crem & 0xFFu;
+                        crem >>= 8;
+                    } else {
+                        c2 = 2u * cls[bytes[ti.w + h]];
                     }
-                h += 1;
-                m = st[0][j];
 #pragma unroll
-                for (int si = 1; si < kPrefR; ++si)
-                    m = min(m, st[si][j]);
-                go = m != kDead16 && h < (uint32_t)len[j];
+                    for (int si = 0; si < kPrefR; ++si)
+                        if (st[si] != kDead16) {
+                            const uint32_t boff = __umul24(st[si], Cp2) + c2;  // < 2^24: S <= 65535, Cp <= 98
+                            st[si] = *reinterpret_cast<const uint16_t *>(tab_bytes + boff);
+                        }
+                    h += 1;
+                    m = st[0];
+#pragma unroll
+                    for (int si = 1; si < kPrefR; ++si)
+                        m = min(m, st[si]);
+                    go = m != kDead16 && h < (uint32_t)len;
+                }
             }
-        }
 
-        // coalesced stores; the alive compare is also the wave's allow mask
-#pragma unroll
-        for (int j = 0; j < kPrefK; ++j) {
-            const int t = base + j * kPrefThreads + tid;
-            const bool in = t < t_hi;
-            const int t0 = base + j * kPrefThreads + wave * kWave;  // a multiple of 64
-            const int w = t0 / 32 + lane;
+            // coalesced stores; the alive compare is also the wave's allow mask
+            const int k = (t0 - wb) / 32;  // this round's first word in the wave's run
 #pragma unroll
             for (int si = 0; si < kPrefR; ++si) {
                 if (si >= nS)
                     break;
-                const uint32_t v = st[si][j];
-                const bool alive = v != kDead16;  // past-the-end slots are DEAD
-                if (in)
-                    next_state[(size_t)(s0 + si) * V + t] = alive ? (int32_t)v : -1;
-                const uint64_t m = __ballot(alive);
-                if (lane < 2 && t0 < t_hi && w < W)
-                    allow[(size_t)(s0 + si) * W + w] = (uint32_t)(m >> (32 * lane));
+                const bool alive = st[si] != kDead16;  // past-the-end slots are DEAD
+                if (t < we)
+                    next_state[(size_t)(s0 + si) * V + t] = alive ? (int32_t)st[si] : -1;
+                const uint64_t mask = __ballot(alive);
+                if (lane < 2)
+                    words[si * 32 + k + lane] = (uint32_t)(mask >> (32 * lane));
             }
         }
+        wave_lds_sync();
+        const int w0 = wb / 32, nw = min((we - wb + 31) / 32, W - w0);
+        for (int i = lane; i < kPrefR * 32; i += kWave) {
+            const int si = i / 32, k = i % 32;
+            if (si < nS && k < nw)
+                allow[(size_t)(s0 + si) * W + w0 + k] = words[i];
+        }
+        wave_lds_sync();  // read before the next run's words are written
     }
 }
 
@@ -602,10 +598,10 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
     const bool prefix = (size_t)S * kPrefixMaxCp * 2 > (size_t)lds_table;
     if (prefix) {
         const int rows = (S + kPrefR - 1) / kPrefR;
-        const int chunk = kPrefThreads * kPrefK;
+        const int chunk = kPrefThreads / kWave * kPrefWaveSpan;
         int nr = (kPrefTargetBlocks + rows - 1) / rows;
         nr = max(1, min(nr, (V + chunk - 1) / chunk));
-        const int range = (int)align_up((size_t)((V + nr - 1) / nr), 64);  // whole allow-word pairs
+        const int range = (int)align_up((size_t)((V + nr - 1) / nr), chunk);  // whole rounds of every wave
         nr = (V + range - 1) / range;
         walk_prefix_kernel<<<dim3(nr, rows), kPrefThreads, kPrefLds, stream>>>(
             ws, table, S, tokinfo, bytes, V, W, lds_table, range, accepting, next_state, allow);

@@ -69,6 +69,17 @@ __device__ __forceinline__ T wave_reduce(T v)
                      pick<MAX>((T)lane_value(v, 32), (T)lane_value(v, 48)));
 }
 
+// Lanes of one wave hand data to each other through LDS: the wave's LDS
+// operations run in order, so a compiler barrier with wavefront-scope
+// ordering is all that is needed (no block barrier: waves do not wait for
+// each other).
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // ---------------------------------------------------------------- alignment
 //
 // Workspace of dv_align (all offsets 256-byte aligned):

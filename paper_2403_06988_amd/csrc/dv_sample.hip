@@ -193,17 +193,6 @@ __device__ __forceinline__ int wave_prefix_small(int cnt, int &total)
     return excl;
 }
 
-// Lanes of one wave hand data to each other through LDS: the wave's LDS
-// operations run in order, so a compiler barrier with wavefront-scope
-// ordering is all that is needed (no block barrier: waves do not wait for
-// each other).
-__device__ __forceinline__ void wave_lds_sync()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
 template <int DT, int THREADS>
 __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
