@@ -559,7 +559,7 @@ def bench_sample(dv, w, ns, al, x, init_d, dev, seed=2024, reps=3):
     return {"us_per_step": t * 1e6, "steps_per_s": 1.0 / t, "temperature": 1.0,
             "allowed_tokens_per_step": allowed / steps, "groups_per_step": groups / steps,
             "graph_matches_eager": same,
-            "roofline": {"kernel": "masked_sample_kernel + sample_finalize_kernel", "bound": "alu",
+            "roofline": {"kernel": "masked_sample_kernel", "bound": "alu",
                          "achieved": achieved / 1e9, "peak": VALU_PEAK_OPS / 1e9, "unit": "Gop/s",
                          "frac": achieved / VALU_PEAK_OPS, "ops_per_launch": ops,
                          "note": f"{SAMPLE_OPS_PER_TOKEN} ops per noised token + {SAMPLE_OPS_PER_GROUP} per "
