@@ -522,26 +522,33 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
         if constexpr (STAGED) {
             // Both first batches are in flight (issued by the caller) and the
             // mask bytes are in LDS: reading them costs no memory trip, so
-            // with SELECT every later batch's addresses are chosen from them
-            // just before its logits are issued.
-            auto issue = [&](uint4 (&d)[U], int vb) {
-                if constexpr (SELECT && MASKED && !SHIFTED) {
-                    uint32_t sel[U];
-                    load_masks(sel, vb);
+            // with SELECT every later batch's addresses are chosen from them.
+            auto issue = [&](uint4 (&d)[U], int vb, const uint32_t (&sel)[U]) {
+                if constexpr (SELECT && MASKED && !SHIFTED)
                     load_batch_bf16_sel<THREADS, U>(d, vrow, vb, v1, sel);
-                } else {
+                else
                     load_batch_bf16<THREADS, U>(d, vrow, vb, v1);
-                }
             };
+            // Each batch's mask bytes are read from LDS once, a batch ahead:
+            // they choose its addresses when it is issued and mask it when it
+            // is reduced, so reading them never stands between consuming a
+            // batch and issuing the next.
+            uint32_t na[U], nb[U];
+            load_masks(ma, v0);
+            load_masks(mb, v0 + kStep);
             for (int vb = v0; vb < v1; vb += 2 * kStep) {
-                load_masks(ma, vb);
+                load_masks(na, vb + 2 * kStep);
                 process_batch(da, ma, vb);
-                issue(da, vb + 2 * kStep);
-                if (vb + kStep < v1) {  // block-uniform
-                    load_masks(mb, vb + kStep);
+                issue(da, vb + 2 * kStep, na);
+                load_masks(nb, vb + 3 * kStep);
+                if (vb + kStep < v1)  // block-uniform
                     process_batch(db, mb, vb + kStep);
+                issue(db, vb + 3 * kStep, nb);
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    ma[u] = na[u];
+                    mb[u] = nb[u];
                 }
-                issue(db, vb + 3 * kStep);
                 // the best so far's next state, loaded outside any branch (a
                 // load under a branch would make the compiler wait for every
                 // load in flight where the branches join)

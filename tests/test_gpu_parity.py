@@ -420,14 +420,18 @@ def test_step_every_row_alignment(dv, B, V, extra_ld, dtype, head):
         np.testing.assert_array_equal(new.cpu().numpy(), new_o)
 
 
-@pytest.mark.parametrize("B,V,offset,extra_ld", [(600, 40000, 0, 0), (520, 30011, 0, 1), (530, 33333, 3, 2),
-                                                 (1030, 24577, 0, 7)])
+@pytest.mark.parametrize("B,V,offset,extra_ld", [
+    (600, 40000, 0, 0), (520, 30011, 0, 1), (530, 33333, 3, 2), (1030, 24577, 0, 7),
+    # fewer than two blocks per compute unit, long chunks: every line is read
+    (256, 128256, 0, 0), (300, 66000, 3, 1), (128, 140000, 0, 0), (64, 260000, 5, 3),
+])
 def test_step_skips_lines_without_allowed_tokens(dv, B, V, offset, extra_ld):
     """Launches of two or more blocks per compute unit do not read vectors
-    whose 8 tokens are all disallowed (from the third batch of a row on).
-    Sparse masks (whole runs of disallowed vectors), few distinct values,
-    planted NaN and signed zeros, aligned and misaligned rows; greedy and
-    opportunistic steps against the oracle."""
+    whose 8 tokens are all disallowed (from the third batch of a chunk on);
+    smaller launches read every line, the same masks deciding.  Sparse masks
+    (whole runs of disallowed vectors), few distinct values, planted NaN and
+    signed zeros, aligned and misaligned rows, rows of one, two and four
+    chunks; greedy and opportunistic steps against the oracle."""
     _say(f"step line skipping B={B} V={V} offset={offset} ld=V+{extra_ld}")
     rng = np.random.default_rng(B + V)
     S = 9
