@@ -76,6 +76,7 @@ constexpr int kPrefWordsOffset = 256 + kPrefR * kPrefStride * 2;  // 4-byte alig
 constexpr int kPrefLds = kPrefWordsOffset + kPrefThreads / 64 * kPrefR * 32 * 4;
 constexpr int kPrefTargetBlocks = 2048;  // four rounds of two resident blocks per compute unit
 constexpr int kTileDeferGrid = 8192;
+constexpr int kLdsPerCu = 160 * 1024;  // gfx950
 static_assert(kPrefR >= 1 && 2 * kPrefLds <= 160 * 1024, "two blocks per compute unit");
 static_assert(kPrefThreads >= 256, "one byte class per thread in the first 256");
 
@@ -606,8 +607,17 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
         walk_prefix_kernel<<<dim3(nr, rows), kPrefThreads, kPrefLds, stream>>>(
             ws, table, S, tokinfo, bytes, V, W, lds_table, range, accepting, next_state, allow);
     }
+    // The tile walk strides over its tiles; when the whole table may be
+    // staged (S <= 512), at most one round of resident blocks is launched,
+    // so that each block stages the table once for several tiles.
     const long long ntiles = (long long)((V + kTokTile - 1) / kTokTile) * ((S + kStateTile - 1) / kStateTile);
-    const int grid = (int)(prefix && ntiles > kTileDeferGrid ? kTileDeferGrid : ntiles);
+    long long cap = prefix ? kTileDeferGrid : ntiles;
+    const int cus = device_compute_units();
+    if (S <= 512 && cus > 0) {
+        const int per_cu = kLdsPerCu / (256 + lds_table + kResLds);
+        cap = min(cap, (long long)(per_cu > 1 ? per_cu : 1) * cus);
+    }
+    const int grid = (int)(ntiles < cap ? ntiles : cap);
     walk_kernel<<<grid, kThreads, 256 + lds_table + kResLds, stream>>>(ws, table, S, tokinfo, bytes, V, W,
                                                                        lds_table, prefix ? 1 : 0, accepting,
                                                                        next_state, allow);

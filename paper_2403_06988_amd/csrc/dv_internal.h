@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace dv {
 
 constexpr int kWave = 64;
@@ -67,6 +69,25 @@ __device__ __forceinline__ T wave_reduce(T v)
     }
     return pick<MAX>(pick<MAX>((T)lane_value(v, 0), (T)lane_value(v, 16)),
                      pick<MAX>((T)lane_value(v, 32), (T)lane_value(v, 48)));
+}
+
+// Compute units of the current device (read once per device), or -1 when
+// the runtime cannot say: launch shapes that depend on it fall back to
+// their plain form.
+inline int device_compute_units()
+{
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int> cus[kMaxDevices];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return -1;
+    int n = cus[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = -1;
+        cus[dev].store(n, std::memory_order_relaxed);
+    }
+    return n;
 }
 
 // Lanes of one wave hand data to each other through LDS: the wave's LDS

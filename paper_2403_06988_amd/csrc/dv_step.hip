@@ -49,7 +49,6 @@ namespace dv {
 namespace {
 
 constexpr int kSmallThreads = 256;  // split rows and fp32 rows
-constexpr int kMaxDevices = 64;
 constexpr int kSmallU = 8;          // 16-byte vectors per lane per batch
 #ifndef DV_STEP_BF16_THREADS
 #define DV_STEP_BF16_THREADS 512
@@ -814,16 +813,7 @@ StepGeometry step_geometry(int B, int V, int dtype)
 // (B = 256 x V = 128256: 15.0 against 13.9 us).
 static bool skip_unread_lines(unsigned blocks)
 {
-    static std::atomic<int> cus[kMaxDevices];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
-        return false;
-    int n = cus[dev].load(std::memory_order_relaxed);
-    if (n == 0) {
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-            n = -1;  // unknown: never skip
-        cus[dev].store(n, std::memory_order_relaxed);
-    }
+    const int n = device_compute_units();  // unknown: never skip
     return n > 0 && blocks >= 2u * (unsigned)n;
 }
 
