@@ -61,6 +61,12 @@ constexpr int kLiveRows = kLiveRowsPerBlock;
 #ifndef DV_ALIGN_PREFIX_R
 #define DV_ALIGN_PREFIX_R 3
 #endif
+#ifndef DV_ALIGN_WHOLE_LOCKSTEP
+#define DV_ALIGN_WHOLE_LOCKSTEP 1
+#endif
+#ifndef DV_ALIGN_WHOLE_G
+#define DV_ALIGN_WHOLE_G 8
+#endif
 #ifndef DV_ALIGN_PREFIX_THREADS
 #define DV_ALIGN_PREFIX_THREADS 1024
 #endif
@@ -76,6 +82,8 @@ constexpr int kPrefWordsOffset = 256 + kPrefR * kPrefStride * 2;  // 4-byte alig
 constexpr int kPrefLds = kPrefWordsOffset + kPrefThreads / 64 * kPrefR * 32 * 4;
 constexpr int kPrefTargetBlocks = 2048;  // four rounds of two resident blocks per compute unit
 constexpr int kTileDeferGrid = 8192;
+constexpr int kWholeG = DV_ALIGN_WHOLE_G;  // states a lane walks at once when the table is whole in LDS
+static_assert(kResLds >= 256 * 2, "the sentinel row fits in the result tile's place");
 constexpr int kLdsPerCu = 160 * 1024;  // gfx950
 static_assert(kPrefR >= 1 && 2 * kPrefLds <= 160 * 1024, "two blocks per compute unit");
 static_assert(kPrefThreads >= 256, "one byte class per thread in the first 256");
@@ -339,6 +347,79 @@ __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
     }
 }
 
+// The tile walk when the whole table is in LDS: a lane walks its token from
+// kWholeG of the tile's states at once, one byte per iteration (the class
+// shared by the states, kWholeG independent LDS reads per iteration instead
+// of one dependent read per move), until every one of them is dead or the
+// token ends.  A dead state is row S, an all-DEAD sentinel row, which every
+// read maps back to S, so the walk needs no branch per state.  Each group's
+// results go straight to coalesced stores; a wave ballot packs the allow
+// words.
+__device__ __forceinline__ void walk_tile_whole(const uint16_t *tab, const uint8_t *cls, int Cp, int S, int s0,
+                                                int nS, const uint8_t *__restrict__ bytes, int t_base, int V,
+                                                int W, const uint4 *__restrict__ tokinfo,
+                                                const uint8_t *__restrict__ accepting,
+                                                int32_t *__restrict__ next_state, uint32_t *__restrict__ allow)
+{
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1), wave = tid / kWave;
+    const int t = t_base + tid;
+    const uint4 ti = t < V ? tokinfo[t] : make_uint4(0, 0, (uint32_t)kPastEnd, 0);
+    const int len = (int)ti.z;
+    const uint64_t classes = ((uint64_t)ti.y << 32) | ti.x;  // the first kRegBytes byte classes
+    const uint32_t dead = (uint32_t)S;
+    const int t0 = t_base + wave * kWave;  // a multiple of 64
+    const int w = t0 / 32 + lane;
+    for (int g = 0; g < nS; g += kWholeG) {
+        uint32_t st[kWholeG];
+#pragma unroll
+        for (int k = 0; k < kWholeG; ++k) {
+            const int s = s0 + g + k;
+            st[k] = g + k < nS ? (uint32_t)s : dead;
+            if (len < 0)  // EOS: only where the scanner may stop; past the last token: dead
+                st[k] = g + k < nS && len == kEosLen && accepting != nullptr && accepting[s] != 0 ? (uint32_t)s
+                                                                                                : dead;
+        }
+        uint32_t m = st[0];
+#pragma unroll
+        for (int k = 1; k < kWholeG; ++k)
+            m = min(m, st[k]);
+        bool go = len > 0 && m != dead;  // an empty token keeps the state
+        uint64_t cr = classes;
+        uint32_t h = 0;
+        while (go) {
+            uint32_t c;
+            if (h < (uint32_t)kRegBytes) {
+                c = (uint32_t)cr & 0xFFu;
+                cr >>= 8;
+            } else {
+                c = cls[bytes[ti.w + h]];
+            }
+#pragma unroll
+            for (int k = 0; k < kWholeG; ++k)
+                st[k] = min((uint32_t)tab[st[k] * (uint32_t)Cp + c], dead);
+            h += 1;
+            m = st[0];
+#pragma unroll
+            for (int k = 1; k < kWholeG; ++k)
+                m = min(m, st[k]);
+            go = m != dead && h < (uint32_t)len;
+        }
+#pragma unroll
+        for (int k = 0; k < kWholeG; ++k) {
+            if (g + k >= nS)
+                break;
+            const int s = s0 + g + k;
+            const bool alive = st[k] != dead;
+            if (t < V)
+                next_state[(size_t)s * V + t] = alive ? (int32_t)st[k] : -1;
+            const uint64_t mask = __ballot(alive);
+            if (lane < 2 && w < W)
+                allow[(size_t)s * W + w] = (uint32_t)(mask >> (32 * lane));
+        }
+    }
+}
+
 __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restrict__ ws,
                                                         const uint16_t *__restrict__ table, int S,
                                                         const uint4 *__restrict__ tokinfo,
@@ -368,6 +449,12 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
         uint32_t *dst = reinterpret_cast<uint32_t *>(tab);
         for (int i = tid; i < n32; i += kThreads)
             dst[i] = src[i];
+#if DV_ALIGN_WHOLE_LOCKSTEP
+        // the sentinel row S (all DEAD) right after the table, in the part
+        // of the allocation the tile results would use: Cp * 2 <= 512 bytes
+        for (int i = tid; i < Cp; i += kThreads)
+            tab[S * Cp + i] = kDead16;
+#endif
     }
     // a grid smaller than the tile count (launched beside the prefix-table
     // walk, so that it exits cheaply when that one owns the table) strides
@@ -386,8 +473,12 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
         }
         __syncthreads();
         if (whole)
+#if DV_ALIGN_WHOLE_LOCKSTEP
+            walk_tile_whole(tab, cls, Cp, S, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state, allow);
+#else
             walk_tile<true>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state,
                             allow);
+#endif
         else
             walk_tile<false>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state,
                              allow);

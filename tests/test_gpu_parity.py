@@ -110,7 +110,9 @@ def test_align_edge_shapes(dv, S, V, max_len, p_empty):
     (600, 70000, 6, 0.0, 200, None),      # tile walk on a strided grid (more tiles than blocks)
     (400, 140000, 5, 0.0, 30, None),      # whole table in LDS, strided grid
     (400, 5000, 8, 0.0, 94, 4999),        # S <= 512 but too large whole: prefix walk, 3 token ranges
-    (65535, 300, 12, 0.02, 90, 7),        # the largest state count: prefix walk, sentinel row 0xFFFF
+    (3000, 5000, 40, 0.01, 2, 4999),      # prefix walk, Cp = 4: most walks survive past the eighth byte
+    (2000, 3000, 60, 0.0, 3, None),       # prefix walk, Cp = 4, tokens up to 60 bytes
+    (65535, 300, 12, 0.02, 90, 7),        # the largest state count: prefix walk, DEAD = 0xFFFF = S
     (65535, 300, 12, 0.0, 200, None),     # the largest state count: tile walk
 ])
 def test_align_large_dfa(dv, S, V, max_len, p_empty, alphabet, eos):
