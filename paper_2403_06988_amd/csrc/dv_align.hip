@@ -19,12 +19,13 @@
 //      one lane per token, over a tile of 16 states x 256 tokens per
 //      block.  The byte classes of each token's first 8 bytes are looked up
 //      once per block and kept in registers, so a move costs one table
-//      read.  The table lives in LDS: the whole table when it fits,
-//      otherwise the block's 16 rows, which serve every walk's first move
-//      (every pair takes one); later moves (about one per pair) read the
-//      cache-resident table with 32-bit offsets, each lane walking its
-//      token's pending states one after the other, and the wave stops as
-//      soon as every walk in it has ended.  One token per lane keeps the
+//      read.  The table lives in LDS: the whole table when it fits (a lane
+//      then walks its token from 8 of the tile's states at once, see
+//      walk_tile_whole), otherwise the block's 16 rows, which serve every
+//      walk's first move (every pair takes one); later moves (about one
+//      per pair) read the cache-resident table with 32-bit offsets, each
+//      lane walking its token's pending states one after the other, and the
+//      wave stops as soon as every walk in it has ended.  One token per lane keeps the
 //      block's LDS small (more resident blocks hide the gathers' latency
 //      better than a second token per lane does).  Stores are coalesced
 //      along tokens; the allow words come from a wave ballot (64 tokens ->
