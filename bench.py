@@ -195,7 +195,7 @@ def cpu_baseline(w, wid, trans, offsets, data, init, x_dev, budget_s):
     # workload statistic for the alignment's L2 roofline: table moves per pair,
     # in all and past the first one and two bytes (the tile walk and the
     # prefix-table walk take those from LDS)
-    srows = rng.integers(0, w.S, 32).astype(np.int32)
+    srows = rng.integers(0, w.S, 256).astype(np.int32)
     hist = oracle.walk_length_hist(trans, offsets, data, srows, lib=lib)
     k = np.arange(len(hist))
     npairs = len(srows) * w.V
