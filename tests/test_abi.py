@@ -119,6 +119,36 @@ def test_masked_step_rejects_before_launch(kw, status):
     assert lib.dv_last_error().startswith(b"dv_masked_step")
 
 
+def test_last_error_is_per_thread():
+    """The detail string belongs to the calling thread: threads failing in
+    different entry points, and one whose calls succeed, each read their
+    own last error while the others keep calling (ctypes releases the
+    interpreter lock around the calls)."""
+    import threading
+    errors = []
+    barrier = threading.Barrier(3)
+
+    def run(call, want, prefix):
+        barrier.wait()
+        for _ in range(300):
+            st = call()
+            msg = lib.dv_last_error()
+            if st != want or not msg.startswith(prefix) or (prefix == b"" and msg != b""):
+                errors.append((want, st, prefix, msg))
+                return
+
+    threads = [threading.Thread(target=run, args=a) for a in (
+        (lambda: _align(S=0), SHAPE, b"dv_align"),
+        (lambda: _step(dtype=2), DTYPE, b"dv_masked_step"),
+        (lambda: _step(B=0), OK, b""),
+    )]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors[:3]
+
+
 def test_masked_step_empty_batch_is_a_noop():
     assert _step(B=0) == OK
     assert lib.dv_last_error() == b""

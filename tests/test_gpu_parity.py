@@ -465,6 +465,62 @@ def test_step_skips_lines_without_allowed_tokens(dv, B, V, offset, extra_ld):
         np.testing.assert_array_equal(new.cpu().numpy(), new_o)
 
 
+def test_calls_on_two_streams_do_not_interfere(dv):
+    """Two streams, each with its own workspaces, interleave greedy steps on
+    rows split over many blocks (which meet in the workspace), sampled steps
+    and an alignment, never waiting for each other: every result equals the
+    oracle's (the library keeps no device state between calls)."""
+    _say("two streams, interleaved calls")
+    rng = np.random.default_rng(2024)
+    S, V, B, steps = 13, 100_000, 3, 6
+    alive = rng.random((S, V)) < rng.choice([0.001, 0.05, 0.6], size=(S, 1))
+    ns = np.where(alive, rng.integers(0, S, (S, V)), -1).astype(np.int32)
+    Wd = (V + 31) // 32
+    pad = np.zeros((S, Wd * 32), bool)
+    pad[:, :V] = alive
+    al = np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(S, Wd)
+    ns_d, al_d = _dev(ns), _dev(al.view(np.int32))
+    trans, offsets, data = _random_case(31, 700, 5000, 10, 0.01, alphabet=np.arange(0x20, 0x7F))
+    runs = []
+    for _ in range(2):
+        x = torch.from_numpy((rng.standard_normal((steps, B, V)) * 3).astype(np.float32)).to(torch.bfloat16)
+        st = rng.integers(-1, S, (steps, B)).astype(np.int32)
+        runs.append(dict(x=x, x_d=x.to(DEV), st=st, st_d=_dev(st),
+                         tok=torch.empty((steps, B), dtype=torch.int32, device=DEV),
+                         new=torch.empty((steps, B), dtype=torch.int32, device=DEV),
+                         stok=torch.empty((steps, B), dtype=torch.int32, device=DEV),
+                         snew=torch.empty((steps, B), dtype=torch.int32, device=DEV),
+                         ws=dv.step_workspace(B, V, DEV), sws=dv.sample_workspace(B, V, DEV),
+                         stream=torch.cuda.Stream(DEV)))
+    tr_d, of_d, da_d = _dev(trans), _dev(offsets), _dev(data)
+    nsa = torch.empty((700, 5000), dtype=torch.int32, device=DEV)
+    ala = torch.empty((700, (5000 + 31) // 32), dtype=torch.int32, device=DEV)
+    wsa = torch.empty(dv.align_workspace_bytes(700, 5000), dtype=torch.uint8, device=DEV)
+    torch.cuda.synchronize()
+    for k in range(steps):
+        for i, r in enumerate(runs):
+            with torch.cuda.stream(r["stream"]):
+                dv.masked_step(ns_d, al_d, r["st_d"][k], r["x_d"][k], token=r["tok"][k], new_state=r["new"][k],
+                               workspace=r["ws"])
+                dv.masked_sample(ns_d, al_d, r["st_d"][k], r["x_d"][k], seed=7 + i, offset=k,
+                                 token=r["stok"][k], new_state=r["snew"][k], workspace=r["sws"])
+                if i == 1 and k == 2:
+                    dv.align(tr_d, of_d, da_d, next_state=nsa, allow=ala, workspace=wsa)
+    torch.cuda.synchronize()
+    for i, r in enumerate(runs):
+        for k in range(steps):
+            xo = to_oracle(r["x"][k])
+            tok_o, new_o = oracle.masked_step(ns, al, r["st"][k], xo)
+            np.testing.assert_array_equal(r["tok"][k].cpu().numpy(), tok_o)
+            np.testing.assert_array_equal(r["new"][k].cpu().numpy(), new_o)
+            stok_o, snew_o = oracle.masked_sample(ns, al, r["st"][k], xo, 1.0, 7 + i, k)
+            np.testing.assert_array_equal(r["stok"][k].cpu().numpy(), stok_o)
+            np.testing.assert_array_equal(r["snew"][k].cpu().numpy(), snew_o)
+    ns_o, al_o = oracle.align(trans, offsets, data)
+    np.testing.assert_array_equal(nsa.cpu().numpy(), ns_o)
+    np.testing.assert_array_equal(u32(ala), al_o)
+
+
 def test_step_empty_batch(dv):
     ns = torch.zeros((2, 10), dtype=torch.int32, device=DEV)
     al = torch.full((2, 1), 0x3FF, dtype=torch.int32, device=DEV)
