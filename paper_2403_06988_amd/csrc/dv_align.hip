@@ -62,9 +62,6 @@ constexpr int kLiveRows = kLiveRowsPerBlock;
 #ifndef DV_ALIGN_PREFIX_R
 #define DV_ALIGN_PREFIX_R 3
 #endif
-#ifndef DV_ALIGN_WHOLE_LOCKSTEP
-#define DV_ALIGN_WHOLE_LOCKSTEP 1
-#endif
 #ifndef DV_ALIGN_WHOLE_G
 #define DV_ALIGN_WHOLE_G 8
 #endif
@@ -219,11 +216,12 @@ __global__ __launch_bounds__(kThreads) void token_info_kernel(const int32_t *__r
     tokinfo[t] = make_uint4(lo, hi, (uint32_t)len, (uint32_t)off);
 }
 
-// 5. the walk.  One block owns a tile of kStateTile states x kTokTile tokens
-// (kTokPerLane tokens per lane, strided by the block size so stores are
-// coalesced).  Dynamic LDS holds the byte-class map, the table (the whole
-// table when S * Cp * 2 fits in `lds_table_bytes`, else the tile's rows) and
-// the tile's results (uint16, DEAD = 0xFFFF).
+// 5. the tile walk.  One block owns a tile of kStateTile states x kTokTile
+// tokens (kTokPerLane tokens per lane, strided by the block size so stores
+// are coalesced).  Dynamic LDS holds the byte-class map, the table (the
+// whole table when S * Cp * 2 fits in `lds_table_bytes`: walk_tile_whole
+// below; else the tile's rows: walk_tile) and the tile's results (uint16,
+// DEAD = 0xFFFF).
 //   phase 1: every pair's first move, lane-parallel, from LDS.  Walks that
 //            end there (dead, or one-byte tokens) are final; the others are
 //            marked pending in a per-token bit set over the tile's states.
@@ -235,7 +233,6 @@ __global__ __launch_bounds__(kThreads) void token_info_kernel(const int32_t *__r
 //            streams give kTokPerLane independent table reads in flight.
 //   phase 3: the tile's results leave LDS as coalesced row stores, and a
 //            wave ballot packs the allow bits.
-template <bool WHOLE>
 __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
                                           const uint16_t *__restrict__ table, const uint8_t *cls,
                                           int Cp, int s0, int nS, const uint8_t *__restrict__ bytes,
@@ -265,7 +262,7 @@ __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
         pend[j] = 0;
     for (int si = 0; si < nS; ++si) {
         const int s = s0 + si;
-        const uint16_t *row = WHOLE ? tab + (uint32_t)s * Cp : tab + (uint32_t)si * Cp;
+        const uint16_t *row = tab + (uint32_t)si * Cp;
         const bool acc = accepting != nullptr && accepting[s] != 0;
 #pragma unroll
         for (int j = 0; j < kTokPerLane; ++j) {
@@ -316,7 +313,7 @@ __device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
                 else
                     c = cls[bytes[off[j] + h[j]]];
                 const uint32_t idx = st[j] * (uint32_t)Cp + c;
-                st[j] = WHOLE ? tab[idx] : table[idx];
+                st[j] = table[idx];
                 h[j] += 1;
                 if (st[j] == kDead16 || h[j] >= (uint32_t)len[j]) {
                     res[cur[j] * kTokTile + j * kThreads + tid] = (uint16_t)st[j];
@@ -450,12 +447,10 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
         uint32_t *dst = reinterpret_cast<uint32_t *>(tab);
         for (int i = tid; i < n32; i += kThreads)
             dst[i] = src[i];
-#if DV_ALIGN_WHOLE_LOCKSTEP
         // the sentinel row S (all DEAD) right after the table, in the part
         // of the allocation the tile results would use: Cp * 2 <= 512 bytes
         for (int i = tid; i < Cp; i += kThreads)
             tab[S * Cp + i] = kDead16;
-#endif
     }
     // a grid smaller than the tile count (launched beside the prefix-table
     // walk, so that it exits cheaply when that one owns the table) strides
@@ -474,15 +469,9 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
         }
         __syncthreads();
         if (whole)
-#if DV_ALIGN_WHOLE_LOCKSTEP
             walk_tile_whole(tab, cls, Cp, S, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state, allow);
-#else
-            walk_tile<true>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state,
-                            allow);
-#endif
         else
-            walk_tile<false>(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state,
-                             allow);
+            walk_tile(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state, allow);
     }
 }
 
