@@ -15,21 +15,18 @@
 //   4. token_info: each token's first 8 byte classes, length and offset.
 //   5. walk (tables of at most 98 columns that do not fit in LDS whole, e.g.
 //      random printable-ASCII DFAs of more than ~330 states): the prefix-table
-//      walk, kernel 6 below.  Otherwise:
-//      one lane per token, over a tile of 16 states x 256 tokens per
-//      block.  The byte classes of each token's first 8 bytes are looked up
-//      once per block and kept in registers, so a move costs one table
-//      read.  The table lives in LDS: the whole table when it fits (a lane
-//      then walks its token from 8 of the tile's states at once, see
-//      walk_tile_whole), otherwise the block's 16 rows, which serve every
-//      walk's first move (every pair takes one); later moves (about one
-//      per pair) read the cache-resident table with 32-bit offsets, each
-//      lane walking its token's pending states one after the other, and the
-//      wave stops as soon as every walk in it has ended.  One token per lane keeps the
-//      block's LDS small (more resident blocks hide the gathers' latency
-//      better than a second token per lane does).  Stores are coalesced
-//      along tokens; the allow words come from a wave ballot (64 tokens ->
-//      2 words).
+//      walk, kernel 6 below.  Otherwise the tile walk: a block owns 16 states
+//      x 256 tokens (one token per lane), with the whole table in LDS when it
+//      fits, else the tile's 16 rows; the byte classes of each token's first
+//      8 bytes are looked up once and kept in registers.  A lane walks its
+//      token from 8 of the tile's states at once, one byte per iteration, so
+//      a long walk is a chain of 8 independent reads per byte, not one
+//      dependent read per move of every state: from LDS when the table is
+//      whole (a dead state reads an all-DEAD sentinel row), else the first
+//      move from the row tile and later ones from the cache-resident table
+//      at 32-bit offsets (a dead state skips its read).  Stores are coalesced
+//      along tokens; the allow words come from a wave ballot (64 tokens -> 2
+//      words).
 #include "dv_internal.h"
 
 namespace dv {
@@ -38,19 +35,20 @@ namespace {
 #ifndef DV_ALIGN_STATE_TILE
 #define DV_ALIGN_STATE_TILE 16
 #endif
-#ifndef DV_ALIGN_TOK_PER_LANE
-#define DV_ALIGN_TOK_PER_LANE 1
+
+#ifndef DV_ALIGN_LOCK_G
+#define DV_ALIGN_LOCK_G 8
 #endif
 
 constexpr int kThreads = 256;
-constexpr int kTokPerLane = DV_ALIGN_TOK_PER_LANE;
-constexpr int kTokTile = kThreads * kTokPerLane;  // a multiple of 64 tokens = 2 allow words
-constexpr int kStateTile = DV_ALIGN_STATE_TILE;   // <= 32: pending states are a 32-bit set
+constexpr int kTokTile = kThreads;                // a multiple of 64 tokens = 2 allow words
+constexpr int kStateTile = DV_ALIGN_STATE_TILE;   // states per tile
+constexpr int kLockG = DV_ALIGN_LOCK_G;           // of which a lane walks this many at once
 constexpr int kRegBytes = 8;                      // token bytes whose classes sit in registers
 constexpr int kRowsLds = kStateTile * 256 * 2;    // worst-case bytes of the row tile
-constexpr int kResLds = kStateTile * kTokTile * 2;
+constexpr int kSentinelLds = 256 * 2;             // the whole table's all-DEAD sentinel row
 constexpr int kWholeLdsMax = 64 * 1024;           // LDS budget for a whole table
-static_assert(kStateTile >= 1 && kStateTile <= 32, "pending set is 32 bits");
+static_assert(kStateTile >= 1 && kLockG >= 1, "tile shape");
 constexpr int kLiveRows = kLiveRowsPerBlock;
 
 // the prefix-table walk: states per block, block size, and the largest
@@ -61,9 +59,6 @@ constexpr int kLiveRows = kLiveRowsPerBlock;
 // tokens per lane per round.
 #ifndef DV_ALIGN_PREFIX_R
 #define DV_ALIGN_PREFIX_R 3
-#endif
-#ifndef DV_ALIGN_WHOLE_G
-#define DV_ALIGN_WHOLE_G 8
 #endif
 #ifndef DV_ALIGN_PREFIX_THREADS
 #define DV_ALIGN_PREFIX_THREADS 1024
@@ -80,8 +75,6 @@ constexpr int kPrefWordsOffset = 256 + kPrefR * kPrefStride * 2;  // 4-byte alig
 constexpr int kPrefLds = kPrefWordsOffset + kPrefThreads / 64 * kPrefR * 32 * 4;
 constexpr int kPrefTargetBlocks = 2048;  // four rounds of two resident blocks per compute unit
 constexpr int kTileDeferGrid = 8192;
-constexpr int kWholeG = DV_ALIGN_WHOLE_G;  // states a lane walks at once when the table is whole in LDS
-static_assert(kResLds >= 256 * 2, "the sentinel row fits in the result tile's place");
 constexpr int kLdsPerCu = 160 * 1024;  // gfx950
 static_assert(kPrefR >= 1 && 2 * kPrefLds <= 160 * 1024, "two blocks per compute unit");
 static_assert(kPrefThreads >= 256, "one byte class per thread in the first 256");
@@ -216,138 +209,16 @@ __global__ __launch_bounds__(kThreads) void token_info_kernel(const int32_t *__r
     tokinfo[t] = make_uint4(lo, hi, (uint32_t)len, (uint32_t)off);
 }
 
-// 5. the tile walk.  One block owns a tile of kStateTile states x kTokTile
-// tokens (kTokPerLane tokens per lane, strided by the block size so stores
-// are coalesced).  Dynamic LDS holds the byte-class map, the table (the
-// whole table when S * Cp * 2 fits in `lds_table_bytes`: walk_tile_whole
-// below; else the tile's rows: walk_tile) and the tile's results (uint16,
-// DEAD = 0xFFFF).
-//   phase 1: every pair's first move, lane-parallel, from LDS.  Walks that
-//            end there (dead, or one-byte tokens) are final; the others are
-//            marked pending in a per-token bit set over the tile's states.
-//   phase 2: each lane runs kTokPerLane independent streams (one per token),
-//            each taking its pending states one after the other and moving
-//            one byte per iteration.  A wave's iteration count is the
-//            longest stream's total number of later moves, not the sum over
-//            states of the longest single walk, so lanes stay busy; the
-//            streams give kTokPerLane independent table reads in flight.
-//   phase 3: the tile's results leave LDS as coalesced row stores, and a
-//            wave ballot packs the allow bits.
-__device__ __forceinline__ void walk_tile(const uint16_t *tab, uint16_t *res,
-                                          const uint16_t *__restrict__ table, const uint8_t *cls,
-                                          int Cp, int s0, int nS, const uint8_t *__restrict__ bytes,
-                                          int t_base, int V, int W, const uint4 *__restrict__ tokinfo,
-                                          const uint8_t *__restrict__ accepting,
-                                          int32_t *__restrict__ next_state, uint32_t *__restrict__ allow)
-{
-    const int tid = threadIdx.x;
-    const int lane = tid & (kWave - 1), wave = tid / kWave;
-
-    int off[kTokPerLane], len[kTokPerLane];
-    uint32_t c03[kTokPerLane], c47[kTokPerLane];
-#pragma unroll
-    for (int j = 0; j < kTokPerLane; ++j) {
-        const int t = t_base + j * kThreads + tid;
-        const uint4 ti = t < V ? tokinfo[t] : make_uint4(0, 0, (uint32_t)kPastEnd, 0);
-        c03[j] = ti.x;
-        c47[j] = ti.y;
-        len[j] = (int)ti.z;  // kPastEnd: never stored, allow bit 0; kEosLen: the EOS token
-        off[j] = (int)ti.w;
-    }
-
-    // phase 1: first moves
-    uint32_t pend[kTokPerLane];
-#pragma unroll
-    for (int j = 0; j < kTokPerLane; ++j)
-        pend[j] = 0;
-    for (int si = 0; si < nS; ++si) {
-        const int s = s0 + si;
-        const uint16_t *row = tab + (uint32_t)si * Cp;
-        const bool acc = accepting != nullptr && accepting[s] != 0;
-#pragma unroll
-        for (int j = 0; j < kTokPerLane; ++j) {
-            const uint32_t c0 = c03[j] & 0xFFu;  // always a column of the table
-            uint32_t st = row[c0];
-            if (len[j] <= 0) {
-                if (len[j] == 0)
-                    st = (uint32_t)s;  // an empty token keeps the state
-                else if (len[j] == kEosLen)
-                    st = acc ? (uint32_t)s : kDead16;  // EOS: only where the scanner may stop
-                else
-                    st = kDead16;
-            }
-            res[si * kTokTile + j * kThreads + tid] = (uint16_t)st;
-            pend[j] |= (uint32_t)(st != kDead16 && len[j] > 1) << si;
-        }
-    }
-
-    // phase 2: later moves of the pending walks
-    uint32_t st[kTokPerLane], h[kTokPerLane], cur[kTokPerLane];
-    bool act[kTokPerLane];
-#pragma unroll
-    for (int j = 0; j < kTokPerLane; ++j) {
-        st[j] = kDead16;
-        h[j] = 0;
-        cur[j] = 0;
-        act[j] = false;
-    }
-    bool work = false;
-#pragma unroll
-    for (int j = 0; j < kTokPerLane; ++j)
-        work |= pend[j] != 0;
-    while (__any(work)) {
-        work = false;
-#pragma unroll
-        for (int j = 0; j < kTokPerLane; ++j) {
-            if (!act[j] && pend[j]) {
-                cur[j] = __builtin_ctz(pend[j]);
-                pend[j] &= pend[j] - 1u;
-                st[j] = res[cur[j] * kTokTile + j * kThreads + tid];
-                h[j] = 1;
-                act[j] = true;
-            }
-            if (act[j]) {
-                uint32_t c;
-                if (h[j] < (uint32_t)kRegBytes)
-                    c = ((h[j] < 4 ? c03[j] : c47[j]) >> (8 * (h[j] & 3))) & 0xFFu;
-                else
-                    c = cls[bytes[off[j] + h[j]]];
-                const uint32_t idx = st[j] * (uint32_t)Cp + c;
-                st[j] = table[idx];
-                h[j] += 1;
-                if (st[j] == kDead16 || h[j] >= (uint32_t)len[j]) {
-                    res[cur[j] * kTokTile + j * kThreads + tid] = (uint16_t)st[j];
-                    act[j] = false;
-                }
-            }
-            work |= act[j] || pend[j] != 0;
-        }
-    }
-    __syncthreads();
-
-    // phase 3: coalesced stores and allow words
-    for (int si = 0; si < nS; ++si) {
-        const int s = s0 + si;
-        int32_t *ns_row = next_state + (size_t)s * V;
-        uint32_t *al_row = allow + (size_t)s * W;
-#pragma unroll
-        for (int j = 0; j < kTokPerLane; ++j) {
-            const int t = t_base + j * kThreads + tid;
-            const uint32_t v = res[si * kTokTile + j * kThreads + tid];
-            const bool alive = len[j] != kPastEnd && v != kDead16;
-            if (t < V)
-                ns_row[t] = alive ? (int32_t)v : -1;
-            const uint64_t m = __ballot(alive);
-            const int w = (t_base + j * kThreads + wave * kWave) / 32 + lane;
-            if (lane < 2 && w < W)
-                al_row[w] = (uint32_t)(m >> (32 * lane));
-        }
-    }
-}
+// 5. the tile walk.  One block owns a tile of kStateTile states x kThreads
+// tokens (one per lane, so stores are coalesced).  Dynamic LDS holds the
+// byte-class map and the table: the whole table when S * Cp * 2 fits in
+// `lds_table_bytes` (then followed by an all-DEAD sentinel row), else the
+// tile's rows.  Either way a lane walks its token from kLockG of the tile's
+// states at once.
 
 // The tile walk when the whole table is in LDS: a lane walks its token from
-// kWholeG of the tile's states at once, one byte per iteration (the class
-// shared by the states, kWholeG independent LDS reads per iteration instead
+// kLockG of the tile's states at once, one byte per iteration (the class
+// shared by the states, kLockG independent LDS reads per iteration instead
 // of one dependent read per move), until every one of them is dead or the
 // token ends.  A dead state is row S, an all-DEAD sentinel row, which every
 // read maps back to S, so the walk needs no branch per state.  Each group's
@@ -368,10 +239,10 @@ __device__ __forceinline__ void walk_tile_whole(const uint16_t *tab, const uint8
     const uint32_t dead = (uint32_t)S;
     const int t0 = t_base + wave * kWave;  // a multiple of 64
     const int w = t0 / 32 + lane;
-    for (int g = 0; g < nS; g += kWholeG) {
-        uint32_t st[kWholeG];
+    for (int g = 0; g < nS; g += kLockG) {
+        uint32_t st[kLockG];
 #pragma unroll
-        for (int k = 0; k < kWholeG; ++k) {
+        for (int k = 0; k < kLockG; ++k) {
             const int s = s0 + g + k;
             st[k] = g + k < nS ? (uint32_t)s : dead;
             if (len < 0)  // EOS: only where the scanner may stop; past the last token: dead
@@ -380,7 +251,7 @@ __device__ __forceinline__ void walk_tile_whole(const uint16_t *tab, const uint8
         }
         uint32_t m = st[0];
 #pragma unroll
-        for (int k = 1; k < kWholeG; ++k)
+        for (int k = 1; k < kLockG; ++k)
             m = min(m, st[k]);
         bool go = len > 0 && m != dead;  // an empty token keeps the state
         uint64_t cr = classes;
@@ -394,21 +265,104 @@ __device__ __forceinline__ void walk_tile_whole(const uint16_t *tab, const uint8
                 c = cls[bytes[ti.w + h]];
             }
 #pragma unroll
-            for (int k = 0; k < kWholeG; ++k)
+            for (int k = 0; k < kLockG; ++k)
                 st[k] = min((uint32_t)tab[st[k] * (uint32_t)Cp + c], dead);
             h += 1;
             m = st[0];
 #pragma unroll
-            for (int k = 1; k < kWholeG; ++k)
+            for (int k = 1; k < kLockG; ++k)
                 m = min(m, st[k]);
             go = m != dead && h < (uint32_t)len;
         }
 #pragma unroll
-        for (int k = 0; k < kWholeG; ++k) {
+        for (int k = 0; k < kLockG; ++k) {
             if (g + k >= nS)
                 break;
             const int s = s0 + g + k;
             const bool alive = st[k] != dead;
+            if (t < V)
+                next_state[(size_t)s * V + t] = alive ? (int32_t)st[k] : -1;
+            const uint64_t mask = __ballot(alive);
+            if (lane < 2 && w < W)
+                allow[(size_t)s * W + w] = (uint32_t)(mask >> (32 * lane));
+        }
+    }
+}
+
+// The tile walk when only the tile's rows are in LDS, in lockstep: a lane
+// walks its token from kLockG of the tile's states at once, the first move
+// from the LDS rows, later ones from the cache-resident table at 32-bit
+// offsets (a dead state skips its read under the exec mask), so a long walk
+// costs a chain of independent reads rather than one dependent read per
+// move of every state.  Results go straight to coalesced stores.
+__device__ __forceinline__ void walk_tile_rows(const uint16_t *tab, const uint16_t *__restrict__ table,
+                                               const uint8_t *cls, int Cp, int s0, int nS,
+                                               const uint8_t *__restrict__ bytes, int t_base, int V, int W,
+                                               const uint4 *__restrict__ tokinfo,
+                                               const uint8_t *__restrict__ accepting,
+                                               int32_t *__restrict__ next_state, uint32_t *__restrict__ allow)
+{
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1), wave = tid / kWave;
+    const int t = t_base + tid;
+    const uint4 ti = t < V ? tokinfo[t] : make_uint4(0, 0, (uint32_t)kPastEnd, 0);
+    const int len = (int)ti.z;
+    const uint64_t classes = ((uint64_t)ti.y << 32) | ti.x;  // the first kRegBytes byte classes
+    const char *tab_bytes = reinterpret_cast<const char *>(table);
+    const uint32_t Cp2 = 2u * (uint32_t)Cp;
+    const int t0 = t_base + wave * kWave;  // a multiple of 64
+    const int w = t0 / 32 + lane;
+    for (int g = 0; g < nS; g += kLockG) {
+        uint32_t st[kLockG];
+        const uint32_t c0 = ti.x & 0xFFu;
+#pragma unroll
+        for (int k = 0; k < kLockG; ++k) {
+            const int s = s0 + g + k;
+            uint32_t v = kDead16;
+            if (g + k < nS) {
+                if (len > 0)
+                    v = tab[(g + k) * Cp + c0];  // the first move, from the row tile
+                else if (len == 0)
+                    v = (uint32_t)s;  // an empty token keeps the state
+                else if (len == kEosLen && accepting != nullptr && accepting[s] != 0)
+                    v = (uint32_t)s;  // EOS: only where the scanner may stop
+            }
+            st[k] = v;
+        }
+        uint32_t m = st[0];
+#pragma unroll
+        for (int k = 1; k < kLockG; ++k)
+            m = min(m, st[k]);
+        bool go = len > 1 && m != kDead16;
+        uint64_t cr = classes >> 8;
+        uint32_t h = 1;
+        while (go) {
+            uint32_t c;
+            if (h < (uint32_t)kRegBytes) {
+                c = (uint32_t)cr & 0xFFu;
+                cr >>= 8;
+            } else {
+                c = cls[bytes[ti.w + h]];
+            }
+#pragma unroll
+            for (int k = 0; k < kLockG; ++k)
+                if (st[k] != kDead16) {
+                    const uint32_t boff = __umul24(st[k], Cp2) + 2u * c;  // < 2^32: S <= 65535, Cp <= 256
+                    st[k] = *reinterpret_cast<const uint16_t *>(tab_bytes + boff);
+                }
+            h += 1;
+            m = st[0];
+#pragma unroll
+            for (int k = 1; k < kLockG; ++k)
+                m = min(m, st[k]);
+            go = m != kDead16 && h < (uint32_t)len;
+        }
+#pragma unroll
+        for (int k = 0; k < kLockG; ++k) {
+            if (g + k >= nS)
+                break;
+            const int s = s0 + g + k;
+            const bool alive = st[k] != kDead16;
             if (t < V)
                 next_state[(size_t)s * V + t] = alive ? (int32_t)st[k] : -1;
             const uint64_t mask = __ballot(alive);
@@ -430,7 +384,6 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
     extern __shared__ __align__(16) uint8_t smem[];
     uint8_t *cls = smem;
     uint16_t *tab = reinterpret_cast<uint16_t *>(smem + 256);
-    uint16_t *res = reinterpret_cast<uint16_t *>(smem + 256 + lds_table_bytes);
 
     const int tid = threadIdx.x;
     const int Cp = reinterpret_cast<const int32_t *>(ws)[1];
@@ -447,8 +400,7 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
         uint32_t *dst = reinterpret_cast<uint32_t *>(tab);
         for (int i = tid; i < n32; i += kThreads)
             dst[i] = src[i];
-        // the sentinel row S (all DEAD) right after the table, in the part
-        // of the allocation the tile results would use: Cp * 2 <= 512 bytes
+        // the sentinel row S (all DEAD) right after the table: Cp * 2 <= kSentinelLds
         for (int i = tid; i < Cp; i += kThreads)
             tab[S * Cp + i] = kDead16;
     }
@@ -471,7 +423,7 @@ __global__ __launch_bounds__(kThreads) void walk_kernel(const uint8_t *__restric
         if (whole)
             walk_tile_whole(tab, cls, Cp, S, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state, allow);
         else
-            walk_tile(tab, res, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state, allow);
+            walk_tile_rows(tab, table, cls, Cp, s0, nS, bytes, t_base, V, W, tokinfo, accepting, next_state, allow);
     }
 }
 
@@ -659,7 +611,7 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
     // LDS beyond the default 64 KB per block must be opted into once.
     static const hipError_t lds_attr = hipFuncSetAttribute(
         reinterpret_cast<const void *>(walk_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-        256 + kWholeLdsMax + kResLds);
+        256 + kWholeLdsMax + kSentinelLds);
     if (lds_attr != hipSuccess)
         return lds_attr;
     static const hipError_t prefix_lds_attr = hipFuncSetAttribute(
@@ -695,11 +647,11 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
     long long cap = prefix ? kTileDeferGrid : ntiles;
     const int cus = device_compute_units();
     if (S <= 512 && cus > 0) {
-        const int per_cu = kLdsPerCu / (256 + lds_table + kResLds);
+        const int per_cu = kLdsPerCu / (256 + lds_table + kSentinelLds);
         cap = min(cap, (long long)(per_cu > 1 ? per_cu : 1) * cus);
     }
     const int grid = (int)(ntiles < cap ? ntiles : cap);
-    walk_kernel<<<grid, kThreads, 256 + lds_table + kResLds, stream>>>(ws, table, S, tokinfo, bytes, V, W,
+    walk_kernel<<<grid, kThreads, 256 + lds_table + kSentinelLds, stream>>>(ws, table, S, tokinfo, bytes, V, W,
                                                                        lds_table, prefix ? 1 : 0, accepting,
                                                                        next_state, allow);
     return hipGetLastError();
