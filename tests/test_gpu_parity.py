@@ -134,6 +134,33 @@ def test_align_large_dfa(dv, S, V, max_len, p_empty, alphabet, eos):
     np.testing.assert_array_equal(u32(al), al_o)
 
 
+@pytest.mark.parametrize("S,live_lo,eos", [(2000, 128, None), (1500, 200, 11)])
+def test_align_wide_alphabet_long_walks(dv, S, live_lo, eos):
+    """A DFA too large to stage whole with most of the 256 bytes live from
+    every state, over BPE-like tokens: walks survive for several bytes (3-4
+    moves per pair), so the tile walk's lockstep groups run long."""
+    _say(f"align wide alphabet S={S} live>={live_lo} eos={eos}")
+    rng = np.random.default_rng(S + live_lo)
+    trans = np.full((S, 256), -1, np.int32)
+    for s in range(S):
+        k = int(rng.integers(live_lo, 257))
+        cols = rng.choice(256, size=k, replace=False)
+        trans[s, cols] = rng.integers(0, S, size=k)
+    offsets, data = W.vocab(8)
+    V = 4000
+    offsets, data = offsets[:V + 1].copy(), data[:offsets[V]].copy()
+    if eos is None:
+        ns, al = _align(dv, trans, offsets, data)
+        ns_o, al_o = oracle.align(trans, offsets, data)
+    else:
+        acc = (rng.random(S) < 0.2).astype(np.uint8)
+        ns, al = dv.align(_dev(trans), _dev(offsets), _dev(data), accepting=_dev(acc), eos_token=eos)
+        torch.cuda.synchronize()
+        ns_o, al_o = oracle.align_eos(trans, offsets, data, acc, eos)
+    np.testing.assert_array_equal(ns.cpu().numpy(), ns_o)
+    np.testing.assert_array_equal(u32(al), al_o)
+
+
 def test_align_all_tokens_empty(dv):
     trans = np.zeros((4, 256), np.int32)
     offsets = np.zeros(70, np.int32)
