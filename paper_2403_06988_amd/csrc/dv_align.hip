@@ -9,7 +9,7 @@
 //      share one extra class whose column is all DEAD (it exists only when
 //      some byte is dead, so the C <= 256 classes always fit in a byte).
 //   3. compact: uint16 table [S][Cp] over the live columns, then the DEAD
-//      column (DEAD = 0xFFFF).
+//      column (DEAD = 0xFFFF).  (3 and 4 run in one launch.)
 //      Random printable-ASCII DFAs keep ~95 of 256 columns, so the table is
 //      ~2.7x smaller than the int32 input and stays resident in each XCD's L2.
 //   4. token_info: each token's first 8 byte classes, length and offset.
@@ -154,9 +154,9 @@ __global__ __launch_bounds__(kThreads) void byte_classes_kernel(const uint32_t *
 
 // 3. compacted uint16 table [S][Cp]; columns C .. Cp-1 (the dead bytes'
 // class and padding) are DEAD.
-__global__ __launch_bounds__(kThreads) void compact_kernel(const int32_t *__restrict__ trans, int S,
-                                                           const uint8_t *__restrict__ ws,
-                                                           uint16_t *__restrict__ table)
+__device__ __forceinline__ void compact_rows(const int32_t *__restrict__ trans, int S,
+                                             const uint8_t *__restrict__ ws, uint16_t *__restrict__ table,
+                                             int block)
 {
     const int32_t *meta = reinterpret_cast<const int32_t *>(ws);
     const int C = meta[0], Cp = meta[1];
@@ -164,7 +164,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const int32_t *__rest
     if (c >= Cp)
         return;
     const int byte = c < C ? ws[512 + c] : 0;
-    const int r0 = blockIdx.x * 16;
+    const int r0 = block * 16;
     const int r1 = min(S, r0 + 16);
 #pragma unroll 4
     for (int s = r0; s < r1; ++s) {
@@ -180,15 +180,14 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const int32_t *__rest
 // 4. per token: the classes of its first kRegBytes bytes (four per word),
 // its length and offset -- read once per block by the walk instead of
 // re-deriving them from the bytes in every block.
-__global__ __launch_bounds__(kThreads) void token_info_kernel(const int32_t *__restrict__ offsets,
-                                                              const uint8_t *__restrict__ bytes, int V,
-                                                              int eos_token, const uint8_t *__restrict__ ws,
-                                                              uint4 *__restrict__ tokinfo)
+__device__ __forceinline__ void token_records(const int32_t *__restrict__ offsets,
+                                              const uint8_t *__restrict__ bytes, int V, int eos_token,
+                                              const uint8_t *__restrict__ ws, uint4 *__restrict__ tokinfo,
+                                              uint8_t *cls, int block)
 {
-    __shared__ uint8_t cls[256];
     cls[threadIdx.x] = ws[256 + threadIdx.x];
     __syncthreads();
-    const int t = blockIdx.x * kThreads + threadIdx.x;
+    const int t = block * kThreads + threadIdx.x;
     if (t >= V)
         return;
     if (t == eos_token) {  // its bytes are ignored: allowed exactly in accepting states
@@ -207,6 +206,21 @@ __global__ __launch_bounds__(kThreads) void token_info_kernel(const int32_t *__r
             hi |= c << (8 * (h - 4));
     }
     tokinfo[t] = make_uint4(lo, hi, (uint32_t)len, (uint32_t)off);
+}
+
+// 3 and 4 share one launch (both need only the byte classes): the first
+// ceil(S / 16) blocks compact the table, the rest build the token records.
+__global__ __launch_bounds__(kThreads) void compact_and_tokens_kernel(
+    const int32_t *__restrict__ trans, int S, const int32_t *__restrict__ offsets,
+    const uint8_t *__restrict__ bytes, int V, int eos_token, const uint8_t *__restrict__ ws,
+    uint16_t *__restrict__ table, uint4 *__restrict__ tokinfo)
+{
+    __shared__ uint8_t cls[256];
+    const int ncompact = (S + 15) / 16;
+    if ((int)blockIdx.x < ncompact)
+        compact_rows(trans, S, ws, table, blockIdx.x);
+    else
+        token_records(offsets, bytes, V, eos_token, ws, tokinfo, cls, blockIdx.x - ncompact);
 }
 
 // 5. the tile walk.  One block owns a tile of kStateTile states x kThreads
@@ -621,9 +635,8 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
 
     live_columns_kernel<<<nblk, kThreads, 0, stream>>>(trans, S, partial);
     byte_classes_kernel<<<1, kThreads, 0, stream>>>(partial, nblk, ws);
-    compact_kernel<<<(S + 15) / 16, kThreads, 0, stream>>>(trans, S, ws, table);
-    token_info_kernel<<<(V + kThreads - 1) / kThreads, kThreads, 0, stream>>>(offsets, bytes, V, eos_token, ws,
-                                                                              tokinfo);
+    compact_and_tokens_kernel<<<(S + 15) / 16 + (V + kThreads - 1) / kThreads, kThreads, 0, stream>>>(
+        trans, S, offsets, bytes, V, eos_token, ws, table, tokinfo);
     // Tables of at most kPrefixMaxCp columns that are not staged whole go to
     // the prefix-table walk; the column count is known only on the device,
     // so when such a table is possible both walks are launched and each
