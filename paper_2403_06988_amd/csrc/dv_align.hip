@@ -73,7 +73,12 @@ constexpr int kPrefStride = kPrefixMaxCp * kPrefixMaxCp + kPrefixMaxCp;  // entr
 constexpr int kPrefWaveSpan = 1024;  // tokens per wave between allow-word writes: 32 words per state
 constexpr int kPrefWordsOffset = 256 + kPrefR * kPrefStride * 2;  // 4-byte aligned: the stride is even
 constexpr int kPrefLds = kPrefWordsOffset + kPrefThreads / 64 * kPrefR * 32 * 4;
+// Token ranges per state group: at least enough for kPrefTargetBlocks
+// blocks, and enough that no block walks more than kPrefMaxChunks rounds of
+// its 16 waves (64K tokens), so the last, partly filled round of resident
+// blocks stays short; each block builds its prefix tables once for them.
 constexpr int kPrefTargetBlocks = 2048;  // four rounds of two resident blocks per compute unit
+constexpr int kPrefMaxChunks = 4;
 constexpr int kTileDeferGrid = 8192;
 constexpr int kLdsPerCu = 160 * 1024;  // gfx950
 static_assert(kPrefR >= 1 && 2 * kPrefLds <= 160 * 1024, "two blocks per compute unit");
@@ -646,8 +651,9 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
     if (prefix) {
         const int rows = (S + kPrefR - 1) / kPrefR;
         const int chunk = kPrefThreads / kWave * kPrefWaveSpan;
-        int nr = (kPrefTargetBlocks + rows - 1) / rows;
-        nr = max(1, min(nr, (V + chunk - 1) / chunk));
+        const int nchunks = (V + chunk - 1) / chunk;
+        int nr = max((kPrefTargetBlocks + rows - 1) / rows, (nchunks + kPrefMaxChunks - 1) / kPrefMaxChunks);
+        nr = max(1, min(nr, nchunks));
         const int range = (int)align_up((size_t)((V + nr - 1) / nr), chunk);  // whole rounds of every wave
         nr = (V + range - 1) / range;
         walk_prefix_kernel<<<dim3(nr, rows), kPrefThreads, kPrefLds, stream>>>(
