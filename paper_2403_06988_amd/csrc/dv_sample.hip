@@ -13,8 +13,10 @@
 // that hold at least one allowed token into an LDS queue (one allow word of
 // 32 tokens per lane, a shuffle prefix sum for the queue offsets), then every
 // lane takes one queued group: one Philox call per group, a logarithm pair
-// per allowed token.  Sparse masks then cost in proportion to their allowed
-// groups and dense ones keep every lane busy.  Lanes combine exact
+// per allowed token.  Where a wave's allowed tokens are hardly more than its
+// groups (sparse masks) it queues single tokens instead, so that no lane
+// waits on a neighbour's second logarithm pair; dense masks keep the groups
+// and so one Philox call per 4 tokens.  Lanes combine exact
 // (order-preserving fp32 key << 32 | ~index) maxima, so ties go to the lowest
 // index and the result does not depend on the order of the work.
 #include "dv_sample.h"
@@ -30,6 +32,18 @@ constexpr int kRowThreads = 1024;   // one block per row once B >= kOneBlockRows
 #define DV_SAMPLE_ONE_BLOCK_ROWS 1024  // four or more rows per CU keep enough waves resident
 #endif
 constexpr int kOneBlockRows = DV_SAMPLE_ONE_BLOCK_ROWS;
+// A wave queues single tokens instead of 4-token groups when its allowed
+// tokens number at most kTokenRatio4 / 4 times its allowed groups: a lane
+// then pays one Philox call and one logarithm pair per trip, where a group
+// trip pays as many pairs as the wave's fullest group holds (two or three
+// on almost every trip of a sparse random mask, while its groups average
+// 1.1 tokens).  Per trip a Philox call is about 63 instructions and a pair
+// about 90, so single tokens cost less up to about twice as many tokens as
+// groups; runs of allowed tokens (4 per group) keep the groups.
+#ifndef DV_SAMPLE_TOKEN_RATIO4
+#define DV_SAMPLE_TOKEN_RATIO4 8
+#endif
+constexpr int kTokenRatio4 = DV_SAMPLE_TOKEN_RATIO4;
 constexpr int kTargetBlocks = 2048;
 constexpr int kMaxChunks = 64;
 
@@ -193,6 +207,22 @@ __device__ __forceinline__ int wave_prefix_small(int cnt, int &total)
     return excl;
 }
 
+// The same for a count in [0, 32] (six ballots).
+__device__ __forceinline__ int wave_prefix_word(int cnt, int &total)
+{
+    int excl = 0, tot = 0;
+#pragma unroll
+    for (int j = 0; j < 6; ++j) {
+        const uint64_t m = __ballot((cnt >> j) & 1);
+        const int below = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        excl += below << j;
+        tot += __popcll(m) << j;
+    }
+    total = tot;
+    return excl;
+}
+
 template <int DT, int THREADS>
 __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
@@ -203,7 +233,7 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
 #pragma clang fp contract(off)
     constexpr int kWaves = THREADS / kWave;
     constexpr int kTokPerIter = THREADS * 32;  // one allow word per lane per iteration
-    __shared__ uint32_t queue[kWaves][kWave * 8];  // up to 8 groups per lane per iteration
+    __shared__ uint32_t queue[kWaves][kWave * 8];  // up to 8 groups per lane per iteration, or 512 tokens
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int b = blockIdx.x / nchunks;
     const int c = blockIdx.x - b * nchunks;
@@ -223,31 +253,56 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
                 word &= (1u << (t1 - tok0)) - 1u;  // a chunk ends inside this word only at V
             // groups (4 tokens) holding an allowed token: bit 4k of `nz`
             uint32_t nz = (word | (word >> 1) | (word >> 2) | (word >> 3)) & 0x11111111u;
-            int total;
-            int pos = wave_prefix_small(__popc(nz), total);  // at most 8 groups per lane
-            while (nz) {
-                const int k = __builtin_ctz(nz) >> 2;
-                nz &= nz - 1u;
-                // token group index (token / 4) and its 4 mask bits
-                queue[wave][pos++] = ((uint32_t)((tok0 >> 2) + k) << 4) | ((word >> (4 * k)) & 0xFu);
+            int groups, toks;
+            const int gpos = wave_prefix_small(__popc(nz), groups);  // at most 8 groups per lane
+            const int tpos = wave_prefix_word(__popc(word), toks);
+            // wave-uniform: single tokens when they fit the queue and are few per group
+            const bool by_token = toks <= kWave * 8 && 4 * toks <= kTokenRatio4 * groups;
+            if (by_token) {
+                int pos = tpos;
+                uint32_t w = word;
+                while (w) {
+                    queue[wave][pos++] = (uint32_t)(tok0 + __builtin_ctz(w));
+                    w &= w - 1u;
+                }
+            } else {
+                int pos = gpos;
+                while (nz) {
+                    const int k = __builtin_ctz(nz) >> 2;
+                    nz &= nz - 1u;
+                    // token group index (token / 4) and its 4 mask bits
+                    queue[wave][pos++] = ((uint32_t)((tok0 >> 2) + k) << 4) | ((word >> (4 * k)) & 0xFu);
+                }
             }
             wave_lds_sync();
-            for (int q = lane; q < total; q += kWave) {
-                const uint32_t entry = queue[wave][q];
-                const uint32_t g = entry >> 4;
-                uint32_t bitsg = entry & 0xFu;
-                // the logits first: their load is in flight during the Philox rounds
-                const uint4 xs = group_logits<DT>(row, aligned, g, bitsg, V);
-                const uint4 rnd = philox4x32_10(g, (uint32_t)b, off_lo, off_hi, seed_lo, seed_hi);
-                while (bitsg) {
-                    const int e = __builtin_ctz(bitsg);
-                    bitsg &= bitsg - 1u;
-                    const int i = (int)(g * 4u) + e;
-                    const float key =
-                        __builtin_fmaf(__uint_as_float(pick(xs, e)), inv_t, gumbel_of_word(pick(rnd, e)));
+            if (by_token) {
+                for (int q = lane; q < toks; q += kWave) {
+                    const uint32_t i = queue[wave][q];
+                    const float x = logit_at<DT>(row, (int)i);  // in flight during the Philox rounds
+                    const uint4 rnd = philox4x32_10(i >> 2, (uint32_t)b, off_lo, off_hi, seed_lo, seed_hi);
+                    const float key = __builtin_fmaf(x, inv_t, gumbel_of_word(pick(rnd, (int)(i & 3u))));
                     const uint64_t packed =
-                        ((uint64_t)order_key(__float_as_uint(key)) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i);
+                        ((uint64_t)order_key(__float_as_uint(key)) << 32) | (uint64_t)(0xFFFFFFFFu - i);
                     best = max_u64(best, packed);
+                }
+            } else {
+                for (int q = lane; q < groups; q += kWave) {
+                    const uint32_t entry = queue[wave][q];
+                    const uint32_t g = entry >> 4;
+                    uint32_t bitsg = entry & 0xFu;
+                    // the logits first: their load is in flight during the Philox rounds
+                    const uint4 xs = group_logits<DT>(row, aligned, g, bitsg, V);
+                    const uint4 rnd = philox4x32_10(g, (uint32_t)b, off_lo, off_hi, seed_lo, seed_hi);
+                    while (bitsg) {
+                        const int e = __builtin_ctz(bitsg);
+                        bitsg &= bitsg - 1u;
+                        const int i = (int)(g * 4u) + e;
+                        const float key =
+                            __builtin_fmaf(__uint_as_float(pick(xs, e)), inv_t, gumbel_of_word(pick(rnd, e)));
+                        const uint64_t packed =
+                            ((uint64_t)order_key(__float_as_uint(key)) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i);
+                        best = max_u64(best, packed);
+                    }
                 }
             }
             wave_lds_sync();  // every lane has read its entries before the next iteration writes

@@ -1147,6 +1147,66 @@ def test_sample_planted_and_random_rows(dv, dtype, inv_t, B, layout):
     np.testing.assert_array_equal(new.cpu().numpy(), n_o)
 
 
+def _queue_mode_masks(rng, S, V):
+    """Allow sets built per aligned 2,048-token window (the tokens one wave
+    compacts per pass), cycling through the patterns on both sides of the
+    sampler's choice between queuing single tokens and 4-token groups:
+    sparse random (about 1.1 tokens per group), runs of whole groups (4 per
+    group), exactly 512 tokens at 2 per group (the queue full, ratio 2),
+    513 tokens (one past the queue), ratio just above 2, empty and full."""
+    alive = np.zeros((S, V), bool)
+    nwin = (V + 2047) // 2048
+    for st in range(S):
+        for w in range(nwin):
+            lo, hi = w * 2048, min(V, (w + 1) * 2048)
+            n = hi - lo
+            kind = (st * nwin + w) % 7
+            m = np.zeros(n, bool)
+            if kind == 0:
+                m = rng.random(n) < 0.05
+            elif kind == 1:  # runs of whole groups
+                for g0 in rng.choice(n // 4, size=min(n // 4, 75), replace=False):
+                    m[4 * g0:4 * g0 + 4] = True
+            elif kind in (2, 3) and n >= 2048:  # 256 groups of 2 (+ one more token for 513)
+                groups = rng.choice(512, size=257, replace=False)
+                for g0 in groups[:256]:
+                    m[4 * g0 + rng.choice(4, size=2, replace=False)] = True
+                if kind == 3:
+                    m[4 * groups[256] + rng.integers(0, 4)] = True
+            elif kind == 4 and n >= 2048:  # 100 groups of 2 and 20 of 3: 4 T = 1,040 > 8 G = 960
+                groups = rng.choice(n // 4, size=120, replace=False)
+                for i, g0 in enumerate(groups):
+                    m[4 * g0 + rng.choice(4, size=2 if i < 100 else 3, replace=False)] = True
+            elif kind == 5:
+                m[:] = True
+            alive[st, lo:hi] = m
+    return alive
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("B", [40, 1030])
+def test_sample_token_and_group_queues(dv, dtype, B):
+    """Masks on both sides of every bound of the token-or-group queue choice
+    (see `_queue_mode_masks`), V = 20,517 (a ragged last window), rows split
+    over blocks (B = 40) and one block per row (B = 1,030)."""
+    rng = np.random.default_rng(9000 + B + (dtype == torch.float32))
+    S, V = 9, 2048 * 10 + 37
+    alive = _queue_mode_masks(rng, S, V)
+    ns = np.where(alive, rng.integers(0, S, (S, V)), -1).astype(np.int32)
+    Wd = (V + 31) // 32
+    pad = np.zeros((S, Wd * 32), bool)
+    pad[:, :V] = alive
+    al = np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(S, Wd)
+    states = np.concatenate([np.arange(S), rng.integers(-1, S, B - S)]).astype(np.int32)
+    x_h = torch.from_numpy((rng.standard_normal((B, V)) * 3).astype(np.float32)).to(dtype)
+    x = x_h.to(DEV)
+    for seed, off in ((3, 0), (4, 17)):
+        tok, new = dv.masked_sample(_dev(ns), _dev(al.view(np.int32)), _dev(states), x, seed, off)
+        t_o, n_o = oracle.masked_sample(ns, al, states, to_oracle(x_h), 1.0, seed, off)
+        np.testing.assert_array_equal(tok.cpu().numpy(), t_o)
+        np.testing.assert_array_equal(new.cpu().numpy(), n_o)
+
+
 def test_sample_is_reproducible_and_graph_safe(dv):
     w = W.WORKLOADS[3]
     trans, offsets, data, ns, al = _workload_table(dv, 3)
