@@ -11,7 +11,8 @@
 // 32x32->64 multiplies) per 4 tokens and two logarithms per token.  Only
 // admissible tokens need noise, so each wave compacts its 4-token groups
 // that hold at least one allowed token into an LDS queue (one allow word of
-// 32 tokens per lane, a shuffle prefix sum for the queue offsets), then every
+// 32 tokens per lane, or half of one when few blocks are resident; ballot
+// prefix sums for the queue offsets), then every
 // lane takes one queued group: one Philox call per group, a logarithm pair
 // per allowed token.  Where a wave's allowed tokens are hardly more than its
 // groups (sparse masks) it queues single tokens instead, so that no lane
@@ -45,28 +46,41 @@ constexpr int kOneBlockRows = DV_SAMPLE_ONE_BLOCK_ROWS;
 #endif
 constexpr int kTokenRatio4 = DV_SAMPLE_TOKEN_RATIO4;
 constexpr int kTargetBlocks = 2048;
+constexpr int kHalfSpanBlocks = 512;
 constexpr int kMaxChunks = 64;
 
 struct SampleGeometry {
     int threads;
-    int chunk_tok;  // a multiple of threads * 32 tokens (one allow word per lane per iteration)
+    int chunk_tok;  // a multiple of threads * span tokens (span tokens per lane per iteration)
     int nchunks;
+    int span;  // tokens per lane per iteration: 32 (a whole allow word) or 16
 };
 
 SampleGeometry sample_geometry(int B, int V)
 {
     if (B >= kOneBlockRows) {
         const int per_iter = kRowThreads * 32;
-        return {kRowThreads, (V + per_iter - 1) / per_iter * per_iter, 1};
+        return {kRowThreads, (V + per_iter - 1) / per_iter * per_iter, 1, 32};
     }
-    const int per_iter = kThreads * 32;
+    const int b = B > 0 ? B : 1;
+    // Below two blocks per compute unit (a row of whole allow words per lane
+    // giving fewer than kHalfSpanBlocks blocks), lanes take half a word each:
+    // twice the waves for the same tokens, which this issue-bound kernel
+    // needs when so few are resident (B = 64 x V = 32,000: 11-12 against
+    // 15.5-16.5 us per step).  Above that the extra blocks only add their
+    // start-up and their meeting in the workspace (B = 64 x V = 128,256:
+    // 17.3 against 11.2 us).
+    int span = 32;
+    if ((int64_t)b * ((V + kThreads * 32 - 1) / (kThreads * 32)) < kHalfSpanBlocks)
+        span = 16;
+    const int per_iter = kThreads * span;
     const int iters = (V + per_iter - 1) / per_iter;
-    int want = (kTargetBlocks + (B > 0 ? B : 1) - 1) / (B > 0 ? B : 1);
+    int want = (kTargetBlocks + b - 1) / b;
     want = want > iters ? iters : want;
     want = want > kMaxChunks ? kMaxChunks : want;
     want = want < 1 ? 1 : want;
     const int per = (iters + want - 1) / want;
-    return {kThreads, per * per_iter, (iters + per - 1) / per};
+    return {kThreads, per * per_iter, (iters + per - 1) / per, span};
 }
 
 __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
@@ -223,7 +237,7 @@ __device__ __forceinline__ int wave_prefix_word(int cnt, int &total)
     return excl;
 }
 
-template <int DT, int THREADS>
+template <int DT, int THREADS, int SPAN>
 __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
     const int32_t *__restrict__ states, const void *__restrict__ logits, int64_t ld, float inv_t, uint32_t seed_lo,
@@ -232,7 +246,8 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
 {
 #pragma clang fp contract(off)
     constexpr int kWaves = THREADS / kWave;
-    constexpr int kTokPerIter = THREADS * 32;  // one allow word per lane per iteration
+    static_assert(SPAN == 32 || SPAN == 16, "a whole allow word or one half of it per lane");
+    constexpr int kTokPerIter = THREADS * SPAN;
     __shared__ uint32_t queue[kWaves][kWave * 8];  // up to 8 groups per lane per iteration, or 512 tokens
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int b = blockIdx.x / nchunks;
@@ -247,10 +262,12 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
         const int t0 = c * chunk_tok;
         const int t1 = min(V, t0 + chunk_tok);
         for (int base = t0; base < t1; base += kTokPerIter) {  // block-uniform trip count
-            const int tok0 = base + tid * 32;
+            const int tok0 = base + tid * SPAN;  // a multiple of SPAN: the word's low or high half
             uint32_t word = tok0 < t1 ? arow[tok0 >> 5] : 0u;
-            if (tok0 < t1 && t1 - tok0 < 32)
-                word &= (1u << (t1 - tok0)) - 1u;  // a chunk ends inside this word only at V
+            if constexpr (SPAN == 16)
+                word = (word >> (tok0 & 16)) & 0xFFFFu;
+            if (tok0 < t1 && t1 - tok0 < SPAN)
+                word &= (1u << (t1 - tok0)) - 1u;  // a chunk ends inside this span only at V
             // groups (4 tokens) holding an allowed token: bit 4k of `nz`
             uint32_t nz = (word | (word >> 1) | (word >> 2) | (word >> 3)) & 0x11111111u;
             int groups, toks;
@@ -346,20 +363,25 @@ hipError_t launch_masked_sample(const int32_t *next_state, const uint32_t *allow
     const unsigned grid = (unsigned)B * (unsigned)g.nchunks;
     const uint32_t s_lo = (uint32_t)seed, s_hi = (uint32_t)(seed >> 32);
     const uint32_t o_lo = (uint32_t)offset, o_hi = (uint32_t)(offset >> 32);
-#define DV_SAMPLE_LAUNCH(DT, T)                                                                                  \
-    masked_sample_kernel<DT, T><<<grid, T, 0, stream>>>(next_state, allow, S, V, W, states, logits, ld,          \
-                                                        inv_temperature, s_lo, s_hi, o_lo, o_hi, g.chunk_tok,    \
-                                                        g.nchunks, meet, token, new_state)
+#define DV_SAMPLE_LAUNCH(DT, T, SP)                                                                              \
+    masked_sample_kernel<DT, T, SP><<<grid, T, 0, stream>>>(next_state, allow, S, V, W, states, logits, ld,      \
+                                                            inv_temperature, s_lo, s_hi, o_lo, o_hi,             \
+                                                            g.chunk_tok, g.nchunks, meet, token, new_state)
     if (g.threads == kRowThreads) {
         if (dtype == 0)
-            DV_SAMPLE_LAUNCH(0, kRowThreads);
+            DV_SAMPLE_LAUNCH(0, kRowThreads, 32);
         else
-            DV_SAMPLE_LAUNCH(1, kRowThreads);
+            DV_SAMPLE_LAUNCH(1, kRowThreads, 32);
+    } else if (g.span == 32) {
+        if (dtype == 0)
+            DV_SAMPLE_LAUNCH(0, kThreads, 32);
+        else
+            DV_SAMPLE_LAUNCH(1, kThreads, 32);
     } else {
         if (dtype == 0)
-            DV_SAMPLE_LAUNCH(0, kThreads);
+            DV_SAMPLE_LAUNCH(0, kThreads, 16);
         else
-            DV_SAMPLE_LAUNCH(1, kThreads);
+            DV_SAMPLE_LAUNCH(1, kThreads, 16);
     }
 #undef DV_SAMPLE_LAUNCH
     return hipGetLastError();

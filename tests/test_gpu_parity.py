@@ -1184,11 +1184,12 @@ def _queue_mode_masks(rng, S, V):
 
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-@pytest.mark.parametrize("B", [40, 1030])
+@pytest.mark.parametrize("B", [40, 200, 1030])
 def test_sample_token_and_group_queues(dv, dtype, B):
     """Masks on both sides of every bound of the token-or-group queue choice
     (see `_queue_mode_masks`), V = 20,517 (a ragged last window), rows split
-    over blocks (B = 40) and one block per row (B = 1,030)."""
+    over blocks with half an allow word per lane (B = 40) and a whole word
+    (B = 200), and one block per row (B = 1,030)."""
     rng = np.random.default_rng(9000 + B + (dtype == torch.float32))
     S, V = 9, 2048 * 10 + 37
     alive = _queue_mode_masks(rng, S, V)
