@@ -589,10 +589,9 @@ def main():
     trans, _ = W.dfa(wid)
     offsets, data = W.vocab(wid)
     init = W.init_states(wid)
-    trans_d = torch.from_numpy(trans).to(dev)
-    offsets_d = torch.from_numpy(offsets).to(dev)
-    data_d = torch.from_numpy(data).to(dev)
-    init_d = torch.from_numpy(init).to(dev)
+    # the workload arrays are cached read-only; torch wants writable ones
+    trans_d, offsets_d, data_d, init_d = (torch.from_numpy(np.require(a, requirements=["C", "W"])).to(dev)
+                                          for a in (trans, offsets, data, init))
     x = W.logits_all(wid, device=dev)
     ns = torch.empty((w.S, w.V), dtype=torch.int32, device=dev)
     al = torch.empty((w.S, w.words), dtype=torch.int32, device=dev)

@@ -35,7 +35,8 @@ DEV = torch.device("cuda:0")
 
 
 def _dev(a):
-    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    # a copy only where the array is not contiguous or is read-only (cached tables)
+    return torch.from_numpy(np.require(a, requirements=["C", "W"])).to(DEV)
 
 
 def _align(dv, trans, offsets, data):
