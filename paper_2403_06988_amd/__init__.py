@@ -146,15 +146,14 @@ def align(trans, offsets, tok_bytes, next_state=None, allow=None, workspace=None
     if next_state.numel() != S * V or allow.numel() != S * Wd:
         raise ValueError("next_state / allow have the wrong size")
     need = align_workspace_bytes(S, max(V, 1))
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    _want(workspace, "workspace", torch.uint8, dev)
+    workspace, ws_bytes = _workspace(workspace, need, dev,
+                                     lambda: torch.empty(max(need, 1), dtype=torch.uint8, device=dev))
     bytes_ptr = _ptr(tok_bytes) if tok_bytes.numel() else None
     if eos_token is None:
         if accepting is not None:
             raise ValueError("accepting is only meaningful with eos_token")
         st = lib.dv_align(_ptr(trans), S, _ptr(offsets), bytes_ptr, V, _ptr(next_state), _ptr(allow),
-                          _ptr(workspace), workspace.numel(), _stream(stream, dev))
+                          _ptr(workspace), ws_bytes, _stream(stream, dev))
         _check(st, "dv_align")
     else:
         if accepting is not None:
@@ -163,7 +162,7 @@ def align(trans, offsets, tok_bytes, next_state=None, allow=None, workspace=None
                 raise ValueError("accepting must have one flag per state")
         st = lib.dv_align_eos(_ptr(trans), S, _ptr(offsets), bytes_ptr, V, _ptr(accepting),
                               int(eos_token), _ptr(next_state), _ptr(allow), _ptr(workspace),
-                              workspace.numel(), _stream(stream, dev))
+                              ws_bytes, _stream(stream, dev))
         _check(st, "dv_align_eos")
     return next_state, allow
 
@@ -175,6 +174,56 @@ def step_workspace(batch: int, num_tokens: int, device) -> torch.Tensor:
     return torch.zeros(max(n, 1), dtype=torch.uint8, device=device)
 
 
+def _out(t, name, n, dev):
+    """A caller-supplied int32 output of n elements (or a new one)."""
+    if t is None:
+        return torch.empty(n, dtype=torch.int32, device=dev)
+    _want(t, name, torch.int32, dev)
+    if t.numel() != n:
+        raise ValueError(f"{name} must have {n} elements, got {t.numel()}")
+    return t
+
+
+def _workspace(ws, need, dev, make):
+    """A caller-supplied workspace of at least ``need`` bytes (or a new one);
+    returns (tensor, its size in bytes)."""
+    if ws is None:
+        ws = make()
+    if not ws.is_cuda or ws.device != dev:
+        raise ValueError(f"workspace must be a device tensor on {dev}")
+    if not ws.is_contiguous():
+        raise ValueError("workspace must be contiguous")
+    nbytes = ws.numel() * ws.element_size()
+    if nbytes < need:
+        raise ValueError(f"workspace holds {nbytes} bytes, {need} needed")
+    return ws, nbytes
+
+
+def _step_args(next_state, allow, states, logits):
+    """Checks shared by the step calls; returns (S, V, B, ld, dtype code)."""
+    dev = states.device
+    _want(next_state, "next_state", torch.int32, dev)
+    _want(allow, "allow", torch.int32, dev)
+    _want(states, "states", torch.int32, dev)
+    dt = _dtype_code(logits)
+    if not logits.is_cuda or logits.device != dev:
+        raise ValueError("logits must be on the same device as states")
+    if next_state.dim() != 2:
+        raise ValueError("next_state must be [S][V]")
+    S, V = next_state.shape
+    if allow.numel() != S * ((V + 31) // 32):
+        raise ValueError("allow must be [S][ceil(V/32)]")
+    B = states.shape[0]
+    if states.dim() != 1:
+        raise ValueError("states must be [B]")
+    if logits.dim() != 2 or logits.shape[0] != B or logits.shape[1] != V:
+        raise ValueError(f"logits must be [{B}][{V}] (a wider row stride is allowed)")
+    if B and logits.stride(1) != 1:
+        raise ValueError("logits must have unit stride along the vocabulary")
+    ld = logits.stride(0) if B > 1 else max(V, logits.stride(0))
+    return S, V, B, ld, dt
+
+
 def masked_step(next_state, allow, states, logits, token=None, new_state=None, workspace=None,
                 stream=None, opportunistic=False):
     """One greedy masked decoding step.  logits [B][ld] (fp32 or bf16, unit
@@ -182,33 +231,14 @@ def masked_step(next_state, allow, states, logits, token=None, new_state=None, w
     ``opportunistic``: check the model's own choice against the mask first
     (dv_masked_step_opportunistic; same results)."""
     dev = states.device
-    _want(next_state, "next_state", torch.int32, dev)
-    _want(allow, "allow", torch.int32, dev)
-    _want(states, "states", torch.int32, dev)
-    if logits.dtype == torch.float32:
-        dt = DV_F32
-    elif logits.dtype == torch.bfloat16:
-        dt = DV_BF16
-    else:
-        raise TypeError(f"logits must be float32 or bfloat16, got {logits.dtype}")
-    if not logits.is_cuda or logits.device != dev:
-        raise ValueError("logits must be on the same device as states")
-    S, V = next_state.shape
-    B = states.shape[0]
-    if logits.dim() != 2 or logits.shape[0] != B or logits.shape[1] != V:
-        raise ValueError(f"logits must be [{B}][{V}] (a wider row stride is allowed)")
-    if B and logits.stride(1) != 1:
-        raise ValueError("logits must have unit stride along the vocabulary")
-    ld = logits.stride(0) if B > 1 else max(V, logits.stride(0))
-    if token is None:
-        token = torch.empty(B, dtype=torch.int32, device=dev)
-    if new_state is None:
-        new_state = torch.empty(B, dtype=torch.int32, device=dev)
-    if workspace is None:
-        workspace = step_workspace(B, V, dev)
+    S, V, B, ld, dt = _step_args(next_state, allow, states, logits)
+    token = _out(token, "token", B, dev)
+    new_state = _out(new_state, "new_state", B, dev)
+    workspace, nbytes = _workspace(workspace, masked_step_workspace_bytes(B, V), dev,
+                                   lambda: step_workspace(B, V, dev))
     fn = lib.dv_masked_step_opportunistic if opportunistic else lib.dv_masked_step
     st = fn(_ptr(next_state), _ptr(allow), S, V, _ptr(states), _ptr(logits), dt, B, ld, _ptr(token),
-            _ptr(new_state), _ptr(workspace), workspace.numel(), _stream(stream, dev))
+            _ptr(new_state), _ptr(workspace), nbytes, _stream(stream, dev))
     _check(st, "dv_masked_step_opportunistic" if opportunistic else "dv_masked_step")
     return token, new_state
 
@@ -231,26 +261,14 @@ def masked_sample(next_state, allow, states, logits, seed: int, offset: int, inv
     (seed, offset, row, token); use a new offset for every step).  logits
     [B][ld] fp32 or bf16.  Returns (token [B], new_state [B])."""
     dev = states.device
-    _want(next_state, "next_state", torch.int32, dev)
-    _want(allow, "allow", torch.int32, dev)
-    _want(states, "states", torch.int32, dev)
-    dt = _dtype_code(logits)
-    S, V = next_state.shape
-    B = states.shape[0]
-    if logits.dim() != 2 or logits.shape[0] != B or logits.shape[1] != V or not logits.is_cuda:
-        raise ValueError(f"logits must be a [{B}][{V}] device tensor (a wider row stride is allowed)")
-    if B and logits.stride(1) != 1:
-        raise ValueError("logits must have unit stride along the vocabulary")
-    ld = logits.stride(0) if B > 1 else max(V, logits.stride(0))
-    if token is None:
-        token = torch.empty(B, dtype=torch.int32, device=dev)
-    if new_state is None:
-        new_state = torch.empty(B, dtype=torch.int32, device=dev)
-    if workspace is None:
-        workspace = sample_workspace(B, V, dev)
+    S, V, B, ld, dt = _step_args(next_state, allow, states, logits)
+    token = _out(token, "token", B, dev)
+    new_state = _out(new_state, "new_state", B, dev)
+    workspace, nbytes = _workspace(workspace, masked_sample_workspace_bytes(B, V), dev,
+                                   lambda: sample_workspace(B, V, dev))
     st = lib.dv_masked_sample(_ptr(next_state), _ptr(allow), S, V, _ptr(states), _ptr(logits), dt, B, ld,
                               float(inv_temperature), int(seed) & (2**64 - 1), int(offset) & (2**64 - 1),
-                              _ptr(token), _ptr(new_state), _ptr(workspace), workspace.numel(),
+                              _ptr(token), _ptr(new_state), _ptr(workspace), nbytes,
                               _stream(stream, dev))
     _check(st, "dv_masked_sample")
     return token, new_state
@@ -286,10 +304,8 @@ def spec_walk(next_state, allow, states, proposals, accepted=None, final_state=N
     S, V = next_state.shape
     B = states.shape[0]
     s, ld = _proposals(proposals, B, dev)
-    if accepted is None:
-        accepted = torch.empty(B, dtype=torch.int32, device=dev)
-    if final_state is None:
-        final_state = torch.empty(B, dtype=torch.int32, device=dev)
+    accepted = _out(accepted, "accepted", B, dev)
+    final_state = _out(final_state, "final_state", B, dev)
     st = lib.dv_spec_walk(_ptr(next_state), _ptr(allow), S, V, _ptr(states),
                           _ptr(proposals) if proposals.numel() else None, s, ld, B, _ptr(accepted),
                           _ptr(final_state), _stream(stream, dev))
@@ -333,18 +349,14 @@ def spec_verify(next_state, allow, states, proposals, logits, token=None, accept
     ld_row, ld_pos = logits.stride(0), logits.stride(1)
     if token is None:
         token = torch.empty((B, s + 1), dtype=torch.int32, device=dev)
-    if accepted is None:
-        accepted = torch.empty(B, dtype=torch.int32, device=dev)
-    if new_state is None:
-        new_state = torch.empty(B, dtype=torch.int32, device=dev)
-    _want(token, "token", torch.int32, dev)
-    if token.numel() != B * (s + 1):
-        raise ValueError("token must be [B][s+1]")
-    if workspace is None:
-        workspace = spec_workspace(B, s, V, dev)
+    token = _out(token, "token", B * (s + 1), dev)
+    accepted = _out(accepted, "accepted", B, dev)
+    new_state = _out(new_state, "new_state", B, dev)
+    workspace, nbytes = _workspace(workspace, spec_verify_workspace_bytes(B, s, V), dev,
+                                   lambda: spec_workspace(B, s, V, dev))
     st = lib.dv_spec_verify(_ptr(next_state), _ptr(allow), S, V, _ptr(states),
                             _ptr(proposals) if proposals.numel() else None, s, ld, _ptr(logits), dt,
                             ld_row, ld_pos, B, _ptr(token), _ptr(accepted), _ptr(new_state),
-                            _ptr(workspace), workspace.numel(), _stream(stream, dev))
+                            _ptr(workspace), nbytes, _stream(stream, dev))
     _check(st, "dv_spec_verify")
     return token, accepted, new_state

@@ -117,7 +117,7 @@ constexpr int kAlignMetaBytes = 1024;
 constexpr int kLiveRowsPerBlock = 16;
 constexpr uint16_t kDead16 = 0xFFFF;
 
-inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+constexpr size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 inline size_t align_live_blocks(int S) { return (size_t)(S + kLiveRowsPerBlock - 1) / kLiveRowsPerBlock; }
 inline size_t align_table_offset(int S) { return align_up(kAlignMetaBytes + align_live_blocks(S) * 32, 256); }
@@ -139,8 +139,8 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
 // that arrives last reads the maximum, puts both back to zero and writes the
 // row's outputs -- one kernel, no second pass, no waiting on other blocks.
 // Layout: best [B] uint64 at 0, arrived [B] uint32 at row_meet_count_offset.
-inline size_t row_meet_count_offset(int B) { return align_up((size_t)(B > 0 ? B : 1) * 8, 256); }
-inline size_t row_meet_bytes(int B) { return row_meet_count_offset(B) + align_up((size_t)(B > 0 ? B : 1) * 4, 256); }
+constexpr size_t row_meet_count_offset(int B) { return align_up((size_t)(B > 0 ? B : 1) * 8, 256); }
+constexpr size_t row_meet_bytes(int B) { return row_meet_count_offset(B) + align_up((size_t)(B > 0 ? B : 1) * 4, 256); }
 
 struct RowMeet {
     uint64_t *best;

@@ -3,10 +3,9 @@
 Alignment tables (next_state, allow with padding bits) and greedy decoding
 chains (token, new_state at every step) are compared with the oracle, which
 computes from the same seeded inputs with its own table and its own previous
-states.  Workloads 1-3 are compared in full; workloads 4-5 (4.2 GB tables) on
-sampled state rows and sampled batch rows, plus properties over the whole
-table.  The launch configuration is the benchmark's (same shapes, same
-calls)."""
+states.  Workloads 1-3 and 6-8 are compared in full here; workloads 4-5
+(10^9-pair tables) in full in test_gpu_parity_large.py.  The launch
+configuration is the benchmark's (same shapes, same calls)."""
 import json
 import os
 
@@ -234,35 +233,6 @@ def test_align_workload_full(dv, wid):
     np.testing.assert_array_equal(u32(al), al_o)
 
 
-@pytest.mark.parametrize("wid", [4, 5])
-def test_align_workload_sampled(dv, wid):
-    w = W.WORKLOADS[wid]
-    _say(f"align workload {w.describe()} (sampled rows)")
-    trans, offsets, data, ns, al = _workload_table(dv, wid)
-    rng = np.random.default_rng(wid)
-    rows = np.unique(np.concatenate([[0, 1, w.S - 1], rng.integers(0, w.S, 45)])).astype(np.int32)
-    ns_o, al_o = oracle.align_rows(trans, offsets, data, rows)
-    idx = torch.from_numpy(rows.astype(np.int64)).to(DEV)
-    np.testing.assert_array_equal(ns.index_select(0, idx).cpu().numpy(), ns_o)
-    np.testing.assert_array_equal(u32(al.index_select(0, idx)), al_o)
-    # properties over the whole table, row block by row block
-    lens = np.diff(offsets)
-    single = np.nonzero(lens == 1)[0]
-    tcol = torch.from_numpy(trans[:, data[offsets[single]]]).to(DEV)
-    tcol = torch.where((tcol >= 0) & (tcol < w.S), tcol, torch.full_like(tcol, -1))
-    assert torch.equal(ns[:, torch.from_numpy(single).to(DEV)], tcol)  # single-byte columns
-    bits = torch.arange(32, device=DEV, dtype=torch.int32)
-    for r0 in range(0, w.S, 512):
-        blk = ns[r0:r0 + 512]
-        alive = (blk != -1)
-        pad = torch.zeros((blk.shape[0], w.words * 32), dtype=torch.bool, device=DEV)
-        pad[:, :w.V] = alive
-        words = (pad.view(blk.shape[0], w.words, 32).to(torch.int64) << bits.to(torch.int64)).sum(-1)
-        assert torch.equal(words.to(torch.int64) & 0xFFFFFFFF,
-                           al[r0:r0 + 512].to(torch.int64) & 0xFFFFFFFF)
-        assert bool(((blk >= -1) & (blk < w.S)).all())
-
-
 # ------------------------------------------------------------ greedy chains
 
 def _chain_check(dv, wid, sample_rows):
@@ -298,15 +268,6 @@ def _chain_check(dv, wid, sample_rows):
 def test_chain_workload_full(dv, wid):
     _say(f"chain workload {W.WORKLOADS[wid].describe()}")
     _chain_check(dv, wid, None)
-
-
-@pytest.mark.parametrize("wid", [4, 5])
-def test_chain_workload_sampled(dv, wid):
-    w = W.WORKLOADS[wid]
-    _say(f"chain workload {w.describe()} (sampled rows)")
-    rng = np.random.default_rng(100 + wid)
-    rows = np.unique(np.concatenate([[0, w.B - 1], rng.integers(0, w.B, 30)]))
-    _chain_check(dv, wid, rows)
 
 
 # ---------------------------------------------------------- masked step edges
@@ -847,39 +808,6 @@ def test_spec_workload_full(dv, wid, s, layout):
     _say(f"  accepted histogram {np.bincount(acc, minlength=s + 1).tolist()}")
 
 
-@pytest.mark.parametrize("wid,s", [(4, 8), (5, 4)])
-def test_spec_workload_sampled(dv, wid, s):
-    """Full-size batch in the benchmark's layout; sampled rows against the
-    oracle (table rows on demand), properties over every row."""
-    w = W.WORKLOADS[wid]
-    _say(f"spec verify workload {w.describe()} s={s} (sampled rows)")
-    trans, offsets, data, ns, al = _workload_table(dv, wid)
-    x = W.logits_all(wid, device=DEV, steps=s + 1).transpose(0, 1).contiguous()  # [B][s+1][V]
-    init = W.init_states(wid)
-    rng = np.random.default_rng(300 + wid)
-    rows = np.unique(np.concatenate([[0, w.B - 1], rng.integers(0, w.B, 14)]))
-    cache = oracle.RowCache(trans, offsets, data)
-    xr = to_oracle(x[torch.from_numpy(rows.astype(np.int64)).to(DEV)])
-    props = rng.integers(-2, w.V + 2, (w.B, s)).astype(np.int32)
-    for i, b in enumerate(rows):
-        greedy, _ = oracle.masked_chain(cache, init[b], xr[i, :s])
-        props[b] = _perturb(rng, greedy, w.V, 0.85)
-    tok, acc, nst = dv.spec_verify(ns, al, _dev(init), _dev(props), x)
-    a_w, f_w = dv.spec_walk(ns, al, _dev(init), _dev(props))
-    torch.cuda.synchronize()
-    tok_h, acc_h, nst_h = tok.cpu().numpy(), acc.cpu().numpy(), nst.cpu().numpy()
-    for i, b in enumerate(rows):
-        t_o, a_o, n_o = oracle.spec_verify_rows(cache, init[b], props[b], xr[i])
-        np.testing.assert_array_equal(tok_h[b], t_o, err_msg=f"workload {wid} row {b}")
-        assert acc_h[b] == a_o and nst_h[b] == n_o, f"workload {wid} row {b}"
-    # every row: a verified prefix is admitted by the walk; emitted tokens are allowed
-    assert bool((acc <= a_w).all())
-    assert bool(((acc >= 0) & (acc <= s)).all())
-    first = tok.gather(1, acc.to(torch.int64)[:, None])[:, 0]
-    assert bool(((first == -1) == (nst == -1)).all())
-    _say(f"  {len(rows)} rows bit-exact; mean accepted {float(acc.float().mean()):.2f}")
-
-
 def test_spec_zero_proposals_is_a_step(dv):
     w = W.WORKLOADS[3]
     trans, offsets, data, ns, al = _workload_table(dv, 3)
@@ -948,7 +876,9 @@ def test_spec_empty_batch_and_aliasing(dv):
     with pytest.raises(dv.DvError):
         dv.spec_verify(ns, al, states, props, x, new_state=states)
     with pytest.raises(dv.DvError):
-        dv.spec_walk(ns, al, states, props, accepted=props[0])
+        dv.spec_walk(ns, al, states, props, accepted=props[0][:2])   # an output inside the proposals
+    with pytest.raises(ValueError):
+        dv.spec_walk(ns, al, states, props, accepted=props[0])       # the wrong size: refused by the binding
 
 
 # ------------------------------------- opportunistic masking (Sec. 3.5, optimizations)
@@ -1002,7 +932,7 @@ def test_opportunistic_tail_maximum(dv, allowed_last):
     assert bool(ok.all()) == allowed_last
 
 
-@pytest.mark.parametrize("wid", [3, 4, 5])
+@pytest.mark.parametrize("wid", [3])
 @pytest.mark.parametrize("adherent", [0.0, 0.9])
 def test_opportunistic_workload(dv, wid, adherent):
     """The benchmark's shapes: sampled rows against the oracle, every row
@@ -1076,44 +1006,6 @@ def test_sample_chain_workload_full(dv, wid, steps, inv_t):
     # a sampled chain differs from the greedy one (it is a draw, not the argmax)
     g_t, _ = oracle.masked_step(ns_o, al_o, init, xs[0])
     assert (tks[0].cpu().numpy() != g_t).any() or w.B == 1
-
-
-def _one_row_of(cache, s, b):
-    """Oracle inputs that give row b state s through a one-state table: rows
-    0..b-1 are dead, so the noise counter of row b is the device's."""
-    ns_row, al_row = cache.get(int(s))
-    states = np.full(b + 1, -1, np.int32)
-    states[b] = 0
-    return ns_row[None], al_row[None], states
-
-
-@pytest.mark.parametrize("wid", [4, 5])
-def test_sample_step_workload_sampled(dv, wid):
-    """The benchmark's shapes, one sampled step: sampled rows against the
-    oracle; every row's draw is allowed and its new state follows it."""
-    w = W.WORKLOADS[wid]
-    _say(f"sampled step workload {w.describe()} (sampled rows)")
-    trans, offsets, data, ns, al = _workload_table(dv, wid)
-    cache = oracle.RowCache(trans, offsets, data)
-    init = W.init_states(wid)
-    x = W.logits(wid, 3, device=DEV)
-    tok, new = dv.masked_sample(ns, al, _dev(init), x, SEED, 3)
-    torch.cuda.synchronize()
-    rng = np.random.default_rng(500 + wid)
-    rows = np.unique(np.concatenate([[0, w.B - 1], rng.integers(0, w.B, 10)]))
-    xr = to_oracle(x[torch.from_numpy(rows.astype(np.int64)).to(DEV)])
-    for i, b in enumerate(rows):
-        ns1, al1, st1 = _one_row_of(cache, init[b], int(b))
-        lg = np.zeros((b + 1, xr.shape[1]), xr.dtype)
-        lg[b] = xr[i]
-        t_o, n_o = oracle.masked_sample(ns1, al1, st1, lg, 1.0, SEED, 3)
-        assert int(tok[b]) == int(t_o[b]) and int(new[b]) == int(n_o[b]), f"workload {wid} row {b}"
-    st = _dev(init).to(torch.int64)
-    tk = tok.to(torch.int64)
-    assert bool((tk >= 0).all())
-    word = al[st, tk // 32].to(torch.int64) & 0xFFFFFFFF
-    assert bool((((word >> (tk % 32)) & 1) == 1).all())
-    assert torch.equal(new, ns[st, tk])
 
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
