@@ -65,6 +65,7 @@ extern "C" {
 #define DV_MAX_BATCH  1048576      /* batch       in [0, DV_MAX_BATCH]   */
 #define DV_MAX_PROPOSED 1024       /* num_proposed in [0, DV_MAX_PROPOSED];
                                       batch * (num_proposed + 1) <= DV_MAX_BATCH */
+#define DV_NOALLOC_MAX_BATCH 65536 /* batch of dv_masked_step_noalloc          */
 
 typedef enum dv_status {
     DV_OK = 0,
@@ -202,6 +203,32 @@ DV_API dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow
                          int32_t batch, int64_t ld_logits,
                          int32_t *token, int32_t *new_state,
                          void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * dv_masked_step_noalloc -- dv_masked_step without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).  Results are
+ * exactly those of dv_masked_step.
+ *
+ * Split rows meet in a scratch array the library holds on each GPU it runs
+ * on (768 KiB, enough for DV_NOALLOC_MAX_BATCH rows; kept until the process
+ * ends).  The first call on a device looks the array up and enqueues a
+ * kernel on `stream` that clears it; every call leaves it all zero.  The
+ * call allocates nothing.  All calls on one GPU share the array: calls that
+ * may overlap on one GPU (other streams, other threads) race and must be
+ * ordered by the caller; give concurrent work dv_masked_step with a
+ * workspace each.
+ *
+ * Arguments as dv_masked_step, without workspace and workspace_bytes.
+ * Errors as dv_masked_step; DV_ERR_SHAPE also for batch >
+ *   DV_NOALLOC_MAX_BATCH; DV_ERR_HIP if the scratch array cannot be found or
+ *   cleared.
+ */
+DV_API dv_status dv_masked_step_noalloc(const int32_t *next_state, const uint32_t *allow,
+                         int32_t num_states, int32_t num_tokens,
+                         const int32_t *states, const void *logits, int32_t dtype,
+                         int32_t batch, int64_t ld_logits,
+                         int32_t *token, int32_t *new_state, void *stream);
 
 /*
  * dv_masked_step_opportunistic -- dv_masked_step with opportunistic masking

@@ -20,7 +20,7 @@ import os
 
 import torch
 
-__all__ = ["align", "masked_step", "masked_sample", "spec_walk", "spec_verify", "align_workspace_bytes",
+__all__ = ["align", "masked_step", "masked_step_noalloc", "masked_sample", "spec_walk", "spec_verify", "align_workspace_bytes",
            "masked_step_workspace_bytes", "masked_sample_workspace_bytes", "spec_verify_workspace_bytes",
            "step_workspace", "sample_workspace", "spec_workspace", "DvError", "DEAD", "library_path", "lib"]
 
@@ -62,6 +62,8 @@ def _load():
     lib.dv_masked_step_workspace_bytes.argtypes = [i32, i32]
     lib.dv_masked_step.restype = ctypes.c_int
     lib.dv_masked_step.argtypes = [vp, vp, i32, i32, vp, vp, i32, i32, i64, vp, vp, vp, sz, vp]
+    lib.dv_masked_step_noalloc.restype = ctypes.c_int
+    lib.dv_masked_step_noalloc.argtypes = [vp, vp, i32, i32, vp, vp, i32, i32, i64, vp, vp, vp]
     lib.dv_masked_step_opportunistic.restype = ctypes.c_int
     lib.dv_masked_step_opportunistic.argtypes = [vp, vp, i32, i32, vp, vp, i32, i32, i64, vp, vp, vp, sz,
                                                  vp]
@@ -240,6 +242,26 @@ def masked_step(next_state, allow, states, logits, token=None, new_state=None, w
     st = fn(_ptr(next_state), _ptr(allow), S, V, _ptr(states), _ptr(logits), dt, B, ld, _ptr(token),
             _ptr(new_state), _ptr(workspace), nbytes, _stream(stream, dev))
     _check(st, "dv_masked_step_opportunistic" if opportunistic else "dv_masked_step")
+    return token, new_state
+
+
+NOALLOC_MAX_BATCH = 65536
+
+
+def masked_step_noalloc(next_state, allow, states, logits, token, new_state, stream=None):
+    """``masked_step`` through dv_masked_step_noalloc: no workspace; split
+    rows meet in the library's own scratch array on the device (batch at
+    most NOALLOC_MAX_BATCH).  The outputs are caller-supplied, so the call
+    allocates nothing.  Calls that may overlap on one GPU race."""
+    dev = states.device
+    S, V, B, ld, dt = _step_args(next_state, allow, states, logits)
+    if token is None or new_state is None:
+        raise ValueError("masked_step_noalloc writes into caller-supplied token and new_state")
+    token = _out(token, "token", B, dev)
+    new_state = _out(new_state, "new_state", B, dev)
+    st = lib.dv_masked_step_noalloc(_ptr(next_state), _ptr(allow), S, V, _ptr(states), _ptr(logits), dt, B, ld,
+                                    _ptr(token), _ptr(new_state), _stream(stream, dev))
+    _check(st, "dv_masked_step_noalloc")
     return token, new_state
 
 

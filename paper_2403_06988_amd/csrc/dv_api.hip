@@ -4,6 +4,9 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <atomic>
+#include <mutex>
+
 #include "../../include/dv.h"
 #include "dv_internal.h"
 #include "dv_sample.h"
@@ -130,7 +133,7 @@ size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens)
 
 // How a step call decodes: greedy, greedy with the check first, or sampled.
 struct StepMode {
-    int kind;  // 0 greedy, 1 opportunistic, 2 sampled
+    int kind;  // 0 greedy, 1 opportunistic, 2 sampled, 3 argument checks only
     float inv_temperature;
     uint64_t seed, offset;
 };
@@ -176,6 +179,8 @@ static dv_status step_common(const char *name, StepMode mode, const int32_t *nex
         if (overlap(out, r_ns) || overlap(out, r_al) || overlap(out, r_st) || overlap(out, r_lg))
             return fail(DV_ERR_ALIAS, "%s: an output overlaps an input "
                                       "(ping-pong two state buffers instead of updating in place)", name);
+    if (mode.kind == 3)
+        return DV_OK;  // argument checks only (the scratch-backed step checks before its set-up)
     const size_t need = mode.kind == 2 ? dv::sample_workspace_bytes(batch, num_tokens)
                                        : dv::step_workspace_bytes(batch, num_tokens);
     if (!workspace || workspace_bytes < need)
@@ -209,6 +214,91 @@ dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow, int32
 {
     return step_common("dv_masked_step", StepMode{0, 1.0f, 0, 0}, next_state, allow, num_states, num_tokens, states, logits,
                        dtype, batch, ld_logits, token, new_state, workspace, workspace_bytes, stream);
+}
+
+// ------------------------------------------------ step without allocation
+//
+// dv_masked_step_noalloc meets split rows in `scratch`, a device array of
+// the library, instead of a caller's workspace.  Its size covers
+// DV_NOALLOC_MAX_BATCH rows (the meeting entries depend on the batch only).
+// Each GPU holds its own copy until the process ends.  Host code never uses
+// the array's name as an address: the device address of each GPU's copy is
+// looked up once per device and kept in g_scratch_ptr.
+namespace {
+
+constexpr size_t kScratchBytes = dv::row_meet_bytes(DV_NOALLOC_MAX_BATCH);
+__device__ __align__(256) uint4 scratch[kScratchBytes / sizeof(uint4)];
+
+constexpr int kMaxScratchDevices = 64;
+std::atomic<void *> g_scratch_ptr[kMaxScratchDevices];
+std::mutex g_scratch_mu;
+
+__global__ void clear_scratch_kernel(uint4 *p, size_t n)
+{
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        p[i] = make_uint4(0, 0, 0, 0);
+}
+
+// The current device's scratch address; on a device's first call, looked up
+// and cleared with a kernel on `stream` (a kernel, not a memset, so that a
+// first call under graph capture records a plain kernel node).
+dv_status scratch_for_current_device(const char *name, hipStream_t stream, void **out)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return fail(DV_ERR_HIP, "%s: hipGetDevice: %s", name, hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxScratchDevices)
+        return fail(DV_ERR_HIP, "%s: device %d beyond the %d devices the scratch table covers", name, dev,
+                    kMaxScratchDevices);
+    void *p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (p) {
+        *out = p;
+        return DV_OK;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(DV_ERR_HIP, "%s: hipGetSymbolAddress(scratch): %s", name, hipGetErrorString(e));
+        const size_t n = kScratchBytes / sizeof(uint4);
+        clear_scratch_kernel<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(static_cast<uint4 *>(p), n);
+        e = hipGetLastError();
+        if (e != hipSuccess)
+            return fail(DV_ERR_HIP, "%s: clearing the scratch array: %s", name, hipGetErrorString(e));
+        g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return DV_OK;
+}
+
+}  // namespace
+
+dv_status dv_masked_step_noalloc(const int32_t *next_state, const uint32_t *allow, int32_t num_states,
+                                 int32_t num_tokens, const int32_t *states, const void *logits, int32_t dtype,
+                                 int32_t batch, int64_t ld_logits, int32_t *token, int32_t *new_state,
+                                 void *stream)
+{
+    const char *name = "dv_masked_step_noalloc";
+    g_error[0] = '\0';
+    if (batch > DV_NOALLOC_MAX_BATCH)
+        return fail(DV_ERR_SHAPE, "%s: batch=%d exceeds DV_NOALLOC_MAX_BATCH=%d (the scratch array's size); "
+                                  "use dv_masked_step with a workspace", name, batch, DV_NOALLOC_MAX_BATCH);
+    // The same checks as dv_masked_step, with a stand-in workspace address
+    // (never dereferenced: a failed check enqueues nothing) so that no HIP
+    // call happens before the arguments are known good.
+    const dv_status pre = step_common(name, StepMode{3, 1.0f, 0, 0}, next_state, allow, num_states, num_tokens,
+                                      states, logits, dtype, batch, ld_logits, token, new_state, nullptr, 0,
+                                      stream);
+    if (pre != DV_OK || batch == 0)
+        return pre;
+    void *ws = nullptr;
+    const dv_status got = scratch_for_current_device(name, static_cast<hipStream_t>(stream), &ws);
+    if (got != DV_OK)
+        return got;
+    return step_common(name, StepMode{0, 1.0f, 0, 0}, next_state, allow, num_states, num_tokens, states, logits,
+                       dtype, batch, ld_logits, token, new_state, ws, kScratchBytes, stream);
 }
 
 dv_status dv_masked_step_opportunistic(const int32_t *next_state, const uint32_t *allow, int32_t num_states,

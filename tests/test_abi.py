@@ -119,6 +119,34 @@ def test_masked_step_rejects_before_launch(kw, status):
     assert lib.dv_last_error().startswith(b"dv_masked_step")
 
 
+def _noalloc(ns=P, allow=P + GB, S=16, V=1000, states=P + 2 * GB, logits=P + 3 * GB, dtype=0, B=8,
+             ld=1000, tok=P + 4 * GB, new=P + 5 * GB):
+    return lib.dv_masked_step_noalloc(ns, allow, S, V, states, logits, dtype, B, ld, tok, new, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(ns=None), INVALID),
+    (dict(logits=None), INVALID),
+    (dict(S=0), SHAPE),
+    (dict(B=-1), SHAPE),
+    (dict(B=65537), SHAPE),                       # beyond the scratch array
+    (dict(ld=999), SHAPE),
+    (dict(dtype=2), DTYPE),
+    (dict(new=P + 2 * GB), ALIAS),                # in-place state update
+    (dict(logits=P + 3 * GB + 1, dtype=1), INVALID),
+])
+def test_masked_step_noalloc_rejects_before_any_hip_call(kw, status):
+    """Every check of the scratch-backed step runs before it looks up or
+    clears its scratch array (no GPU here: a HIP call would fail)."""
+    assert _noalloc(**kw) == status
+    assert lib.dv_last_error().startswith(b"dv_masked_step_noalloc")
+
+
+def test_masked_step_noalloc_empty_batch_is_a_noop():
+    assert _noalloc(B=0, states=None, logits=None, tok=None, new=None) == OK
+    assert lib.dv_last_error() == b""
+
+
 def test_last_error_is_per_thread():
     """The detail string belongs to the calling thread: threads failing in
     different entry points, and one whose calls succeed, each read their
