@@ -21,9 +21,14 @@ Reported (one JSON line):
   sample       the decode chain sampled at temperature 1 (Sec. 4), ALU roofline
   spec_verify  greedy verification of s = 8 proposed tokens per row (Sec. 3.6)
                over windows of the job's decode chain, with its own roofline
+  floors       the masked step's measured floors at its own launch shape
+               (probes in libdv_probes.so): an empty step, a loads-only pass
+               over whole rows and one over exactly the lines the step reads
+  extra        decode legs of the other bandwidth-sized workloads (3 and 5):
+               us per step, touched-line roofline, traffic, floors
   cpu_baseline the CPU oracle on a bounded sample of the same workload
 
-Usage: python bench.py [--steps K] [--warmup W] [--workload 1..5] [--no-cpu]
+Usage: python bench.py [--steps K] [--warmup W] [--workload 1..8] [--no-cpu]
 """
 import argparse
 import hashlib
@@ -43,10 +48,14 @@ KERNEL_SOURCES = {"masked_step": ("dv_step.hip", "dv_internal.h"),
                   "align": ("dv_align.hip", "dv_internal.h"),
                   "spec_verify": ("dv_step.hip", "dv_spec.hip", "dv_internal.h")}
 TRAFFIC_FILES = {
-    "masked_step": "masked_step_bf16_kernel__grammar-lexer-union_S8192_V128256_B256.traffic.txt",
-    "align": "walk_prefix_kernel__grammar-lexer-union_S8192_V128256.traffic.txt",
-    "spec_verify": "spec_verify__grammar-lexer-union_S8192_V128256_B256_s8.traffic.txt",
+    ("masked_step", 3): "masked_step_bf16_kernel__llm-tokenizer-scale_S1024_V128256_B64.traffic.txt",
+    ("masked_step", 4): "masked_step_bf16_kernel__grammar-lexer-union_S8192_V128256_B256.traffic.txt",
+    ("masked_step", 5): "masked_step_bf16_kernel__large-vocab-high-batch_S4096_V256000_B1024.traffic.txt",
+    ("align", 4): "walk_prefix_kernel__grammar-lexer-union_S8192_V128256.traffic.txt",
+    ("spec_verify", 4): "spec_verify__grammar-lexer-union_S8192_V128256_B256_s8.traffic.txt",
 }
+PROBE_LIB = os.path.join(ROOT, "paper_2403_06988_amd", "libdv_probes.so")
+EXTRA_WORKLOADS = (3, 5)
 
 
 def kernel_source_hash(which):
@@ -67,6 +76,8 @@ def parse():
     ap.add_argument("--no-spec", action="store_true", help="skip the speculative-verification leg")
     ap.add_argument("--no-opportunistic", action="store_true", help="skip the opportunistic-masking leg")
     ap.add_argument("--no-sample", action="store_true", help="skip the masked-sampling leg")
+    ap.add_argument("--no-floors", action="store_true", help="skip the masked step's floor probes")
+    ap.add_argument("--no-extra", action="store_true", help="skip the decode legs of workloads 3 and 5")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
 
@@ -133,9 +144,10 @@ def traffic_record(which, workload_id):
     summary (FETCH_SIZE + WRITE_SIZE, each scaled by what the counter reads
     for a streaming probe of known size), if it covers this workload and was
     taken on the current kernel source; else None."""
-    if workload_id != 4:
+    name = TRAFFIC_FILES.get((which, workload_id))
+    if name is None:
         return None
-    path = os.path.join(PROFILES, TRAFFIC_FILES[which])
+    path = os.path.join(PROFILES, name)
     if not os.path.exists(path):
         return None
     rec = {}
@@ -279,23 +291,98 @@ def all_cores(w, lib, cache, init, x_dev, steps, trans, offsets, data, budget_s)
             "seconds": round(t_dec + t_al, 2)}
 
 
-def run_probes(dv, dev, table_bytes):
-    """Measured rates of the memory paths the kernels use (roofline probes in
-    libdv.so): HBM stream read / write, dependent random gathers from a table
-    the size of the workload's compacted DFA (L1/L2), and from LDS."""
+def probe_lib():
+    """The roofline probes (libdv_probes.so, include/dv_probes.h): measurement
+    code kept out of libdv.so."""
     import ctypes
 
-    import torch
-
-    lib = dv.lib
-    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    if not os.path.exists(PROBE_LIB):
+        raise SystemExit(f"{PROBE_LIB} not built (python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(PROBE_LIB)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     lib.dvprobe_stream_read.argtypes = [vp, sz, vp, vp]
     lib.dvprobe_stream_write.argtypes = [vp, sz, vp]
     lib.dvprobe_gather.argtypes = [vp, i32, i32, i32, i32, vp, vp]
     lib.dvprobe_lds_gather.argtypes = [vp, i32, i32, i32, i32, vp, vp]
+    lib.dvprobe_step_floor.argtypes = [i32, vp, i32, i64, vp, i32, vp, i32, vp, vp, vp, i64, vp]
     for f in (lib.dvprobe_stream_read, lib.dvprobe_stream_write, lib.dvprobe_gather,
-              lib.dvprobe_lds_gather):
+              lib.dvprobe_lds_gather, lib.dvprobe_step_floor):
         f.restype = i32
+    return lib
+
+
+def graph_seconds(launches, dev, reps=3):
+    """Seconds per replay of a HIP graph of ``launches()`` (run once eagerly
+    on a side stream first, then captured), timed with HIP events on the
+    replaying stream; the minimum over ``reps`` replays."""
+    import torch
+
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(side):
+        launches()
+    torch.cuda.current_stream(dev).wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        launches()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    best = None
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        graph.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        t = a.elapsed_time(b) / 1e3
+        best = t if best is None else min(best, t)
+    del graph
+    return best
+
+
+def step_floors(probes, w, al, x, states_all, dev, step_us, bytes_per_launch):
+    """The masked step's floors at its own launch shape (same blocks and block
+    size), each over the job's steps with the job's own states, graph-replayed:
+    an empty step (launch + state read + outputs), a loads-only pass over
+    whole rows, and a loads-only pass over exactly the 128-byte lines holding
+    an allowed token (the bytes the roofline counts; mask bytes read first)."""
+    import torch
+
+    if w.dtype != "bf16":
+        return None
+    tok = torch.empty(w.B, dtype=torch.int32, device=dev)
+    new = torch.empty(w.B, dtype=torch.int32, device=dev)
+    sink_words = w.B * 64
+    sink = torch.empty(sink_words, dtype=torch.int32, device=dev)
+    out = {}
+    for mode, key in ((0, "empty_step_us"), (1, "loads_whole_rows_us"), (2, "loads_touched_lines_us")):
+        def launches():
+            sh = torch.cuda.current_stream(dev).cuda_stream
+            for k in range(w.steps):
+                rc = probes.dvprobe_step_floor(mode, x[k].data_ptr(), w.V, w.V, al.data_ptr(), w.S,
+                                               states_all[k].data_ptr(), w.B, tok.data_ptr(), new.data_ptr(),
+                                               sink.data_ptr(), sink_words, sh)
+                if rc != 0:
+                    raise RuntimeError(f"dvprobe_step_floor mode {mode} failed with status {rc}")
+        out[key] = graph_seconds(launches, dev) / w.steps * 1e6
+    touched = out["loads_touched_lines_us"]
+    out["step_us"] = step_us
+    out["step_over_touched_floor"] = step_us / touched
+    out["frac_at_touched_floor"] = bytes_per_launch / (touched * 1e-6) / 1e9 / HBM_PEAK_GBS
+    out["note"] = ("probes at the step's grid and block size, graph-replayed over the job's steps and states; "
+                   "frac_at_touched_floor = the roofline fraction a step as fast as the loads-only pass over "
+                   "its touched lines would reach")
+    return out
+
+
+def run_probes(probes, dev, table_bytes):
+    """Measured rates of the memory paths the kernels use (libdv_probes.so):
+    HBM stream read / write, dependent random gathers from a table the size
+    of the workload's compacted DFA (L1/L2), and from LDS."""
+    import torch
+
+    lib = probes
     stream = torch.cuda.current_stream(dev)
     sh = stream.cuda_stream
 
@@ -334,6 +421,64 @@ def run_probes(dv, dev, table_bytes):
     t = timed(lambda: lib.dvprobe_lds_gather(perm.data_ptr(), lds_entries, lanes, chains, steps,
                                              sink.data_ptr(), sh))
     out["lds_gather_per_s"] = lanes * chains * steps / t
+    return out
+
+
+def extra_leg(dv, probes, wid, dev, floors=True):
+    """Decode leg of another bandwidth-sized workload: its table built once,
+    then its whole greedy chain graph-replayed (inputs resident in HBM),
+    with the touched-line roofline, the traffic record and the floors."""
+    import numpy as np
+    import torch
+
+    import workloads as W
+
+    w = W.WORKLOADS[wid]
+    log(f"extra workload: {w.describe()}")
+    trans, _ = W.dfa(wid)
+    offsets, data = W.vocab(wid)
+    init = W.init_states(wid)
+    trans_d, offsets_d, data_d, init_d = (torch.from_numpy(np.require(a, requirements=["C", "W"])).to(dev)
+                                          for a in (trans, offsets, data, init))
+    ns = torch.empty((w.S, w.V), dtype=torch.int32, device=dev)
+    al = torch.empty((w.S, w.words), dtype=torch.int32, device=dev)
+    ws_align = torch.empty(dv.align_workspace_bytes(w.S, w.V), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    align_ms = []
+    for _ in range(4):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        dv.align(trans_d, offsets_d, data_d, next_state=ns, allow=al, workspace=ws_align)
+        b.record(stream)
+        torch.cuda.synchronize()
+        align_ms.append(a.elapsed_time(b))
+    x = W.logits_all(wid, device=dev)
+    ws = dv.step_workspace(w.B, w.V, dev)
+    states_all = torch.empty((w.steps + 1, w.B), dtype=torch.int32, device=dev)
+    tokens_all = torch.empty((w.steps, w.B), dtype=torch.int32, device=dev)
+    states_all[0].copy_(init_d)
+
+    def launches():
+        for k in range(w.steps):
+            dv.masked_step(ns, al, states_all[k], x[k], token=tokens_all[k], new_state=states_all[k + 1],
+                           workspace=ws)
+
+    t = graph_seconds(launches, dev) / w.steps
+    live_per_step = (states_all[:-1] >= 0).sum(dim=1).cpu().numpy()
+    logit_bytes = [touched_line_bytes(al, states_all[k], x[k].data_ptr(), w.V, w.V, w.elt) for k in range(w.steps)]
+    bytes_per_launch = float(np.mean([step_bytes(w, lb, int(n), w.B) for lb, n in zip(logit_bytes, live_per_step)]))
+    whole_rows = float(np.mean(live_per_step)) * w.V * w.elt
+    achieved = bytes_per_launch / t / 1e9
+    out = {"workload": w.describe(), "align_ms": float(np.median(align_ms[1:])),
+           "align_per_s": w.S * w.V / (float(np.median(align_ms[1:])) / 1e3),
+           "us_per_step": t * 1e6, "steps_per_s": 1.0 / t, "rows_steps_per_s": w.B / t,
+           "roofline": {"kernel": "masked_step_bf16_kernel" if w.dtype == "bf16" else "masked_step_kernel",
+                        "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": achieved / HBM_PEAK_GBS, "bytes_per_launch": bytes_per_launch,
+                        "logit_lines_read_fraction": float(np.mean(logit_bytes)) / whole_rows if whole_rows else None,
+                        "traffic": traffic_record("masked_step", wid)}}
+    if floors:
+        out["floors"] = step_floors(probes, w, al, x, states_all, dev, t * 1e6, bytes_per_launch)
     return out
 
 
@@ -708,6 +853,10 @@ def main():
                            "traffic": traffic_record("align", wid)},
         "kernel_source_hash": {k: kernel_source_hash(k) for k in KERNEL_SOURCES},
     }
+    probes = probe_lib() if not (args.no_probes and args.no_floors) else None
+    if not args.no_floors and w.dtype == "bf16":
+        log("masked-step floors")
+        out["floors"] = step_floors(probes, w, al, x, states_all, dev, mean_launch_s * 1e6, bytes_per_launch)
     if not args.no_opportunistic and w.dtype == "bf16":
         log("opportunistic masking")
         out["opportunistic"] = bench_opportunistic(dv, w, ns, al, x, tokens_all, states_all, dev)
@@ -720,7 +869,7 @@ def main():
         out["spec_verify"] = bench_spec(dv, w, wid, ns, al, x, tokens_all, states_all, dev)
     if not args.no_probes:
         log("roofline probes")
-        out["probes"] = run_probes(dv, dev, w.S * 96 * 2)
+        out["probes"] = run_probes(probes, dev, w.S * 96 * 2)
     if not args.no_cpu:
         log("cpu baseline (oracle, 1 thread)")
         out["cpu_baseline"] = cpu_baseline(w, wid, trans, offsets, data, init, x, args.cpu_seconds)
@@ -736,6 +885,12 @@ def main():
                                     "note": f"gathers = table moves past byte {depth} (the LDS part of the walk); "
                                             "peak = measured random-gather rate of the probe; "
                                             "gathers that hit L1 can push frac above 1"}
+    if not args.no_extra:
+        out["extra"] = {}
+        for e in EXTRA_WORKLOADS:
+            if e != wid:
+                out["extra"][str(e)] = extra_leg(dv, probes or probe_lib(), e, dev, floors=not args.no_floors)
+                torch.cuda.empty_cache()
     print(json.dumps(out), flush=True)
 
 

@@ -1,5 +1,6 @@
 /*
- * dv_probes.h -- roofline probes for libdv.so (measurement, not the hot path).
+ * dv_probes.h -- roofline probes (libdv_probes.so: measurement, not the hot
+ * path; libdv.so does not contain them).
  *
  * Each probe enqueues one kernel on `stream` that exercises one memory path
  * of the GPU the way the alignment and masked-step kernels do, so the rates
@@ -55,6 +56,25 @@ DVPROBE_API int32_t dvprobe_gather(const uint32_t *table, int32_t table_entries,
 DVPROBE_API int32_t dvprobe_lds_gather(const uint32_t *table, int32_t table_entries,
                                        int32_t lanes, int32_t chains, int32_t steps,
                                        uint32_t *sink, void *stream);
+
+/* Floors of the bf16 masked step (dv_masked_step) at its own launch shape
+ * for `batch` rows of `num_tokens` logits (the same blocks and block size):
+ *   mode 0  each block reads its row's state and writes the outputs
+ *           (token = -1, new_state = the state): the launch and one
+ *           dependent trip, nothing streamed;
+ *   mode 1  loads of every 16-byte vector of the rows, streamed as the step
+ *           streams them, with no mask and no arithmetic;
+ *   mode 2  loads of exactly the 128-byte lines holding an allowed token of
+ *           each row's state (allow [S][ceil(V/32)] as for dv_masked_step),
+ *           the mask bytes read first and choosing the addresses.
+ * logits: [batch][ld_logits] bf16, rows 16-byte aligned; states [batch];
+ * token, new_state [batch]; sink: at least batch * 64 uint32 (contents
+ * meaningless).  Returns 0, 1 for a bad argument, 6 for a HIP error. */
+DVPROBE_API int32_t dvprobe_step_floor(int32_t mode, const void *logits, int32_t num_tokens,
+                                       int64_t ld_logits, const uint32_t *allow, int32_t num_states,
+                                       const int32_t *states, int32_t batch, int32_t *token,
+                                       int32_t *new_state, uint32_t *sink, int64_t sink_words,
+                                       void *stream);
 
 #ifdef __cplusplus
 }

@@ -1,4 +1,6 @@
-"""Compile libdv.so (the HIP kernels and the C ABI) for gfx950 with hipcc."""
+"""Compile libdv.so (the HIP kernels and the C ABI of include/dv.h) and
+libdv_probes.so (the roofline probes of include/dv_probes.h, measurement
+only) for gfx950 with hipcc."""
 from __future__ import annotations
 
 import os
@@ -8,8 +10,10 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["dv_api.hip", "dv_align.hip", "dv_step.hip", "dv_spec.hip", "dv_sample.hip", "dv_probes.hip"]
+SOURCES = ["dv_api.hip", "dv_align.hip", "dv_step.hip", "dv_spec.hip", "dv_sample.hip"]
+PROBE_SOURCES = ["dv_probes.hip"]
 LIB = os.path.join(HERE, "libdv.so")
+PROBE_LIB = os.path.join(HERE, "libdv_probes.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -21,14 +25,19 @@ FLAGS = [
 ]
 
 
-def build(out: str = LIB, verbose: bool = False, defines: tuple = ()) -> str:
-    cmd = [HIPCC, *FLAGS, *[f"-D{d}" for d in defines], "-o", out + ".tmp",
-           *[os.path.join(CSRC, s) for s in SOURCES]]
+def _compile(out: str, sources, verbose: bool) -> str:
+    cmd = [HIPCC, *FLAGS, "-o", out + ".tmp", *[os.path.join(CSRC, s) for s in sources]]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(out + ".tmp", out)
     return out
+
+
+def build(verbose: bool = False) -> str:
+    """Both libraries; returns the path of libdv.so."""
+    _compile(PROBE_LIB, PROBE_SOURCES, verbose)
+    return _compile(LIB, SOURCES, verbose)
 
 
 if __name__ == "__main__":

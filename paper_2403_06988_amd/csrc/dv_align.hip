@@ -32,18 +32,10 @@
 namespace dv {
 namespace {
 
-#ifndef DV_ALIGN_STATE_TILE
-#define DV_ALIGN_STATE_TILE 16
-#endif
-
-#ifndef DV_ALIGN_LOCK_G
-#define DV_ALIGN_LOCK_G 8
-#endif
-
 constexpr int kThreads = 256;
 constexpr int kTokTile = kThreads;                // a multiple of 64 tokens = 2 allow words
-constexpr int kStateTile = DV_ALIGN_STATE_TILE;   // states per tile
-constexpr int kLockG = DV_ALIGN_LOCK_G;           // of which a lane walks this many at once
+constexpr int kStateTile = 16;                    // states per tile
+constexpr int kLockG = 8;                         // of which a lane walks this many at once
 constexpr int kRegBytes = 8;                      // token bytes whose classes sit in registers
 constexpr int kRowsLds = kStateTile * 256 * 2;    // worst-case bytes of the row tile
 constexpr int kSentinelLds = 256 * 2;             // the whole table's all-DEAD sentinel row
@@ -57,18 +49,9 @@ constexpr int kLiveRows = kLiveRowsPerBlock;
 // it takes.  Three states (57 KB of LDS) leave room for two 1024-lane blocks
 // per compute unit; measured against two and four states, and against two
 // tokens per lane per round.
-#ifndef DV_ALIGN_PREFIX_R
-#define DV_ALIGN_PREFIX_R 3
-#endif
-#ifndef DV_ALIGN_PREFIX_THREADS
-#define DV_ALIGN_PREFIX_THREADS 1024
-#endif
-constexpr int kPrefR = DV_ALIGN_PREFIX_R;
-constexpr int kPrefThreads = DV_ALIGN_PREFIX_THREADS;
-#ifndef DV_ALIGN_PREFIX_MAX_CP
-#define DV_ALIGN_PREFIX_MAX_CP 98
-#endif
-constexpr int kPrefixMaxCp = DV_ALIGN_PREFIX_MAX_CP;
+constexpr int kPrefR = 3;
+constexpr int kPrefThreads = 1024;
+constexpr int kPrefixMaxCp = 98;
 constexpr int kPrefStride = kPrefixMaxCp * kPrefixMaxCp + kPrefixMaxCp;  // entries per state
 constexpr int kPrefWaveSpan = 1024;  // tokens per wave between allow-word writes: 32 words per state
 constexpr int kPrefWordsOffset = 256 + kPrefR * kPrefStride * 2;  // 4-byte aligned: the stride is even

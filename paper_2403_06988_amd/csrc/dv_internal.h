@@ -177,16 +177,62 @@ __device__ __forceinline__ bool meet_row(RowMeet m, int b, int nchunks, uint64_t
 // A row of V logits is split into `nchunks` chunks of `chunk_vec` 16-byte
 // vectors, one block of `threads` lanes each; with more than one chunk the
 // blocks meet in the workspace (above).  bf16 rows use 512-lane blocks, one
-// per row once B >= kStepOneBlockRows; below that, about 32 / sqrt(B) chunks
-// per row (step_geometry).
+// per row once B >= kStepOneBlockRows (a block per compute unit already) or
+// when B >= 64 and a row holds at most kStepSingleBlockRowBytes (a second
+// block per row buys nothing there); otherwise about 32 / sqrt(B) chunks per
+// row.  fp32 rows use 256-lane blocks and the same chunk rule.
 constexpr int kStepOneBlockRows = 256;
+constexpr int kStepSmallThreads = 256;   // fp32 rows
+constexpr int kStepBigThreads = 512;     // bf16 rows
+constexpr int kStepStageWords = 8192;    // mask words a bf16 block may stage in LDS
+constexpr int kStepMaxChunkVec = (kStepStageWords - 1) * 4 / kStepBigThreads * kStepBigThreads;
+constexpr int64_t kStepSingleBlockRowBytes = 65536;
+static_assert(kStepMaxChunkVec % kStepBigThreads == 0, "chunks are whole batches of lanes");
 
 struct StepGeometry {
     int chunk_vec;
     int nchunks;
     int threads;
 };
-StepGeometry step_geometry(int B, int V, int dtype);
+
+inline StepGeometry step_geometry(int B, int V, int dtype)
+{
+    const bool bf16 = dtype == 1;
+    const int vec = bf16 ? 8 : 4;  // elements per 16-byte vector
+    const int threads = bf16 ? kStepBigThreads : kStepSmallThreads;
+    const int nvec = V / vec;
+    int want;
+    if (bf16 && B >= kStepOneBlockRows) {
+        want = 1;
+    } else if (bf16 && B >= 64 && (int64_t)V * 2 <= kStepSingleBlockRowBytes) {
+        want = 1;
+    } else {
+        // Chunks per row ~ 32 / sqrt(B): about 32 sqrt(B) blocks per launch
+        // (at most 256).  Since split rows meet in the workspace instead of a
+        // second kernel, this is what measures fastest from B = 1 to 128 at
+        // V = 32000 .. 256000: fewer blocks leave bandwidth unused, more
+        // make each block's stream too short for its fixed start-up cost.
+        int r = 1;
+        while (r * r < B)
+            ++r;  // ceil(sqrt(B))
+        const int blocks = 32 * r < 256 ? 32 * r : 256;
+        want = (blocks + B / 2) / (B > 0 ? B : 1);
+    }
+    // at least one vector per lane per chunk
+    const int max_chunks = nvec / threads > 1 ? nvec / threads : 1;
+    want = want > max_chunks ? max_chunks : want;
+    want = want < 1 ? 1 : want;
+    int chunk_vec = (nvec + want - 1) / want;
+    chunk_vec = (chunk_vec + threads - 1) / threads * threads;
+    if (chunk_vec == 0)
+        chunk_vec = threads;
+    if (bf16 && chunk_vec > kStepMaxChunkVec)  // the staged mask bytes must fit
+        chunk_vec = kStepMaxChunkVec;
+    int nchunks = (nvec + chunk_vec - 1) / chunk_vec;
+    if (nchunks < 1)
+        nchunks = 1;
+    return {chunk_vec, nchunks, threads};
+}
 
 inline size_t step_workspace_bytes(int B, int V)
 {

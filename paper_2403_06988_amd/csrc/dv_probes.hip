@@ -1,7 +1,9 @@
-// Roofline probes (declared in include/dv_probes.h): HBM streaming read and
-// write, dependent random 2-byte gathers from global memory (L1/L2) and from
-// LDS.  Used by the benchmark to put the hot-path kernels' rates next to what
-// the same memory path reaches on its own.
+// Roofline probes (libdv_probes.so, declared in include/dv_probes.h): HBM
+// streaming read and write, dependent random 2-byte gathers from global
+// memory (L1/L2) and from LDS, and the floors of the bf16 masked step at its
+// own launch shape.  Used by the benchmark to put the hot-path kernels'
+// rates next to what the same memory path reaches on its own.  Measurement
+// code: not part of libdv.so.
 #include "../../include/dv_probes.h"
 #include "dv_internal.h"
 
@@ -82,6 +84,149 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const uint32_t *__rest
     sink[lane] = acc;
 }
 
+// ------------------------------------------------- masked-step floors
+//
+// The grid and block size of the bf16 masked step (step_geometry): each
+// block owns chunk c of row b.  MODE 0: the row's state is read and the
+// outputs written, nothing else (the launch and its one dependent trip).
+// MODE 1: the chunk's 16-byte vectors are streamed as the step streams
+// them (512 lanes, two vectors per lane per batch, two batches in flight,
+// non-temporal), with no mask and no arithmetic.  MODE 2: only the vectors
+// whose mask byte is nonzero (the 128-byte lines holding an allowed token of
+// the row's state): the row's state is read, its mask bytes are loaded two
+// batches ahead of their logits and choose the addresses (a vector with no
+// allowed token reads one fixed, cached location instead), as a loads-only
+// kernel over exactly the lines the step must read.  Rows must be 16-byte
+// aligned.
+constexpr int kFloorThreads = 512;
+constexpr int kFloorU = 2;
+static_assert(kFloorThreads == kStepBigThreads, "the step's block size");
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ uint4 g_floor_unread;
+
+__device__ __forceinline__ uint4 nt_load(const char *p)
+{
+    const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+    return make_uint4(x[0], x[1], x[2], x[3]);
+}
+
+__device__ __forceinline__ void floor_batch(uint4 (&d)[kFloorU], const char *crow, int vb, int n)
+{
+#pragma unroll
+    for (int u = 0; u < kFloorU; ++u)
+        d[u] = nt_load(crow + (size_t)min(vb + u * kFloorThreads + (int)threadIdx.x, n - 1) * 16);
+}
+
+__device__ __forceinline__ void floor_batch_sel(uint4 (&d)[kFloorU], const char *crow, int vb, int n,
+                                                const uint32_t (&m)[kFloorU])
+{
+#pragma unroll
+    for (int u = 0; u < kFloorU; ++u) {
+        const char *p = crow + (size_t)min(vb + u * kFloorThreads + (int)threadIdx.x, n - 1) * 16;
+        d[u] = nt_load(m[u] ? p : reinterpret_cast<const char *>(&g_floor_unread));
+    }
+}
+
+__device__ __forceinline__ void floor_masks(uint32_t (&m)[kFloorU], const uint8_t *mb, int vb, int n)
+{
+#pragma unroll
+    for (int u = 0; u < kFloorU; ++u)
+        m[u] = mb[min(vb + u * kFloorThreads + (int)threadIdx.x, n - 1)];
+}
+
+__device__ __forceinline__ uint32_t fold(const uint4 (&d)[kFloorU])
+{
+    uint32_t a = 0;
+#pragma unroll
+    for (int u = 0; u < kFloorU; ++u)
+        a ^= d[u].x ^ d[u].y ^ d[u].z ^ d[u].w;
+    return a;
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kFloorThreads) void step_floor_kernel(const void *__restrict__ logits, int V, int64_t ld,
+                                                                   const uint32_t *__restrict__ allow, int S,
+                                                                   const int32_t *__restrict__ states,
+                                                                   int chunk_vec, int nchunks,
+                                                                   int32_t *__restrict__ token,
+                                                                   int32_t *__restrict__ new_state,
+                                                                   uint32_t *__restrict__ sink)
+{
+    constexpr int K = kFloorThreads * kFloorU;
+    const int b = blockIdx.x / nchunks, c = blockIdx.x - b * nchunks;
+    const int s = states[b];
+    const int nvec = V / 8;
+    const int v0 = c * chunk_vec, n = min(nvec, v0 + chunk_vec) - v0;
+    const char *crow = static_cast<const char *>(logits) + (size_t)b * ld * 2 + (size_t)v0 * 16;
+    uint32_t acc = 0;
+    if (MODE == 1 && n > 0) {
+        uint4 da[kFloorU], db[kFloorU];
+        floor_batch(da, crow, 0, n);
+        for (int vb = 0; vb < n; vb += 2 * K) {
+            floor_batch(db, crow, vb + K, n);
+            acc ^= fold(da);
+            floor_batch(da, crow, vb + 2 * K, n);
+            acc ^= fold(db);
+        }
+    } else if (MODE == 2 && n > 0 && (uint32_t)s < (uint32_t)S) {
+        const uint8_t *mb = reinterpret_cast<const uint8_t *>(allow + (size_t)s * ((V + 31) / 32)) + v0;
+        uint4 da[kFloorU], db[kFloorU];
+        uint32_t m0[kFloorU], m1[kFloorU], m2[kFloorU], m3[kFloorU];
+        // the first two batches are read whole (issued before the state is
+        // known); the issue order is pinned: the load counter is in order
+        floor_batch(da, crow, 0, n);
+        __builtin_amdgcn_sched_barrier(0);
+        floor_masks(m2, mb, 2 * K, n);
+        __builtin_amdgcn_sched_barrier(0);
+        floor_masks(m3, mb, 3 * K, n);
+        __builtin_amdgcn_sched_barrier(0);
+        floor_batch(db, crow, K, n);
+        __builtin_amdgcn_sched_barrier(0);
+        acc ^= fold(da);
+        floor_batch_sel(da, crow, 2 * K, n, m2);
+        __builtin_amdgcn_sched_barrier(0);
+        floor_masks(m0, mb, 4 * K, n);
+        __builtin_amdgcn_sched_barrier(0);
+        acc ^= fold(db);
+        floor_batch_sel(db, crow, 3 * K, n, m3);
+        __builtin_amdgcn_sched_barrier(0);
+        floor_masks(m1, mb, 5 * K, n);
+        __builtin_amdgcn_sched_barrier(0);
+        for (int vb = 2 * K; vb < n; vb += 4 * K) {
+            acc ^= fold(da);
+            floor_batch_sel(da, crow, vb + 2 * K, n, m0);
+            __builtin_amdgcn_sched_barrier(0);
+            floor_masks(m2, mb, vb + 4 * K, n);
+            __builtin_amdgcn_sched_barrier(0);
+            acc ^= fold(db);
+            floor_batch_sel(db, crow, vb + 3 * K, n, m1);
+            __builtin_amdgcn_sched_barrier(0);
+            floor_masks(m3, mb, vb + 5 * K, n);
+            __builtin_amdgcn_sched_barrier(0);
+            acc ^= fold(da);
+            floor_batch_sel(da, crow, vb + 4 * K, n, m2);
+            __builtin_amdgcn_sched_barrier(0);
+            floor_masks(m0, mb, vb + 6 * K, n);
+            __builtin_amdgcn_sched_barrier(0);
+            acc ^= fold(db);
+            floor_batch_sel(db, crow, vb + 5 * K, n, m3);
+            __builtin_amdgcn_sched_barrier(0);
+            floor_masks(m1, mb, vb + 7 * K, n);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    acc = wave_reduce<true>(acc);
+    if (threadIdx.x == 0) {
+        sink[blockIdx.x] = acc;
+        if (c == 0) {
+            token[b] = -1;
+            new_state[b] = s;
+        }
+    }
+}
+
 template <bool LDS>
 hipError_t launch_gather(const uint32_t *table, int entries, int lanes, int chains, int steps,
                          uint32_t *sink, hipStream_t stream)
@@ -125,6 +270,33 @@ static bool gather_args_ok(const uint32_t *table, int32_t entries, int32_t lanes
 {
     return table && sink && entries >= 1 && entries <= max_entries && lanes >= 256 && lanes % 256 == 0 &&
            (chains == 1 || chains == 2 || chains == 4 || chains == 8) && steps >= 1;
+}
+
+int32_t dvprobe_step_floor(int32_t mode, const void *logits, int32_t num_tokens, int64_t ld_logits,
+                           const uint32_t *allow, int32_t num_states, const int32_t *states, int32_t batch,
+                           int32_t *token, int32_t *new_state, uint32_t *sink, int64_t sink_words, void *stream)
+{
+    if (mode < 0 || mode > 2 || !states || !token || !new_state || !sink || batch < 1 || num_tokens < 8 ||
+        ld_logits < num_tokens || num_states < 1 || (mode > 0 && !logits) || (mode == 2 && !allow))
+        return 1;
+    if (mode > 0 && ((reinterpret_cast<uintptr_t>(logits) & 15) || (ld_logits * 2) % 16))
+        return 1;  // rows must be 16-byte aligned
+    const dv::StepGeometry g = dv::step_geometry(batch, num_tokens, 1);
+    const int64_t grid = (int64_t)batch * g.nchunks;
+    if (grid > sink_words || grid > (1 << 30))
+        return 1;
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+#define DV_FLOOR(M)                                                                                            \
+    dv::step_floor_kernel<M><<<(unsigned)grid, dv::kFloorThreads, 0, st>>>(                                   \
+        logits, num_tokens, ld_logits, allow, num_states, states, g.chunk_vec, g.nchunks, token, new_state, sink)
+    if (mode == 0)
+        DV_FLOOR(0);
+    else if (mode == 1)
+        DV_FLOOR(1);
+    else
+        DV_FLOOR(2);
+#undef DV_FLOOR
+    return hipGetLastError() == hipSuccess ? 0 : 6;
 }
 
 int32_t dvprobe_gather(const uint32_t *table, int32_t table_entries, int32_t lanes, int32_t chains,

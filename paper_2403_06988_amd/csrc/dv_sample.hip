@@ -29,10 +29,7 @@ constexpr int kThreads = 256;       // split rows: several blocks per row, meeti
 constexpr int kRowThreads = 1024;   // one block per row once B >= kOneBlockRows
                                     // (below that, split rows keep more waves per CU, which this
                                     // latency-laden arithmetic needs more than it saves a launch)
-#ifndef DV_SAMPLE_ONE_BLOCK_ROWS
-#define DV_SAMPLE_ONE_BLOCK_ROWS 1024  // four or more rows per CU keep enough waves resident
-#endif
-constexpr int kOneBlockRows = DV_SAMPLE_ONE_BLOCK_ROWS;
+constexpr int kOneBlockRows = 1024;  // four or more rows per CU keep enough waves resident
 // A wave queues single tokens instead of 4-token groups when its allowed
 // tokens number at most kTokenRatio4 / 4 times its allowed groups: a lane
 // then pays one Philox call and one logarithm pair per trip, where a group
@@ -41,10 +38,7 @@ constexpr int kOneBlockRows = DV_SAMPLE_ONE_BLOCK_ROWS;
 // 1.1 tokens).  Per trip a Philox call is about 63 instructions and a pair
 // about 90, so single tokens cost less up to about twice as many tokens as
 // groups; runs of allowed tokens (4 per group) keep the groups.
-#ifndef DV_SAMPLE_TOKEN_RATIO4
-#define DV_SAMPLE_TOKEN_RATIO4 8
-#endif
-constexpr int kTokenRatio4 = DV_SAMPLE_TOKEN_RATIO4;
+constexpr int kTokenRatio4 = 8;
 constexpr int kTargetBlocks = 2048;
 constexpr int kHalfSpanBlocks = 512;
 constexpr int kMaxChunks = 64;

@@ -48,16 +48,10 @@
 namespace dv {
 namespace {
 
-constexpr int kSmallThreads = 256;  // split rows and fp32 rows
-constexpr int kSmallU = 8;          // 16-byte vectors per lane per batch
-#ifndef DV_STEP_BF16_THREADS
-#define DV_STEP_BF16_THREADS 512
-#endif
-#ifndef DV_STEP_BF16_U
-#define DV_STEP_BF16_U 2
-#endif
-constexpr int kBigThreads = DV_STEP_BF16_THREADS;  // lanes per bf16 block
-constexpr int kBigU = DV_STEP_BF16_U;              // vectors per lane per batch (x2: double-buffered)
+constexpr int kSmallThreads = kStepSmallThreads;  // fp32 rows
+constexpr int kSmallU = 8;                         // 16-byte vectors per lane per batch
+constexpr int kBigThreads = kStepBigThreads;       // lanes per bf16 block
+constexpr int kBigU = 2;                           // vectors per lane per batch (x2: double-buffered)
 
 // Order-preserving key of an fp32 bit pattern under the step's value rules:
 // NaN ranks as -inf and -0.0 equals +0.0.  Every real value's key is
@@ -73,10 +67,6 @@ __device__ __forceinline__ uint32_t f32_key(uint32_t u)
 
 typedef short s16x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
-#ifndef DV_STEP_NT_LOADS
-#define DV_STEP_NT_LOADS 1
-#endif
 
 // Fast 16-bit keys of the two bf16 values in w (flip all bits of negatives,
 // set the sign bit of non-negatives).  Exact except: -0.0 -> 0x7FFF (+0.0 ->
@@ -114,6 +104,33 @@ __device__ __forceinline__ uint64_t block_max(uint64_t v)
 // "next state not loaded yet": the winner was not a vector-path best.
 constexpr int kNsUnknown = INT_MIN;
 
+// The meeting word of a bf16 row split over several blocks: the winner's
+// 16-bit key (a bf16 value's exact 32-bit key is that key followed by 16
+// fixed bits), 2^24 - 1 - its index (V <= 2^24), and its next state + 1 in
+// the low 24 bits -- so the 64-bit maximum orders by key, then by lowest
+// index, and hands the last block the winner's next state as well.  A next
+// state outside [-1, 2^24 - 2] (a table not written by dv_align) is marked
+// with the top value and read again.  0 = nothing allowed.
+constexpr uint32_t kSplitNsReload = 0xFFFFFFu;
+
+__device__ __forceinline__ uint64_t pack_split(uint64_t best, int tok, int ns)
+{
+    const uint32_t nsf = (ns >= -1 && ns < (int)kSplitNsReload - 1) ? (uint32_t)(ns + 1) : kSplitNsReload;
+    return (best >> 48) << 48 | (uint64_t)(0xFFFFFFu - (uint32_t)tok) << 24 | nsf;
+}
+
+__device__ __forceinline__ void unpack_split(uint64_t w, int &tok, int &ns)
+{
+    if (!w) {
+        tok = -1;
+        ns = -1;
+        return;
+    }
+    tok = (int)(0xFFFFFFu - (uint32_t)((w >> 24) & 0xFFFFFFu));
+    const uint32_t nsf = (uint32_t)w & 0xFFFFFFu;
+    ns = nsf == kSplitNsReload ? kNsUnknown : (int)nsf - 1;
+}
+
 // block_max, also returning (in thread 0) the next state of the winner when
 // its wave had already loaded it: `vec_pack` is the wave's vector-path best
 // (wave-uniform) and `vec_ns` its next state.
@@ -144,14 +161,12 @@ __device__ __forceinline__ uint64_t block_max_ns(uint64_t v, uint64_t vec_pack, 
 
 template <int DT> struct Elt;
 template <> struct Elt<0> {  // fp32
-    static constexpr int kVec = 4;
     __device__ static uint32_t bits(const char *row, int64_t i)
     {
         return reinterpret_cast<const uint32_t *>(row)[i];
     }
 };
 template <> struct Elt<1> {  // bf16: the high half of an fp32
-    static constexpr int kVec = 8;
     __device__ static uint32_t bits(const char *row, int64_t i)
     {
         return (uint32_t)reinterpret_cast<const uint16_t *>(row)[i] << 16;
@@ -329,14 +344,10 @@ __device__ __forceinline__ void load_batch_bf16(uint4 (&d)[U], const char *row, 
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int v = min(vb + u * THREADS + tid, v1 - 1);
-#if DV_STEP_NT_LOADS
         // logits are read once: a non-temporal load keeps them from
         // displacing reusable lines (mask rows, tables) in the caches
         const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(row + (size_t)v * 16));
         d[u] = make_uint4(x[0], x[1], x[2], x[3]);
-#else
-        d[u] = *reinterpret_cast<const uint4 *>(row + (size_t)v * 16);
-#endif
     }
 }
 
@@ -357,12 +368,8 @@ __device__ __forceinline__ void load_batch_bf16_sel(uint4 (&d)[U], const char *r
     for (int u = 0; u < U; ++u) {
         const int v = min(vb + u * THREADS + tid, v1 - 1);
         const char *p = sel[u] ? row + (size_t)v * 16 : reinterpret_cast<const char *>(&g_unread_vector);
-#if DV_STEP_NT_LOADS
         const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
         d[u] = make_uint4(x[0], x[1], x[2], x[3]);
-#else
-        d[u] = *reinterpret_cast<const uint4 *>(p);
-#endif
     }
 }
 
@@ -597,9 +604,8 @@ __device__ __forceinline__ uint64_t scan_chunk_bf16(const char *row, const uint3
 
 // Mask words staged per block: the chunk's mask bytes (one per vector, plus
 // one for a shifted head) in at most kStageWords words, so chunks are capped
-// at kMaxChunkVec vectors.
-constexpr int kStageWords = 8192;
-constexpr int kMaxChunkVec = (kStageWords - 1) * 4 / 512 * 512;
+// at kStepMaxChunkVec vectors.
+constexpr int kStageWords = kStepStageWords;
 
 // Copies allow-row words [w0, w0 + nwords) (nwords <= kStageWords) of `arow`
 // (a row of W words) into LDS: every lane's loads first (clamped into the
@@ -689,20 +695,26 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
                 c == 0, c == nchunks - 1, V, lut, da, db, vec_pack, vec_ns);
     }
     int ns;
-    uint64_t best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
+    const uint64_t best = block_max_ns<THREADS>(mine, vec_pack, vec_ns, ns);
     if (threadIdx.x != 0)
         return;
-    if (nchunks > 1) {
-        const uint64_t own = best;
-        if (!meet_row(meet, b, nchunks, own, best))
-            return;  // another block of the row finishes it
-        if (best != own)
-            ns = kNsUnknown;  // another block's token: its next state is read below
-    }
     const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
     const bool found = tok >= 0 && tok < V;  // always true for a found token; guards the read
-    token[b] = found ? tok : -1;
-    new_state[b] = !found ? -1 : ns != kNsUnknown ? ns : next_state[(size_t)s * V + tok];
+    const int nsv = !found ? -1 : ns != kNsUnknown ? ns : next_state[(size_t)s * V + tok];
+    if (nchunks == 1) {
+        token[b] = found ? tok : -1;
+        new_state[b] = nsv;
+        return;
+    }
+    // Split rows: the meeting word carries the winner's next state, so the
+    // block that arrives last needs no further read.
+    uint64_t fin;
+    if (!meet_row(meet, b, nchunks, found ? pack_split(best, tok, nsv) : 0ull, fin))
+        return;  // another block of the row finishes it
+    int ftok, fns;
+    unpack_split(fin, ftok, fns);
+    token[b] = ftok;
+    new_state[b] = fns != kNsUnknown ? fns : next_state[(size_t)s * V + ftok];
 }
 
 // Opportunistic masking (Sec. 3.5, further optimizations), one block per
@@ -760,50 +772,6 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
 }
 
 }  // namespace
-
-#ifndef DV_STEP_SINGLE_BLOCK_ROW_BYTES
-#define DV_STEP_SINGLE_BLOCK_ROW_BYTES 65536
-#endif
-
-StepGeometry step_geometry(int B, int V, int dtype)
-{
-    const int vec = dtype == 0 ? Elt<0>::kVec : Elt<1>::kVec;
-    const bool bf16 = dtype == 1;
-    const int threads = bf16 ? kBigThreads : kSmallThreads;
-    const int nvec = V / vec;
-    static_assert(kMaxChunkVec % kBigThreads == 0, "chunks are whole batches of lanes");
-    int want;
-    if (bf16 && B >= kStepOneBlockRows) {
-        want = 1;  // a block per compute unit already
-    } else if (bf16 && B >= 64 && (int64_t)V * 2 <= DV_STEP_SINGLE_BLOCK_ROW_BYTES) {
-        want = 1;  // short rows: a second block per row buys nothing at this batch
-    } else {
-        // Chunks per row ~ 32 / sqrt(B): about 32 sqrt(B) blocks per launch
-        // (at most 256).  Since split rows meet in the workspace instead of a
-        // second kernel, this is what measures fastest from B = 1 to 128 at
-        // V = 32000 .. 256000: fewer blocks leave bandwidth unused, more
-        // make each block's stream too short for its fixed start-up cost.
-        int r = 1;
-        while (r * r < B)
-            ++r;  // ceil(sqrt(B))
-        const int blocks = 32 * r < 256 ? 32 * r : 256;
-        want = (blocks + B / 2) / (B > 0 ? B : 1);
-    }
-    // at least one vector per lane per chunk
-    const int max_chunks = nvec / threads > 1 ? nvec / threads : 1;
-    want = want > max_chunks ? max_chunks : want;
-    want = want < 1 ? 1 : want;
-    int chunk_vec = (nvec + want - 1) / want;
-    chunk_vec = (chunk_vec + threads - 1) / threads * threads;
-    if (chunk_vec == 0)
-        chunk_vec = threads;
-    if (bf16 && chunk_vec > kMaxChunkVec)  // the staged mask bytes must fit
-        chunk_vec = kMaxChunkVec;
-    int nchunks = (nvec + chunk_vec - 1) / chunk_vec;
-    if (nchunks < 1)
-        nchunks = 1;
-    return {chunk_vec, nchunks, threads};
-}
 
 // Whether a bf16 launch of `blocks` blocks stages its mask bytes in LDS and
 // skips lines with no allowed token.  Staging puts the whole chunk's mask

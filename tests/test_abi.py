@@ -20,23 +20,46 @@ P = 0x7F0000000000  # fake device address (never dereferenced)
 GB = 1 << 30
 
 
-def declared_functions():
-    names = []
-    for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
-        text = open(os.path.join(ROOT, "include", h)).read()
-        names += re.findall(r"^(?:DV_API|DVPROBE_API)\s+[\w\s\*]+?\b(dv\w+)\s*\(", text, flags=re.M)
-    return names
+PROBE_LIB = os.path.join(ROOT, "paper_2403_06988_amd", "libdv_probes.so")
+
+
+def declared_functions(header):
+    text = open(os.path.join(ROOT, "include", header)).read()
+    return re.findall(r"^(?:DV_API|DVPROBE_API)\s+[\w\s\*]+?\b(dv\w+)\s*\(", text, flags=re.M)
 
 
 def test_every_declared_symbol_is_exported():
-    names = declared_functions()
+    """dv.h's functions from libdv.so; the probes of dv_probes.h from their
+    own library, and none of them from libdv.so."""
+    names = declared_functions("dv.h")
     assert {"dv_align_workspace_bytes", "dv_align", "dv_masked_step_workspace_bytes",
-            "dv_masked_step", "dv_status_string", "dv_last_error", "dv_version",
-            "dvprobe_stream_read", "dvprobe_stream_write", "dvprobe_gather",
-            "dvprobe_lds_gather"} <= set(names)
+            "dv_masked_step", "dv_status_string", "dv_last_error", "dv_version"} <= set(names)
     raw = ctypes.CDLL(dv.library_path)
     for n in names:
         assert hasattr(raw, n), n
+    probes = declared_functions("dv_probes.h")
+    assert {"dvprobe_stream_read", "dvprobe_stream_write", "dvprobe_gather", "dvprobe_lds_gather",
+            "dvprobe_step_floor"} <= set(probes)
+    plib = ctypes.CDLL(PROBE_LIB)
+    for n in probes:
+        assert hasattr(plib, n), n
+        assert not hasattr(raw, n), f"{n} is measurement code: it belongs in libdv_probes.so only"
+
+
+def test_step_floor_probe_rejects_bad_arguments():
+    plib = ctypes.CDLL(PROBE_LIB)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    f = plib.dvprobe_step_floor
+    f.restype = i32
+    f.argtypes = [i32, vp, i32, i64, vp, i32, vp, i32, vp, vp, vp, i64, vp]
+
+    def call(mode=1, logits=P, V=1000, ld=1000, allow=P + GB, S=16, states=P + 2 * GB, B=8, tok=P + 3 * GB,
+             new=P + 4 * GB, sink=P + 5 * GB, sink_words=8 * 64):
+        return f(mode, logits, V, ld, allow, S, states, B, tok, new, sink, sink_words, None)
+
+    for kw in (dict(mode=3), dict(mode=-1), dict(logits=None), dict(mode=2, allow=None), dict(states=None),
+               dict(B=0), dict(ld=999), dict(logits=P + 8), dict(ld=1001), dict(sink_words=7), dict(V=4)):
+        assert call(**kw) == 1, kw
 
 
 def test_status_strings_and_version():
