@@ -3,7 +3,7 @@
 Alignment tables (next_state, allow with padding bits) and greedy decoding
 chains (token, new_state at every step) are compared with the oracle, which
 computes from the same seeded inputs with its own table and its own previous
-states.  Workloads 1-3 and 6-8 are compared in full here; workloads 4-5
+states.  Workloads 1-3 and 6-10 are compared in full here; workloads 4-5
 (10^9-pair tables) in full in test_gpu_parity_large.py.  The launch
 configuration is the benchmark's (same shapes, same calls)."""
 import json
@@ -224,7 +224,7 @@ def _workload_table(dv, wid):
     return _Cache.data
 
 
-@pytest.mark.parametrize("wid", [1, 2, 3, 6, 7, 8])
+@pytest.mark.parametrize("wid", [1, 2, 3, 6, 7, 8, 9, 10])
 def test_align_workload_full(dv, wid):
     _say(f"align workload {W.WORKLOADS[wid].describe()}")
     trans, offsets, data, ns, al = _workload_table(dv, wid)
@@ -264,7 +264,7 @@ def _chain_check(dv, wid, sample_rows):
     assert bool(((tk == -1) == (sts[1:] == -1)).all())
 
 
-@pytest.mark.parametrize("wid", [1, 2, 3, 6, 7, 8])
+@pytest.mark.parametrize("wid", [1, 2, 3, 6, 7, 8, 9, 10])
 def test_chain_workload_full(dv, wid):
     _say(f"chain workload {W.WORKLOADS[wid].describe()}")
     _chain_check(dv, wid, None)
@@ -675,7 +675,7 @@ def test_align_eos_paper_example(dv):
     np.testing.assert_array_equal(u32(al)[:, 0], np.array([int(x, 16) for x in e["expected_allow"]], np.uint32))
 
 
-@pytest.mark.parametrize("wid", [1, 2, 3, 7, 8])
+@pytest.mark.parametrize("wid", [1, 2, 3, 7, 8, 10])
 @pytest.mark.parametrize("where", ["first", "middle", "last"])
 def test_align_eos_workloads(dv, wid, where):
     w = W.WORKLOADS[wid]
@@ -785,7 +785,7 @@ def test_spec_paper_example(dv, dtype):
     np.testing.assert_array_equal(f_w.cpu().numpy(), sp["expected_walk_final_state"])
 
 
-@pytest.mark.parametrize("wid,s", [(1, 4), (2, 4), (2, 8), (3, 6), (6, 8), (7, 8), (8, 8)])
+@pytest.mark.parametrize("wid,s", [(1, 4), (2, 4), (2, 8), (3, 6), (6, 8), (7, 8), (8, 8), (9, 8), (10, 8)])
 @pytest.mark.parametrize("layout", ["rows", "steps"])
 def test_spec_workload_full(dv, wid, s, layout):
     """Every row and position against the oracle.  ``rows``: the model's
@@ -983,7 +983,8 @@ def _sample_chain(dv, ns, al, init_states, x, seed, inv_t, ws):
 
 
 @pytest.mark.parametrize("wid,steps,inv_t", [(1, 64, 1.0), (2, 64, 1.0), (2, 16, 0.5), (3, 16, 1.0),
-                                             (6, 32, 1.0), (7, 32, 2.0), (8, 32, 1.0)])
+                                             (6, 32, 1.0), (7, 32, 2.0), (8, 32, 1.0), (9, 32, 1.0),
+                                             (10, 32, 0.5)])
 def test_sample_chain_workload_full(dv, wid, steps, inv_t):
     """Every row and step against the oracle's own sampled chain (its own
     table, its own previous states)."""

@@ -1,12 +1,15 @@
-"""The scanner workloads' automata against Python's own regular-expression
+"""The Appendix C grammar automata against Python's own regular-expression
 engine (an independent implementation), on the CPU.
 
 ``workloads.regex_dfa`` compiles byte regexes to minimal trimmed DFAs; these
-tests check, for every terminal of the JSON and C scanners, the JSON-schema
-expression and the scanners themselves (``(?:t1|...|tn)*``, Sec. 3.2), that
-the automaton accepts exactly the strings ``re.fullmatch`` accepts -- on
-corpus text, its substrings, mutated copies and random strings -- and that
-every state is reachable from the start and can still reach acceptance.
+tests check, for every terminal of the basic-JSON, simple-C and XML scanners,
+for the scanners themselves (R = r+ over the terminals, the lemma of Sec.
+3.2) and for the GSM8K and fixed-template grammars (one expression each),
+that the automaton accepts exactly the strings ``re.fullmatch`` accepts -- on
+corpus text, its substrings, mutated copies and random strings -- that whole
+documents of each grammar's shape are accepted and that every prefix of one
+stays alive, and that every state is reachable from the start and can still
+reach acceptance.
 """
 import re
 
@@ -25,6 +28,15 @@ def accepts(trans, accepting, text: bytes) -> bool:
         if s < 0:
             return False
     return bool(accepting[s])
+
+
+def alive(trans, text: bytes) -> bool:
+    s = 0
+    for b in text:
+        s = int(trans[s, b])
+        if s < 0:
+            return False
+    return True
 
 
 def _samples(rng, docs, alphabet, n, max_len):
@@ -54,67 +66,126 @@ def _samples(rng, docs, alphabet, n, max_len):
     return out
 
 
+def _mutants(rng, docs, alphabet, n):
+    """Whole documents with one byte changed, inserted or dropped."""
+    out = []
+    for _ in range(n):
+        t = bytearray(docs[int(rng.integers(len(docs)))].encode())
+        j = int(rng.integers(0, len(t) + 1))
+        c = int(alphabet[rng.integers(len(alphabet))])
+        op = rng.integers(3)
+        if op == 0 and j < len(t):
+            t[j] = c
+        elif op == 1:
+            t.insert(j, c)
+        elif j < len(t):
+            del t[j]
+        out.append(bytes(t))
+    return out
+
+
 @pytest.fixture(scope="module")
 def docs():
-    return G.corpus(np.random.default_rng(5), 300_000)
+    return G.corpus(np.random.default_rng(5), 400_000)
+
+
+def _of(docs, kind):
+    """The corpus documents of one kind (each generator's shape is distinct)."""
+    if kind == "gsm8k":
+        return [d for d in docs if '"thoughts"' in d]
+    if kind == "template":
+        return [d for d in docs if '"A nimble fighter"' in d]
+    if kind == "xml":
+        return [d for d in docs if d.startswith("<person>")]
+    if kind == "json":
+        return [d for d in docs if d.startswith("{") and '"name"' in d and '"thoughts"' not in d
+                and "nimble" not in d]
+    if kind == "c":
+        return [d for d in docs if d.split(" ", 1)[0] in ("int", "float", "char")]
+    raise KeyError(kind)
 
 
 JSON_BYTES = np.frombuffer(b' \t\n{}[]:,"\\/bfnrtu0123456789abcdefABCDEF.eE+-xyz\x01\xc3', np.uint8)
-C_BYTES = np.frombuffer(b' \t\n/*#_azAZ09xXuUlL.eE+-\'"\\{}[]();,?:~!<>=&|^%@$\x80', np.uint8)
+C_BYTES = np.frombuffer(b' \t\n/*_azAZ09xX.eE+-"\\{}[]();,<>=!#\'%&|\x80', np.uint8)
+XML_BYTES = np.frombuffer(b' \t\n</>personamgjobfridtlsy0123456789ABZ"&\xc3', np.uint8)
+TEMPLATE_BYTES = np.frombuffer(b' \t\n\r{}[]:,"idescrptonamgwhlfANb0123456789xyz', np.uint8)
+ALPHA = {"json-scanner": JSON_BYTES, "gsm8k-json": JSON_BYTES, "c-scanner": C_BYTES,
+         "xml-scanner": XML_BYTES, "template": TEMPLATE_BYTES}
+DOC_KIND = {"json-scanner": "json", "gsm8k-json": "gsm8k", "c-scanner": "c", "xml-scanner": "xml",
+            "template": "template"}
+TERMINALS = {"json": G.JSON_TERMINALS, "c": G.C_TERMINALS, "xml": G.XML_TERMINALS}
+TERM_BYTES = {"json": JSON_BYTES, "c": C_BYTES, "xml": XML_BYTES}
 
 
-@pytest.mark.parametrize("i", range(len(G.JSON_TERMINALS)))
-def test_json_terminal_matches_re(i, docs):
-    pat = G.JSON_TERMINALS[i]
+@pytest.mark.parametrize("grammar,i", [(g, i) for g in TERMINALS for i in range(len(TERMINALS[g]))])
+def test_terminal_matches_re(grammar, i, docs):
+    pat = TERMINALS[grammar][i]
     trans, acc = compile_regex(pat)
     rx = re.compile(pat.encode())
-    for s in _samples(np.random.default_rng(i), docs, JSON_BYTES, 3000, 24):
+    for s in _samples(np.random.default_rng(i), docs, TERM_BYTES[grammar], 2000, 24):
         assert accepts(trans, acc, s) == bool(rx.fullmatch(s)), (pat, s)
 
 
-@pytest.mark.parametrize("i", range(len(G.C_TERMINALS)))
-def test_c_terminal_matches_re(i, docs):
-    pat = G.C_TERMINALS[i]
-    trans, acc = compile_regex(pat)
-    rx = re.compile(pat.encode())
-    for s in _samples(np.random.default_rng(100 + i), docs, C_BYTES, 3000, 24):
-        assert accepts(trans, acc, s) == bool(rx.fullmatch(s)), (pat, s)
-
-
-@pytest.mark.parametrize("name", ["json-scanner", "json-schema", "c-lexer"])
+@pytest.mark.parametrize("name", list(G.AUTOMATA))
 def test_workload_automaton_matches_re(name, docs):
-    if name == "json-scanner":
-        (trans, acc), pat, alpha = G.json_scanner(), "(?:" + "|".join(f"(?:{t})" for t in G.JSON_TERMINALS) + ")*", JSON_BYTES
-    elif name == "json-schema":
-        (trans, acc), pat, alpha = G.json_schema(), G.json_schema_regex(), JSON_BYTES
-    else:
-        (trans, acc), pat, alpha = G.c_scanner(), "(?:" + "|".join(f"(?:{t})" for t in G.C_TERMINALS) + ")*", C_BYTES
-    rx = re.compile(pat.encode())
+    """Fragments of every kind of document, mutated copies and random strings;
+    whole documents of the grammar's shape; and, for the two grammars that
+    are one expression each, whole-document mutants.  (A scanner's
+    ``(?:t1|...|tn)+`` splits a long text in exponentially many ways, which
+    a backtracking engine explores when the text fails to match: the
+    scanners are compared on fragments only.)"""
+    build, regex = G.AUTOMATA[name]
+    trans, acc = build()
+    rx = re.compile(regex().encode())
+    alpha = ALPHA[name]
     rng = np.random.default_rng(7)
-    samples = _samples(rng, docs, alpha, 2500, 20)
-    hits = 0
-    for s in samples:
-        got = accepts(trans, acc, s)
-        assert got == bool(rx.fullmatch(s)), (name, s)
-        hits += got
-    if name != "json-schema":
-        assert 0 < hits < len(samples)
+    for s in _samples(rng, docs, alpha, 2500, 20):
+        assert accepts(trans, acc, s) == bool(rx.fullmatch(s)), (name, s)
+    whole = _of(docs, DOC_KIND[name])[:150]
+    assert len(whole) >= 50
+    for d in whole:                                  # every document of the shape is accepted
+        assert accepts(trans, acc, d.encode()), (name, d)
+    if name not in ("gsm8k-json", "template"):
         return
-    # the schema matches whole documents only: whole documents of its shape
-    # (compact and pretty-printed) and one-byte mutations of them
-    whole = [d.strip() for d in docs if d.startswith('{') and '"enabled"' in d and '"id"' in d][:300]
-    assert len(whole) > 100
-    mutated = _samples(rng, whole, alpha, 3000, 400)
     hits = 0
-    for s in [d.encode() for d in whole] + [m for m in mutated if len(m) > 40]:
-        got = accepts(trans, acc, s)
-        assert got == bool(rx.fullmatch(s)), (name, s)
+    for m in _mutants(rng, whole, alpha, 1500):
+        got = accepts(trans, acc, m)
+        assert got == bool(rx.fullmatch(m)), (name, m)
         hits += got
-    assert hits >= len(whole)
-    assert not accepts(trans, acc, b'{"name": "x", "id": 1, "price": 2, "tags": [], "enabled": true}')
+    assert hits < 1500 // 2                          # the fixed shapes reject most mutants
 
 
-@pytest.mark.parametrize("wid", [6, 7, 8])
+def test_prefixes_of_real_text_stay_alive(docs):
+    """No prefix of a document of a grammar's shape walks into DEAD (the
+    mask of Sec. 2 allows exactly continuations that can still complete)."""
+    for name, (build, _) in G.AUTOMATA.items():
+        trans, acc = build()
+        for d in _of(docs, DOC_KIND[name])[:40]:
+            s = 0
+            for b in d.encode():
+                s = int(trans[s, b])
+                assert s >= 0, (name, d)
+            assert acc[s], name
+
+
+def test_fixed_shapes_reject_out_of_order_or_missing_fields():
+    g, ga = G.gsm8k_json()
+    ok = b'{"thoughts": [{"step": "a", "calculation": "1 + 1 = 2", "result": 2}], "answer": 2}'
+    assert accepts(g, ga, ok)
+    assert not accepts(g, ga, ok.replace(b'"thoughts":', b'"thoughts" :'))    # no ws before the colon
+    assert not accepts(g, ga, b'{"thoughts": [], "answer": 2}')                 # at least one thought
+    assert not accepts(g, ga, ok.replace(b'"result": 2', b'"result": 02'))     # no leading zero
+    t, ta = G.template()
+    doc = ('{"id": 1, "description": "A nimble fighter", "name": "Ann", "age": 30, "armor": "plate", '
+           '"weapon": "bow", "class": "rogue", "mantra": "Go", "strength": 9, "items": ["a", "b", "c"]}')
+    assert accepts(t, ta, doc.encode())
+    assert not accepts(t, ta, doc.replace('"plate"', '"cloth"').encode())       # armor is one of three
+    assert not accepts(t, ta, doc.replace('"b", ', '').encode())                # exactly three items
+    assert not accepts(t, ta, doc.replace('"name": "Ann"', '"name": ""').encode())   # STRING is non-empty
+    assert not accepts(t, ta, doc.replace("A nimble", "A strong").encode())     # the fixed description
+
+
+@pytest.mark.parametrize("wid", [6, 7, 8, 9, 10])
 def test_workload_automata_are_trimmed(wid):
     """Every state is reachable from state 0 and can reach an accepting state
     (so DEAD means "cannot be completed"); no move leaves [0, S)."""
@@ -142,15 +213,15 @@ def test_workload_automata_are_trimmed(wid):
     assert len(good) == S
 
 
-def test_prefixes_of_real_text_stay_alive(docs):
-    """Prefixes of documents the automata accept never walk into DEAD."""
-    trans, acc = G.json_scanner()
-    for d in [x.encode() for x in docs if x.startswith("{")][:100]:
-        s = 0
-        for b in d:
-            s = int(trans[s, b])
-            assert s >= 0
-        assert acc[s]
+def test_scanner_is_r_plus():
+    """R = r+ (Sec. 3.2): non-empty terminal sequences only."""
+    t, a = scanner(["a", "bc"])
+    assert not accepts(t, a, b"") and accepts(t, a, b"a") and accepts(t, a, b"abca")
+    assert not accepts(t, a, b"ab") and alive(t, b"ab")
+    j, ja = G.json_scanner()
+    assert not ja[0]                               # an empty output is not a JSON terminal sequence
+    assert accepts(j, ja, b'{"a": [1, 2.5e3, true]}') and accepts(j, ja, b"}}{")   # terminals in any order
+    assert not alive(j, b"tru3") and not alive(j, b"01x")
 
 
 def test_small_automata_by_hand():
@@ -160,10 +231,9 @@ def test_small_automata_by_hand():
     assert accepts(t, a, b"aa") and accepts(t, a, b"aaa") and not accepts(t, a, b"a") and not accepts(t, a, b"aaaa")
     t, a = compile_regex("[^\\x00-\\xfe]")
     assert accepts(t, a, b"\xff") and not accepts(t, a, b"a")
-    t, a = scanner(["a", "bc"])
-    assert accepts(t, a, b"") and accepts(t, a, b"abca") and not accepts(t, a, b"ab")
     t, a = compile_regex("a(?:b[^\\x00-\\xff])")  # b can never be completed: trimmed away
     assert t.shape[0] == 1 and (t == -1).all() and a[0] == 0
+    assert G.lit("a{b}[c].*") == "a\\{b\\}\\[c\\]\\.\\*"
 
 
 def test_bpe_vocabulary_shape():
@@ -172,5 +242,6 @@ def test_bpe_vocabulary_shape():
     assert len(toks) == 32000 and len(set(toks)) == 32000
     assert toks[:256] == [bytes([b]) for b in range(256)]
     assert all(len(t) >= 2 and max(t) < 0x80 for t in toks[256:])
-    bridges = {b'":', b'",', b'"}', b'},', b'],'}
-    assert bridges <= set(toks)  # tokens that cross JSON terminal boundaries
+    # tokens that cross terminal boundaries of the grammars
+    bridges = {b'":', b'",', b'"}', b'},', b'],', b'</', b');'}
+    assert bridges <= set(toks), bridges - set(toks)

@@ -17,19 +17,23 @@ these generators stand in for them with the shapes below.  Five workloads:
  3     llm-tokenizer-scale         1,024    128,256   64      512    bf16   N(0, 3)
  4     grammar-lexer-union         8,192    128,256   256     256    bf16   N(0, 3)
  5     large-vocab-high-batch      4,096    256,000   1,024   128    bf16   N(0, 3)
- 6     json-scanner-bpe32k         22       32,000    64      256    bf16   N(0, 3)
- 7     json-schema-bpe32k          83       32,000    64      256    bf16   N(0, 3)
- 8     c-lexer-bpe32k              50       32,000    64      256    bf16   N(0, 3)
+ 6     json-scanner-bpe32k         23       32,000    64      256    bf16   N(0, 3)
+ 7     gsm8k-json-bpe32k           92       32,000    64      256    bf16   N(0, 3)
+ 8     c-scanner-bpe32k            62       32,000    64      256    bf16   N(0, 3)
+ 9     xml-scanner-bpe32k          30       32,000    64      256    bf16   N(0, 3)
+ 10    template-bpe32k             175      32,000    64      256    bf16   N(0, 3)
 ====  ==========================  =======  ========  ======  =====  =====  ===========
 
-Workloads 6-8 are real grammars' automata (``workloads.grammars``): the
-Sec. 3.2 scanner of JSON's lexical terminals, one JSON object shape as a
-single regular expression, and the scanner of C's lexical terminals, each
-compiled from regular expressions by ``workloads.regex_dfa`` (minimal,
-trimmed: every state can still reach acceptance).  They share one byte-level
-BPE vocabulary of 32,000 tokens trained on a seeded synthetic corpus (the
-size of the paper's two models' vocabularies); the accepting states are the
-automata's own.
+Workloads 6-10 are the automata of the paper's five Appendix C grammars
+(``workloads.grammars``): the Sec. 3.2 scanners (R = r+ over the
+terminals) of the basic JSON, simple C and XML-with-schema grammars, whose
+productions nest, and the GSM8K reasoning grammar and the fixed RPG
+template, which are regular and compile to one automaton each; all compiled
+from regular expressions by ``workloads.regex_dfa`` (minimal, trimmed:
+every state can still reach acceptance).  They share one byte-level BPE
+vocabulary of 32,000 tokens trained on a seeded synthetic corpus of those
+grammars' document shapes (the size of the paper's two models'
+vocabularies); the accepting states are the automata's own.
 
 Readings of points the workload description leaves open:
 
@@ -95,7 +99,7 @@ class Workload:
     lengths: tuple         # ("uniform", lo, hi) or ("geometric", p, hi)
     p_printable: float
     init: str              # "zero" or "uniform"
-    kind: str = "random"   # "random", "union" or a grammar: "json-scanner", "json-schema", "c-lexer"
+    kind: str = "random"   # "random", "union" or an Appendix C grammar (workloads.grammars.AUTOMATA)
     vocab_from: int = 0    # reuse another workload's vocabulary stream
 
     @property
@@ -121,12 +125,16 @@ WORKLOADS = {
                 ("geometric", 0.2, 32), 0.90, "zero", kind="union", vocab_from=3),
     5: Workload(5, "large-vocab-high-batch", 4096, 256000, 1024, 128, "bf16", 3.0, (8, 96),
                 ("geometric", 0.2, 48), 0.90, "uniform"),
-    6: Workload(6, "json-scanner-bpe32k", 22, 32000, 64, 256, "bf16", 3.0, (0, 0), ("bpe",), 1.0, "zero",
+    6: Workload(6, "json-scanner-bpe32k", 23, 32000, 64, 256, "bf16", 3.0, (0, 0), ("bpe",), 1.0, "zero",
                 kind="json-scanner"),
-    7: Workload(7, "json-schema-bpe32k", 83, 32000, 64, 256, "bf16", 3.0, (0, 0), ("bpe",), 1.0, "zero",
-                kind="json-schema", vocab_from=6),
-    8: Workload(8, "c-lexer-bpe32k", 50, 32000, 64, 256, "bf16", 3.0, (0, 0), ("bpe",), 1.0, "zero",
-                kind="c-lexer", vocab_from=6),
+    7: Workload(7, "gsm8k-json-bpe32k", 92, 32000, 64, 256, "bf16", 3.0, (0, 0), ("bpe",), 1.0, "zero",
+                kind="gsm8k-json", vocab_from=6),
+    8: Workload(8, "c-scanner-bpe32k", 62, 32000, 64, 256, "bf16", 3.0, (0, 0), ("bpe",), 1.0, "zero",
+                kind="c-scanner", vocab_from=6),
+    9: Workload(9, "xml-scanner-bpe32k", 30, 32000, 64, 256, "bf16", 3.0, (0, 0), ("bpe",), 1.0, "zero",
+                kind="xml-scanner", vocab_from=6),
+    10: Workload(10, "template-bpe32k", 175, 32000, 64, 256, "bf16", 3.0, (0, 0), ("bpe",), 1.0, "zero",
+                 kind="template", vocab_from=6),
 }
 
 
@@ -260,9 +268,7 @@ def dfa(workload: int):
     else:
         from . import grammars
 
-        build = {"json-scanner": grammars.json_scanner, "json-schema": grammars.json_schema,
-                 "c-lexer": grammars.c_scanner}[w.kind]
-        trans, acc = (a.copy() for a in build())
+        trans, acc = (a.copy() for a in grammars.AUTOMATA[w.kind][0]())
         if trans.shape[0] != w.S:
             raise RuntimeError(f"{w.name}: automaton has {trans.shape[0]} states, {w.S} expected")
     trans.setflags(write=False)

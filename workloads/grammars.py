@@ -1,27 +1,42 @@
-"""Scanner automata of real grammars and a byte-level BPE vocabulary.
+"""Automata of the paper's Appendix C grammars and a byte-level BPE vocabulary.
 
-Stand-ins for the paper's grammar workloads (Sec. 4: JSON, C; Appendix C)
-and its models' 32,000-token vocabularies, none of which are available here:
+The paper measures constrained decoding on five grammars, listed in its
+Appendix C (Sec. 4, efficiency).  Their automata are built here from the
+productions as the appendix gives them, restated as byte regular
+expressions:
 
-* ``JSON_TERMINALS`` -- the lexical terminals of JSON (whitespace,
-  punctuation, string, number, true / false / null), written from the JSON
-  grammar of RFC 8259; ``json_scanner()`` is the Sec. 3.2 scanner over them
-  (any terminal may follow any other).
-* ``json_schema()`` -- one fixed JSON object shape (keys, value types, a list
-  of strings) as a single regular expression: the kind of constraint that
-  schema-driven generation produces, with every separator and key forced.
-* ``C_TERMINALS`` / ``c_scanner()`` -- the lexical terminals of C
-  (identifiers and keywords, integer and floating constants, character and
-  string literals, comments, preprocessor lines, punctuators), written from
-  the C language's lexical grammar.
+* ``json_scanner()`` -- the basic JSON grammar is context-free (objects and
+  arrays nest), so its automaton is the Sec. 3.2 scanner: R = r+ over the
+  grammar's terminals ``JSON_TERMINALS`` (the six punctuation literals, the
+  three keyword literals, ``string``, ``number`` and whitespace).
+* ``gsm8k_json()`` -- the guided-math-reasoning (GSM8K) grammar never
+  recurses from ``root`` (``object`` holds a list of ``thought`` objects and
+  an answer; ``value`` and ``array`` are unreachable), so the whole grammar
+  is one regular expression, ``gsm8k_regex()``, and one automaton.
+* ``c_scanner()`` -- the simple C program grammar nests statements, so its
+  automaton is the scanner over ``C_TERMINALS`` (keywords, punctuation and
+  operators, identifiers, numbers, strings, both comment forms, whitespace).
+* ``xml_scanner()`` -- the XML-with-schema grammar nests persons inside
+  ``friends``: the scanner over ``XML_TERMINALS`` (the fourteen tags,
+  ``NAME`` / ``NUMBER`` = ``[^<]+``, whitespace).
+* ``template()`` -- the fixed RPG-character template is one regular
+  expression, ``template_regex()``.  The listing declares ``WS`` without
+  saying where it may occur; it is read as whitespace that may appear
+  between any two tokens and around the document (how such a declared
+  whitespace terminal is used in that grammar notation).
+
 * ``bpe_vocab(V)`` -- a byte-level BPE vocabulary trained with the
-  ``tokenizers`` library on a seeded synthetic corpus (pseudo-word prose,
-  JSON documents, C-like code), pre-split into words with an optional
-  leading space, digit groups of up to three, runs of other symbols with an
-  optional leading space, and whitespace.  Its first 256 tokens are the 256
-  single bytes (every byte string stays encodable), then the learned tokens
-  in merge order.  Multi-symbol tokens such as ``":``, ``",`` or ``});``
-  cross terminal boundaries: the bridge tokens the alignment exists for.
+  ``tokenizers`` library on a seeded synthetic corpus whose documents have
+  the shapes these grammars constrain (person objects in JSON and XML,
+  step-by-step JSON reasoning records, RPG character profiles, small C
+  programs) plus pseudo-word prose.  All text is generated from seeded
+  pseudo-words and numbers.  The text is pre-split into words with an
+  optional leading space, digit groups of up to three, runs of other symbols
+  with an optional leading space, and whitespace.  Its first 256 tokens are
+  the 256 single bytes (every byte string stays encodable), then the learned
+  tokens in merge order.  Multi-symbol tokens such as ``":``, ``",`` or
+  ``</`` cross terminal boundaries: the bridge tokens the alignment exists
+  for.
 
 Only inputs are built here (no walk, no mask, no argmax).
 """
@@ -31,49 +46,86 @@ import functools
 
 import numpy as np
 
-from .regex_dfa import compile_regex, scanner
+from .regex_dfa import compile_regex, scanner, scanner_regex
 
-WS = r"[ \t\n\r]"
-
-JSON_TERMINALS = [
-    WS + "+",
-    r"[{}\[\]:,]",
-    r'"(?:[^"\\\x00-\x1f]|\\(?:["\\/bfnrt]|u[0-9a-fA-F]{4}))*"',
-    r"-?(?:0|[1-9][0-9]*)(?:\.[0-9]+)?(?:[eE][+-]?[0-9]+)?",
-    r"true|false|null",
-]
-
-_JSTR = JSON_TERMINALS[2]
-_JNUM = JSON_TERMINALS[3]
-_JINT = r"-?(?:0|[1-9][0-9]*)"
-
-C_TERMINALS = [
-    r"[ \t\n\r\f\v]+",
-    r"//[^\n]*",
-    r"/\*(?:[^*]|\*+[^*/])*\*+/",
-    r"#[^\n]*",
-    r"[A-Za-z_][A-Za-z0-9_]*",
-    r"(?:0[xX][0-9a-fA-F]+|0[0-7]*|[1-9][0-9]*)(?:[uU](?:l|L|ll|LL)?|(?:l|L|ll|LL)[uU]?)?",
-    r"(?:[0-9]+\.[0-9]*|\.[0-9]+)(?:[eE][+-]?[0-9]+)?[fFlL]?|[0-9]+[eE][+-]?[0-9]+[fFlL]?",
-    r"'(?:[^'\\\n]|\\.)+'",
-    r'"(?:[^"\\\n]|\\.)*"',
-    r"->|\+\+|--|<<=?|>>=?|[<>=!]=|&&|\|\||[-+*/%&|^]=|\.\.\.|[{}\[\]();,.?:~!<>=+\-*/%&|^]",
-]
+_META = set("\\()[]{}.|*+?")
 
 
-def _kv(key: str, value: str) -> str:
+def lit(s: str) -> str:
+    """A regular expression matching exactly the string ``s``."""
+    return "".join("\\" + c if c in _META else c for c in s)
+
+
+WS = r"[ \t\n]"              # the grammars' whitespace characters
+
+# ----------------------------------------------------- basic JSON (Appendix C)
+# string ::= '"' ( [^"\\] | '\' ( ["\/bfnrt] | 'u' hex hex hex hex ) )* '"'
+JSON_STRING = r'"(?:[^"\\]|\\(?:["\\/bfnrt]|u[0-9a-fA-F]{4}))*"'
+# number ::= '-'? ( [0-9] | [1-9] [0-9]* ) ( '.' [0-9]+ )? ( [eE] [-+]? [0-9]+ )?
+JSON_NUMBER = r"-?(?:[0-9]|[1-9][0-9]*)(?:\.[0-9]+)?(?:[eE][-+]?[0-9]+)?"
+JSON_TERMINALS = ([lit(c) for c in "{}[],:"] + ["true", "false", "null", JSON_STRING, JSON_NUMBER, WS + "+"])
+
+
+# ------------------------------------------------- GSM8K reasoning (Appendix C)
+def gsm8k_regex() -> str:
+    """The guided-math-reasoning grammar as one regular expression:
+    object ::= ws '{' ws '"thoughts"' ':' ws '[' ws thought (ws ',' ws thought)* ']' ws ',' ws
+               '"answer"' ':' ws number ws '}' ws
+    thought ::= '{' ws '"step"' ':' ws string ',' ws '"calculation"' ':' ws string ',' ws
+                '"result"' ':' ws number '}' ws
+    where string and number carry their trailing ws (as in the grammar) and
+    ws ::= ([ \\t\\n] ws)? is any run of whitespace (possibly empty)."""
     w = WS + "*"
-    return f'"{key}"{w}:{w}{value}'
+    string = JSON_STRING + w
+    number = JSON_NUMBER + w
+    thought = (r"\{" + w + lit('"step"') + ":" + w + string + "," + w + lit('"calculation"') + ":" + w + string
+               + "," + w + lit('"result"') + ":" + w + number + r"\}" + w)
+    return (w + r"\{" + w + lit('"thoughts"') + ":" + w + r"\[" + w + thought + f"(?:{w},{w}{thought})*" + r"\]"
+            + w + "," + w + lit('"answer"') + ":" + w + number + w + r"\}" + w)
 
 
-def json_schema_regex() -> str:
-    """{"id": int, "name": string, "price": number, "tags": [string, ...],
-    "enabled": true|false|null}, keys in this order, any JSON whitespace."""
+# ----------------------------------------------------- simple C (Appendix C)
+C_KEYWORDS = ["int", "float", "char", "return", "while", "for", "if", "else"]
+C_PUNCT = ["(", ")", "{", "}", "=", ";", "[", "]", "<=", "<", "==", "!=", ">=", ">", "+", "-", "*", "/", ","]
+C_IDENTIFIER = r"[a-zA-Z_][a-zA-Z_0-9]*"
+C_NUMBER = r"[0-9]+"
+C_LINE_COMMENT = r"//[^\n]*\n"                      # singleLineComment ::= '//' [^\n]* '\n'
+C_BLOCK_COMMENT = r"/\*(?:[^*]|\*[^/])*\*/"         # multiLineComment ::= '/*' ( [^*] | '*' [^/] )* '*/'
+C_TERMINALS = ([lit(k) for k in C_KEYWORDS] + [lit(p) for p in C_PUNCT]
+               + [C_IDENTIFIER, C_NUMBER, JSON_STRING, C_LINE_COMMENT, C_BLOCK_COMMENT, WS + "+"])
+
+# ------------------------------------------------ XML with schema (Appendix C)
+XML_TAGS = ["person", "name", "age", "job", "friends", "title", "salary"]
+XML_TEXT = r"[^<]+"                                  # NAME ::= ( [^<] )+ ; NUMBER ::= ( [^<] )+
+XML_TERMINALS = ([lit(f"<{t}>") for t in XML_TAGS] + [lit(f"</{t}>") for t in XML_TAGS]
+                 + [XML_TEXT, WS + "+"])
+
+
+# -------------------------------------------------- fixed template (Appendix C)
+TEMPLATE_STRING = r'"[^\n\r"]+"'                     # STRING: /"[^\n\r"]+"/
+TEMPLATE_NUMBER = r"[0-9]+"                          # NUMBER: /[0-9]+/
+
+
+def template_regex() -> str:
+    """dict: '{' content '}' with the ten pairs of the listing in order
+    (id NUMBER, description the fixed string, name STRING, age NUMBER, armor
+    one of three strings, weapon one of three, class / mantra STRING,
+    strength NUMBER, items a list of exactly three STRINGs), each key a
+    quoted literal followed by ':'; whitespace may separate any two tokens."""
     w = WS + "*"
-    tags = rf"\[{w}(?:{_JSTR}(?:{w},{w}{_JSTR})*)?{w}\]"
-    fields = [_kv("id", _JINT), _kv("name", _JSTR), _kv("price", _JNUM), _kv("tags", tags),
-              _kv("enabled", "(?:true|false|null)")]
-    return r"\{" + w + f"{w},{w}".join(fields) + w + r"\}"
+
+    def pair(key, value):
+        return lit(f'"{key}"') + w + ":" + w + value
+
+    def one_of(*xs):
+        return "(?:" + "|".join(lit(f'"{x}"') for x in xs) + ")"
+
+    s, n = TEMPLATE_STRING, TEMPLATE_NUMBER
+    items = r"\[" + w + s + w + "," + w + s + w + "," + w + s + w + r"\]"
+    pairs = [pair("id", n), pair("description", lit('"A nimble fighter"')), pair("name", s), pair("age", n),
+             pair("armor", one_of("leather", "chainmail", "plate")), pair("weapon", one_of("sword", "axe", "bow")),
+             pair("class", s), pair("mantra", s), pair("strength", n), pair("items", items)]
+    return w + r"\{" + w + (w + "," + w).join(pairs) + w + r"\}" + w
 
 
 @functools.lru_cache(maxsize=None)
@@ -82,8 +134,8 @@ def json_scanner():
 
 
 @functools.lru_cache(maxsize=None)
-def json_schema():
-    return compile_regex(json_schema_regex())
+def gsm8k_json():
+    return compile_regex(gsm8k_regex())
 
 
 @functools.lru_cache(maxsize=None)
@@ -91,12 +143,29 @@ def c_scanner():
     return scanner(C_TERMINALS)
 
 
+@functools.lru_cache(maxsize=None)
+def xml_scanner():
+    return scanner(XML_TERMINALS)
+
+
+@functools.lru_cache(maxsize=None)
+def template():
+    return compile_regex(template_regex())
+
+
+# Each workload automaton with the regular expression it accepts (for tests).
+AUTOMATA = {
+    "json-scanner": (json_scanner, lambda: scanner_regex(JSON_TERMINALS)),
+    "gsm8k-json": (gsm8k_json, gsm8k_regex),
+    "c-scanner": (c_scanner, lambda: scanner_regex(C_TERMINALS)),
+    "xml-scanner": (xml_scanner, lambda: scanner_regex(XML_TERMINALS)),
+    "template": (template, template_regex),
+}
+
 # ------------------------------------------------------------------- the corpus
 
 _CONS = "bcdfghjklmnprstvwz"
 _VOW = "aeiou"
-_C_TYPES = ["int", "char", "float", "double", "void", "long", "unsigned", "short", "size_t", "struct node"]
-_C_OPS = ["+", "-", "*", "/", "%", "<<", ">>", "&", "|", "^", "==", "!=", "<", ">", "<=", ">=", "&&", "||"]
 
 
 def _words(rng: np.random.Generator, n: int) -> list:
@@ -114,6 +183,10 @@ def _words(rng: np.random.Generator, n: int) -> list:
 
 
 class _Corpus:
+    """Seeded documents of the shapes the Appendix C grammars constrain.  The
+    ``*_doc`` generators of the JSON-reasoning, template, XML and C kinds
+    always conform to their grammar; prose and some JSON do not need to."""
+
     def __init__(self, rng: np.random.Generator):
         self.rng = rng
         self.words = _words(rng, 20000)
@@ -122,24 +195,36 @@ class _Corpus:
         self.p = p / p.sum()          # Zipf frequencies
         self.buf = []
 
+    def r(self, n) -> int:
+        return int(self.rng.integers(n))
+
     def word(self) -> str:
         if not self.buf:              # word ranks drawn in batches
             self.buf = self.rng.choice(len(self.words), size=100_000, p=self.p).tolist()[::-1]
         return self.words[self.buf.pop()]
 
+    def name(self) -> str:
+        return " ".join(self.word().capitalize() for _ in range(1 + self.r(2)))
+
+    def integer(self, digits=4) -> str:
+        return str(int(self.rng.integers(0, 10 ** int(self.rng.integers(1, digits + 1)))))
+
     def number(self) -> str:
-        r = self.rng.random()
-        if r < 0.5:
-            return str(int(self.rng.integers(0, 10 ** int(self.rng.integers(1, 7)))))
-        if r < 0.9:
-            return f"{self.rng.uniform(-1000, 1000):.{int(self.rng.integers(0, 4))}f}"
-        return f"{self.rng.uniform(0, 10):.2e}"
+        x = self.rng.random()
+        if x < 0.5:
+            return self.integer(6)
+        if x < 0.9:
+            return f"{self.rng.uniform(-1000, 1000):.{int(self.rng.integers(1, 4))}f}"
+        return f"{self.rng.uniform(1, 10):.2e}"
+
+    def phrase(self, lo=2, hi=8) -> str:
+        return " ".join(self.word() for _ in range(int(self.rng.integers(lo, hi))))
 
     def sentence(self) -> str:
         n = int(self.rng.integers(4, 18))
         ws = [self.word() for _ in range(n)]
         if self.rng.random() < 0.2:
-            ws[int(self.rng.integers(n))] = self.number()
+            ws[self.r(n)] = self.number()
         ws[0] = ws[0].capitalize()
         parts = []
         for i, w in enumerate(ws):
@@ -151,85 +236,143 @@ class _Corpus:
     def prose(self) -> str:
         return " ".join(self.sentence() for _ in range(int(self.rng.integers(2, 7)))) + "\n"
 
-    def json_value(self, depth: int) -> str:
-        r = self.rng.random()
-        if depth < 3 and r < 0.15:
-            return self.json_object(depth + 1)
-        if depth < 3 and r < 0.3:
-            return "[" + ", ".join(self.json_value(depth + 1) for _ in range(int(self.rng.integers(0, 5)))) + "]"
-        if r < 0.6:
-            return '"' + " ".join(self.word() for _ in range(int(self.rng.integers(1, 4)))) + '"'
-        if r < 0.85:
-            return self.number()
-        return str(self.rng.choice(["true", "false", "null"]))
+    # -- layout: compact or pretty-printed JSON-like text
+    def _layout(self, items, open_, close, depth, pretty):
+        if not items:
+            return open_ + close
+        if not pretty:
+            return open_ + ", ".join(items) + close
+        pad, inner = "  " * depth, "  " * (depth + 1)
+        return open_ + "\n" + ",\n".join(inner + it for it in items) + "\n" + pad + close
 
-    def json_object(self, depth: int = 0) -> str:
-        n = int(self.rng.integers(1, 6))
-        items = [f'"{self.word()}": {self.json_value(depth)}' for _ in range(n)]
-        return "{" + ", ".join(items) + "}"
+    # -- basic JSON: a person, with friends
+    def json_person(self, depth=0, pretty=False) -> str:
+        items = [f'"name": "{self.name()}"', f'"age": {self.integer(2)}']
+        if self.rng.random() < 0.6:
+            items.append(f'"email": "{self.word()}@{self.word()}.com"')
+        if self.rng.random() < 0.5:
+            items.append(f'"married": {self.rng.choice(["true", "false", "null"])}')
+        if self.rng.random() < 0.4:
+            items.append(f'"address": ' + self._layout([f'"street": "{self.integer(3)} {self.name()}"',
+                                                        f'"city": "{self.name()}"'], "{", "}", depth + 1, pretty))
+        if depth < 2 and self.rng.random() < 0.5:
+            friends = [self.json_person(depth + 2, pretty) for _ in range(self.r(3) + 1)]
+            items.append('"friends": ' + self._layout(friends, "[", "]", depth + 1, pretty))
+        if self.rng.random() < 0.3:
+            items.append(f'"score": {self.number()}')
+        return self._layout(items, "{", "}", depth, pretty)
 
     def json_doc(self) -> str:
-        if self.rng.random() < 0.5:  # the schema's shape
-            tags = ", ".join(f'"{self.word()}"' for _ in range(int(self.rng.integers(0, 5))))
-            name = " ".join(self.word() for _ in range(int(self.rng.integers(1, 4))))
-            doc = (f'{{"id": {int(self.rng.integers(0, 10**6))}, "name": "{name}", "price": {self.number()}, '
-                   f'"tags": [{tags}], "enabled": {self.rng.choice(["true", "false", "null"])}}}')
-        else:
-            doc = self.json_object()
-        if self.rng.random() < 0.4:  # pretty-printed
-            doc = doc.replace("{", "{\n  ").replace(", ", ",\n  ").replace("}", "\n}")
-        return doc + "\n"
+        return self.json_person(pretty=self.rng.random() < 0.5) + "\n"
 
-    def c_expr(self, depth: int = 0) -> str:
-        r = self.rng.random()
-        if depth < 2 and r < 0.35:
-            return f"{self.c_expr(depth + 1)} {self.rng.choice(_C_OPS)} {self.c_expr(depth + 1)}"
-        if depth < 2 and r < 0.45:
-            return f"{self.word()}({', '.join(self.c_expr(depth + 1) for _ in range(int(self.rng.integers(0, 3))))})"
-        if r < 0.7:
+    # -- step-by-step JSON reasoning records (the GSM8K grammar's shape)
+    def gsm8k_doc(self) -> str:
+        pretty = self.rng.random() < 0.6
+        thoughts = []
+        for _ in range(1 + self.r(4)):
+            a, b = int(self.rng.integers(1, 200)), int(self.rng.integers(1, 50))
+            op = str(self.rng.choice(["+", "-", "*", "/"]))
+            res = {"+": a + b, "-": a - b, "*": a * b, "/": a // b}[op]
+            calc = f"{a} {op} {b} = {res}"
+            thoughts.append(self._layout([f'"step": "{self.phrase(3, 10).capitalize()}"',
+                                          f'"calculation": "{calc}"', f'"result": {res}'], "{", "}", 2, pretty))
+        body = [f'"thoughts": ' + self._layout(thoughts, "[", "]", 1, pretty), f'"answer": {self.integer(4)}']
+        return self._layout(body, "{", "}", 0, pretty) + "\n"
+
+    # -- RPG character profiles (the fixed template's shape)
+    def template_doc(self) -> str:
+        pretty = self.rng.random() < 0.6
+        items = [f'"id": {self.integer(4)}', '"description": "A nimble fighter"', f'"name": "{self.name()}"',
+                 f'"age": {self.integer(2)}', f'"armor": "{self.rng.choice(["leather", "chainmail", "plate"])}"',
+                 f'"weapon": "{self.rng.choice(["sword", "axe", "bow"])}"', f'"class": "{self.word()}"',
+                 f'"mantra": "{self.phrase(2, 7).capitalize()}"', f'"strength": {self.integer(2)}',
+                 '"items": [' + ", ".join(f'"{self.phrase(1, 3)}"' for _ in range(3)) + "]"]
+        return self._layout(items, "{", "}", 0, pretty) + "\n"
+
+    # -- XML persons (the XML-with-schema grammar's shape)
+    def xml_person(self, depth=0) -> str:
+        pad, inner = "  " * depth, "  " * (depth + 1)
+        job = (f"{inner}<job>\n{inner}  <title>{self.phrase(1, 4).title()}</title>\n"
+               f"{inner}  <salary>{self.integer(6)}</salary>\n{inner}</job>\n")
+        out = (f"{pad}<person>\n{inner}<name>{self.name()}</name>\n{inner}<age>{self.integer(2)}</age>\n" + job)
+        if depth < 2 and self.rng.random() < 0.4:
+            out += f"{inner}<friends>\n" + "".join(self.xml_person(depth + 2) for _ in range(1 + self.r(2)))
+            out += f"{inner}</friends>\n"
+        return out + f"{pad}</person>\n"
+
+    def xml_doc(self) -> str:
+        return self.xml_person()
+
+    # -- small C programs (the simple C grammar's statements and expressions)
+    def c_expr(self, depth=0) -> str:
+        x = self.rng.random()
+        if depth < 2 and x < 0.35:
+            return f"{self.c_expr(depth + 1)} {self.rng.choice(['+', '-', '*', '/'])} {self.c_expr(depth + 1)}"
+        if depth < 2 and x < 0.45:
+            return f"{self.word()}({', '.join(self.c_expr(depth + 1) for _ in range(self.r(3)))})"
+        if depth < 2 and x < 0.5:
+            return f"({self.c_expr(depth + 1)})"
+        if x < 0.75:
             return self.word()
-        if r < 0.8:
-            return f"0x{int(self.rng.integers(0, 65536)):x}"
-        if r < 0.9:
-            return self.number().lstrip("-")
-        return f"'{self.rng.choice(list('abcxyz0'))}'"
+        if x < 0.9:
+            return self.integer(3)
+        return f'"{self.sentence()}\\n"'
 
-    def c_stmt(self, indent: str) -> str:
-        r = self.rng.random()
-        if r < 0.4:
-            return f"{indent}{self.word()} = {self.c_expr()};\n"
-        if r < 0.55:
-            return f"{indent}if ({self.c_expr()}) {{\n{indent}    {self.word()}++;\n{indent}}}\n"
-        if r < 0.65:
-            v = self.word()
-            return f"{indent}for (int {v} = 0; {v} < {self.c_expr()}; {v}++) {{\n{indent}    {self.c_stmt('').strip()}\n{indent}}}\n"
-        if r < 0.75:
-            return f'{indent}printf("{self.sentence()}\\n", {self.word()});\n'
-        if r < 0.85:
-            return f"{indent}// {self.sentence()}\n"
-        return f"{indent}return {self.c_expr()};\n"
+    def c_cond(self) -> str:
+        return f"{self.c_expr(1)} {self.rng.choice(['<', '<=', '==', '!=', '>=', '>'])} {self.c_expr(1)}"
 
-    def c_func(self) -> str:
-        head = ""
-        if self.rng.random() < 0.3:
-            head = f"#include <{self.word()}.h>\n#define {self.word().upper()} {self.number().lstrip('-')}\n"
-        if self.rng.random() < 0.3:
-            head += f"/* {self.sentence()} */\n"
-        args = ", ".join(f"{self.rng.choice(_C_TYPES)} {self.word()}" for _ in range(int(self.rng.integers(0, 4))))
-        body = "".join(self.c_stmt("    ") for _ in range(int(self.rng.integers(2, 8))))
-        return f"{head}{self.rng.choice(_C_TYPES)} {self.word()}({args}) {{\n{body}}}\n"
+    def c_stmt(self, ind, depth=0) -> str:
+        x = self.rng.random()
+        t = self.rng.choice(["int", "float", "char"])
+        v = self.word()
+        if x < 0.25:
+            return f"{ind}{t} {v} = {self.c_expr()};\n"
+        if x < 0.35:
+            return f"{ind}{t} {v}[{self.integer(2)}];\n"
+        if x < 0.5:
+            return f"{ind}{v} = {self.c_expr()};\n"
+        if x < 0.62:
+            return f'{ind}printf("{self.sentence()}\\n", {self.word()});\n'
+        if depth < 2 and x < 0.72:
+            body = "".join(self.c_stmt(ind + "    ", depth + 1) for _ in range(1 + self.r(3)))
+            return f"{ind}for(int {v} = 0; {v} < {self.c_expr(1)}; {v} = {v} + 1){{\n{body}{ind}}}\n"
+        if depth < 2 and x < 0.8:
+            body = "".join(self.c_stmt(ind + "    ", depth + 1) for _ in range(1 + self.r(3)))
+            return f"{ind}while({self.c_cond()}) {{\n{body}{ind}}}\n"
+        if depth < 2 and x < 0.88:
+            body = "".join(self.c_stmt(ind + "    ", depth + 1) for _ in range(1 + self.r(2)))
+            return f"{ind}if({self.c_cond()}){{\n{body}{ind}}}\n"
+        if x < 0.94:
+            return f"{ind}// {self.sentence()}\n"
+        return f"{ind}/* {self.sentence()} */\n"
+
+    def c_doc(self) -> str:
+        out = ""
+        for _ in range(1 + self.r(2)):
+            t = self.rng.choice(["int", "float", "char"])
+            par = f"{self.rng.choice(['int', 'float', 'char'])} {self.word()}" if self.rng.random() < 0.6 else ""
+            body = "".join(self.c_stmt("    ") for _ in range(2 + self.r(6)))
+            out += f"{t} {self.word()}({par}) {{\n{body}    return {self.c_expr()};\n}}\n"
+        return out
 
 
-def corpus(rng: np.random.Generator, n_bytes: int) -> list:
-    """Seeded training text, about n_bytes long: prose, JSON and C-like code
-    in a 4 : 3 : 3 byte mix, as separate documents."""
+KINDS = ("prose", "json", "gsm8k", "template", "xml", "c")
+_SHARE = np.array([0.25, 0.15, 0.15, 0.15, 0.15, 0.15])
+
+
+def corpus(rng: np.random.Generator, n_bytes: int, kinds=KINDS) -> list:
+    """Seeded training text, about n_bytes long, as separate documents of the
+    given kinds (prose, JSON persons, JSON reasoning records, RPG profiles,
+    XML persons, C programs) in fixed byte shares."""
     c = _Corpus(rng)
+    make = {"prose": c.prose, "json": c.json_doc, "gsm8k": c.gsm8k_doc, "template": c.template_doc,
+            "xml": c.xml_doc, "c": c.c_doc}
+    share = np.array([_SHARE[KINDS.index(k)] for k in kinds])
     docs = []
-    sizes = [0, 0, 0]
-    share = np.array([0.4, 0.3, 0.3])
-    while sum(sizes) < n_bytes:
-        k = int(np.argmin(np.array(sizes) / share))
-        d = (c.prose, c.json_doc, c.c_func)[k]()
+    sizes = np.zeros(len(kinds))
+    while sizes.sum() < n_bytes:
+        k = int(np.argmin(sizes / share))
+        d = make[kinds[k]]()
         sizes[k] += len(d)
         docs.append(d)
     return docs

@@ -7,7 +7,7 @@ partition refinement minimises it, and states from which no accepting state
 can be reached are removed, so that a move to DEAD means exactly "this text
 can no longer be completed".  A scanner over several terminals, each of
 which may follow any other (the chaining of Sec. 3.2), is the automaton of
-``(?:t1|t2|...)*``.
+``(?:t1|t2|...)+`` (the lemma's R = r+).
 
 Like the rest of ``workloads``, this builds inputs only: it walks no
 vocabulary and computes no mask.
@@ -336,9 +336,18 @@ def _finish(ctab: np.ndarray, accepting: np.ndarray, classes):
     return trans, acc
 
 
-def scanner(terminals) -> tuple:
-    """The scanner automaton of Sec. 3.2 for a list of terminal regexes: any
-    sequence of terminals, each one allowed to follow any other."""
+def scanner_regex(terminals) -> str:
+    """R = r+ with r the union of the terminal regexes (the lemma of Sec.
+    3.2): every non-empty sequence of terminals, each one allowed to follow
+    any other."""
     body = "|".join(f"(?:{t})" for t in terminals)
-    return compile_regex(f"(?:{body})*")
+    return f"(?:{body})+"
+
+
+def scanner(terminals) -> tuple:
+    """The scanner automaton of Sec. 3.2 for a list of terminal regexes (the
+    automaton of ``scanner_regex``).  Its start state accepts only if some
+    terminal matches the empty string: an empty output is not a terminal
+    sequence."""
+    return compile_regex(scanner_regex(terminals))
 
