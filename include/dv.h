@@ -105,9 +105,10 @@ DV_API size_t dv_align_workspace_bytes(int32_t num_states, int32_t num_tokens);
  * Inputs (device, read only):
  *   trans      [S][256] int32, row-major: trans[s*256 + b] is the move of
  *              state s on byte b.  Values outside [0, S) read as DV_DEAD.
- *   offsets    [V+1] int32, offsets[0] = 0, non-decreasing (precondition,
- *              not checked on the device): token t is bytes[offsets[t] ..
- *              offsets[t+1]).
+ *   offsets    [V+1] int32, offsets[0] = 0, non-decreasing, offsets[V] <=
+ *              the size of bytes (a precondition this call does not check:
+ *              dv_validate_vocab does): token t is bytes[offsets[t] ..
+ *              offsets[t+1]); a decreasing pair reads as an empty token.
  *   bytes      [offsets[V]] uint8, the concatenated token strings.  May be
  *              NULL only when every token is empty.
  * Outputs (device, written in full):
@@ -149,6 +150,28 @@ DV_API dv_status dv_align_eos(const int32_t *trans, int32_t num_states,
                        const uint8_t *accepting, int32_t eos_token,
                        int32_t *next_state, uint32_t *allow,
                        void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * dv_validate_vocab -- checks the CSR layout of a vocabulary on the device:
+ * the precondition of dv_align / dv_align_eos, whose kernels read
+ * bytes[offsets[t] .. offsets[t+1]) without bounds checks.
+ *
+ * Writes to *first_bad (device, one int32) -1 when offsets[0] = 0, offsets
+ * is non-decreasing and offsets[V] <= num_bytes; otherwise the smallest t
+ * in [0, V] at which that fails (t = 0: offsets[0] != 0; t >= 1:
+ * offsets[t] < offsets[t-1] or offsets[t] > num_bytes).  The result is
+ * valid once the stream has reached the call.
+ *
+ * offsets    [V+1] int32 (device), num_tokens = V in [1, DV_MAX_TOKENS];
+ * num_bytes  the number of bytes the caller's bytes array holds (>= 0).
+ * (dv_align itself reads a decreasing pair as an empty token, never as
+ * anything else; bytes past the array are the case only this check
+ * catches.)
+ * Errors: DV_ERR_INVALID_ARG (NULL), DV_ERR_SHAPE, DV_ERR_ALIAS (first_bad
+ *   inside offsets), DV_ERR_HIP.
+ */
+DV_API dv_status dv_validate_vocab(const int32_t *offsets, int32_t num_tokens, int64_t num_bytes,
+                                   int32_t *first_bad, void *stream);
 
 /*
  * dv_masked_step_workspace_bytes -- device workspace dv_masked_step needs for

@@ -43,18 +43,41 @@ BF16 = 1
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "dv_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "libdv_oracle.so")
+SANITIZED_LIB_PATH = os.path.join(_HERE, "libdv_oracle_san.so")
 _lib = None
 BUILD_FLAGS = ("-O2", "-std=c11")
+# AddressSanitizer + UndefinedBehaviorSanitizer build (host code only: gcc);
+# a process loading it needs the two runtimes preloaded (sanitizer_env).
+SANITIZE_FLAGS = ("-O1", "-g", "-std=c11", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                  "-fno-sanitize-recover=all")
 
 
-def build(force: bool = False, out: str | None = None, defines: tuple = ()) -> str:
+def build(force: bool = False, out: str | None = None, defines: tuple = (), sanitize: bool = False) -> str:
     """Compile ``dv_oracle.c`` with gcc into a shared library; returns its path."""
-    out = out or _LIB_PATH
+    out = out or (SANITIZED_LIB_PATH if sanitize else _LIB_PATH)
     if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(_SRC):
-        cmd = ["gcc", *BUILD_FLAGS, "-shared", "-fPIC", "-o", out, _SRC, "-lm"]
+        flags = SANITIZE_FLAGS if sanitize else BUILD_FLAGS
+        cmd = ["gcc", *flags, "-shared", "-fPIC", "-o", out, _SRC, "-lm"]
         cmd += [f"-D{d}" for d in defines]
         subprocess.run(cmd, check=True)
     return out
+
+
+def sanitizer_env() -> dict:
+    """Environment for a child process that loads the sanitized oracle
+    (``DV_ORACLE_LIBRARY``): the gcc sanitizer runtimes preloaded, leak
+    checks off (the interpreter's own allocations), any report fatal."""
+    runtimes = []
+    for name in ("libasan.so", "libubsan.so"):
+        path = subprocess.run(["gcc", f"-print-file-name={name}"], capture_output=True, text=True,
+                              check=True).stdout.strip()
+        runtimes.append(os.path.realpath(path))
+    env = dict(os.environ)
+    env["LD_PRELOAD"] = ":".join(runtimes)
+    env["ASAN_OPTIONS"] = "detect_leaks=0:abort_on_error=1:halt_on_error=1"
+    env["UBSAN_OPTIONS"] = "halt_on_error=1:print_stacktrace=1"
+    env["DV_ORACLE_LIBRARY"] = build(sanitize=True)
+    return env
 
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
@@ -119,7 +142,8 @@ def load(path: str | None = None):
     if path is not None:
         return _bind(ctypes.CDLL(path))
     if _lib is None:
-        _lib = _bind(ctypes.CDLL(build()))
+        chosen = os.environ.get("DV_ORACLE_LIBRARY")
+        _lib = _bind(ctypes.CDLL(chosen if chosen else build()))
     return _lib
 
 

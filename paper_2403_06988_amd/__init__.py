@@ -20,7 +20,7 @@ import os
 
 import torch
 
-__all__ = ["align", "masked_step", "masked_step_noalloc", "masked_sample", "spec_walk", "spec_verify", "align_workspace_bytes",
+__all__ = ["align", "validate_vocab", "masked_step", "masked_step_noalloc", "masked_sample", "spec_walk", "spec_verify", "align_workspace_bytes",
            "masked_step_workspace_bytes", "masked_sample_workspace_bytes", "spec_verify_workspace_bytes",
            "step_workspace", "sample_workspace", "spec_workspace", "DvError", "DEAD", "library_path", "lib"]
 
@@ -56,6 +56,8 @@ def _load():
     lib.dv_align_workspace_bytes.argtypes = [i32, i32]
     lib.dv_align.restype = ctypes.c_int
     lib.dv_align.argtypes = [vp, i32, vp, vp, i32, vp, vp, vp, sz, vp]
+    lib.dv_validate_vocab.restype = ctypes.c_int
+    lib.dv_validate_vocab.argtypes = [vp, i32, i64, vp, vp]
     lib.dv_align_eos.restype = ctypes.c_int
     lib.dv_align_eos.argtypes = [vp, i32, vp, vp, i32, vp, i32, vp, vp, vp, sz, vp]
     lib.dv_masked_step_workspace_bytes.restype = sz
@@ -122,19 +124,39 @@ def masked_step_workspace_bytes(batch: int, num_tokens: int) -> int:
     return int(lib.dv_masked_step_workspace_bytes(batch, num_tokens))
 
 
+def validate_vocab(offsets, tok_bytes, stream=None) -> int:
+    """dv_validate_vocab: -1 when offsets [V+1] is a valid CSR layout over
+    tok_bytes (starts at 0, non-decreasing, ends within tok_bytes), else the
+    first index at which it is not.  Synchronizes the stream."""
+    dev = offsets.device
+    _want(offsets, "offsets", torch.int32, dev)
+    _want(tok_bytes, "tok_bytes", torch.uint8, dev)
+    out = torch.empty(1, dtype=torch.int32, device=dev)
+    st = lib.dv_validate_vocab(_ptr(offsets), offsets.numel() - 1, tok_bytes.numel(), _ptr(out),
+                               _stream(stream, dev))
+    _check(st, "dv_validate_vocab")
+    return int(out.item())
+
+
 def align(trans, offsets, tok_bytes, next_state=None, allow=None, workspace=None, stream=None,
-          accepting=None, eos_token=None):
+          accepting=None, eos_token=None, validate=True):
     """Alignment table of a byte DFA and a vocabulary (device tensors).
 
     trans [S][256] int32, offsets [V+1] int32, tok_bytes [offsets[V]] uint8.
     With ``eos_token`` (and optionally ``accepting`` [S] uint8), that token is
-    allowed exactly in accepting states (dv_align_eos).
+    allowed exactly in accepting states (dv_align_eos).  ``validate``: check
+    the vocabulary's layout first (validate_vocab; one synchronization) and
+    raise ValueError if it is malformed.
     Returns (next_state [S][V] int32, allow [S][ceil(V/32)] int32 holding the
     uint32 bit pattern)."""
     dev = trans.device
     _want(trans, "trans", torch.int32, dev)
     _want(offsets, "offsets", torch.int32, dev)
     _want(tok_bytes, "tok_bytes", torch.uint8, dev)
+    if validate and offsets.numel() >= 2:
+        bad = validate_vocab(offsets, tok_bytes, stream)
+        if bad >= 0:
+            raise ValueError(f"malformed vocabulary: offsets break the CSR layout at index {bad}")
     if trans.dim() != 2 or trans.shape[1] != 256:
         raise ValueError("trans must be [S][256]")
     S, V = trans.shape[0], offsets.shape[0] - 1

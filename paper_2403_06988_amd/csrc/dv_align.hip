@@ -183,7 +183,7 @@ __device__ __forceinline__ void token_records(const int32_t *__restrict__ offset
         return;
     }
     const int off = offsets[t];
-    const int len = offsets[t + 1] - off;
+    const int len = max(0, offsets[t + 1] - off);  // a decreasing pair reads as an empty token
     uint32_t lo = 0, hi = 0;
     const int n = min(len, kRegBytes);
     for (int h = 0; h < n; ++h) {
@@ -585,6 +585,38 @@ __global__ __launch_bounds__(kPrefThreads) void walk_prefix_kernel(
 }
 
 }  // namespace
+
+// The vocabulary's CSR layout, checked by one block: the smallest t in
+// [0, V] at which it breaks (offsets[0] != 0 at t = 0; offsets[t] <
+// offsets[t - 1] or offsets[t] > num_bytes at t >= 1), or -1.
+__global__ __launch_bounds__(1024) void validate_vocab_kernel(const int32_t *__restrict__ offsets, int V,
+                                                              int64_t num_bytes, int32_t *__restrict__ first_bad)
+{
+    __shared__ int wave_min[1024 / kWave];
+    int bad = INT_MAX;
+    for (int t = (int)threadIdx.x; t <= V && bad == INT_MAX; t += 1024) {
+        const int o = offsets[t];
+        const bool broken = t == 0 ? o != 0 : (o < offsets[t - 1] || (int64_t)o > num_bytes);
+        if (broken)
+            bad = t;
+    }
+    bad = (int)wave_reduce<false>((uint32_t)bad);
+    if ((threadIdx.x & (kWave - 1)) == 0)
+        wave_min[threadIdx.x / kWave] = bad;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < 1024 / kWave; ++w)
+            bad = min(bad, wave_min[w]);
+        *first_bad = bad == INT_MAX ? -1 : bad;
+    }
+}
+
+hipError_t launch_validate_vocab(const int32_t *offsets, int V, int64_t num_bytes, int32_t *first_bad,
+                                 hipStream_t stream)
+{
+    validate_vocab_kernel<<<1, 1024, 0, stream>>>(offsets, V, num_bytes, first_bad);
+    return hipGetLastError();
+}
 
 hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, const uint8_t *bytes,
                         int V, const uint8_t *accepting, int eos_token, int32_t *next_state,

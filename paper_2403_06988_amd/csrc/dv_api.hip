@@ -124,6 +124,24 @@ dv_status dv_align_eos(const int32_t *trans, int32_t num_states, const int32_t *
                         next_state, allow, workspace, workspace_bytes, stream);
 }
 
+dv_status dv_validate_vocab(const int32_t *offsets, int32_t num_tokens, int64_t num_bytes, int32_t *first_bad,
+                            void *stream)
+{
+    g_error[0] = '\0';
+    const char *name = "dv_validate_vocab";
+    if (!offsets || !first_bad)
+        return fail(DV_ERR_INVALID_ARG, "%s: offsets and first_bad must be non-NULL", name);
+    if (num_tokens < 1 || num_tokens > DV_MAX_TOKENS)
+        return fail(DV_ERR_SHAPE, "%s: num_tokens=%d outside [1, %d]", name, num_tokens, DV_MAX_TOKENS);
+    if (num_bytes < 0)
+        return fail(DV_ERR_SHAPE, "%s: num_bytes=%lld must be >= 0", name, (long long)num_bytes);
+    if (overlap(range_of(first_bad, 4), range_of(offsets, ((size_t)num_tokens + 1) * 4)))
+        return fail(DV_ERR_ALIAS, "%s: first_bad overlaps offsets", name);
+    return hip_status(dv::launch_validate_vocab(offsets, num_tokens, num_bytes, first_bad,
+                                                static_cast<hipStream_t>(stream)),
+                      "dv_validate_vocab launch");
+}
+
 size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens)
 {
     if (batch < 0 || batch > DV_MAX_BATCH || num_tokens < 1 || num_tokens > DV_MAX_TOKENS)

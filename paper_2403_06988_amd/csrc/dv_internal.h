@@ -125,6 +125,11 @@ inline size_t align_tokinfo_offset(int S) { return align_up(align_table_offset(S
 // per token: byte classes of its first 8 bytes (4 per word), its length, its offset
 inline size_t align_workspace_bytes(int S, int V) { return align_tokinfo_offset(S) + (size_t)V * 16; }
 
+// first_bad <- the smallest t at which the CSR layout of the vocabulary
+// breaks, or -1 (dv_validate_vocab).
+hipError_t launch_validate_vocab(const int32_t *offsets, int V, int64_t num_bytes, int32_t *first_bad,
+                                 hipStream_t stream);
+
 // eos_token = -1: no end-of-sequence token; accepting may then be NULL.
 hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, const uint8_t *bytes,
                         int V, const uint8_t *accepting, int eos_token, int32_t *next_state,

@@ -170,6 +170,21 @@ def test_masked_step_noalloc_empty_batch_is_a_noop():
     assert lib.dv_last_error() == b""
 
 
+@pytest.mark.parametrize("kw,status", [
+    (dict(offsets=None), INVALID),
+    (dict(out=None), INVALID),
+    (dict(V=0), SHAPE),
+    (dict(V=1 << 25), SHAPE),
+    (dict(nbytes=-1), SHAPE),
+    (dict(out=P + 40), ALIAS),                    # the result inside offsets
+])
+def test_validate_vocab_rejects_before_launch(kw, status):
+    a = dict(offsets=P, V=1000, nbytes=5000, out=P + GB)
+    a.update(kw)
+    assert lib.dv_validate_vocab(a["offsets"], a["V"], a["nbytes"], a["out"], None) == status
+    assert lib.dv_last_error().startswith(b"dv_validate_vocab")
+
+
 def test_last_error_is_per_thread():
     """The detail string belongs to the calling thread: threads failing in
     different entry points, and one whose calls succeed, each read their

@@ -198,6 +198,39 @@ def test_align_every_byte_value(dv, dead_byte):
     np.testing.assert_array_equal(u32(al), al_o)
 
 
+def test_validate_vocab_and_decreasing_offsets(dv):
+    """dv_validate_vocab finds the first index at which the CSR layout breaks;
+    align refuses such a vocabulary; a decreasing pair whose bytes all lie in
+    the buffer, aligned without the check, is an empty token on both sides
+    (the oracle walks the empty range)."""
+    trans, _ = W.dfa(2)
+    offsets, data = W.vocab(2)
+    V = offsets.shape[0] - 1
+    assert dv.validate_vocab(_dev(offsets), _dev(data)) == -1
+    bad = offsets.copy()
+    bad[0] = 1
+    assert dv.validate_vocab(_dev(bad), _dev(data)) == 0
+    bad = offsets.copy()
+    bad[700] = bad[699] - 1
+    assert dv.validate_vocab(_dev(bad), _dev(data)) == 700
+    assert dv.validate_vocab(_dev(offsets), _dev(data[:-1])) == V       # ends past the bytes
+    bad = offsets.copy()
+    bad[V - 5:] = offsets[V] + 7
+    assert dv.validate_vocab(_dev(bad), _dev(data)) == V - 5               # the first entry past the bytes
+    with pytest.raises(ValueError):
+        dv.align(_dev(trans), _dev(bad), _dev(data))
+    # a decreasing pair inside the buffer: token 1000 spans [o[1000], o[999]) backwards
+    dec = offsets.copy()
+    dec[1000] = offsets[998]
+    assert dv.validate_vocab(_dev(dec), _dev(data)) == 1000
+    ns, al = dv.align(_dev(trans), _dev(dec), _dev(data), validate=False)
+    torch.cuda.synchronize()
+    ns_o, al_o = oracle.align(trans, dec, data)
+    np.testing.assert_array_equal(ns.cpu().numpy(), ns_o)
+    np.testing.assert_array_equal(u32(al), al_o)
+    assert (ns_o[:, 999] == np.arange(trans.shape[0])).all()          # empty: the state is kept
+
+
 def test_align_is_deterministic(dv):
     trans, _ = W.dfa(2)
     offsets, data = W.vocab(2)
