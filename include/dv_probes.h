@@ -57,6 +57,16 @@ DVPROBE_API int32_t dvprobe_lds_gather(const uint32_t *table, int32_t table_entr
                                        int32_t lanes, int32_t chains, int32_t steps,
                                        uint32_t *sink, void *stream);
 
+/* The alignment walk's later moves in isolation: lanes * chains chases of
+ * `steps` dependent 2-byte reads st = table[st * num_classes + c] through a
+ * uint16 state table [num_states][num_classes] (values >= num_states are
+ * folded back in range), c a per-step pseudo-random byte class; 1024-lane
+ * blocks.  lanes: a multiple of 1024; chains: 1 or 3 (the prefix walk's
+ * states per lane); num_states * num_classes <= 2^24.  sink: lanes uint32. */
+DVPROBE_API int32_t dvprobe_walk_gather(const uint16_t *table, int32_t num_states, int32_t num_classes,
+                                        int32_t lanes, int32_t chains, int32_t steps, uint32_t *sink,
+                                        void *stream);
+
 /* Floors of the bf16 masked step (dv_masked_step) at its own launch shape
  * for `batch` rows of `num_tokens` logits (the same blocks and block size):
  *   mode 0  each block reads its row's state and writes the outputs

@@ -27,6 +27,8 @@
 //      at 32-bit offsets (a dead state skips its read).  Stores are coalesced
 //      along tokens; the allow words come from a wave ballot (64 tokens -> 2
 //      words).
+#include <algorithm>
+
 #include "dv_internal.h"
 
 namespace dv {
@@ -586,35 +588,31 @@ __global__ __launch_bounds__(kPrefThreads) void walk_prefix_kernel(
 
 }  // namespace
 
-// The vocabulary's CSR layout, checked by one block: the smallest t in
-// [0, V] at which it breaks (offsets[0] != 0 at t = 0; offsets[t] <
-// offsets[t - 1] or offsets[t] > num_bytes at t >= 1), or -1.
-__global__ __launch_bounds__(1024) void validate_vocab_kernel(const int32_t *__restrict__ offsets, int V,
-                                                              int64_t num_bytes, int32_t *__restrict__ first_bad)
+// The vocabulary's CSR layout: the smallest t in [0, V] at which it breaks
+// (offsets[0] != 0 at t = 0; offsets[t] < offsets[t - 1] or offsets[t] >
+// num_bytes at t >= 1), or -1.  The answer is an unsigned minimum over the
+// broken indices, started at all ones (= -1 as int32) by a one-lane kernel.
+__global__ void validate_vocab_init_kernel(uint32_t *first_bad) { *first_bad = 0xFFFFFFFFu; }
+
+__global__ __launch_bounds__(256) void validate_vocab_kernel(const int32_t *__restrict__ offsets, int V,
+                                                             int64_t num_bytes, uint32_t *__restrict__ first_bad)
 {
-    __shared__ int wave_min[1024 / kWave];
-    int bad = INT_MAX;
-    for (int t = (int)threadIdx.x; t <= V && bad == INT_MAX; t += 1024) {
+    const int stride = gridDim.x * blockDim.x;
+    for (int t = blockIdx.x * blockDim.x + (int)threadIdx.x; t <= V; t += stride) {
         const int o = offsets[t];
         const bool broken = t == 0 ? o != 0 : (o < offsets[t - 1] || (int64_t)o > num_bytes);
         if (broken)
-            bad = t;
-    }
-    bad = (int)wave_reduce<false>((uint32_t)bad);
-    if ((threadIdx.x & (kWave - 1)) == 0)
-        wave_min[threadIdx.x / kWave] = bad;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        for (int w = 1; w < 1024 / kWave; ++w)
-            bad = min(bad, wave_min[w]);
-        *first_bad = bad == INT_MAX ? -1 : bad;
+            atomicMin(first_bad, (uint32_t)t);
     }
 }
 
 hipError_t launch_validate_vocab(const int32_t *offsets, int V, int64_t num_bytes, int32_t *first_bad,
                                  hipStream_t stream)
 {
-    validate_vocab_kernel<<<1, 1024, 0, stream>>>(offsets, V, num_bytes, first_bad);
+    uint32_t *out = reinterpret_cast<uint32_t *>(first_bad);
+    validate_vocab_init_kernel<<<1, 1, 0, stream>>>(out);
+    const int blocks = (int)std::min<int64_t>(((int64_t)V + 256) / 256, 4096);
+    validate_vocab_kernel<<<blocks, 256, 0, stream>>>(offsets, V, num_bytes, out);
     return hipGetLastError();
 }
 

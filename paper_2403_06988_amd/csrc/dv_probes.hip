@@ -227,6 +227,37 @@ __global__ __launch_bounds__(kFloorThreads) void step_floor_kernel(const void *_
     }
 }
 
+// The alignment walk's own gather: a chase through a uint16 table [S][Cp]
+// of states, st = table[st * Cp + c] with the byte class c drawn per step
+// from the lane and step (2-byte reads at 32-bit byte offsets, as the walk
+// makes them), CHAINS independent chases per lane, 1024-lane blocks.
+template <int CHAINS>
+__global__ __launch_bounds__(1024) void walk_gather_kernel(const uint16_t *__restrict__ table, int S, int Cp,
+                                                           int steps, uint32_t *__restrict__ sink)
+{
+    const uint32_t lane = blockIdx.x * 1024 + threadIdx.x;
+    const char *tb = reinterpret_cast<const char *>(table);
+    uint32_t st[CHAINS];
+#pragma unroll
+    for (int k = 0; k < CHAINS; ++k)
+        st[k] = mix(lane * CHAINS + k) % (uint32_t)S;
+    uint32_t h = mix(lane);
+    for (int i = 0; i < steps; ++i) {
+        h = h * 1664525u + 1013904223u;
+#pragma unroll
+        for (int k = 0; k < CHAINS; ++k) {
+            const uint32_t c = ((h >> (4 * k)) & 0xFFFu) % (uint32_t)Cp;
+            const uint32_t v = *reinterpret_cast<const uint16_t *>(tb + (st[k] * (uint32_t)Cp + c) * 2u);
+            st[k] = v < (uint32_t)S ? v : v % (uint32_t)S;  // stays in bounds
+        }
+    }
+    uint32_t acc = 0;
+#pragma unroll
+    for (int k = 0; k < CHAINS; ++k)
+        acc += st[k];
+    sink[lane] = acc;
+}
+
 template <bool LDS>
 hipError_t launch_gather(const uint32_t *table, int entries, int lanes, int chains, int steps,
                          uint32_t *sink, hipStream_t stream)
@@ -296,6 +327,20 @@ int32_t dvprobe_step_floor(int32_t mode, const void *logits, int32_t num_tokens,
     else
         DV_FLOOR(2);
 #undef DV_FLOOR
+    return hipGetLastError() == hipSuccess ? 0 : 6;
+}
+
+int32_t dvprobe_walk_gather(const uint16_t *table, int32_t num_states, int32_t num_classes, int32_t lanes,
+                            int32_t chains, int32_t steps, uint32_t *sink, void *stream)
+{
+    if (!table || !sink || num_states < 1 || num_classes < 1 || (int64_t)num_states * num_classes > (1 << 24) ||
+        lanes < 1024 || lanes % 1024 || (chains != 1 && chains != 3) || steps < 1)
+        return 1;
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    if (chains == 1)
+        dv::walk_gather_kernel<1><<<lanes / 1024, 1024, 0, st>>>(table, num_states, num_classes, steps, sink);
+    else
+        dv::walk_gather_kernel<3><<<lanes / 1024, 1024, 0, st>>>(table, num_states, num_classes, steps, sink);
     return hipGetLastError() == hipSuccess ? 0 : 6;
 }
 

@@ -39,7 +39,7 @@ def test_every_declared_symbol_is_exported():
         assert hasattr(raw, n), n
     probes = declared_functions("dv_probes.h")
     assert {"dvprobe_stream_read", "dvprobe_stream_write", "dvprobe_gather", "dvprobe_lds_gather",
-            "dvprobe_step_floor"} <= set(probes)
+            "dvprobe_step_floor", "dvprobe_walk_gather"} <= set(probes)
     plib = ctypes.CDLL(PROBE_LIB)
     for n in probes:
         assert hasattr(plib, n), n
