@@ -263,8 +263,9 @@ DV_API dv_status dv_masked_step_noalloc(const int32_t *next_state, const uint32_
  * maximum at the lowest index is also the masked one), so the two are
  * interchangeable; this one reads less memory when the model mostly picks
  * allowed tokens and reads a row twice when it does not.  The check runs
- * first for bf16 rows that one block covers (batch >= 256, or rows of at
- * most 32768 tokens); other shapes take dv_masked_step's kernels.
+ * first for bf16 rows that one block covers (batch >= 256, or batch >= 64
+ * with rows of at most 32768 tokens); other shapes (fp32 rows, rows split
+ * over several blocks) take dv_masked_step's kernels.
  * Arguments, workspace (dv_masked_step_workspace_bytes) and errors as
  *   dv_masked_step.
  */

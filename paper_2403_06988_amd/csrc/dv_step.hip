@@ -4,13 +4,19 @@
 // The step reads B x V logits once: it is bound by HBM read bandwidth, so
 // the design is about keeping enough bytes in flight and spending few ALU
 // operations per element.
-//   * Launch shape (bf16).  A row is one 512-lane block once B >= 256
-//     (every CU gets at least one row), or when it holds at most 32768
-//     logits (a second pass would cost more than the split saves).  Smaller
-//     batches split each row into chunks, one block each, and a tiny second
-//     kernel (one lane per row) combines the chunks -- no atomics and no
-//     device-wide fences in the streaming kernel (a release fence at device
-//     scope writes back and invalidates the XCD's L2 on gfx950).
+//   * Launch shape (bf16, step_geometry).  A row is one 512-lane block once
+//     B >= 256 (every CU gets at least one row), or when B >= 64 and the row
+//     holds at most 32768 logits (a second block per row buys nothing
+//     there).  Otherwise each row is split into about 32 / sqrt(B) chunks,
+//     one block each, and the chunks meet in the workspace: each block folds
+//     its best into the row's 64-bit entry with a device-scope atomic
+//     maximum, then counts itself with a device-scope atomic add whose
+//     operand depends on the maximum's result; the block that counts last
+//     takes the row's result and puts both entries back to zero.  For bf16
+//     the entry also carries the winner's next state, so that block reads
+//     nothing more.  No second kernel and no device-wide fences (a release
+//     fence at device scope writes back and invalidates the XCD's L2 on
+//     gfx950).
 //   * Each lane streams batches of 2 independent non-temporal 16-byte loads
 //     with a register double buffer: batch i + 1 is in flight while batch i
 //     is reduced.  Loads are branch-free and in a fixed order, because the
