@@ -7,7 +7,7 @@ any code with each other.
 
 The paper's workloads (the JSON / C / XML / template grammars of its
 Appendix C, the Mistral-7B and Llama-2-13B tokenizers) are not available here;
-these generators stand in for them with the shapes below.  Five workloads:
+these generators stand in for them with the shapes below.  Ten workloads:
 
 ====  ==========================  =======  ========  ======  =====  =====  ===========
  id    name                        S        V         B       steps  dtype  logits
