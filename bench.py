@@ -15,7 +15,10 @@ Reported (one JSON line):
                algorithmic bytes per launch / mean launch time (HIP events
                around the replay of the job's decode steps, captured once as
                a HIP graph, on the launch stream; divided by the step count)
+               (with the probes: frac_of_measured_read, the same rate against
+               this box's streaming-read probe)
   roofline_align  dv_align against the HBM write roofline (4.125 B / pair)
+               (frac_of_measured_write: against the streaming-write probe)
   opportunistic  the decode chain with the model's own choice checked first
                (Sec. 3.5), on the workload's logits and on adherent logits
   sample       the decode chain sampled at temperature 1 (Sec. 4), ALU roofline
@@ -28,7 +31,7 @@ Reported (one JSON line):
                us per step, touched-line roofline, traffic, floors
   cpu_baseline the CPU oracle on a bounded sample of the same workload
 
-Usage: python bench.py [--steps K] [--warmup W] [--workload 1..8] [--no-cpu]
+Usage: python bench.py [--steps K] [--warmup W] [--workload 1..10] [--no-cpu]
 """
 import argparse
 import hashlib
@@ -890,6 +893,9 @@ def main():
     if not args.no_probes:
         log("roofline probes")
         out["probes"] = run_probes(probes, dev, w.S * 96 * 2)
+        # the same achieved rates against what this box's streaming probes reach
+        out["roofline"]["frac_of_measured_read"] = achieved / out["probes"]["hbm_read_GBs"]
+        out["roofline_align"]["frac_of_measured_write"] = align_achieved / out["probes"]["hbm_write_GBs"]
     if not args.no_cpu:
         log("cpu baseline (oracle, 1 thread)")
         out["cpu_baseline"] = cpu_baseline(w, wid, trans, offsets, data, init, x, args.cpu_seconds)
