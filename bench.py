@@ -30,6 +30,8 @@ Reported (one JSON line):
   extra        decode legs of the other bandwidth-sized workloads (3 and 5):
                us per step, touched-line roofline, traffic, floors
   cpu_baseline the CPU oracle on a bounded sample of the same workload
+  inputs       SHA-256 of the DFA, the vocabulary and the initial states, and
+               the realised token lengths
 
 Usage: python bench.py [--steps K] [--warmup W] [--workload 1..10] [--no-cpu]
 """
@@ -66,6 +68,24 @@ def kernel_source_hash(which):
     for f in KERNEL_SOURCES[which]:
         h.update(open(os.path.join(CSRC, f), "rb").read())
     return h.hexdigest()[:16]
+
+
+def inputs_record(trans, offsets, data, init):
+    """SHA-256 of the workload's inputs (the DFA, the vocabulary, the
+    initial states) and the realised token lengths, so that a result names
+    exactly what it was measured on."""
+    import numpy as np
+
+    def sha(*arrays):
+        h = hashlib.sha256()
+        for a in arrays:
+            h.update(np.ascontiguousarray(a).tobytes())
+        return h.hexdigest()
+
+    lens = np.diff(np.asarray(offsets, dtype=np.int64))
+    return {"dfa_sha256": sha(trans), "vocab_sha256": sha(offsets, data), "init_states_sha256": sha(init),
+            "token_len_mean": float(lens.mean()) if lens.size else 0.0, "token_len_max": int(lens.max(initial=0)),
+            "token_bytes": int(lens.sum())}
 
 
 def parse():
@@ -875,6 +895,7 @@ def main():
                            "frac": align_achieved / HBM_PEAK_GBS, "bytes_per_launch": align_bytes,
                            "traffic": traffic_record("align", wid)},
         "kernel_source_hash": {k: kernel_source_hash(k) for k in KERNEL_SOURCES},
+        "inputs": inputs_record(trans, offsets, data, init),
     }
     probes = probe_lib() if not (args.no_probes and args.no_floors) else None
     if not args.no_floors and w.dtype == "bf16":

@@ -45,3 +45,23 @@ def test_touched_line_bytes_whole_rows_when_all_allowed():
     states = torch.zeros(B, dtype=torch.int32)
     assert bench.touched_line_bytes(al, states, 0, V, V, 2) == B * V * 2  # rows are whole lines
     assert bench.touched_line_bytes(al, torch.full((B,), -1, dtype=torch.int32), 0, V, V, 2) == 0
+
+
+def test_inputs_record_names_the_inputs():
+    """The bench line's input record: hashes that change with any input
+    byte, and the realised token lengths."""
+    trans = np.full((3, 256), -1, np.int32)
+    trans[0, 97] = 1
+    offsets = np.array([0, 1, 3, 3, 7], np.int32)
+    data = np.frombuffer(b"abcdefg", np.uint8)
+    init = np.zeros(2, np.int32)
+    r = bench.inputs_record(trans, offsets, data, init)
+    assert r["token_len_mean"] == 7 / 4 and r["token_len_max"] == 4 and r["token_bytes"] == 7
+    assert r == bench.inputs_record(trans.copy(), offsets.copy(), data.copy(), init.copy())
+    t2 = trans.copy()
+    t2[2, 5] = 0
+    d2 = data.copy()
+    d2[6] = ord("h")
+    assert bench.inputs_record(t2, offsets, data, init)["dfa_sha256"] != r["dfa_sha256"]
+    assert bench.inputs_record(trans, offsets, d2, init)["vocab_sha256"] != r["vocab_sha256"]
+    assert bench.inputs_record(trans, offsets, data, init + 1)["init_states_sha256"] != r["init_states_sha256"]
