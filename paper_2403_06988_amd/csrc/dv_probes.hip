@@ -94,8 +94,8 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const uint32_t *__rest
 // non-temporal), with no mask and no arithmetic.  MODE 2: only the vectors
 // whose mask byte is nonzero (the 128-byte lines holding an allowed token of
 // the row's state): the row's state is read, its mask bytes are loaded two
-// batches ahead of their logits and choose the addresses (a vector with no
-// allowed token reads one fixed, cached location instead), as a loads-only
+// batches ahead of their logits and choose the offsets (a vector with no
+// allowed token gets one past the buffer's records and is not read), as a loads-only
 // kernel over exactly the lines the step must read.  Rows must be 16-byte
 // aligned.
 constexpr int kFloorThreads = 512;
@@ -104,29 +104,33 @@ static_assert(kFloorThreads == kStepBigThreads, "the step's block size");
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-__device__ uint4 g_floor_unread;
-
-__device__ __forceinline__ uint4 nt_load(const char *p)
+// The step's loads: raw buffers over the chunk's vectors, so a lane past the
+// chunk, and (MODE 2) a vector with no allowed token, which gets an offset
+// past the records, read zeros without a memory access.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t floor_buffer(const char *p, uint32_t bytes)
 {
-    const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ uint4 nt_load(__amdgpu_buffer_rsrc_t r, uint32_t off)
+{
+    const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 2);  // non-temporal
     return make_uint4(x[0], x[1], x[2], x[3]);
 }
 
-__device__ __forceinline__ void floor_batch(uint4 (&d)[kFloorU], const char *crow, int vb, int n)
+__device__ __forceinline__ void floor_batch(uint4 (&d)[kFloorU], __amdgpu_buffer_rsrc_t r, int vb)
 {
 #pragma unroll
     for (int u = 0; u < kFloorU; ++u)
-        d[u] = nt_load(crow + (size_t)min(vb + u * kFloorThreads + (int)threadIdx.x, n - 1) * 16);
+        d[u] = nt_load(r, (uint32_t)(vb + u * kFloorThreads + (int)threadIdx.x) * 16u);
 }
 
-__device__ __forceinline__ void floor_batch_sel(uint4 (&d)[kFloorU], const char *crow, int vb, int n,
+__device__ __forceinline__ void floor_batch_sel(uint4 (&d)[kFloorU], __amdgpu_buffer_rsrc_t r, int vb,
                                                 const uint32_t (&m)[kFloorU])
 {
 #pragma unroll
-    for (int u = 0; u < kFloorU; ++u) {
-        const char *p = crow + (size_t)min(vb + u * kFloorThreads + (int)threadIdx.x, n - 1) * 16;
-        d[u] = nt_load(m[u] ? p : reinterpret_cast<const char *>(&g_floor_unread));
-    }
+    for (int u = 0; u < kFloorU; ++u)
+        d[u] = nt_load(r, m[u] ? (uint32_t)(vb + u * kFloorThreads + (int)threadIdx.x) * 16u : 0xFFFFFFF0u);
 }
 
 __device__ __forceinline__ void floor_masks(uint32_t (&m)[kFloorU], const uint8_t *mb, int vb, int n)
@@ -160,14 +164,15 @@ __global__ __launch_bounds__(kFloorThreads) void step_floor_kernel(const void *_
     const int nvec = V / 8;
     const int v0 = c * chunk_vec, n = min(nvec, v0 + chunk_vec) - v0;
     const char *crow = static_cast<const char *>(logits) + (size_t)b * ld * 2 + (size_t)v0 * 16;
+    const __amdgpu_buffer_rsrc_t rb = floor_buffer(crow, (uint32_t)(n > 0 ? n : 0) * 16u);
     uint32_t acc = 0;
     if (MODE == 1 && n > 0) {
         uint4 da[kFloorU], db[kFloorU];
-        floor_batch(da, crow, 0, n);
+        floor_batch(da, rb, 0);
         for (int vb = 0; vb < n; vb += 2 * K) {
-            floor_batch(db, crow, vb + K, n);
+            floor_batch(db, rb, vb + K);
             acc ^= fold(da);
-            floor_batch(da, crow, vb + 2 * K, n);
+            floor_batch(da, rb, vb + 2 * K);
             acc ^= fold(db);
         }
     } else if (MODE == 2 && n > 0 && (uint32_t)s < (uint32_t)S) {
@@ -176,42 +181,42 @@ __global__ __launch_bounds__(kFloorThreads) void step_floor_kernel(const void *_
         uint32_t m0[kFloorU], m1[kFloorU], m2[kFloorU], m3[kFloorU];
         // the first two batches are read whole (issued before the state is
         // known); the issue order is pinned: the load counter is in order
-        floor_batch(da, crow, 0, n);
+        floor_batch(da, rb, 0);
         __builtin_amdgcn_sched_barrier(0);
         floor_masks(m2, mb, 2 * K, n);
         __builtin_amdgcn_sched_barrier(0);
         floor_masks(m3, mb, 3 * K, n);
         __builtin_amdgcn_sched_barrier(0);
-        floor_batch(db, crow, K, n);
+        floor_batch(db, rb, K);
         __builtin_amdgcn_sched_barrier(0);
         acc ^= fold(da);
-        floor_batch_sel(da, crow, 2 * K, n, m2);
+        floor_batch_sel(da, rb, 2 * K, m2);
         __builtin_amdgcn_sched_barrier(0);
         floor_masks(m0, mb, 4 * K, n);
         __builtin_amdgcn_sched_barrier(0);
         acc ^= fold(db);
-        floor_batch_sel(db, crow, 3 * K, n, m3);
+        floor_batch_sel(db, rb, 3 * K, m3);
         __builtin_amdgcn_sched_barrier(0);
         floor_masks(m1, mb, 5 * K, n);
         __builtin_amdgcn_sched_barrier(0);
         for (int vb = 2 * K; vb < n; vb += 4 * K) {
             acc ^= fold(da);
-            floor_batch_sel(da, crow, vb + 2 * K, n, m0);
+            floor_batch_sel(da, rb, vb + 2 * K, m0);
             __builtin_amdgcn_sched_barrier(0);
             floor_masks(m2, mb, vb + 4 * K, n);
             __builtin_amdgcn_sched_barrier(0);
             acc ^= fold(db);
-            floor_batch_sel(db, crow, vb + 3 * K, n, m1);
+            floor_batch_sel(db, rb, vb + 3 * K, m1);
             __builtin_amdgcn_sched_barrier(0);
             floor_masks(m3, mb, vb + 5 * K, n);
             __builtin_amdgcn_sched_barrier(0);
             acc ^= fold(da);
-            floor_batch_sel(da, crow, vb + 4 * K, n, m2);
+            floor_batch_sel(da, rb, vb + 4 * K, m2);
             __builtin_amdgcn_sched_barrier(0);
             floor_masks(m0, mb, vb + 6 * K, n);
             __builtin_amdgcn_sched_barrier(0);
             acc ^= fold(db);
-            floor_batch_sel(db, crow, vb + 5 * K, n, m3);
+            floor_batch_sel(db, rb, vb + 5 * K, m3);
             __builtin_amdgcn_sched_barrier(0);
             floor_masks(m1, mb, vb + 7 * K, n);
             __builtin_amdgcn_sched_barrier(0);

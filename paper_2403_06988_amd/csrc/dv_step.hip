@@ -22,12 +22,16 @@
 //     is reduced.  Loads are branch-free and in a fixed order, because the
 //     load counter is in order: waiting for one load waits for every earlier
 //     one.  The first batch is issued before the row's state is known.
+//     Rows that start on a 16-byte boundary are read as raw buffers whose
+//     records end at the chunk's end: one add per load for the address, and
+//     a lane past the chunk reads zeros (no clamp, no memory access).
 //   * Mask bytes (one per 8 logits).  With one block per compute unit they
 //     are loaded beside their batch's logits.  With two or more, the block
 //     first copies its chunk's mask bytes into LDS; each later batch's
-//     addresses are then chosen from them, and a vector with no allowed
-//     token is read from one cached location instead, so a 128-byte line
-//     with no allowed token is never fetched.
+//     offsets are then chosen from them, and a vector with no allowed token
+//     gets an offset past the buffer's records, which reads zeros without a
+//     memory access, so a 128-byte line with no allowed token is never
+//     fetched.
 //   * bf16 arithmetic, two VALU operations per logit: per 32-bit word (two
 //     logits) one v_pk_ashrrev_i16 and one bit operation give
 //     order-preserving 16-bit keys, an AND with two 16-bit lane masks (from
@@ -357,26 +361,47 @@ __device__ __forceinline__ void load_batch_bf16(uint4 (&d)[U], const char *row, 
     }
 }
 
-// Read in place of a vector with no allowed token: every block reads the
-// same 16 bytes, so they stay in cache.
-__device__ uint4 g_unread_vector;
-
-// load_batch_bf16, except that a vector whose mask byte `sel[u]` is 0 (no
-// allowed token) is read from g_unread_vector: its logits are never used,
-// and a 128-byte line none of whose vectors is needed is not fetched.  The
-// address is selected, not branched on, so the loads stay branch-free.
-template <int THREADS, int U>
-__device__ __forceinline__ void load_batch_bf16_sel(uint4 (&d)[U], const char *row, int vb, int v1,
-                                                    const uint32_t (&sel)[U])
+// Buffer loads for aligned rows: the row's vectors [0, v1) and their mask
+// bytes as raw buffers whose records end at the chunk's end, so a lane past
+// it reads zeros (an allowed-nothing mask byte) with no clamp and no memory
+// access; the per-lane offset is one add per load.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_buffer(const void *p, uint32_t bytes)
 {
-    const int tid = threadIdx.x;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+template <int THREADS, int U>
+__device__ __forceinline__ void load_batch_buf(uint4 (&d)[U], __amdgpu_buffer_rsrc_t r, int vb)
+{
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        const int v = min(vb + u * THREADS + tid, v1 - 1);
-        const char *p = sel[u] ? row + (size_t)v * 16 : reinterpret_cast<const char *>(&g_unread_vector);
-        const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+        const uint32_t off = (uint32_t)(vb + u * THREADS + (int)threadIdx.x) * 16u;
+        const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 2);  // non-temporal
         d[u] = make_uint4(x[0], x[1], x[2], x[3]);
     }
+}
+
+// As load_batch_buf for the staged scan: a vector whose mask byte `sel[u]`
+// is 0 gets an offset past the records, which reads zeros without touching
+// memory, so a 128-byte line none of whose vectors is needed is not fetched.
+template <int THREADS, int U>
+__device__ __forceinline__ void load_batch_buf_sel(uint4 (&d)[U], __amdgpu_buffer_rsrc_t r, int vb,
+                                                   const uint32_t (&sel)[U])
+{
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const uint32_t off = sel[u] ? (uint32_t)(vb + u * THREADS + (int)threadIdx.x) * 16u : 0xFFFFFFF0u;
+        const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 2);
+        d[u] = make_uint4(x[0], x[1], x[2], x[3]);
+    }
+}
+
+template <int THREADS, int U>
+__device__ __forceinline__ void load_masks_buf(uint32_t (&m)[U], __amdgpu_buffer_rsrc_t r, int vb)
+{
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+        m[u] = __builtin_amdgcn_raw_buffer_load_b8(r, vb + u * THREADS + (int)threadIdx.x, 0, 0);
 }
 
 // A row is read as a head of `head` < 8 elements (its first 16-byte
@@ -409,7 +434,7 @@ __device__ __forceinline__ RowSplit split_row(const char *row, int V)
 // (moff = 0) or the chunk's bytes staged in LDS.  `db` holds the second
 // batch when STAGED (issued by the caller before the staging finished).
 // SELECT (STAGED only): vectors with no allowed token are not read (see
-// load_batch_bf16_sel).
+// load_batch_buf_sel).
 template <int THREADS, int U, bool MASKED, bool SHIFTED, bool STAGED, bool SELECT>
 __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *arow, const uint8_t *mbytes,
                                               int moff, const int32_t *ns_row, RowSplit rs, int v0, int v1,
@@ -448,11 +473,14 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
         // (logits, then their mask bytes), so while batch i is reduced,
         // batch i + 1 is in flight; the in-order load counter lets batch i
         // be consumed without waiting for batch i + 1.
+        // (the buffer loads of the aligned streaming scan already read a
+        // zero mask byte past the chunk)
+        constexpr bool kZeroPast = MASKED && !SHIFTED && !STAGED;
         auto process_batch = [&](const uint4 (&d)[U], const uint32_t (&raw)[U], int vb) {
             uint32_t mk[U];
 #pragma unroll
             for (int u = 0; u < U; ++u)
-                mk[u] = vb + u * THREADS + tid < v1 ? raw[u] : 0u;
+                mk[u] = kZeroPast || vb + u * THREADS + tid < v1 ? raw[u] : 0u;
             uint32_t acc = 0, any = 0;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -535,9 +563,10 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
             // Both first batches are in flight (issued by the caller) and the
             // mask bytes are in LDS: reading them costs no memory trip, so
             // with SELECT every later batch's addresses are chosen from them.
+            const __amdgpu_buffer_rsrc_t rl = raw_buffer(vrow, (uint32_t)v1 * 16u);
             auto issue = [&](uint4 (&d)[U], int vb, const uint32_t (&sel)[U]) {
                 if constexpr (SELECT && MASKED && !SHIFTED)
-                    load_batch_bf16_sel<THREADS, U>(d, vrow, vb, v1, sel);
+                    load_batch_buf_sel<THREADS, U>(d, rl, vb, sel);
                 else
                     load_batch_bf16<THREADS, U>(d, vrow, vb, v1);
             };
@@ -565,6 +594,20 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
                 // load under a branch would make the compiler wait for every
                 // load in flight where the branches join)
                 best_ns = ns_row[best_idx];
+            }
+        } else if constexpr (MASKED && !SHIFTED) {
+            const __amdgpu_buffer_rsrc_t rl = raw_buffer(vrow, (uint32_t)v1 * 16u);
+            const __amdgpu_buffer_rsrc_t rm = raw_buffer(mbytes - moff, (uint32_t)v1);
+            load_masks_buf<THREADS, U>(ma, rm, v0);
+            for (int vb = v0; vb < v1; vb += 2 * kStep) {
+                load_batch_buf<THREADS, U>(db, rl, vb + kStep);
+                load_masks_buf<THREADS, U>(mb, rm, vb + kStep);
+                process_batch(da, ma, vb);
+                load_batch_buf<THREADS, U>(da, rl, vb + 2 * kStep);
+                load_masks_buf<THREADS, U>(ma, rm, vb + 2 * kStep);
+                if (vb + kStep < v1)  // block-uniform
+                    process_batch(db, mb, vb + kStep);
+                best_ns = ns_row[best_idx];  // as above
             }
         } else {
             load_masks(ma, v0);
