@@ -435,13 +435,14 @@ __device__ __forceinline__ RowSplit split_row(const char *row, int V)
 // batch when STAGED (issued by the caller before the staging finished).
 // SELECT (STAGED only): vectors with no allowed token are not read (see
 // load_batch_buf_sel).
-template <int THREADS, int U, bool MASKED, bool SHIFTED, bool STAGED, bool SELECT>
+template <int THREADS, int U, bool MASKED, bool SHIFTED, bool STAGED, bool SELECT, bool AHEAD2 = false>
 __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *arow, const uint8_t *mbytes,
                                               int moff, const int32_t *ns_row, RowSplit rs, int v0, int v1,
                                               bool first, bool last, int V, const uint4 *lut, uint4 (&da)[U],
                                               uint4 (&db)[U], uint64_t &vec_pack, int &vec_ns)
 {
     static_assert(!SELECT || STAGED, "selection reads the staged mask bytes");
+    static_assert(!AHEAD2 || (MASKED && !STAGED), "two batches ahead: the streamed mask bytes choose the loads");
     constexpr int kVec = 8;
     constexpr int kStep = THREADS * U;  // vectors per batch
     const int tid = threadIdx.x;
@@ -595,7 +596,7 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
                 // load in flight where the branches join)
                 best_ns = ns_row[best_idx];
             }
-        } else if constexpr (MASKED && !SHIFTED) {
+        } else if constexpr (MASKED && !SHIFTED && !AHEAD2) {
             const __amdgpu_buffer_rsrc_t rl = raw_buffer(vrow, (uint32_t)v1 * 16u);
             const __amdgpu_buffer_rsrc_t rm = raw_buffer(mbytes - moff, (uint32_t)v1);
             load_masks_buf<THREADS, U>(ma, rm, v0);
@@ -607,6 +608,49 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
                 load_masks_buf<THREADS, U>(ma, rm, vb + 2 * kStep);
                 if (vb + kStep < v1)  // block-uniform
                     process_batch(db, mb, vb + kStep);
+                best_ns = ns_row[best_idx];  // as above
+            }
+        } else if constexpr (MASKED && !SHIFTED) {
+            // Mask bytes two batches ahead of their logits: each batch from
+            // the third on is issued with its vectors' offsets chosen by
+            // them, so a vector with no allowed token is not read.  Four
+            // batches per trip, so no register holding a load in flight is
+            // ever copied (a copy would wait for the load).
+            const __amdgpu_buffer_rsrc_t rl = raw_buffer(vrow, (uint32_t)v1 * 16u);
+            const __amdgpu_buffer_rsrc_t rm = raw_buffer(mbytes - moff, (uint32_t)v1);
+            uint32_t mc[U], md[U];
+            load_masks_buf<THREADS, U>(ma, rm, v0);
+            load_masks_buf<THREADS, U>(mb, rm, v0 + kStep);
+            __builtin_amdgcn_sched_barrier(0);
+            load_batch_buf<THREADS, U>(db, rl, v0 + kStep);
+            __builtin_amdgcn_sched_barrier(0);
+            load_masks_buf<THREADS, U>(mc, rm, v0 + 2 * kStep);
+            load_masks_buf<THREADS, U>(md, rm, v0 + 3 * kStep);
+            __builtin_amdgcn_sched_barrier(0);
+            for (int vb = v0; vb < v1; vb += 4 * kStep) {
+                process_batch(da, ma, vb);
+                load_batch_buf_sel<THREADS, U>(da, rl, vb + 2 * kStep, mc);
+                __builtin_amdgcn_sched_barrier(0);
+                load_masks_buf<THREADS, U>(ma, rm, vb + 4 * kStep);
+                __builtin_amdgcn_sched_barrier(0);
+                if (vb + kStep < v1)  // block-uniform
+                    process_batch(db, mb, vb + kStep);
+                load_batch_buf_sel<THREADS, U>(db, rl, vb + 3 * kStep, md);
+                __builtin_amdgcn_sched_barrier(0);
+                load_masks_buf<THREADS, U>(mb, rm, vb + 5 * kStep);
+                __builtin_amdgcn_sched_barrier(0);
+                if (vb + 2 * kStep < v1)
+                    process_batch(da, mc, vb + 2 * kStep);
+                load_batch_buf_sel<THREADS, U>(da, rl, vb + 4 * kStep, ma);
+                __builtin_amdgcn_sched_barrier(0);
+                load_masks_buf<THREADS, U>(mc, rm, vb + 6 * kStep);
+                __builtin_amdgcn_sched_barrier(0);
+                if (vb + 3 * kStep < v1)
+                    process_batch(db, md, vb + 3 * kStep);
+                load_batch_buf_sel<THREADS, U>(db, rl, vb + 5 * kStep, mb);
+                __builtin_amdgcn_sched_barrier(0);
+                load_masks_buf<THREADS, U>(md, rm, vb + 7 * kStep);
+                __builtin_amdgcn_sched_barrier(0);
                 best_ns = ns_row[best_idx];  // as above
             }
         } else {
@@ -638,15 +682,15 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
 // ANY_ALIGN false: the caller has checked that every row is 16-byte aligned,
 // so only the aligned scan is compiled (fewer registers: more resident
 // blocks where several share a CU).
-template <int THREADS, int U, bool MASKED, bool ANY_ALIGN, bool STAGED, bool SELECT>
+template <int THREADS, int U, bool MASKED, bool ANY_ALIGN, bool STAGED, bool SELECT, bool AHEAD2 = false>
 __device__ __forceinline__ uint64_t scan_chunk_bf16(const char *row, const uint32_t *arow, const uint8_t *mbytes,
                                                     int moff, const int32_t *ns_row, RowSplit rs, int v0, int v1,
                                                     bool first, bool last, int V, const uint4 *lut, uint4 (&da)[U],
                                                     uint4 (&db)[U], uint64_t &vec_pack, int &vec_ns)
 {
     if (!ANY_ALIGN || rs.head == 0)
-        return scan_bf16<THREADS, U, MASKED, false, STAGED, SELECT>(row, arow, mbytes, moff, ns_row, rs, v0, v1,
-                                                                    first, last, V, lut, da, db, vec_pack, vec_ns);
+        return scan_bf16<THREADS, U, MASKED, false, STAGED, SELECT, AHEAD2>(
+            row, arow, mbytes, moff, ns_row, rs, v0, v1, first, last, V, lut, da, db, vec_pack, vec_ns);
     return scan_bf16<THREADS, U, MASKED, true, STAGED, SELECT>(row, arow, mbytes, moff, ns_row, rs, v0, v1, first,
                                                                last, V, lut, da, db, vec_pack, vec_ns);
 }
@@ -682,7 +726,7 @@ __device__ __forceinline__ void stage_mask_words(uint32_t *lds, const uint32_t *
 // LDS bytes of a launch's staged mask words (chunks of chunk_vec vectors).
 inline size_t staged_mask_bytes(int chunk_vec) { return ((size_t)chunk_vec / 4 + 1) * 4; }
 
-template <int THREADS, int U, bool ANY_ALIGN, bool SELECT>
+template <int THREADS, int U, bool ANY_ALIGN, bool SELECT, bool AHEAD2>
 __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     const int32_t *__restrict__ next_state, const uint32_t *__restrict__ allow, int S, int V, int W,
     const int32_t *__restrict__ states, const void *__restrict__ logits, RowMap map, int chunk_vec,
@@ -739,7 +783,7 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
         fill_lut(lut);
         lds_barrier();
         if (live)
-            mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN, false, false>(
+            mine = scan_chunk_bf16<THREADS, U, true, ANY_ALIGN, false, false, AHEAD2>(
                 row, arow, reinterpret_cast<const uint8_t *>(arow), 0, next_state + (size_t)s * V, rs, v0, v1,
                 c == 0, c == nchunks - 1, V, lut, da, db, vec_pack, vec_ns);
     }
@@ -828,6 +872,11 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
 // unit other blocks hide that and the saved bytes win (B = 1024 x V =
 // 256000: 82 against 85 us per step), with one block per unit it shows
 // (B = 256 x V = 128256: 15.0 against 13.9 us).
+// Chunks of at least 8 batches per lane (8 x 512 lanes x 2 vectors = 64K
+// tokens) read their loads two batches ahead of the mask bytes that choose
+// them; shorter chunks are over before that pays for its longer start.
+constexpr int kAhead2MinVec = 8 * kBigThreads * kBigU;
+
 static bool skip_unread_lines(unsigned blocks)
 {
     const int n = device_compute_units();  // unknown: never skip
@@ -849,17 +898,24 @@ hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, 
     else {
         const bool aligned = map.rows_aligned(logits, 2), select = skip_unread_lines(grid);
         const size_t lds = select ? staged_mask_bytes(g.chunk_vec) : 0;
-#define DV_STEP_BF16(A, SEL)                                                                                   \
-    masked_step_bf16_kernel<kBigThreads, kBigU, A, SEL><<<grid, kBigThreads, lds, stream>>>(                  \
+        // long chunks streamed with one block per compute unit choose their
+        // loads from mask bytes read two batches ahead
+        const bool ahead2 = !select && g.chunk_vec >= kAhead2MinVec;
+#define DV_STEP_BF16(A, SEL, A2)                                                                               \
+    masked_step_bf16_kernel<kBigThreads, kBigU, A, SEL, A2><<<grid, kBigThreads, lds, stream>>>(              \
         next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, meet)
         if (aligned && select)
-            DV_STEP_BF16(false, true);
+            DV_STEP_BF16(false, true, false);
+        else if (aligned && ahead2)
+            DV_STEP_BF16(false, false, true);
         else if (aligned)
-            DV_STEP_BF16(false, false);
+            DV_STEP_BF16(false, false, false);
         else if (select)
-            DV_STEP_BF16(true, true);
+            DV_STEP_BF16(true, true, false);
+        else if (ahead2)
+            DV_STEP_BF16(true, false, true);
         else
-            DV_STEP_BF16(true, false);
+            DV_STEP_BF16(true, false, false);
 #undef DV_STEP_BF16
     }
     return hipGetLastError();
