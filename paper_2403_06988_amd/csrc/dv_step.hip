@@ -613,12 +613,98 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
         } else if constexpr (MASKED && !SHIFTED) {
             // Mask bytes two batches ahead of their logits: each batch from
             // the third on is issued with its vectors' offsets chosen by
-            // them, so a vector with no allowed token is not read.  Four
+            // them, so a vector with no allowed token is not read.  A batch
+            // is first folded into its masked keys (the mask-table entries
+            // read from LDS a batch ahead), and the next batch's loads are
+            // issued right then, before the wave-wide maximum and the
+            // search for its position, which work on the masked keys.  Four
             // batches per trip, so no register holding a load in flight is
             // ever copied (a copy would wait for the load).
             const __amdgpu_buffer_rsrc_t rl = raw_buffer(vrow, (uint32_t)v1 * 16u);
             const __amdgpu_buffer_rsrc_t rm = raw_buffer(mbytes - moff, (uint32_t)v1);
             uint32_t mc[U], md[U];
+            uint4 la[U], lb[U];  // mask-table entries of the batch being folded and of the next
+            auto read_lut = [&](uint4 (&l)[U], const uint32_t (&m)[U]) {
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    l[u] = lut[m[u]];
+            };
+            // masked 16-bit keys of a batch (two per word; 0 where not
+            // allowed) and whether the lane has an allowed element in it
+            auto fold = [&](const uint4 (&d)[U], const uint4 (&l)[U], const uint32_t (&m)[U],
+                            uint32_t (&km)[4 * U]) -> uint32_t {
+                uint32_t any = 0;
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    any |= m[u];
+                    km[4 * u + 0] = fast_key2(d[u].x) & l[u].x;
+                    km[4 * u + 1] = fast_key2(d[u].y) & l[u].y;
+                    km[4 * u + 2] = fast_key2(d[u].z) & l[u].z;
+                    km[4 * u + 3] = fast_key2(d[u].w) & l[u].w;
+                }
+                return any;
+            };
+            // the batch's wave-wide maximum against the wave's best so far
+            // (as process_batch, on the masked keys)
+            auto reduce = [&](const uint32_t (&km)[4 * U], uint32_t any, int vb) {
+                uint32_t acc = 0;
+#pragma unroll
+                for (int i = 0; i < 4 * U; ++i)
+                    acc = pk_max_u16(acc, km[i]);
+                const uint32_t lane_max = max(acc & 0xFFFFu, acc >> 16);
+                const uint32_t top = wave_reduce_u32((lane_max << 1) | (any ? 1u : 0u), true);
+                const uint32_t k16 = top >> 1;
+                if (k16 == 0 && (top & 1u) == 0)
+                    return;  // nothing allowed in this batch
+                const bool special = k16 <= 0x007Fu || k16 == 0x7FFFu || k16 == 0x8000u || k16 > 0xFF80u;
+                if (!special) {
+                    const uint32_t h = (k16 & 0x8000u) ? (k16 & 0x7FFFu) : (~k16 & 0xFFFFu);
+                    const uint32_t key = f32_key(h << 16);
+                    if (key <= best_key)
+                        return;
+                    // a non-special k16 is not 0, so a masked key equal to it
+                    // is an allowed element with bits h
+                    int pos = 0x7FFFFFFF;
+                    if (lane_max == k16) {
+#pragma unroll
+                        for (int i = 4 * U - 1; i >= 0; --i) {
+                            const int e = head + (vb + (i / 4) * THREADS + tid) * kVec + 2 * (i % 4);
+                            if ((km[i] >> 16) == k16)
+                                pos = e + 1;
+                            if ((km[i] & 0xFFFFu) == k16)
+                                pos = e;
+                        }
+                    }
+                    best_idx = (int)wave_reduce_u32((uint32_t)pos, false);
+                    best_key = key;
+                } else {
+                    // exact keys (NaN or a signed zero at the top): logits and
+                    // mask bytes re-read from memory, a rare path
+                    uint32_t bk = 0;
+                    int bi = 0;
+#pragma unroll 1
+                    for (int u = 0; u < U; ++u) {
+                        const int v = vb + u * THREADS + tid;
+                        const uint32_t mb = v < v1 ? mbytes[v - moff] : 0u;
+#pragma unroll 1
+                        for (int e = 0; e < kVec; ++e) {
+                            if ((mb >> e) & 1u) {
+                                const int i = head + v * kVec + e;
+                                const uint32_t key = f32_key(Elt<1>::bits(row, i));
+                                if (key > bk) {
+                                    bk = key;
+                                    bi = i;
+                                }
+                            }
+                        }
+                    }
+                    const uint32_t kmax = wave_reduce_u32(bk, true);
+                    if (kmax > best_key) {
+                        best_idx = (int)wave_reduce_u32(bk == kmax ? (uint32_t)bi : 0x7FFFFFFFu, false);
+                        best_key = kmax;
+                    }
+                }
+            };
             load_masks_buf<THREADS, U>(ma, rm, v0);
             load_masks_buf<THREADS, U>(mb, rm, v0 + kStep);
             __builtin_amdgcn_sched_barrier(0);
@@ -627,32 +713,31 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
             load_masks_buf<THREADS, U>(mc, rm, v0 + 2 * kStep);
             load_masks_buf<THREADS, U>(md, rm, v0 + 3 * kStep);
             __builtin_amdgcn_sched_barrier(0);
+            read_lut(la, ma);
+            // one batch: fold, issue the loads two batches on, read the next
+            // batch's table entries, reduce
+#define DV_AHEAD2_BATCH(D, L, LN, M, MN, MSEL, K)                                                              \
+    {                                                                                                          \
+        uint32_t km[4 * U];                                                                                    \
+        const bool in = vb + (K) * kStep < v1; /* block-uniform */                                             \
+        const uint32_t any = in ? fold(D, L, M, km) : 0u;                                                      \
+        __builtin_amdgcn_sched_barrier(0);                                                                     \
+        load_batch_buf_sel<THREADS, U>(D, rl, vb + ((K) + 2) * kStep, MSEL);                                   \
+        __builtin_amdgcn_sched_barrier(0);                                                                     \
+        load_masks_buf<THREADS, U>(M, rm, vb + ((K) + 4) * kStep);                                             \
+        __builtin_amdgcn_sched_barrier(0);                                                                     \
+        read_lut(LN, MN);                                                                                      \
+        if (in)                                                                                                \
+            reduce(km, any, vb + (K) * kStep);                                                                 \
+    }
             for (int vb = v0; vb < v1; vb += 4 * kStep) {
-                process_batch(da, ma, vb);
-                load_batch_buf_sel<THREADS, U>(da, rl, vb + 2 * kStep, mc);
-                __builtin_amdgcn_sched_barrier(0);
-                load_masks_buf<THREADS, U>(ma, rm, vb + 4 * kStep);
-                __builtin_amdgcn_sched_barrier(0);
-                if (vb + kStep < v1)  // block-uniform
-                    process_batch(db, mb, vb + kStep);
-                load_batch_buf_sel<THREADS, U>(db, rl, vb + 3 * kStep, md);
-                __builtin_amdgcn_sched_barrier(0);
-                load_masks_buf<THREADS, U>(mb, rm, vb + 5 * kStep);
-                __builtin_amdgcn_sched_barrier(0);
-                if (vb + 2 * kStep < v1)
-                    process_batch(da, mc, vb + 2 * kStep);
-                load_batch_buf_sel<THREADS, U>(da, rl, vb + 4 * kStep, ma);
-                __builtin_amdgcn_sched_barrier(0);
-                load_masks_buf<THREADS, U>(mc, rm, vb + 6 * kStep);
-                __builtin_amdgcn_sched_barrier(0);
-                if (vb + 3 * kStep < v1)
-                    process_batch(db, md, vb + 3 * kStep);
-                load_batch_buf_sel<THREADS, U>(db, rl, vb + 5 * kStep, mb);
-                __builtin_amdgcn_sched_barrier(0);
-                load_masks_buf<THREADS, U>(md, rm, vb + 7 * kStep);
-                __builtin_amdgcn_sched_barrier(0);
+                DV_AHEAD2_BATCH(da, la, lb, ma, mb, mc, 0)
+                DV_AHEAD2_BATCH(db, lb, la, mb, mc, md, 1)
+                DV_AHEAD2_BATCH(da, la, lb, mc, md, ma, 2)
+                DV_AHEAD2_BATCH(db, lb, la, md, ma, mb, 3)
                 best_ns = ns_row[best_idx];  // as above
             }
+#undef DV_AHEAD2_BATCH
         } else {
             load_masks(ma, v0);
             for (int vb = v0; vb < v1; vb += 2 * kStep) {
