@@ -470,34 +470,63 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
             for (int u = 0; u < U; ++u)
                 m[u] = mask_of(min(vb + u * THREADS + tid, v1 - 1));
         };
-        // One batch: U vectors per lane.  Loads are issued a batch ahead
-        // (logits, then their mask bytes), so while batch i is reduced,
-        // batch i + 1 is in flight; the in-order load counter lets batch i
-        // be consumed without waiting for batch i + 1.
-        // (the buffer loads of the aligned streaming scan already read a
-        // zero mask byte past the chunk)
+        // One batch is U vectors per lane, taken in two parts.  fold: the
+        // batch's masked 16-bit keys (two per word, 0 where not allowed) from
+        // its logits and the mask-table entries of its mask bytes; after it
+        // the logits' registers are free, so the loads of a later batch are
+        // issued right then.  reduce: the wave-wide maximum and, when it
+        // beats the wave's best so far, the search for its lowest position,
+        // both on the masked keys.  Loads are branch-free and in a fixed
+        // order (the load counter is in order: waiting for one load waits
+        // for every earlier one), so while a batch is reduced the next is in
+        // flight.
+        //
+        // Mask bytes with the lanes past the chunk zeroed (the buffer loads
+        // of the aligned streaming scans already read zeros there).
         constexpr bool kZeroPast = MASKED && !SHIFTED && !STAGED;
-        auto process_batch = [&](const uint4 (&d)[U], const uint32_t (&raw)[U], int vb) {
-            uint32_t mk[U];
+        auto live = [&](uint32_t (&m)[U], int vb) {
+            if constexpr (!kZeroPast) {
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-                mk[u] = kZeroPast || vb + u * THREADS + tid < v1 ? raw[u] : 0u;
-            uint32_t acc = 0, any = 0;
+                for (int u = 0; u < U; ++u)
+                    m[u] = vb + u * THREADS + tid < v1 ? m[u] : 0u;
+            }
+        };
+        // mask-table entries of live mask bytes: two 16-bit lane masks per word
+        auto entries = [&](uint4 (&l)[U], const uint32_t (&m)[U]) {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                uint4 M;
                 if constexpr (MASKED) {
-                    M = lut[mk[u]];
+                    l[u] = lut[m[u]];
                 } else {
-                    const uint32_t all = mk[u] ? 0xFFFFFFFFu : 0u;
-                    M = make_uint4(all, all, all, all);
+                    const uint32_t all = m[u] ? 0xFFFFFFFFu : 0u;
+                    l[u] = make_uint4(all, all, all, all);
                 }
-                any |= mk[u];
-                acc = pk_max_u16(acc, fast_key2(d[u].x) & M.x);
-                acc = pk_max_u16(acc, fast_key2(d[u].y) & M.y);
-                acc = pk_max_u16(acc, fast_key2(d[u].z) & M.z);
-                acc = pk_max_u16(acc, fast_key2(d[u].w) & M.w);
             }
+        };
+        // masked keys of a batch; returns whether the lane has an allowed
+        // element in it
+        auto fold = [&](const uint4 (&d)[U], const uint4 (&l)[U], const uint32_t (&m)[U],
+                        uint32_t (&km)[4 * U]) -> uint32_t {
+            uint32_t any = 0;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                any |= m[u];
+                km[4 * u + 0] = fast_key2(d[u].x) & l[u].x;
+                km[4 * u + 1] = fast_key2(d[u].y) & l[u].y;
+                km[4 * u + 2] = fast_key2(d[u].z) & l[u].z;
+                km[4 * u + 3] = fast_key2(d[u].w) & l[u].w;
+            }
+            return any;
+        };
+        // The batch's wave-wide maximum against the wave's best so far.  Per
+        // lane, elements are in increasing index order and a later batch
+        // replaces the best only when strictly larger, so the wave keeps the
+        // lowest index of its maximum.
+        auto reduce = [&](const uint32_t (&km)[4 * U], uint32_t any, int vb) {
+            uint32_t acc = 0;
+#pragma unroll
+            for (int i = 0; i < 4 * U; ++i)
+                acc = pk_max_u16(acc, km[i]);
             const uint32_t lane_max = max(acc & 0xFFFFu, acc >> 16);
             const uint32_t top = wave_reduce_u32((lane_max << 1) | (any ? 1u : 0u), true);
             const uint32_t k16 = top >> 1;
@@ -509,35 +538,32 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
                 const uint32_t key = f32_key(h << 16);
                 if (key <= best_key)
                     return;  // an earlier batch of this wave (lower indices) is at least as good
-                // first allowed element whose bits are h (for a non-special
-                // key, equal keys means equal bf16 bit patterns)
+                // first allowed element whose bits are h: a non-special k16
+                // is not 0, and the fast key is one-to-one, so a masked key
+                // equal to k16 is exactly that
                 int pos = 0x7FFFFFFF;
                 if (lane_max == k16) {
 #pragma unroll
-                    for (int u = U - 1; u >= 0; --u) {
-                        const uint32_t w[4] = {d[u].x, d[u].y, d[u].z, d[u].w};
-                        const int v = vb + u * THREADS + tid;
-#pragma unroll
-                        for (int k = 3; k >= 0; --k) {
-                            if ((w[k] >> 16) == h && ((mk[u] >> (2 * k + 1)) & 1u))
-                                pos = head + v * kVec + 2 * k + 1;
-                            if ((w[k] & 0xFFFFu) == h && ((mk[u] >> (2 * k)) & 1u))
-                                pos = head + v * kVec + 2 * k;
-                        }
+                    for (int i = 4 * U - 1; i >= 0; --i) {
+                        const int e = head + (vb + (i / 4) * THREADS + tid) * kVec + 2 * (i % 4);
+                        if ((km[i] >> 16) == k16)
+                            pos = e + 1;
+                        if ((km[i] & 0xFFFFu) == k16)
+                            pos = e;
                     }
                 }
                 best_idx = (int)wave_reduce_u32((uint32_t)pos, false);
                 best_key = key;
             } else {
                 // exact keys for this batch (NaN or a signed zero at the top),
-                // logits re-read from memory: a rare path, kept out of the
-                // registers
+                // logits and mask bytes re-read from memory: a rare path, kept
+                // out of the registers
                 uint32_t bk = 0;
                 int bi = 0;
 #pragma unroll 1
                 for (int u = 0; u < U; ++u) {
                     const int v = vb + u * THREADS + tid;
-                    const uint32_t mb = mk[u];
+                    const uint32_t mb = v < v1 ? mask_of(v) : 0u;
 #pragma unroll 1
                     for (int e = 0; e < kVec; ++e) {
                         if ((mb >> e) & 1u) {
@@ -557,13 +583,14 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
                 }
             }
         };
-        // The next batch's loads are issued unconditionally (past the chunk
-        // they are harmless reloads, masked out when reduced).
         uint32_t ma[U], mb[U];
+        uint4 la[U], lb[U];  // mask-table entries of the batch being folded and of the next
         if constexpr (STAGED) {
             // Both first batches are in flight (issued by the caller) and the
             // mask bytes are in LDS: reading them costs no memory trip, so
             // with SELECT every later batch's addresses are chosen from them.
+            // Each batch's mask bytes are read from LDS once, two batches
+            // ahead, and serve both its addresses and its fold.
             const __amdgpu_buffer_rsrc_t rl = raw_buffer(vrow, (uint32_t)v1 * 16u);
             auto issue = [&](uint4 (&d)[U], int vb, const uint32_t (&sel)[U]) {
                 if constexpr (SELECT && MASKED && !SHIFTED)
@@ -571,21 +598,37 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
                 else
                     load_batch_bf16<THREADS, U>(d, vrow, vb, v1);
             };
-            // Each batch's mask bytes are read from LDS once, a batch ahead:
-            // they choose its addresses when it is issued and mask it when it
-            // is reduced, so reading them never stands between consuming a
-            // batch and issuing the next.
             uint32_t na[U], nb[U];
             load_masks(ma, v0);
+            live(ma, v0);
             load_masks(mb, v0 + kStep);
+            live(mb, v0 + kStep);
+            entries(la, ma);
             for (int vb = v0; vb < v1; vb += 2 * kStep) {
                 load_masks(na, vb + 2 * kStep);
-                process_batch(da, ma, vb);
-                issue(da, vb + 2 * kStep, na);
+                live(na, vb + 2 * kStep);
+                {
+                    uint32_t km[4 * U];
+                    const uint32_t any = fold(da, la, ma, km);
+                    __builtin_amdgcn_sched_barrier(0);
+                    issue(da, vb + 2 * kStep, na);
+                    __builtin_amdgcn_sched_barrier(0);
+                    entries(lb, mb);
+                    reduce(km, any, vb);
+                }
                 load_masks(nb, vb + 3 * kStep);
-                if (vb + kStep < v1)  // block-uniform
-                    process_batch(db, mb, vb + kStep);
-                issue(db, vb + 3 * kStep, nb);
+                live(nb, vb + 3 * kStep);
+                {
+                    uint32_t km[4 * U];
+                    const bool in = vb + kStep < v1;  // block-uniform
+                    const uint32_t any = in ? fold(db, lb, mb, km) : 0u;
+                    __builtin_amdgcn_sched_barrier(0);
+                    issue(db, vb + 3 * kStep, nb);
+                    __builtin_amdgcn_sched_barrier(0);
+                    entries(la, na);
+                    if (in)
+                        reduce(km, any, vb + kStep);
+                }
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     ma[u] = na[u];
@@ -597,114 +640,44 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
                 best_ns = ns_row[best_idx];
             }
         } else if constexpr (MASKED && !SHIFTED && !AHEAD2) {
+            // Mask bytes one batch ahead, each issued before its batch's
+            // logits, so reading a batch's table entries waits for no logits.
             const __amdgpu_buffer_rsrc_t rl = raw_buffer(vrow, (uint32_t)v1 * 16u);
             const __amdgpu_buffer_rsrc_t rm = raw_buffer(mbytes - moff, (uint32_t)v1);
             load_masks_buf<THREADS, U>(ma, rm, v0);
+            load_masks_buf<THREADS, U>(mb, rm, v0 + kStep);
+            __builtin_amdgcn_sched_barrier(0);
+            load_batch_buf<THREADS, U>(db, rl, v0 + kStep);
+            __builtin_amdgcn_sched_barrier(0);
+            entries(la, ma);
+#define DV_STREAM_BATCH(D, L, LN, M, MN, K)                                                                    \
+    {                                                                                                          \
+        uint32_t km[4 * U];                                                                                    \
+        const bool in = vb + (K) * kStep < v1; /* block-uniform */                                             \
+        const uint32_t any = in ? fold(D, L, M, km) : 0u;                                                      \
+        __builtin_amdgcn_sched_barrier(0);                                                                     \
+        load_masks_buf<THREADS, U>(M, rm, vb + ((K) + 2) * kStep);                                             \
+        load_batch_buf<THREADS, U>(D, rl, vb + ((K) + 2) * kStep);                                             \
+        __builtin_amdgcn_sched_barrier(0);                                                                     \
+        entries(LN, MN);                                                                                       \
+        if (in)                                                                                                \
+            reduce(km, any, vb + (K) * kStep);                                                                 \
+    }
             for (int vb = v0; vb < v1; vb += 2 * kStep) {
-                load_batch_buf<THREADS, U>(db, rl, vb + kStep);
-                load_masks_buf<THREADS, U>(mb, rm, vb + kStep);
-                process_batch(da, ma, vb);
-                load_batch_buf<THREADS, U>(da, rl, vb + 2 * kStep);
-                load_masks_buf<THREADS, U>(ma, rm, vb + 2 * kStep);
-                if (vb + kStep < v1)  // block-uniform
-                    process_batch(db, mb, vb + kStep);
+                DV_STREAM_BATCH(da, la, lb, ma, mb, 0)
+                DV_STREAM_BATCH(db, lb, la, mb, ma, 1)
                 best_ns = ns_row[best_idx];  // as above
             }
+#undef DV_STREAM_BATCH
         } else if constexpr (MASKED && !SHIFTED) {
             // Mask bytes two batches ahead of their logits: each batch from
             // the third on is issued with its vectors' offsets chosen by
-            // them, so a vector with no allowed token is not read.  A batch
-            // is first folded into its masked keys (the mask-table entries
-            // read from LDS a batch ahead), and the next batch's loads are
-            // issued right then, before the wave-wide maximum and the
-            // search for its position, which work on the masked keys.  Four
+            // them, so a vector with no allowed token is not read.  Four
             // batches per trip, so no register holding a load in flight is
             // ever copied (a copy would wait for the load).
             const __amdgpu_buffer_rsrc_t rl = raw_buffer(vrow, (uint32_t)v1 * 16u);
             const __amdgpu_buffer_rsrc_t rm = raw_buffer(mbytes - moff, (uint32_t)v1);
             uint32_t mc[U], md[U];
-            uint4 la[U], lb[U];  // mask-table entries of the batch being folded and of the next
-            auto read_lut = [&](uint4 (&l)[U], const uint32_t (&m)[U]) {
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-                    l[u] = lut[m[u]];
-            };
-            // masked 16-bit keys of a batch (two per word; 0 where not
-            // allowed) and whether the lane has an allowed element in it
-            auto fold = [&](const uint4 (&d)[U], const uint4 (&l)[U], const uint32_t (&m)[U],
-                            uint32_t (&km)[4 * U]) -> uint32_t {
-                uint32_t any = 0;
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    any |= m[u];
-                    km[4 * u + 0] = fast_key2(d[u].x) & l[u].x;
-                    km[4 * u + 1] = fast_key2(d[u].y) & l[u].y;
-                    km[4 * u + 2] = fast_key2(d[u].z) & l[u].z;
-                    km[4 * u + 3] = fast_key2(d[u].w) & l[u].w;
-                }
-                return any;
-            };
-            // the batch's wave-wide maximum against the wave's best so far
-            // (as process_batch, on the masked keys)
-            auto reduce = [&](const uint32_t (&km)[4 * U], uint32_t any, int vb) {
-                uint32_t acc = 0;
-#pragma unroll
-                for (int i = 0; i < 4 * U; ++i)
-                    acc = pk_max_u16(acc, km[i]);
-                const uint32_t lane_max = max(acc & 0xFFFFu, acc >> 16);
-                const uint32_t top = wave_reduce_u32((lane_max << 1) | (any ? 1u : 0u), true);
-                const uint32_t k16 = top >> 1;
-                if (k16 == 0 && (top & 1u) == 0)
-                    return;  // nothing allowed in this batch
-                const bool special = k16 <= 0x007Fu || k16 == 0x7FFFu || k16 == 0x8000u || k16 > 0xFF80u;
-                if (!special) {
-                    const uint32_t h = (k16 & 0x8000u) ? (k16 & 0x7FFFu) : (~k16 & 0xFFFFu);
-                    const uint32_t key = f32_key(h << 16);
-                    if (key <= best_key)
-                        return;
-                    // a non-special k16 is not 0, so a masked key equal to it
-                    // is an allowed element with bits h
-                    int pos = 0x7FFFFFFF;
-                    if (lane_max == k16) {
-#pragma unroll
-                        for (int i = 4 * U - 1; i >= 0; --i) {
-                            const int e = head + (vb + (i / 4) * THREADS + tid) * kVec + 2 * (i % 4);
-                            if ((km[i] >> 16) == k16)
-                                pos = e + 1;
-                            if ((km[i] & 0xFFFFu) == k16)
-                                pos = e;
-                        }
-                    }
-                    best_idx = (int)wave_reduce_u32((uint32_t)pos, false);
-                    best_key = key;
-                } else {
-                    // exact keys (NaN or a signed zero at the top): logits and
-                    // mask bytes re-read from memory, a rare path
-                    uint32_t bk = 0;
-                    int bi = 0;
-#pragma unroll 1
-                    for (int u = 0; u < U; ++u) {
-                        const int v = vb + u * THREADS + tid;
-                        const uint32_t mb = v < v1 ? mbytes[v - moff] : 0u;
-#pragma unroll 1
-                        for (int e = 0; e < kVec; ++e) {
-                            if ((mb >> e) & 1u) {
-                                const int i = head + v * kVec + e;
-                                const uint32_t key = f32_key(Elt<1>::bits(row, i));
-                                if (key > bk) {
-                                    bk = key;
-                                    bi = i;
-                                }
-                            }
-                        }
-                    }
-                    const uint32_t kmax = wave_reduce_u32(bk, true);
-                    if (kmax > best_key) {
-                        best_idx = (int)wave_reduce_u32(bk == kmax ? (uint32_t)bi : 0x7FFFFFFFu, false);
-                        best_key = kmax;
-                    }
-                }
-            };
             load_masks_buf<THREADS, U>(ma, rm, v0);
             load_masks_buf<THREADS, U>(mb, rm, v0 + kStep);
             __builtin_amdgcn_sched_barrier(0);
@@ -713,9 +686,7 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
             load_masks_buf<THREADS, U>(mc, rm, v0 + 2 * kStep);
             load_masks_buf<THREADS, U>(md, rm, v0 + 3 * kStep);
             __builtin_amdgcn_sched_barrier(0);
-            read_lut(la, ma);
-            // one batch: fold, issue the loads two batches on, read the next
-            // batch's table entries, reduce
+            entries(la, ma);
 #define DV_AHEAD2_BATCH(D, L, LN, M, MN, MSEL, K)                                                              \
     {                                                                                                          \
         uint32_t km[4 * U];                                                                                    \
@@ -726,7 +697,7 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
         __builtin_amdgcn_sched_barrier(0);                                                                     \
         load_masks_buf<THREADS, U>(M, rm, vb + ((K) + 4) * kStep);                                             \
         __builtin_amdgcn_sched_barrier(0);                                                                     \
-        read_lut(LN, MN);                                                                                      \
+        entries(LN, MN);                                                                                       \
         if (in)                                                                                                \
             reduce(km, any, vb + (K) * kStep);                                                                 \
     }
@@ -739,6 +710,16 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
             }
 #undef DV_AHEAD2_BATCH
         } else {
+            // rows of any alignment, and the unmasked scan: the same parts
+            // in sequence, the next batch's loads issued ahead of each
+            auto process_batch = [&](const uint4 (&d)[U], uint32_t (&m)[U], int vb) {
+                live(m, vb);
+                uint4 l[U];
+                entries(l, m);
+                uint32_t km[4 * U];
+                const uint32_t any = fold(d, l, m, km);
+                reduce(km, any, vb);
+            };
             load_masks(ma, v0);
             for (int vb = v0; vb < v1; vb += 2 * kStep) {
                 load_batch_bf16<THREADS, U>(db, vrow, vb + kStep, v1);
