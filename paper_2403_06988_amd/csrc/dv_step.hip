@@ -678,13 +678,15 @@ __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *a
             const __amdgpu_buffer_rsrc_t rl = raw_buffer(vrow, (uint32_t)v1 * 16u);
             const __amdgpu_buffer_rsrc_t rm = raw_buffer(mbytes - moff, (uint32_t)v1);
             uint32_t mc[U], md[U];
+            // (the mask bytes that choose the third and fourth batches are
+            // issued ahead of the second batch, so choosing them waits for
+            // no logits)
             load_masks_buf<THREADS, U>(ma, rm, v0);
             load_masks_buf<THREADS, U>(mb, rm, v0 + kStep);
-            __builtin_amdgcn_sched_barrier(0);
-            load_batch_buf<THREADS, U>(db, rl, v0 + kStep);
-            __builtin_amdgcn_sched_barrier(0);
             load_masks_buf<THREADS, U>(mc, rm, v0 + 2 * kStep);
             load_masks_buf<THREADS, U>(md, rm, v0 + 3 * kStep);
+            __builtin_amdgcn_sched_barrier(0);
+            load_batch_buf<THREADS, U>(db, rl, v0 + kStep);
             __builtin_amdgcn_sched_barrier(0);
             entries(la, ma);
 #define DV_AHEAD2_BATCH(D, L, LN, M, MN, MSEL, K)                                                              \
