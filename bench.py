@@ -51,7 +51,8 @@ PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2403_06988_amd", "csrc")
 KERNEL_SOURCES = {"masked_step": ("dv_step.hip", "dv_internal.h"),
                   "align": ("dv_align.hip", "dv_internal.h"),
-                  "spec_verify": ("dv_step.hip", "dv_spec.hip", "dv_internal.h")}
+                  "spec_verify": ("dv_step.hip", "dv_spec.hip", "dv_internal.h"),
+                  "sample": ("dv_sample.hip", "dv_sample.h", "dv_internal.h")}
 TRAFFIC_FILES = {
     ("masked_step", 3): "masked_step_bf16_kernel__llm-tokenizer-scale_S1024_V128256_B64.traffic.txt",
     ("masked_step", 4): "masked_step_bf16_kernel__grammar-lexer-union_S8192_V128256_B256.traffic.txt",
@@ -64,9 +65,15 @@ EXTRA_WORKLOADS = (3, 5)
 
 
 def kernel_source_hash(which):
+    """Hash of the kernel sources without their comments and blank lines, so
+    that a recorded measurement stays attached to the code it was taken on
+    through edits of the comments alone."""
     h = hashlib.sha256()
     for f in KERNEL_SOURCES[which]:
-        h.update(open(os.path.join(CSRC, f), "rb").read())
+        for line in open(os.path.join(CSRC, f), encoding="utf-8"):
+            code = line.split("//", 1)[0].rstrip()
+            if code:
+                h.update(code.encode() + b"\n")
     return h.hexdigest()[:16]
 
 

@@ -25,20 +25,23 @@
 //     Rows that start on a 16-byte boundary are read as raw buffers whose
 //     records end at the chunk's end: one add per load for the address, and
 //     a lane past the chunk reads zeros (no clamp, no memory access).
-//   * Mask bytes (one per 8 logits).  With one block per compute unit they
-//     are loaded beside their batch's logits.  With two or more, the block
-//     first copies its chunk's mask bytes into LDS; each later batch's
-//     offsets are then chosen from them, and a vector with no allowed token
-//     gets an offset past the buffer's records, which reads zeros without a
-//     memory access, so a 128-byte line with no allowed token is never
-//     fetched.
-//   * bf16 arithmetic, two VALU operations per logit: per 32-bit word (two
-//     logits) one v_pk_ashrrev_i16 and one bit operation give
-//     order-preserving 16-bit keys, an AND with two 16-bit lane masks (from
-//     an LDS table indexed by the mask byte) drops the disallowed ones, and
-//     v_pk_max_u16 folds them.  One wave-wide max per batch (DPP moves, no
-//     LDS and no barrier); only the wave(s) holding the maximum look up its
-//     lowest index.  The fast key differs from the exact ordering only for
+//   * Mask bytes (one per 8 logits).  With two or more blocks per compute
+//     unit, the block first copies its chunk's mask bytes into LDS; with one,
+//     chunks of at least 8 batches read each batch's mask bytes from memory
+//     two batches ahead of its logits.  Either way each later batch's
+//     offsets are chosen from them: a vector with no allowed token gets an
+//     offset past the buffer's records, which reads zeros without a memory
+//     access, so a 128-byte line with no allowed token is never fetched.
+//     Shorter chunks at one block per unit read their mask bytes beside
+//     their logits, and every line.
+//   * bf16 arithmetic, a batch at a time in two parts.  Fold: per 32-bit
+//     word (two logits) a v_pk_ashrrev_i16 and two bit operations give the
+//     order-preserving 16-bit keys ANDed with two 16-bit lane masks (from an
+//     LDS table indexed by the mask byte, read a batch ahead), so disallowed
+//     tokens key as 0; the loads of a later batch are issued right after it.
+//     Reduce: v_pk_max_u16 over the masked keys and one wave-wide max per
+//     batch (DPP moves, no LDS and no barrier); only the wave(s) holding the
+//     maximum search their masked keys for its lowest index.  The fast key differs from the exact ordering only for
 //     NaN (which must rank as -inf) and -0.0 (which must tie with +0.0); a
 //     batch whose maximum is one of those few key values is redone with
 //     exact keys.
