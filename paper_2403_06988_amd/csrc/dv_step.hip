@@ -944,8 +944,13 @@ __global__ __launch_bounds__(THREADS) void opportunistic_step_bf16_kernel(
 // 256000: 82 against 85 us per step), with one block per unit it shows
 // (B = 256 x V = 128256: 15.0 against 13.9 us).
 // Chunks of at least 8 batches per lane (8 x 512 lanes x 2 vectors = 64K
-// tokens) read their loads two batches ahead of the mask bytes that choose
-// them; shorter chunks are over before that pays for its longer start.
+// tokens) instead choose their loads from mask bytes read two batches ahead
+// when the launch has at most four blocks per compute unit (B = 1024 x V =
+// 256000: 80.4-81.0 against 82.3 us; the speculative verification of B =
+// 64 x 9 positions x V = 128256 24.7 against 28.6); at nine per unit the
+// staged form, with fewer registers and so more resident blocks, stays
+// ahead (B = 256 x 9 x 128256: 70.2-70.7 against 71.9-72.5).  Shorter
+// chunks are over before the two-ahead form pays for its longer start.
 constexpr int kAhead2MinVec = 8 * kBigThreads * kBigU;
 
 static bool skip_unread_lines(unsigned blocks)
@@ -967,11 +972,15 @@ hipError_t launch_masked_rows(const int32_t *next_state, const uint32_t *allow, 
         masked_step_kernel<kSmallThreads, kSmallU><<<grid, kSmallThreads, 0, stream>>>(
             next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, meet);
     else {
-        const bool aligned = map.rows_aligned(logits, 2), select = skip_unread_lines(grid);
+        const bool aligned = map.rows_aligned(logits, 2);
+        // long chunks at up to four blocks per compute unit choose their
+        // loads from mask bytes read two batches ahead; more blocks per unit
+        // stage the mask bytes in LDS (the two-ahead scan's registers allow
+        // fewer resident blocks)
+        const int cus = device_compute_units();
+        const bool ahead2 = g.chunk_vec >= kAhead2MinVec && (cus <= 0 || grid <= 4u * (unsigned)cus);
+        const bool select = !ahead2 && skip_unread_lines(grid);
         const size_t lds = select ? staged_mask_bytes(g.chunk_vec) : 0;
-        // long chunks streamed with one block per compute unit choose their
-        // loads from mask bytes read two batches ahead
-        const bool ahead2 = !select && g.chunk_vec >= kAhead2MinVec;
 #define DV_STEP_BF16(A, SEL, A2)                                                                               \
     masked_step_bf16_kernel<kBigThreads, kBigU, A, SEL, A2><<<grid, kBigThreads, lds, stream>>>(              \
         next_state, allow, S, V, W, states, logits, map, g.chunk_vec, g.nchunks, token, new_state, meet)

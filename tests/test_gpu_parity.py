@@ -446,13 +446,17 @@ def test_step_every_row_alignment(dv, B, V, extra_ld, dtype, head):
 
 @pytest.mark.parametrize("B,V,offset,extra_ld", [
     (600, 40000, 0, 0), (520, 30011, 0, 1), (530, 33333, 3, 2), (1030, 24577, 0, 7),
+    # two to four blocks per compute unit, long rows: mask bytes two batches ahead
+    (600, 140000, 0, 0), (530, 133333, 3, 2), (1024, 70000, 0, 0),
     # fewer than two blocks per compute unit, long chunks: every line is read
     (256, 128256, 0, 0), (300, 66000, 3, 1), (128, 140000, 0, 0), (64, 260000, 5, 3),
 ])
 def test_step_skips_lines_without_allowed_tokens(dv, B, V, offset, extra_ld):
-    """Launches of two or more blocks per compute unit do not read vectors
-    whose 8 tokens are all disallowed (from the third batch of a chunk on);
-    smaller launches read every line, the same masks deciding.  Sparse masks
+    """Vectors whose 8 tokens are all disallowed are not read (from the
+    third batch of a chunk on) by launches of two or more blocks per compute
+    unit (mask bytes staged in LDS) and by chunks of at least 8 batches at up
+    to four blocks per unit (mask bytes two batches ahead); shorter chunks at
+    one block per unit read every line, the same masks deciding.  Sparse masks
     (whole runs of disallowed vectors), few distinct values, planted NaN and
     signed zeros, aligned and misaligned rows, rows of one, two and four
     chunks; greedy and opportunistic steps against the oracle."""
