@@ -12,6 +12,10 @@
 //      column (DEAD = 0xFFFF).  (3 and 4 run in one launch.)
 //      Random printable-ASCII DFAs keep ~95 of 256 columns, so the table is
 //      ~2.7x smaller than the int32 input and stays resident in each XCD's L2.
+//      The walks write their outputs (4.125 bytes per pair) with
+//      non-temporal stores: that stream passes the caches by, so it neither
+//      evicts the compacted table the walks gather from nor leaves the
+//      caches full of dirty lines for the kernels that follow to write back.
 //   4. token_info: each token's first 8 byte classes, length and offset.
 //   5. walk (tables of at most 98 columns that do not fit in LDS whole, e.g.
 //      random printable-ASCII DFAs of more than ~330 states): the prefix-table
@@ -285,10 +289,10 @@ __device__ __forceinline__ void walk_tile_whole(const uint16_t *tab, const uint8
             const int s = s0 + g + k;
             const bool alive = st[k] != dead;
             if (t < V)
-                next_state[(size_t)s * V + t] = alive ? (int32_t)st[k] : -1;
+                __builtin_nontemporal_store(alive ? (int32_t)st[k] : -1, &next_state[(size_t)s * V + t]);
             const uint64_t mask = __ballot(alive);
             if (lane < 2 && w < W)
-                allow[(size_t)s * W + w] = (uint32_t)(mask >> (32 * lane));
+                __builtin_nontemporal_store((uint32_t)(mask >> (32 * lane)), &allow[(size_t)s * W + w]);
         }
     }
 }
@@ -368,10 +372,10 @@ __device__ __forceinline__ void walk_tile_rows(const uint16_t *tab, const uint16
             const int s = s0 + g + k;
             const bool alive = st[k] != kDead16;
             if (t < V)
-                next_state[(size_t)s * V + t] = alive ? (int32_t)st[k] : -1;
+                __builtin_nontemporal_store(alive ? (int32_t)st[k] : -1, &next_state[(size_t)s * V + t]);
             const uint64_t mask = __ballot(alive);
             if (lane < 2 && w < W)
-                allow[(size_t)s * W + w] = (uint32_t)(mask >> (32 * lane));
+                __builtin_nontemporal_store((uint32_t)(mask >> (32 * lane)), &allow[(size_t)s * W + w]);
         }
     }
 }
@@ -569,7 +573,7 @@ __global__ __launch_bounds__(kPrefThreads) void walk_prefix_kernel(
                     break;
                 const bool alive = st[si] != kDead16;  // past-the-end slots are DEAD
                 if (t < we)
-                    next_state[(size_t)(s0 + si) * V + t] = alive ? (int32_t)st[si] : -1;
+                    __builtin_nontemporal_store(alive ? (int32_t)st[si] : -1, &next_state[(size_t)(s0 + si) * V + t]);
                 const uint64_t mask = __ballot(alive);
                 if (lane < 2)
                     words[si * 32 + k + lane] = (uint32_t)(mask >> (32 * lane));
@@ -580,7 +584,7 @@ __global__ __launch_bounds__(kPrefThreads) void walk_prefix_kernel(
         for (int i = lane; i < kPrefR * 32; i += kWave) {
             const int si = i / 32, k = i % 32;
             if (si < nS && k < nw)
-                allow[(size_t)(s0 + si) * W + w0 + k] = words[i];
+                __builtin_nontemporal_store(words[i], &allow[(size_t)(s0 + si) * W + w0 + k]);
         }
         wave_lds_sync();  // read before the next run's words are written
     }
