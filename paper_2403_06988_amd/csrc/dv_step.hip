@@ -428,16 +428,18 @@ __device__ __forceinline__ RowSplit split_row(const char *row, int V)
 // vectors [v0, v1) of `row` past its head, plus the head when `first` and
 // the tail when `last`.  `da` holds the first batch (loaded by the caller,
 // so it can be in flight before the row's state is known).  SHIFTED: the
-// head is not empty, so mask bits straddle two bytes.  Whenever the wave's
-// vector-path best improves, its entry of `ns_row` (the row state's
-// next-state row) is loaded at once, so the final gather is in flight long
-// before the block's maximum is known: `vec_pack` and `vec_ns` return that
-// best and its next state (wave-uniform).  The mask byte of vector v (bits
-// 8v .. 8v + 7 of the allow row) is mbytes[v - moff]: the allow row itself
-// (moff = 0) or the chunk's bytes staged in LDS.  `db` holds the second
-// batch when STAGED (issued by the caller before the staging finished).
-// SELECT (STAGED only): vectors with no allowed token are not read (see
-// load_batch_buf_sel).
+// head is not empty, so mask bits straddle two bytes.  The entry of
+// `ns_row` (the row state's next-state row) at the wave's vector-path best
+// is loaded once the stream is done, before the block's maximum is known:
+// `vec_pack` and `vec_ns` return that best and its next state
+// (wave-uniform).  The mask byte of vector v (bits 8v .. 8v + 7 of the
+// allow row) is mbytes[v - moff]: the allow row itself (moff = 0) or the
+// chunk's bytes staged in LDS.  `db` holds the second batch when STAGED
+// (issued by the caller before the staging finished).  SELECT (STAGED
+// only): vectors with no allowed token are not read (see
+// load_batch_buf_sel).  AHEAD2 (aligned rows streamed from memory): the
+// mask bytes are read two batches ahead of their logits and choose the
+// loads in the same way.
 template <int THREADS, int U, bool MASKED, bool SHIFTED, bool STAGED, bool SELECT, bool AHEAD2 = false>
 __device__ __forceinline__ uint64_t scan_bf16(const char *row, const uint32_t *arow, const uint8_t *mbytes,
                                               int moff, const int32_t *ns_row, RowSplit rs, int v0, int v1,
