@@ -1169,3 +1169,45 @@ def test_sample_is_reproducible_and_graph_safe(dv):
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(tk, t1) and torch.equal(nw, n1), f"replay {rep}"
+
+
+@pytest.mark.parametrize("B,V,head,extra_ld", [
+    (256, 128_256, 0, 0), (300, 70_001, 3, 5), (256, 4099, 7, 1), (260, 9, 1, 0), (256, 5, 0, 3),
+    (1030, 20_517, 5, 0), (512, 65_536, 0, 0),
+])
+def test_sample_large_batches_every_alignment(dv, B, V, head, extra_ld):
+    """bf16 batches of 256 rows or more: every row-start alignment (`head`
+    elements before the first 16-byte boundary), rows shorter than a vector,
+    random masks from empty to full, planted NaN, +-inf and ties, dead and
+    out-of-range states; two draws against the oracle."""
+    _say(f"sample large batches B={B} V={V} head={head} ld=V+{extra_ld}")
+    rng = np.random.default_rng(B * 31 + V + head)
+    S = 9
+    alive = rng.random((S, V)) < rng.choice([0.0, 0.002, 0.05, 0.3, 0.97, 1.0], size=(S, 1))
+    alive[S - 1, : V // 2] = True                 # a dense half, then an empty half
+    alive[S - 1, V // 2:] = False
+    ns = np.where(alive, rng.integers(0, S, (S, V)), -1).astype(np.int32)
+    Wd = (V + 31) // 32
+    pad = np.zeros((S, Wd * 32), bool)
+    pad[:, :V] = alive
+    al = np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(S, Wd)
+    states = rng.integers(-2, S + 2, B).astype(np.int32)
+    ld = V + extra_ld
+    offset = (8 - head) % 8
+    vals = (rng.standard_normal(B * ld + offset + 8) * 3).astype(np.float32)
+    buf = torch.from_numpy(vals).to(torch.bfloat16)
+    special = torch.tensor([float("nan"), float("inf"), -float("inf"), 1.5], dtype=torch.bfloat16)
+    pos = torch.from_numpy(rng.integers(0, buf.numel(), max(8, buf.numel() // 500)))
+    buf[pos] = special[torch.from_numpy(rng.integers(0, 4, pos.numel()))]
+    base = torch.empty(buf.numel() + 64, dtype=torch.bfloat16, device=DEV)
+    shift = (-(base.data_ptr() // 2)) % 8               # first 16-byte boundary of base
+    buf_d = base[shift:shift + buf.numel()]
+    buf_d.copy_(buf.to(DEV))
+    x = buf_d[offset:offset + B * ld].view(B, ld)[:, :V]
+    assert (x.data_ptr() // 2 + head) % 8 == 0
+    xo = to_oracle(buf[offset:offset + B * ld].view(B, ld))
+    for seed, off in ((5, 0), (6, 123)):
+        tok, new = dv.masked_sample(_dev(ns), _dev(al.view(np.int32)), _dev(states), x, seed, off)
+        t_o, n_o = oracle.masked_sample(ns, al, states, xo, 1.0, seed, off)
+        np.testing.assert_array_equal(tok.cpu().numpy(), t_o)
+        np.testing.assert_array_equal(new.cpu().numpy(), n_o)
