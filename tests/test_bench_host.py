@@ -65,3 +65,19 @@ def test_inputs_record_names_the_inputs():
     assert bench.inputs_record(t2, offsets, data, init)["dfa_sha256"] != r["dfa_sha256"]
     assert bench.inputs_record(trans, offsets, d2, init)["vocab_sha256"] != r["vocab_sha256"]
     assert bench.inputs_record(trans, offsets, data, init + 1)["init_states_sha256"] != r["init_states_sha256"]
+
+
+def test_kernel_source_hash_ignores_comments_only(tmp_path, monkeypatch):
+    """A recorded measurement stays attached to its kernel through edits of
+    the comments alone, and detaches on any change of code."""
+    import bench
+
+    src = tmp_path / "k.hip"
+    monkeypatch.setattr(bench, "CSRC", str(tmp_path))
+    monkeypatch.setattr(bench, "KERNEL_SOURCES", {"k": ("k.hip",)})
+    src.write_text("// header\nint f(int x) { return x + 1; }  // add one\n\n")
+    h0 = bench.kernel_source_hash("k")
+    src.write_text("// a longer header\n\n// more words\nint f(int x) { return x + 1; }  // adds one\n")
+    assert bench.kernel_source_hash("k") == h0
+    src.write_text("// header\nint f(int x) { return x + 2; }  // add one\n")
+    assert bench.kernel_source_hash("k") != h0
