@@ -1211,3 +1211,51 @@ def test_sample_large_batches_every_alignment(dv, B, V, head, extra_ld):
         t_o, n_o = oracle.masked_sample(ns, al, states, xo, 1.0, seed, off)
         np.testing.assert_array_equal(tok.cpu().numpy(), t_o)
         np.testing.assert_array_equal(new.cpu().numpy(), n_o)
+
+
+def _random_step_case(i):
+    rng = np.random.default_rng(0xC0FFEE + i)
+    B = int(rng.choice([1, 2, 7, 33, 64, 100, 255, 256, 257, 300, 513, 1024, 1100]))
+    V = int(rng.choice([1, 8, 9, 31, 4099, 32000, 50257, 65536, 70001, 128256, 140000, 262147]))
+    if B * V > 60_000_000:
+        V = max(1, 60_000_000 // B)
+    dtype = torch.bfloat16 if rng.random() < 0.75 else torch.float32
+    extra_ld = int(rng.choice([0, 0, 1, 3, 8, 13]))
+    offset = int(rng.integers(0, 8))
+    return rng, B, V, dtype, extra_ld, offset
+
+
+@pytest.mark.parametrize("case", range(40))
+def test_step_random_shapes(dv, case):
+    """Seeded random shapes across every launch form of the greedy step (one
+    block per row or split rows, mask bytes staged, two ahead or streamed,
+    aligned or shifted rows, bf16 and fp32): batch, vocabulary, row stride
+    and start offset, mask densities per state, dead and out-of-range
+    states, planted NaN, +-inf and signed zeros; greedy and opportunistic
+    steps against the oracle."""
+    rng, B, V, dtype, extra_ld, offset = _random_step_case(case)
+    _say(f"random step case {case}: B={B} V={V} {dtype} ld=V+{extra_ld} offset={offset}")
+    S = 7
+    alive = rng.random((S, V)) < rng.choice([0.0, 0.001, 0.05, 0.4, 0.95, 1.0], size=(S, 1))
+    ns = np.where(alive, rng.integers(0, S, (S, V)), -1).astype(np.int32)
+    Wd = (V + 31) // 32
+    pad = np.zeros((S, Wd * 32), bool)
+    pad[:, :V] = alive
+    al = np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(S, Wd)
+    states = rng.integers(-2, S + 1, B).astype(np.int32)
+    ld = V + extra_ld
+    n = B * ld + offset + 8
+    vals = rng.integers(-4, 5, n).astype(np.float32) if rng.random() < 0.5 else \
+        (rng.standard_normal(n) * 3).astype(np.float32)
+    buf = torch.from_numpy(vals).to(dtype)
+    special = torch.tensor([float("nan"), float("inf"), -float("inf"), -0.0, 0.0], dtype=dtype)
+    pos = torch.from_numpy(rng.integers(0, n, max(4, n // 2000)))
+    buf[pos] = special[torch.from_numpy(rng.integers(0, 5, pos.numel()))]
+    buf_d = buf.to(DEV)
+    x = buf_d[offset:offset + B * ld].view(B, ld)[:, :V]
+    xo = to_oracle(buf[offset:offset + B * ld].view(B, ld))
+    tok_o, new_o = oracle.masked_step(ns, al, states, xo)
+    for opp in (False, True):
+        tok, new = dv.masked_step(_dev(ns), _dev(al.view(np.int32)), _dev(states), x, opportunistic=opp)
+        np.testing.assert_array_equal(tok.cpu().numpy(), tok_o, err_msg=f"case {case} opportunistic={opp}")
+        np.testing.assert_array_equal(new.cpu().numpy(), new_o, err_msg=f"case {case} opportunistic={opp}")
