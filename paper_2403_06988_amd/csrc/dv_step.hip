@@ -41,10 +41,10 @@
 //     tokens key as 0; the loads of a later batch are issued right after it.
 //     Reduce: v_pk_max_u16 over the masked keys and one wave-wide max per
 //     batch (DPP moves, no LDS and no barrier); only the wave(s) holding the
-//     maximum search their masked keys for its lowest index.  The fast key differs from the exact ordering only for
-//     NaN (which must rank as -inf) and -0.0 (which must tie with +0.0); a
-//     batch whose maximum is one of those few key values is redone with
-//     exact keys.
+//     maximum search their masked keys for its lowest index.  The fast key
+//     differs from the exact ordering only for NaN (which must rank as -inf)
+//     and -0.0 (which must tie with +0.0); a batch whose maximum is one of
+//     those few key values is redone with exact keys.
 //   * A bf16 row need not be 16-byte aligned (any row stride): the elements
 //     before its first 16-byte boundary are read one by one and the mask
 //     bits of each vector are taken from two mask bytes, shifted.
