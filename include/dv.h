@@ -176,10 +176,11 @@ DV_API dv_status dv_validate_vocab(const int32_t *offsets, int32_t num_tokens, i
 /*
  * dv_masked_step_workspace_bytes -- device workspace dv_masked_step needs for
  * `batch` rows of `num_tokens` logits, for either dtype: where a row is
- * split over several blocks, they meet there (a running maximum and an
- * arrival count per row; the last block to arrive writes the row's outputs
- * and puts its entries back to zero).  Returns 0 when a size is outside its
- * limit.
+ * split over several blocks, they meet there (up to four blocks per row in
+ * pairs, one 64-bit word per pair; more through a running maximum and an
+ * arrival count per row; the block that finishes the row writes its
+ * outputs and puts its words back to zero).  Returns 0 when a size is
+ * outside its limit.
  */
 DV_API size_t dv_masked_step_workspace_bytes(int32_t batch, int32_t num_tokens);
 

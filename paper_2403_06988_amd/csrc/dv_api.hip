@@ -238,7 +238,10 @@ dv_status dv_masked_step(const int32_t *next_state, const uint32_t *allow, int32
 //
 // dv_masked_step_noalloc meets split rows in `scratch`, a device array of
 // the library, instead of a caller's workspace.  Its size covers
-// DV_NOALLOC_MAX_BATCH rows (the meeting entries depend on the batch only).
+// DV_NOALLOC_MAX_BATCH rows that meet through a maximum and a count (12
+// bytes a row); rows that meet in pairs need up to 24 bytes a row but occur
+// only below 256 rows, and the workspace check below refuses any call the
+// array would not cover.
 // Each GPU holds its own copy until the process ends.  Host code never uses
 // the array's name as an address: the device address of each GPU's copy is
 // looked up once per device and kept in g_scratch_ptr.

@@ -138,14 +138,40 @@ hipError_t launch_align(const int32_t *trans, int S, const int32_t *offsets, con
 // ----------------------------------------------------- split rows meet here
 //
 // When a row is split over several blocks, the blocks meet in the
-// workspace: per row a 64-bit maximum of (key << 32 | ~index) and a 32-bit
-// count of the blocks that have arrived, both zero between calls.  Each
-// block folds its best into the maximum and then counts itself; the block
-// that arrives last reads the maximum, puts both back to zero and writes the
-// row's outputs -- one kernel, no second pass, no waiting on other blocks.
-// Layout: best [B] uint64 at 0, arrived [B] uint32 at row_meet_count_offset.
+// workspace, whose words are all zero between calls; one lane per block
+// takes part, and no block ever waits for another.
+//
+// Up to kMeetTreeChunks chunks the blocks meet in pairs, as a binary tree
+// over the chunk indices: per row nchunks - 1 64-bit words, pair p of
+// level l at word (pairs below level l) + p.  A block folds its value into
+// its pair's word with a device-scope atomic maximum; the block that
+// finds the word zero arrived first and leaves, the other one has both
+// values (the maximum of the old word and its own), puts the word back to
+// zero and goes on to the next level; a chunk without a partner at a level
+// (an odd count) goes on without a trip.  The value of a block with
+// nothing allowed is 1, which every found value exceeds, so that zero
+// always means "not arrived".  The last block thus learns the row's
+// maximum after ceil(log2 nchunks) round trips, one per level.
+//
+// More chunks use two words per row: a 64-bit maximum and a 32-bit count
+// of the blocks that have arrived.  Each block folds its value into the
+// maximum and then counts itself; the block that arrives last reads the
+// maximum and puts both back to zero: three round trips.
+//
+// Layout: pairs [B][nchunks - 1] uint64 from 0 (up to kMeetTreeChunks
+// chunks); otherwise best [B] uint64 at 0 and arrived [B] uint32 at
+// row_meet_count_offset.
+constexpr int kMeetTreeChunks = 4;
 constexpr size_t row_meet_count_offset(int B) { return align_up((size_t)(B > 0 ? B : 1) * 8, 256); }
 constexpr size_t row_meet_bytes(int B) { return row_meet_count_offset(B) + align_up((size_t)(B > 0 ? B : 1) * 4, 256); }
+// the bytes a launch of B rows split into nchunks chunks needs (either layout)
+constexpr size_t row_meet_bytes(int B, int nchunks)
+{
+    const size_t pairs = nchunks >= 2 && nchunks <= kMeetTreeChunks
+                             ? align_up((size_t)(B > 0 ? B : 1) * (size_t)(nchunks - 1) * 8, 256)
+                             : 0;
+    return pairs > row_meet_bytes(B) ? pairs : row_meet_bytes(B);
+}
 
 struct RowMeet {
     uint64_t *best;
@@ -158,14 +184,40 @@ inline RowMeet row_meet(void *workspace, int B)
     return {reinterpret_cast<uint64_t *>(w), reinterpret_cast<uint32_t *>(w + row_meet_count_offset(B))};
 }
 
-// Called by one lane of each of the `nchunks` blocks of row b.  Both
-// updates are device-scope atomics (performed where every XCD sees them).
-// The arrival is counted only once the maximum has been performed: its
-// operand depends on the value the maximum returned.  Returns true in the
-// block that arrives last, with the row's maximum in `fin` and the row's
-// entries back at zero.
-__device__ __forceinline__ bool meet_row(RowMeet m, int b, int nchunks, uint64_t best, uint64_t &fin)
+// Called by one lane of each of the `nchunks` blocks of row b (this block
+// holds chunk c) with the block's best value, 0 when it found nothing.
+// All updates are device-scope atomics (performed where every XCD sees
+// them); each step's operand depends on the value the previous one
+// returned.  Returns true in the block that finishes the row, with the
+// row's maximum in `fin` (0 when nothing was found) and the row's words
+// back at zero.
+__device__ __forceinline__ bool meet_row(RowMeet m, int b, int c, int nchunks, uint64_t best, uint64_t &fin)
 {
+    if (nchunks <= kMeetTreeChunks) {
+        static_assert(kMeetTreeChunks == 4, "two levels at most");
+        uint64_t *pairs = m.best + (size_t)b * (size_t)(nchunks - 1);
+        uint64_t v = best ? best : 1ull;
+        // level 1: chunks 2k and 2k + 1 at word k (with three chunks, chunk 2
+        // has no partner there); level 2: the two survivors at word n / 2
+        if (nchunks != 3 || c < 2) {
+            uint64_t *w = pairs + (c >> 1);
+            const uint64_t other = __hip_atomic_fetch_max(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (!other)
+                return false;  // the partner carries both values on
+            (void)__hip_atomic_exchange(w, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            v = other > v ? other : v;
+        }
+        if (nchunks > 2) {
+            uint64_t *w = pairs + (nchunks >> 1);
+            const uint64_t other = __hip_atomic_fetch_max(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (!other)
+                return false;
+            (void)__hip_atomic_exchange(w, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            v = other > v ? other : v;
+        }
+        fin = v == 1ull ? 0ull : v;
+        return true;
+    }
     const uint64_t before = __hip_atomic_fetch_max(m.best + b, best, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     uint32_t one = 1u;
     asm volatile("" : "+v"(one) : "v"(before) : "memory");
@@ -239,10 +291,12 @@ inline StepGeometry step_geometry(int B, int V, int dtype)
     return {chunk_vec, nchunks, threads};
 }
 
+// either dtype's launch shape
 inline size_t step_workspace_bytes(int B, int V)
 {
-    (void)V;
-    return row_meet_bytes(B);
+    const size_t a = row_meet_bytes(B, step_geometry(B, V, 0).nchunks);
+    const size_t b = row_meet_bytes(B, step_geometry(B, V, 1).nchunks);
+    return a > b ? a : b;
 }
 
 hipError_t launch_masked_step(const int32_t *next_state, const uint32_t *allow, int S, int V,

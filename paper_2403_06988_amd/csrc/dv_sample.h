@@ -5,8 +5,9 @@
 
 namespace dv {
 
-// Workspace: the meeting slots of rows split over blocks (row_meet_bytes;
-// zero before the first call, left zero by every call).
+// Workspace: the meeting words of rows split over blocks (row_meet_bytes
+// for the launch's chunks per row; zero before the first call, left zero
+// by every call).
 size_t sample_workspace_bytes(int B, int V);
 
 hipError_t launch_masked_sample(const int32_t *next_state, const uint32_t *allow, int S, int V,

@@ -328,7 +328,7 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
     if (tid == 0) {
         for (int w = 1; w < kWaves; ++w)
             best = max_u64(best, red[w]);
-        if (nchunks == 1 || meet_row(meet, b, nchunks, best, best)) {  // else another block finishes the row
+        if (nchunks == 1 || meet_row(meet, b, c, nchunks, best, best)) {  // else another block finishes the row
             const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
             const bool found = live && tok >= 0 && tok < V;  // guards the read
             token[b] = found ? tok : -1;
@@ -342,8 +342,7 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
 
 size_t sample_workspace_bytes(int B, int V)
 {
-    (void)V;
-    return row_meet_bytes(B);
+    return row_meet_bytes(B, sample_geometry(B, V).nchunks);
 }
 
 hipError_t launch_masked_sample(const int32_t *next_state, const uint32_t *allow, int S, int V,

@@ -8,15 +8,16 @@
 //     B >= 256 (every CU gets at least one row), or when B >= 64 and the row
 //     holds at most 32768 logits (a second block per row buys nothing
 //     there).  Otherwise each row is split into about 32 / sqrt(B) chunks,
-//     one block each, and the chunks meet in the workspace: each block folds
-//     its best into the row's 64-bit entry with a device-scope atomic
-//     maximum, then counts itself with a device-scope atomic add whose
-//     operand depends on the maximum's result; the block that counts last
-//     takes the row's result and puts both entries back to zero.  For bf16
-//     the entry also carries the winner's next state, so that block reads
-//     nothing more.  No second kernel and no device-wide fences (a release
-//     fence at device scope writes back and invalidates the XCD's L2 on
-//     gfx950).
+//     one block each, and the chunks meet in the workspace (meet_row): up
+//     to four chunks in pairs, each pair's second block learning both
+//     values from one device-scope atomic maximum (one round trip per
+//     level); more chunks through a device-scope atomic maximum and then an
+//     atomic count whose operand depends on the maximum's result, the block
+//     that counts last taking the row's result.  The finishing block puts
+//     the entries back to zero.  For bf16 the 64-bit entry also carries the
+//     winner's next state, so that block reads nothing more.  No second
+//     kernel and no device-wide fences (a release fence at device scope
+//     writes back and invalidates the XCD's L2 on gfx950).
 //   * Each lane streams batches of 2 independent non-temporal 16-byte loads
 //     with a register double buffer: batch i + 1 is in flight while batch i
 //     is reduced.  Loads are branch-free and in a fixed order, because the
@@ -286,7 +287,7 @@ __global__ __launch_bounds__(THREADS) void masked_step_kernel(
     uint64_t best = block_max<THREADS>(pack(best_key, best_idx));
     if (threadIdx.x != 0)
         return;
-    if (nchunks > 1 && !meet_row(meet, b, nchunks, best, best))
+    if (nchunks > 1 && !meet_row(meet, b, c, nchunks, best, best))
         return;  // another block of the row finishes it
     const int tok = best ? (int)(0xFFFFFFFFu - (uint32_t)best) : -1;
     const bool found = tok >= 0 && tok < V;  // always true for a found token; guards the read
@@ -875,7 +876,7 @@ __global__ __launch_bounds__(THREADS) void masked_step_bf16_kernel(
     // Split rows: the meeting word carries the winner's next state, so the
     // block that arrives last needs no further read.
     uint64_t fin;
-    if (!meet_row(meet, b, nchunks, found ? pack_split(best, tok, nsv) : 0ull, fin))
+    if (!meet_row(meet, b, c, nchunks, found ? pack_split(best, tok, nsv) : 0ull, fin))
         return;  // another block of the row finishes it
     int ftok, fns;
     unpack_split(fin, ftok, fns);

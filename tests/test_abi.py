@@ -79,6 +79,18 @@ def test_workspace_queries():
     assert lib.dv_masked_step_workspace_bytes(0, 10) > 0
 
 
+def test_step_workspace_fits_the_noalloc_array():
+    """dv_masked_step_noalloc passes its scratch array as the workspace, sized
+    for DV_NOALLOC_MAX_BATCH rows meeting through a maximum and a count (12
+    bytes a row): every batch it accepts must need no more, including the
+    batches whose rows meet in pairs (up to 24 bytes a row)."""
+    cap = 768 * 1024
+    for V in (1, 1000, 32000, 70001, 128256, 256000, 1 << 24):
+        for B in list(range(1, 300)) + [511, 512, 1000, 4096, 65535, 65536]:
+            need = lib.dv_masked_step_workspace_bytes(B, V)
+            assert 0 < need <= cap, (B, V, need)
+
+
 def _align(trans=P, S=16, offsets=P + GB, bytes_=P + 2 * GB, V=1000, ns=P + 3 * GB,
            allow=P + 4 * GB, ws=P + 5 * GB, ws_bytes=None):
     if ws_bytes is None:

@@ -1213,6 +1213,47 @@ def test_sample_large_batches_every_alignment(dv, B, V, head, extra_ld):
         np.testing.assert_array_equal(new.cpu().numpy(), n_o)
 
 
+def test_split_rows_every_meeting_form_one_workspace(dv):
+    """Rows split in two, three and four chunks (which meet in pairs) and in
+    more (which meet through a maximum and a count), greedy in both dtypes and
+    sampled, all through one workspace: every call against the oracle, with
+    chunks and whole rows that hold no allowed token, and the workspace all
+    zero after every call."""
+    rng = np.random.default_rng(4242)
+    S = 6
+    calls = [("step", torch.bfloat16, 64, 128256), ("step", torch.bfloat16, 100, 128256),
+             ("step", torch.bfloat16, 128, 128256), ("step", torch.bfloat16, 33, 128256),
+             ("step", torch.float32, 64, 70001), ("step", torch.float32, 100, 70001),
+             ("step", torch.float32, 150, 40000), ("step", torch.float32, 20, 70001),
+             ("sample", torch.bfloat16, 512, 32000), ("sample", torch.bfloat16, 700, 32000),
+             ("sample", torch.float32, 1000, 32000), ("sample", torch.bfloat16, 256, 32000)]
+    need = max(dv.masked_step_workspace_bytes(B, V) if k == "step" else dv.masked_sample_workspace_bytes(B, V)
+               for k, _, B, V in calls)
+    ws = torch.zeros(need, dtype=torch.uint8, device=DEV)
+    for i, (kind, dtype, B, V) in enumerate(calls):
+        _say(f"meeting forms: {kind} {dtype} B={B} V={V}")
+        alive = rng.random((S, V)) < np.array([[0.0], [0.0005], [0.05], [0.6], [1.0], [0.0]])
+        alive[5, V // 3: V // 3 + 40] = True          # allowed tokens in one chunk only
+        ns = np.where(alive, rng.integers(0, S, (S, V)), -1).astype(np.int32)
+        Wd = (V + 31) // 32
+        pad = np.zeros((S, Wd * 32), bool)
+        pad[:, :V] = alive
+        al = np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(S, Wd)
+        states = rng.integers(-1, S, B).astype(np.int32)
+        x = torch.from_numpy((rng.standard_normal((B, V)) * 3).astype(np.float32)).to(dtype)
+        xo = to_oracle(x)
+        if kind == "step":
+            tok, new = dv.masked_step(_dev(ns), _dev(al.view(np.int32)), _dev(states), x.to(DEV), workspace=ws)
+            t_o, n_o = oracle.masked_step(ns, al, states, xo)
+        else:
+            tok, new = dv.masked_sample(_dev(ns), _dev(al.view(np.int32)), _dev(states), x.to(DEV), 9, i,
+                                        workspace=ws)
+            t_o, n_o = oracle.masked_sample(ns, al, states, xo, 1.0, 9, i)
+        np.testing.assert_array_equal(tok.cpu().numpy(), t_o, err_msg=f"{kind} {dtype} B={B} V={V}")
+        np.testing.assert_array_equal(new.cpu().numpy(), n_o, err_msg=f"{kind} {dtype} B={B} V={V}")
+        assert int(torch.count_nonzero(ws)) == 0, f"workspace left non-zero after {kind} {dtype} B={B} V={V}"
+
+
 def _random_step_case(i):
     rng = np.random.default_rng(0xC0FFEE + i)
     B = int(rng.choice([1, 2, 7, 33, 64, 100, 255, 256, 257, 300, 513, 1024, 1100]))
