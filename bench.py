@@ -342,10 +342,90 @@ def probe_lib():
     return lib
 
 
-def graph_seconds(launches, dev, reps=3):
-    """Seconds per replay of a HIP graph of ``launches()`` (run once eagerly
-    on a side stream first, then captured), timed with HIP events on the
-    replaying stream; the minimum over ``reps`` replays."""
+_HIP_RT = None
+
+
+def _hip_runtime():
+    """The HIP runtime library (already loaded by torch), for its own graph calls."""
+    import ctypes
+
+    global _HIP_RT
+    if _HIP_RT is None:
+        lib = ctypes.CDLL("libamdhip64.so")
+        vp, i32 = ctypes.c_void_p, ctypes.c_int
+        lib.hipStreamBeginCapture.argtypes = [vp, i32]
+        lib.hipStreamEndCapture.argtypes = [vp, ctypes.POINTER(vp)]
+        lib.hipGraphInstantiate.argtypes = [ctypes.POINTER(vp), vp, vp, ctypes.c_char_p, ctypes.c_size_t]
+        lib.hipGraphLaunch.argtypes = [vp, vp]
+        lib.hipGraphExecDestroy.argtypes = [vp]
+        lib.hipGraphDestroy.argtypes = [vp]
+        for f in (lib.hipStreamBeginCapture, lib.hipStreamEndCapture, lib.hipGraphInstantiate,
+                  lib.hipGraphLaunch, lib.hipGraphExecDestroy, lib.hipGraphDestroy):
+            f.restype = i32
+        lib.hipGetErrorString.argtypes = [i32]
+        lib.hipGetErrorString.restype = ctypes.c_char_p
+        _HIP_RT = lib
+    return _HIP_RT
+
+
+class HipGraph:
+    """``launches()`` captured into a HIP graph by the HIP runtime's own stream
+    capture (global mode, so any allocation or synchronization inside fails
+    the capture instead of running outside the graph) on a side stream, and
+    replayed with hipGraphLaunch on the current stream.
+
+    torch.cuda.graph is not used for timing: on this PyTorch build for ROCm,
+    once a process has made one torch capture, every later kernel of that
+    process runs longer (the same loads-only kernel over 256 rows of 128,256
+    bf16: 11.0 us per dispatch before and 11.8 us after, in rocprofv3 kernel
+    traces; captures made through the HIP API, in any capture mode, leave it
+    at 11.0)."""
+
+    def __init__(self, launches, dev):
+        import ctypes
+        import torch
+
+        self._lib = lib = _hip_runtime()
+        self._dev = dev
+        side = torch.cuda.Stream(dev)
+        side.wait_stream(torch.cuda.current_stream(dev))
+        torch.cuda.synchronize()
+        graph = ctypes.c_void_p()
+        self._check(lib.hipStreamBeginCapture(side.cuda_stream, 0), "hipStreamBeginCapture")
+        try:
+            with torch.cuda.stream(side):
+                launches()
+        finally:
+            rc = lib.hipStreamEndCapture(side.cuda_stream, ctypes.byref(graph))
+        self._check(rc, "hipStreamEndCapture")
+        self._graph = graph
+        self._exec = ctypes.c_void_p()
+        self._check(lib.hipGraphInstantiate(ctypes.byref(self._exec), graph, None, None, 0), "hipGraphInstantiate")
+        self._side = side
+
+    def _check(self, rc, what):
+        if rc != 0:
+            raise RuntimeError(f"{what}: {self._lib.hipGetErrorString(rc).decode()}")
+
+    def replay(self):
+        import torch
+
+        self._check(self._lib.hipGraphLaunch(self._exec, torch.cuda.current_stream(self._dev).cuda_stream),
+                    "hipGraphLaunch")
+
+    def close(self):
+        import torch
+
+        if self._exec:
+            torch.cuda.synchronize()
+            self._lib.hipGraphExecDestroy(self._exec)
+            self._lib.hipGraphDestroy(self._graph)
+            self._exec = None
+
+
+def capture(launches, dev):
+    """Run ``launches()`` once on a side stream (lazy set-up happens outside
+    the capture), then capture it (HipGraph)."""
     import torch
 
     side = torch.cuda.Stream(dev)
@@ -354,10 +434,16 @@ def graph_seconds(launches, dev, reps=3):
         launches()
     torch.cuda.current_stream(dev).wait_stream(side)
     torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        launches()
-    torch.cuda.synchronize()
+    return HipGraph(launches, dev)
+
+
+def graph_seconds(launches, dev, reps=3):
+    """Seconds per replay of a HIP graph of ``launches()`` (run once eagerly
+    on a side stream first, then captured), timed with HIP events on the
+    replaying stream; the minimum over ``reps`` replays."""
+    import torch
+
+    graph = capture(launches, dev)
     stream = torch.cuda.current_stream(dev)
     best = None
     for _ in range(reps):
@@ -368,7 +454,7 @@ def graph_seconds(launches, dev, reps=3):
         torch.cuda.synchronize()
         t = a.elapsed_time(b) / 1e3
         best = t if best is None else min(best, t)
-    del graph
+    graph.close()
     return best
 
 
@@ -563,16 +649,7 @@ def bench_spec(dv, w, wid, ns, al, x, tokens_all, states_all, dev, s=8, keep=0.9
     launches()
     torch.cuda.synchronize()
     ref = (tok.clone(), acc.clone(), nst.clone())
-    graph = torch.cuda.CUDAGraph()
-    side = torch.cuda.Stream(dev)
-    side.wait_stream(torch.cuda.current_stream(dev))
-    with torch.cuda.stream(side):
-        launches()
-    torch.cuda.current_stream(dev).wait_stream(side)
-    torch.cuda.synchronize()
-    with torch.cuda.graph(graph):
-        launches()
-    torch.cuda.synchronize()
+    graph = capture(launches, dev)
     stream = torch.cuda.current_stream(dev)
     times = []
     for _ in range(reps):
@@ -582,6 +659,7 @@ def bench_spec(dv, w, wid, ns, al, x, tokens_all, states_all, dev, s=8, keep=0.9
         b.record(stream)
         torch.cuda.synchronize()
         times.append(a.elapsed_time(b) / 1e3 / n_win)
+    graph.close()
     same = bool(torch.equal(tok, ref[0]) and torch.equal(acc, ref[1]) and torch.equal(nst, ref[2]))
     t = float(np.median(times))
     emitted = float((acc + (tok.gather(2, acc.to(torch.int64)[..., None])[..., 0] != -1)).sum()) / n_win
@@ -644,15 +722,7 @@ def bench_opportunistic(dv, w, ns, al, x, tokens_all, states_all, dev, adherent=
         launches()
         torch.cuda.synchronize()
         same_eager = bool(torch.equal(tks, tokens_all))
-        graph = torch.cuda.CUDAGraph()
-        side = torch.cuda.Stream(dev)
-        side.wait_stream(stream)
-        with torch.cuda.stream(side):
-            launches()
-        stream.wait_stream(side)
-        torch.cuda.synchronize()
-        with torch.cuda.graph(graph):
-            launches()
+        graph = capture(launches, dev)
         times = []
         for _ in range(reps):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -661,6 +731,7 @@ def bench_opportunistic(dv, w, ns, al, x, tokens_all, states_all, dev, adherent=
             b.record(stream)
             torch.cuda.synchronize()
             times.append(a.elapsed_time(b) / 1e3 / steps)
+        graph.close()
         same = same_eager and bool(torch.equal(tks, tokens_all))
         free = torch.stack([xv[k].float().argmax(dim=1) for k in range(steps)]).to(torch.int64)
         st = states_all[:-1].to(torch.int64)
@@ -716,15 +787,7 @@ def bench_sample(dv, w, ns, al, x, init_d, dev, seed=2024, reps=3):
     launches()
     torch.cuda.synchronize()
     ref = (tks.clone(), sts.clone())
-    graph = torch.cuda.CUDAGraph()
-    side = torch.cuda.Stream(dev)
-    side.wait_stream(stream)
-    with torch.cuda.stream(side):
-        launches()
-    stream.wait_stream(side)
-    torch.cuda.synchronize()
-    with torch.cuda.graph(graph):
-        launches()
+    graph = capture(launches, dev)
     times = []
     for _ in range(reps):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -733,6 +796,7 @@ def bench_sample(dv, w, ns, al, x, init_d, dev, seed=2024, reps=3):
         b.record(stream)
         torch.cuda.synchronize()
         times.append(a.elapsed_time(b) / 1e3 / steps)
+    graph.close()
     same = bool(torch.equal(tks, ref[0]) and torch.equal(sts, ref[1]))
     t = float(np.median(times))
     # work along the chain: allowed tokens and 4-token groups holding one
@@ -817,17 +881,8 @@ def main():
     # The per-token decode loop is launch-bound from Python (a ctypes call per
     # step costs more host time than the kernel takes), so it is captured once
     # in a HIP graph and replayed, as a serving loop would run it.
-    graph = torch.cuda.CUDAGraph()
-    side = torch.cuda.Stream(dev)
-    side.wait_stream(torch.cuda.current_stream(dev))
-    with torch.cuda.stream(side):
-        states_all[0].copy_(init_d)
-        decode_launches()
-    torch.cuda.current_stream(dev).wait_stream(side)
-    torch.cuda.synchronize()
-    with torch.cuda.graph(graph):
-        decode_launches()
-    torch.cuda.synchronize()
+    states_all[0].copy_(init_d)
+    graph = capture(decode_launches, dev)
     stream = torch.cuda.current_stream(dev)
 
     def mk():
@@ -848,6 +903,7 @@ def main():
         d1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    graph.close()
     graph_ok = bool(torch.equal(tokens_all, eager_tokens) and torch.equal(states_all, eager_states))
 
     align_ms = [a0.elapsed_time(a1) for (a0, a1, _, _) in ev]

@@ -11,36 +11,68 @@ namespace dv {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kProbeBlocks = 2048;
 
-__global__ __launch_bounds__(kThreads) void stream_read_kernel(const uint4 *__restrict__ src, size_t n16,
-                                                               uint32_t *__restrict__ sink)
+// HBM streaming: each block reads (writes) one contiguous chunk of the
+// buffer, four 16-byte vectors per lane in flight.  Against a grid-stride
+// loop over the whole buffer (2,048 blocks of 256 lanes, cached loads) this
+// form reaches about 7.2 TB/s of reads instead of 5.5, and 6.0-6.2 TB/s of
+// writes instead of 5.0 (2 GiB buffers, one MI355X): a sweep over chunked
+// and grid-stride forms, 256 to 4,096 blocks of 256 to 1,024 lanes, 1 to 8
+// vectors in flight, cached and non-temporal, found these among the best.
+constexpr int kStreamThreads = 512;
+constexpr int kStreamU = 4;
+constexpr int kStreamReadBlocks = 512;
+constexpr int kStreamWriteBlocks = 2048;
+
+typedef unsigned int stream_u32x4 __attribute__((ext_vector_type(4)));
+
+// [begin, end) of block `blk`'s chunk of n16 vectors over `blocks` blocks
+__device__ __forceinline__ void stream_chunk(size_t n16, int blocks, int blk, size_t &begin, size_t &end)
 {
-    constexpr int kU = 8;
-    const size_t stride = (size_t)gridDim.x * kThreads;
+    const size_t per = n16 / (size_t)blocks, extra = n16 % (size_t)blocks;
+    begin = (size_t)blk * per + ((size_t)blk < extra ? (size_t)blk : extra);
+    end = begin + per + ((size_t)blk < extra ? 1 : 0);
+}
+
+__global__ __launch_bounds__(kStreamThreads) void stream_read_kernel(const uint4 *__restrict__ src, size_t n16,
+                                                                     uint32_t *__restrict__ sink)
+{
+    const stream_u32x4 *p = reinterpret_cast<const stream_u32x4 *>(src);
+    size_t begin, end;
+    stream_chunk(n16, (int)gridDim.x, (int)blockIdx.x, begin, end);
     uint32_t acc = 0;
-    size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
-    for (; i + (kU - 1) * stride < n16; i += kU * stride) {
-        uint4 v[kU];
+    size_t i = begin + threadIdx.x;
+    for (; i + (size_t)(kStreamU - 1) * kStreamThreads < end; i += (size_t)kStreamU * kStreamThreads) {
+        stream_u32x4 v[kStreamU];
 #pragma unroll
-        for (int u = 0; u < kU; ++u)
-            v[u] = src[i + u * stride];
+        for (int u = 0; u < kStreamU; ++u)
+            v[u] = __builtin_nontemporal_load(p + i + (size_t)u * kStreamThreads);
 #pragma unroll
-        for (int u = 0; u < kU; ++u)
+        for (int u = 0; u < kStreamU; ++u)
             acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
     }
-    for (; i < n16; i += stride) {
-        const uint4 v = src[i];
+    for (; i < end; i += kStreamThreads) {
+        const stream_u32x4 v = __builtin_nontemporal_load(p + i);
         acc ^= v.x ^ v.y ^ v.z ^ v.w;
     }
     if (acc == 0x9E3779B9u)  // practically never: keeps the loads alive
         sink[blockIdx.x & 4095] = acc;
 }
 
-__global__ __launch_bounds__(kThreads) void stream_write_kernel(uint4 *__restrict__ dst, size_t n16)
+__global__ __launch_bounds__(kStreamThreads) void stream_write_kernel(uint4 *__restrict__ dst, size_t n16)
 {
-    const size_t stride = (size_t)gridDim.x * kThreads;
-    for (size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x; i < n16; i += stride) {
+    size_t begin, end;
+    stream_chunk(n16, (int)gridDim.x, (int)blockIdx.x, begin, end);
+    size_t i = begin + threadIdx.x;
+    for (; i + (size_t)(kStreamU - 1) * kStreamThreads < end; i += (size_t)kStreamU * kStreamThreads) {
+#pragma unroll
+        for (int u = 0; u < kStreamU; ++u) {
+            const size_t j = i + (size_t)u * kStreamThreads;
+            const uint32_t x = (uint32_t)j;
+            dst[j] = make_uint4(x, x + 1, x + 2, x + 3);
+        }
+    }
+    for (; i < end; i += kStreamThreads) {
         const uint32_t x = (uint32_t)i;
         dst[i] = make_uint4(x, x + 1, x + 2, x + 3);
     }
@@ -287,7 +319,7 @@ int32_t dvprobe_stream_read(const void *src, size_t n_bytes, uint32_t *sink, voi
 {
     if (!src || !sink || n_bytes < 4096 || (n_bytes & 15) || (reinterpret_cast<uintptr_t>(src) & 15))
         return 1;
-    dv::stream_read_kernel<<<dv::kProbeBlocks, dv::kThreads, 0, static_cast<hipStream_t>(stream)>>>(
+    dv::stream_read_kernel<<<dv::kStreamReadBlocks, dv::kStreamThreads, 0, static_cast<hipStream_t>(stream)>>>(
         static_cast<const uint4 *>(src), n_bytes / 16, sink);
     return hipGetLastError() == hipSuccess ? 0 : 6;
 }
@@ -296,7 +328,7 @@ int32_t dvprobe_stream_write(void *dst, size_t n_bytes, void *stream)
 {
     if (!dst || n_bytes < 4096 || (n_bytes & 15) || (reinterpret_cast<uintptr_t>(dst) & 15))
         return 1;
-    dv::stream_write_kernel<<<dv::kProbeBlocks, dv::kThreads, 0, static_cast<hipStream_t>(stream)>>>(
+    dv::stream_write_kernel<<<dv::kStreamWriteBlocks, dv::kStreamThreads, 0, static_cast<hipStream_t>(stream)>>>(
         static_cast<uint4 *>(dst), n_bytes / 16);
     return hipGetLastError() == hipSuccess ? 0 : 6;
 }
