@@ -659,10 +659,12 @@ def test_step_rejects_in_place_update(dv):
     assert e.value.status == 4
 
 
+@pytest.mark.parametrize("capture", ["torch", "hip"])
 @pytest.mark.parametrize("wid", [2, 3, 4])
-def test_step_graph_replay_matches_eager(dv, wid):
-    """The decode loop captured as a HIP graph (as the benchmark runs it) gives
-    the eager results on every replay, with eager work in between."""
+def test_step_graph_replay_matches_eager(dv, wid, capture):
+    """The decode loop captured as a HIP graph gives the eager results on
+    every replay, with eager work in between: captured by torch.cuda.graph,
+    and by the HIP API's own stream capture as the benchmark captures it."""
     w = W.WORKLOADS[wid]
     trans, offsets, data, ns, al = _workload_table(dv, wid)
     steps = 16
@@ -686,9 +688,13 @@ def test_step_graph_replay_matches_eager(dv, wid):
         launches()
     torch.cuda.current_stream(DEV).wait_stream(side)
     torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        launches()
+    if capture == "torch":
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            launches()
+    else:
+        import bench
+        g = bench.HipGraph(launches, DEV)
     for rep in range(3):
         tk.fill_(-7)
         st[1:].fill_(-7)
@@ -696,6 +702,8 @@ def test_step_graph_replay_matches_eager(dv, wid):
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(tk, ref_t) and torch.equal(st, ref_s), f"replay {rep}"
+    if capture == "hip":
+        g.close()
 
 
 # ------------------------------------------------------- end-of-sequence column
