@@ -184,8 +184,8 @@ inline RowMeet row_meet(void *workspace, int B)
     return {reinterpret_cast<uint64_t *>(w), reinterpret_cast<uint32_t *>(w + row_meet_count_offset(B))};
 }
 
-// Called by one lane of each of the `nchunks` blocks of row b (this block
-// holds chunk c) with the block's best value, 0 when it found nothing.
+// Called by one lane of each of the `nchunks` (>= 2) blocks of row b (this
+// block holds chunk c) with the block's best value, 0 when it found nothing.
 // All updates are device-scope atomics (performed where every XCD sees
 // them); each step's operand depends on the value the previous one
 // returned.  Returns true in the block that finishes the row, with the
