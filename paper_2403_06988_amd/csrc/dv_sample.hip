@@ -98,6 +98,37 @@ __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_
     return make_uint4(c0, c1, c2, c3);
 }
 
+// Word e (0 .. 3) of philox4x32_10's output, for a lane that needs only
+// that word: the same ten rounds, the last of which computes only the
+// product the word comes from (words 0 and 1 from the multiple of c2,
+// words 2 and 3 from the multiple of c0) -- one 32 x 32 -> 64-bit
+// multiply fewer per call.
+__device__ __forceinline__ uint32_t philox4x32_10_word(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                                       uint32_t k0, uint32_t k1, int e)
+{
+#pragma unroll
+    for (int round = 0; round < 9; ++round) {
+        if (round > 0) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        c1 = (uint32_t)p1;
+        c3 = (uint32_t)p0;
+        c0 = n0;
+        c2 = n2;
+    }
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+    const bool from_c2 = e < 2;
+    const uint64_t p = (uint64_t)(from_c2 ? 0xCD9E8D57u : 0xD2511F53u) * (from_c2 ? c2 : c0);
+    const uint32_t high = (uint32_t)(p >> 32) ^ (from_c2 ? (c1 ^ k0) : (c3 ^ k1));
+    return (e & 1) ? (uint32_t)p : high;
+}
+
 // ln of a positive normal binary32: x = m 2^e, m in [sqrt(1/2), sqrt(2));
 // z = (m - 1) / (m + 1) with the reciprocal by four Newton steps from 1/2;
 // ln m = 2 (z + z^3 (1/3 + w (1/5 + w (1/7 + w / 9)))), w = z^2;
@@ -290,8 +321,9 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
                 for (int q = lane; q < toks; q += kWave) {
                     const uint32_t i = queue[wave][q];
                     const float x = logit_at<DT>(row, (int)i);  // in flight during the Philox rounds
-                    const uint4 rnd = philox4x32_10(i >> 2, (uint32_t)b, off_lo, off_hi, seed_lo, seed_hi);
-                    const float key = __builtin_fmaf(x, inv_t, gumbel_of_word(pick(rnd, (int)(i & 3u))));
+                    const uint32_t word =
+                        philox4x32_10_word(i >> 2, (uint32_t)b, off_lo, off_hi, seed_lo, seed_hi, (int)(i & 3u));
+                    const float key = __builtin_fmaf(x, inv_t, gumbel_of_word(word));
                     const uint64_t packed =
                         ((uint64_t)order_key(__float_as_uint(key)) << 32) | (uint64_t)(0xFFFFFFFFu - i);
                     best = max_u64(best, packed);
