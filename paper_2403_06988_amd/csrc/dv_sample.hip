@@ -77,6 +77,13 @@ SampleGeometry sample_geometry(int B, int V)
     return {kThreads, per * per_iter, (iters + per - 1) / per, span};
 }
 
+// a ^ b ^ c in one v_bitop3_b32 (truth table 0x96); the compiler leaves
+// the Philox rounds' three-way XORs as two instructions otherwise.
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c)
+{
+    return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
 __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
                                                uint32_t k1)
 {
@@ -88,8 +95,8 @@ __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_
         }
         const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
         const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
-        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
-        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        const uint32_t n0 = xor3((uint32_t)(p1 >> 32), c1, k0);
+        const uint32_t n2 = xor3((uint32_t)(p0 >> 32), c3, k1);
         c1 = (uint32_t)p1;
         c3 = (uint32_t)p0;
         c0 = n0;
@@ -114,8 +121,8 @@ __device__ __forceinline__ uint32_t philox4x32_10_word(uint32_t c0, uint32_t c1,
         }
         const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
         const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
-        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
-        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        const uint32_t n0 = xor3((uint32_t)(p1 >> 32), c1, k0);
+        const uint32_t n2 = xor3((uint32_t)(p0 >> 32), c3, k1);
         c1 = (uint32_t)p1;
         c3 = (uint32_t)p0;
         c0 = n0;
@@ -125,7 +132,7 @@ __device__ __forceinline__ uint32_t philox4x32_10_word(uint32_t c0, uint32_t c1,
     k1 += 0xBB67AE85u;
     const bool from_c2 = e < 2;
     const uint64_t p = (uint64_t)(from_c2 ? 0xCD9E8D57u : 0xD2511F53u) * (from_c2 ? c2 : c0);
-    const uint32_t high = (uint32_t)(p >> 32) ^ (from_c2 ? (c1 ^ k0) : (c3 ^ k1));
+    const uint32_t high = xor3((uint32_t)(p >> 32), from_c2 ? c1 : c3, from_c2 ? k0 : k1);
     return (e & 1) ? (uint32_t)p : high;
 }
 
