@@ -227,15 +227,6 @@ __device__ __forceinline__ uint4 group_logits(const char *row, bool aligned, uin
     return v;
 }
 
-__device__ __forceinline__ uint32_t pick(uint4 v, int e)
-{
-    uint32_t r = v.x;
-    r = e == 1 ? v.y : r;
-    r = e == 2 ? v.z : r;
-    r = e == 3 ? v.w : r;
-    return r;
-}
-
 // Exclusive prefix sum over the wave of a count in [0, 15], and the wave's
 // total, from four ballots of the count's bits (no LDS, no waits).
 __device__ __forceinline__ int wave_prefix_small(int cnt, int &total)
@@ -339,20 +330,28 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
                 for (int q = lane; q < groups; q += kWave) {
                     const uint32_t entry = queue[wave][q];
                     const uint32_t g = entry >> 4;
-                    uint32_t bitsg = entry & 0xFu;
+                    const uint32_t bitsg = entry & 0xFu;
                     // the logits first: their load is in flight during the Philox rounds
                     const uint4 xs = group_logits<DT>(row, aligned, g, bitsg, V);
                     const uint4 rnd = philox4x32_10(g, (uint32_t)b, off_lo, off_hi, seed_lo, seed_hi);
-                    while (bitsg) {
-                        const int e = __builtin_ctz(bitsg);
-                        bitsg &= bitsg - 1u;
-                        const int i = (int)(g * 4u) + e;
-                        const float key =
-                            __builtin_fmaf(__uint_as_float(pick(xs, e)), inv_t, gumbel_of_word(pick(rnd, e)));
+                    // one guarded pass per position of the group (a pass runs
+                    // when any lane of the wave has that token allowed): the
+                    // logit and the Philox word are then fixed registers
+                    auto noise = [&](uint32_t x, uint32_t word, uint32_t e) {
+                        const uint32_t i = g * 4u + e;
+                        const float key = __builtin_fmaf(__uint_as_float(x), inv_t, gumbel_of_word(word));
                         const uint64_t packed =
-                            ((uint64_t)order_key(__float_as_uint(key)) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i);
+                            ((uint64_t)order_key(__float_as_uint(key)) << 32) | (uint64_t)(0xFFFFFFFFu - i);
                         best = max_u64(best, packed);
-                    }
+                    };
+                    if (bitsg & 1u)
+                        noise(xs.x, rnd.x, 0u);
+                    if (bitsg & 2u)
+                        noise(xs.y, rnd.y, 1u);
+                    if (bitsg & 4u)
+                        noise(xs.z, rnd.z, 2u);
+                    if (bitsg & 8u)
+                        noise(xs.w, rnd.w, 3u);
                 }
             }
             wave_lds_sync();  // every lane has read its entries before the next iteration writes
