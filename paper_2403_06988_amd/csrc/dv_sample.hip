@@ -177,15 +177,17 @@ __device__ __forceinline__ float gumbel_of_word(uint32_t w)
     return -ln_f32(-ln_f32(u));
 }
 
-// Order-preserving key of an fp32 bit pattern: NaN ranks as -inf, -0.0 as
-// +0.0; every value's key is > 0, so 0 stands for "nothing yet".
-__device__ __forceinline__ uint32_t order_key(uint32_t u)
+// Order-preserving key of a binary32 value: NaN ranks as -inf, -0.0 as
+// +0.0; every value's key is > 0, so 0 stands for "nothing yet".  Adding
+// +0.0 turns -0.0 into +0.0 and leaves every other value as it is (round to
+// nearest); then negatives have all their bits flipped, the rest their sign.
+__device__ __forceinline__ uint32_t order_key(float x)
 {
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u)
-        u = 0xFF800000u;
-    if (u == 0x80000000u)
-        u = 0u;
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+#pragma clang fp contract(off)
+    float c = x + 0.0f;
+    c = c != c ? -__builtin_inff() : c;
+    const uint32_t u = __float_as_uint(c);
+    return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
 }
 
 __device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return a > b ? a : b; }
@@ -323,7 +325,7 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
                         philox4x32_10_word(i >> 2, (uint32_t)b, off_lo, off_hi, seed_lo, seed_hi, (int)(i & 3u));
                     const float key = __builtin_fmaf(x, inv_t, gumbel_of_word(word));
                     const uint64_t packed =
-                        ((uint64_t)order_key(__float_as_uint(key)) << 32) | (uint64_t)(0xFFFFFFFFu - i);
+                        ((uint64_t)order_key(key) << 32) | (uint64_t)(0xFFFFFFFFu - i);
                     best = max_u64(best, packed);
                 }
             } else {
@@ -341,7 +343,7 @@ __global__ __launch_bounds__(THREADS) void masked_sample_kernel(
                         const uint32_t i = g * 4u + e;
                         const float key = __builtin_fmaf(__uint_as_float(x), inv_t, gumbel_of_word(word));
                         const uint64_t packed =
-                            ((uint64_t)order_key(__float_as_uint(key)) << 32) | (uint64_t)(0xFFFFFFFFu - i);
+                            ((uint64_t)order_key(key) << 32) | (uint64_t)(0xFFFFFFFFu - i);
                         best = max_u64(best, packed);
                     };
                     if (bitsg & 1u)
